@@ -1,0 +1,22 @@
+"""CPU oracle for the SLiM compressed linear layer and SLoPe's double-pruned backward.
+
+TEST INFRASTRUCTURE ONLY. Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package. The HIP product path
+never calls it and shares no code with it.
+
+Everything here is plain NumPy in float64 (pure Python in ``brute``), written from
+the thesis' definitions:
+
+* 2:4 magnitude mask along the reduction dimension (SLoPe, "Double-pruned Backward
+  Pass"; background section "Sparse Tensor Core Acceleration").
+* Group-wise symmetric AbsMax int4 quantisation of the kept weights (SLiM, section
+  "Quantization" under the preliminaries and eq. symmetric_quantization, group size
+  128 as in the SLiM experimental setup and "Low-rank adapter quantization").
+* The compressed layer Y = X Wc^T + (X L) R (SLiM, sparse plus low-rank; SLoPe
+  eq. sparse_plus_low_rank).
+* SLoPe's double-pruned input gradient dX = dY W^{R,C} (eq. sparse_backward_input)
+  and Lemma sparsity_ratio.
+
+Parity status per function is stated in ``slim_oracle``'s module docstring.
+"""
+from . import slim_oracle  # noqa: F401
