@@ -1,0 +1,186 @@
+/*
+ * slim.h - C ABI of libslim: the SLiM compressed linear layer on AMD Instinct MI355X (gfx950).
+ *
+ * The layer (thesis "Compression Trinity", SLiM chapter, section "Quantized sparse plus
+ * low-rank approximation of LLMs"; SLoPe chapter, eq. sparse_plus_low_rank) is
+ *
+ *     Y = X * Wc^T + (X * L) * R,      Wc = dequant(Q(M (.) W))
+ *
+ * where M keeps two of every four consecutive weights along the reduction dimension K,
+ * Q is symmetric AbsMax 4-bit quantisation per group of 128 weights of a row, and L*R is
+ * a rank-r adapter kept as a parallel dense path. SLoPe's double-pruned input gradient
+ * (SLoPe chapter, "Double-pruned Backward Pass", eq. sparse_backward_input) is
+ *
+ *     dX = dY * W^{R,C} + (dY * R^T) * L^T,
+ *
+ * where W^{R,C} is Wc pruned 2:4 a second time along N, so that the backward contraction is
+ * sparse along its own reduction dimension too.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Shapes: W is [N x K] (N output features, K input features), X is [M x K], Y is [M x N],
+ * L is [K x r], R is [r x N], dY is [M x N], dX is [M x K]. Everything is dense row-major
+ * with no padding between rows.
+ *
+ * Pointers: every array argument is a DEVICE pointer unless the comment says "host". The
+ * caller allocates and owns every buffer, including workspace. The library never frees
+ * anything and never keeps a pointer after a call returns.
+ *
+ * Alignment: device arrays must be 16-byte aligned.
+ *
+ * Streams: `stream` is a hipStream_t cast to void* (NULL = the null stream). Work is
+ * enqueued on it; slim_linear and slim_linear_bwd_dx return without synchronising, and a
+ * kernel fault shows up at the caller's next synchronisation of that stream.
+ *
+ * Errors: every entry point returns an slim_status. Argument checks run on the host before
+ * anything is enqueued; when a check fails nothing is launched and the outputs are not
+ * touched. No C++ exception crosses the ABI.
+ *
+ * Packed format (all multi-byte words little-endian)
+ * --------------------------------------------------
+ *   codes  uint8 [N, K/4]: read as uint32 words [N, K/16]. Word b of row n covers K positions
+ *          16b..16b+15, which form four groups of four (c = 0..3). Bits 4c..4c+3 hold the code
+ *          u = q + 8 of group c's lower kept position; bits 16+4c..16+4c+3 hold that of its
+ *          higher kept position. q is in [-7, 7], so u is in [1, 15].
+ *   meta   uint8 [N, K/8]: read as uint16 half-words [N, K/16]. Half-word b holds, for group c of
+ *          the same 16 positions, the kept offsets i0 < i1 (0..3) as i0 in bits 4c..4c+1 and
+ *          i1 in bits 4c+2..4c+3.
+ *   scales uint16 [N, K/128]: fp16 bit patterns, s16 = fp16_RNE(fp32(max|w| of the group) / 7).
+ *   The value of kept weight (n, k) is (u - 8) * s16[n, k/128]; every other weight is zero.
+ *
+ * Backward pack: the same code/meta format along N instead of K, one row per input feature:
+ *   codesT uint8 [K, N/4], metaT uint8 [K, N/8], scalesT uint16 [K/128, N] (scales transposed).
+ */
+#ifndef SLIM_H
+#define SLIM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SLIM_ABI_VERSION 1
+
+typedef enum {
+  SLIM_OK = 0,
+  SLIM_EINVAL = 1,        /* a required pointer is NULL, or an argument is out of range */
+  SLIM_ESHAPE = 2,        /* a size breaks a divisibility or range rule */
+  SLIM_EDTYPE = 3,        /* unsupported dtype code */
+  SLIM_EALIGN = 4,        /* a device array is not 16-byte aligned */
+  SLIM_ENONFINITE = 5,    /* W holds a NaN or an infinity */
+  SLIM_ERANGE = 6,        /* a group scale max|w|/7 overflows fp16 */
+  SLIM_EWORKSPACE = 7,    /* workspace missing or smaller than the query returned */
+  SLIM_EDEVICE = 8,       /* a HIP runtime call or a kernel launch failed */
+  SLIM_EUNSUPPORTED = 9   /* valid but not supported by this build (e.g. no gfx950 device) */
+} slim_status;
+
+typedef enum { SLIM_F16 = 0, SLIM_BF16 = 1 } slim_dtype;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* slim_status_string(int status);
+
+/* SLIM_ABI_VERSION of the built library. */
+int slim_abi_version(void);
+
+/*
+ * slim_pack - one-time forward pack of a dense fp32 weight.
+ * Thesis: 2:4 magnitude pruning along the reduction dimension (SLoPe "Double-pruned Backward
+ * Pass"; background "Sparse Tensor Core Acceleration"); symmetric AbsMax quantisation
+ * (SLiM preliminaries, eq. symmetric_quantization) with groups of 128 (SLiM setup).
+ *
+ *   W       fp32 [N, K], device.
+ *   N, K    N >= 1; K >= 128 and K % 128 == 0.
+ *   codes   out, uint8 [N, K/4]; meta out, uint8 [N, K/8]; scales out, uint16 [N, K/128].
+ *   mask    out, optional (NULL to skip): uint8 [N, K], 1 where the weight is kept.
+ * Mask rule: in each aligned group of four along K, keep the two largest |w|; on equal
+ * magnitude the lower position wins (-0 and +0 are equal). Codes: q = clamp(rint(w / s16), -7, 7)
+ * with the division done in double precision and ties rounded to even; q = 0 when s16 == 0.
+ * Returns SLIM_ENONFINITE if W holds a NaN/Inf and SLIM_ERANGE if a scale overflows fp16; the
+ * outputs are then unspecified. This call synchronises `stream` (it reads back a status word)
+ * and allocates 4 bytes of device memory for that word for the duration of the call.
+ */
+int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, uint8_t* meta,
+              uint16_t* scales, uint8_t* mask, void* stream);
+
+/*
+ * slim_pack_bwd - one-time backward pack: prune the packed forward weight a second time,
+ * 2:4 along N, for the transposed contraction of the input gradient.
+ * Thesis: SLoPe "Double-pruned Backward Pass" (W^{R,C}, eq. sparse_backward_input; Lemma
+ * sparsity_ratio gives the extra zeros, 9.375% for 2:4).
+ *
+ *   codes, meta, scales   a forward pack of an [N, K] weight (from slim_pack), device.
+ *   N, K                  N >= 16 and N % 16 == 0; K % 128 == 0.
+ *   codesT  out, uint8 [K, N/4]; metaT out, uint8 [K, N/8]; scalesT out, uint16 [K/128, N].
+ *   mask_rc out, optional (NULL to skip): uint8 [N, K], 1 on the support of W^{R,C}.
+ * Rule: for each column k and aligned group of four rows, keep two slots ranked by
+ * (|Wc| descending, forward-kept descending, row ascending). A kept slot carries its forward
+ * code (8, i.e. zero, if the forward mask had dropped it). Asynchronous on `stream`.
+ */
+int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const uint16_t* scales, int64_t N,
+                  int64_t K, uint8_t* codesT, uint8_t* metaT, uint16_t* scalesT, uint8_t* mask_rc,
+                  void* stream);
+
+/*
+ * slim_linear_workspace - bytes of device workspace slim_linear needs for these sizes
+ * (written to *bytes, host pointer). Depends only on the sizes. Pure host function.
+ */
+int slim_linear_workspace(int64_t M, int64_t N, int64_t K, int64_t r, size_t* bytes);
+
+/*
+ * slim_bwd_dx_workspace - bytes of device workspace slim_linear_bwd_dx needs. Pure host function.
+ */
+int slim_bwd_dx_workspace(int64_t M, int64_t N, int64_t K, int64_t r, size_t* bytes);
+
+/*
+ * slim_workspace_init - zero a workspace before its first use (its leading control words must
+ * start at zero; every successful call leaves them at zero again). Asynchronous on `stream`.
+ */
+int slim_workspace_init(void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * slim_linear - Y = X * Wc^T + (X * L) * R, fp32 accumulation, fp32 output.
+ * Thesis: SLiM "SLiM-LoRA low-rank adapters" (W ~ W^C + L R) and SLoPe eq. sparse_plus_low_rank
+ * with the adapter as a parallel path; the adapter product is fused into the same kernels.
+ *
+ *   X       [M, K] in `xdtype` (SLIM_BF16 or SLIM_F16), device.
+ *   M, N, K M >= 1, N >= 1, K % 128 == 0.
+ *   codes, meta, scales   forward pack of W (slim_pack).
+ *   L, R    fp16 [K, r] and [r, N]; both NULL when r == 0. r % 16 == 0.
+ *   Y       out, fp32 [M, N]. Must not alias any input.
+ *   ws      device workspace of at least slim_linear_workspace(M, N, K, r) bytes, zeroed once
+ *           with slim_workspace_init before its first use. Two calls that overlap in time must
+ *           not share a workspace.
+ * Operand precision: bf16 activations are converted to fp16 (exact for |x| in
+ * [2^-14, 65504]); dequantised weights are (u-8)*s16 rounded to fp16; the adapter intermediate
+ * X*L is kept in fp32 and rounded to fp16 for the second product. Deterministic: identical
+ * inputs give identical bits.
+ */
+int slim_linear(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const uint8_t* codes,
+                const uint8_t* meta, const uint16_t* scales, const uint16_t* L, const uint16_t* R,
+                int64_t r, float* Y, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * slim_linear_bwd_dx - dX = dY * W^{R,C} + (dY * R^T) * L^T, fp32 accumulation, fp32 output.
+ * Thesis: SLoPe eq. sparse_backward_input (BWD-2 with the double-pruned weight) plus the adapter
+ * path's input gradient.
+ *
+ *   dY      [M, N] in `dydtype` (SLIM_BF16 or SLIM_F16), device.
+ *   M, N, K M >= 1, N % 16 == 0, K % 128 == 0.
+ *   codesT, metaT, scalesT   backward pack (slim_pack_bwd).
+ *   L, R    fp16 [K, r] and [r, N]; both NULL when r == 0. r % 16 == 0.
+ *   dX      out, fp32 [M, K].
+ *   ws      workspace of at least slim_bwd_dx_workspace(M, N, K, r) bytes, zeroed once.
+ * Operand precision: the weight codes enter the matrix cores as exact small integers and the
+ * fp16 scale is folded into dY per (row n, 128-group of k), rounded to fp16.
+ */
+int slim_linear_bwd_dx(const void* dY, int dydtype, int64_t M, int64_t N, int64_t K,
+                       const uint8_t* codesT, const uint8_t* metaT, const uint16_t* scalesT,
+                       const uint16_t* L, const uint16_t* R, int64_t r, float* dX, void* ws,
+                       size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SLIM_H */

@@ -1,0 +1,155 @@
+// api.cpp - status strings, version, argument checks, launch plans and workspace queries.
+// Pure host code: nothing here touches the GPU, so these paths are testable without one.
+#include <algorithm>
+
+#include "slim_host.h"
+
+namespace {
+constexpr int64_t kMaxDim = int64_t(1) << 31;
+constexpr size_t kCounterSlots = SLIM_COUNTER_SLOTS;
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
+}  // namespace
+
+extern "C" const char* slim_status_string(int status) {
+  switch (status) {
+    case SLIM_OK: return "SLIM_OK";
+    case SLIM_EINVAL: return "SLIM_EINVAL: null pointer or argument out of range";
+    case SLIM_ESHAPE: return "SLIM_ESHAPE: size breaks a divisibility or range rule";
+    case SLIM_EDTYPE: return "SLIM_EDTYPE: unsupported dtype";
+    case SLIM_EALIGN: return "SLIM_EALIGN: device array not 16-byte aligned";
+    case SLIM_ENONFINITE: return "SLIM_ENONFINITE: weight holds NaN or Inf";
+    case SLIM_ERANGE: return "SLIM_ERANGE: group scale overflows fp16";
+    case SLIM_EWORKSPACE: return "SLIM_EWORKSPACE: workspace missing or too small";
+    case SLIM_EDEVICE: return "SLIM_EDEVICE: HIP runtime or launch failure";
+    case SLIM_EUNSUPPORTED: return "SLIM_EUNSUPPORTED: not supported by this build";
+    default: return "unknown slim status";
+  }
+}
+
+extern "C" int slim_abi_version(void) { return SLIM_ABI_VERSION; }
+
+int slim_check_pack(const float* W, int64_t N, int64_t K, const void* codes, const void* meta,
+                    const void* scales, const void* mask) {
+  if (!W || !codes || !meta || !scales) return SLIM_EINVAL;
+  if (N < 1 || K < 128 || N >= kMaxDim || K >= kMaxDim) return SLIM_ESHAPE;
+  if (K % 128) return SLIM_ESHAPE;
+  if (!slim_aligned16(W) || !slim_aligned16(codes) || !slim_aligned16(meta) || !slim_aligned16(scales) ||
+      (mask && !slim_aligned16(mask)))
+    return SLIM_EALIGN;
+  return SLIM_OK;
+}
+
+int slim_check_pack_bwd(const void* codes, const void* meta, const void* scales, int64_t N, int64_t K,
+                        const void* codesT, const void* metaT, const void* scalesT, const void* mask_rc) {
+  if (!codes || !meta || !scales || !codesT || !metaT || !scalesT) return SLIM_EINVAL;
+  if (N < 16 || K < 128 || N >= kMaxDim || K >= kMaxDim) return SLIM_ESHAPE;
+  if (N % 16 || K % 128) return SLIM_ESHAPE;
+  if (!slim_aligned16(codes) || !slim_aligned16(meta) || !slim_aligned16(scales) || !slim_aligned16(codesT) ||
+      !slim_aligned16(metaT) || !slim_aligned16(scalesT) || (mask_rc && !slim_aligned16(mask_rc)))
+    return SLIM_EALIGN;
+  return SLIM_OK;
+}
+
+int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPlan* p) {
+  if (M < 1 || N < 16 || K < 128 || M >= kMaxDim || N >= kMaxDim || K >= kMaxDim) return SLIM_ESHAPE;
+  if (N % 16 || K % 128 || r < 0 || r % 16 || r >= kMaxDim) return SLIM_ESHAPE;
+  if (bwd && N % 128) return SLIM_ESHAPE;
+  const int64_t rows = bwd ? K : N, red = bwd ? N : K;
+  SlimPlan q;
+  // adapter GEMM: 64 x 64 output tiles of [M x r], split along the reduction until ~256 blocks
+  if (r > 0) {
+    q.ad_tiles_m = (int)cdiv(M, 64);
+    q.ad_tiles_j = (int)cdiv(r, 64);
+    const int64_t tiles = (int64_t)q.ad_tiles_m * q.ad_tiles_j;
+    int64_t split = std::max<int64_t>(1, std::min<int64_t>(256 / tiles, red / 256));
+    int64_t slice = cdiv(cdiv(red, split), 64) * 64;
+    q.ad_split = (int)cdiv(red, slice);
+    q.ad_slice = slice;
+  }
+  // sparse contraction
+  const int64_t nchunks = red / 128;
+  if (M <= 64) {
+    q.decode = true;
+    q.dec_fm = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+    q.sp_rows_tile = 64;
+    q.sp_cols_tile = 16 * q.dec_fm;
+    q.sp_row_tiles = cdiv(rows, 64);
+    q.sp_col_tiles = 1;
+    // staged activations [16*fm x (cps*128 + 8)] fp16 must fit in 56 KB of LDS (64 KB with the
+    // kernel's static LDS)
+    const int64_t max_cps = std::max<int64_t>(1, (57344 / (32 * q.dec_fm) - 8) / 128);
+    int64_t want = std::max<int64_t>(1, 512 / q.sp_row_tiles);           // ~512 blocks in flight
+    int64_t cps = std::min<int64_t>(max_cps, std::max<int64_t>(1, cdiv(nchunks, want)));
+    q.sp_chunks_per_split = cps;
+    q.sp_split = (int)cdiv(nchunks, cps);
+    if (q.sp_split > 1 && q.sp_row_tiles > kCounterSlots / 2) {   // too many tiles to count: no split
+      q.sp_chunks_per_split = nchunks;
+      q.sp_split = 1;
+    }
+    q.lds_bytes = (size_t)(16 * q.dec_fm) * (size_t)(cps * 128 + 8) * 2;
+  } else {
+    q.decode = false;
+    q.sp_rows_tile = bwd ? 128 : 256;
+    q.sp_cols_tile = 128;
+    q.sp_row_tiles = cdiv(rows, q.sp_rows_tile);
+    q.sp_col_tiles = cdiv(M, q.sp_cols_tile);
+    q.sp_split = 1;
+    q.sp_chunks_per_split = nchunks;
+    q.lds_bytes = 2 * (size_t)q.sp_cols_tile * (128 + 8) * 2;
+  }
+  // workspace: [counters][T or U: M x r fp32][adapter partials][sparse partials]
+  const size_t ad_counters = r > 0 && q.ad_split > 1 ? (size_t)q.ad_tiles_m * q.ad_tiles_j : 0;
+  const size_t sp_counters = q.sp_split > 1 ? (size_t)(q.sp_row_tiles * q.sp_col_tiles) : 0;
+  q.n_counters = ad_counters + sp_counters;
+  q.sp_counter_base = ad_counters;
+  q.off_counters = 0;
+  if (q.n_counters > kCounterSlots) return SLIM_EUNSUPPORTED;
+  // the counter region has a fixed size so that it stays at zero across calls with other sizes
+  size_t off = kCounterSlots * 4;
+  q.off_t = off;
+  off = round256(off + (size_t)M * (size_t)r * 4);
+  q.off_tpart = off;
+  if (r > 0 && q.ad_split > 1) off = round256(off + (size_t)q.ad_split * q.ad_tiles_m * q.ad_tiles_j * 64 * 64 * 4);
+  q.off_ypart = off;
+  if (q.sp_split > 1)
+    off = round256(off + (size_t)q.sp_split * (size_t)(q.sp_row_tiles * q.sp_col_tiles) * q.sp_rows_tile *
+                             q.sp_cols_tile * 4);
+  q.total = off;
+  *p = q;
+  return SLIM_OK;
+}
+
+int slim_check_linear(bool bwd, const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const void* codes,
+                      const void* meta, const void* scales, const void* L, const void* R, int64_t r, const void* Y,
+                      const void* ws, size_t ws_bytes, SlimPlan* plan) {
+  if (!X || !codes || !meta || !scales || !Y) return SLIM_EINVAL;
+  if (r < 0) return SLIM_EINVAL;
+  if (r == 0 ? (L != nullptr || R != nullptr) : (!L || !R)) return SLIM_EINVAL;
+  if (xdtype != SLIM_F16 && xdtype != SLIM_BF16) return SLIM_EDTYPE;
+  int st = slim_make_plan(bwd, M, N, K, r, plan);
+  if (st != SLIM_OK) return st;
+  if (!slim_aligned16(X) || !slim_aligned16(codes) || !slim_aligned16(meta) || !slim_aligned16(scales) ||
+      !slim_aligned16(Y) || (L && !slim_aligned16(L)) || (R && !slim_aligned16(R)))
+    return SLIM_EALIGN;
+  if (!ws || ws_bytes < plan->total) return SLIM_EWORKSPACE;
+  if (!slim_aligned16(ws)) return SLIM_EALIGN;
+  return SLIM_OK;
+}
+
+extern "C" int slim_linear_workspace(int64_t M, int64_t N, int64_t K, int64_t r, size_t* bytes) {
+  if (!bytes) return SLIM_EINVAL;
+  SlimPlan p;
+  int st = slim_make_plan(false, M, N, K, r, &p);
+  if (st == SLIM_OK) *bytes = p.total;
+  return st;
+}
+
+extern "C" int slim_bwd_dx_workspace(int64_t M, int64_t N, int64_t K, int64_t r, size_t* bytes) {
+  if (!bytes) return SLIM_EINVAL;
+  SlimPlan p;
+  int st = slim_make_plan(true, M, N, K, r, &p);
+  if (st == SLIM_OK) *bytes = p.total;
+  return st;
+}

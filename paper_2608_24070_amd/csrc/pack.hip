@@ -1,0 +1,233 @@
+// pack.hip - one-time packing kernels: forward 2:4 + int4 group-128 pack, and the SLoPe
+// double-pruned backward pack (2:4 along N of the packed forward weight).
+#include "slim_device.h"
+#include "slim_host.h"
+
+namespace {
+
+constexpr int kPackThreads = 256;
+
+// One thread per aligned 4-group of one row; the 32 threads of a half-wave cover one
+// 128-wide quantisation group (rows hold K/4 groups and K % 128 == 0, so groups never
+// straddle half-waves).
+__global__ void __launch_bounds__(kPackThreads)
+k_pack(const float4* __restrict__ W, int64_t total4, int64_t K, uint32_t* __restrict__ codes,
+       uint16_t* __restrict__ meta, uint16_t* __restrict__ scales, uint32_t* __restrict__ mask,
+       int* __restrict__ status) {
+  const int64_t t = (int64_t)blockIdx.x * kPackThreads + threadIdx.x;
+  const bool valid = t < total4;
+  float4 v = valid ? W[t] : make_float4(0.f, 0.f, 0.f, 0.f);
+  const float w[4] = {v.x, v.y, v.z, v.w};
+  float a[4];
+  int bad = 0;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    a[p] = fabsf(w[p]);
+    if (!__builtin_isfinite(w[p])) bad = 1;
+  }
+  // group absmax over the 32 lanes of this half-wave
+  float gmax = fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3]));
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) gmax = fmaxf(gmax, __shfl_xor(gmax, off, 32));
+  // s16 = fp16_RNE(fp32 absmax / 7), IEEE division
+  const float s32 = __fdiv_rn(gmax, 7.0f);
+  const _Float16 s16 = (_Float16)s32;
+  const uint16_t s16bits = __builtin_bit_cast(uint16_t, s16);
+  if (!__builtin_isfinite((float)s16)) bad |= 2;
+  if (valid && bad) atomicOr(status, bad);
+
+  // top-2 of the four by (|w| desc, position asc)
+  int keep[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    int rank = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q != p && (a[q] > a[p] || (a[q] == a[p] && q < p))) ++rank;
+    keep[p] = rank < 2;
+  }
+  int i0 = -1, i1 = -1;
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+    if (keep[p]) {
+      if (i0 < 0) i0 = p;
+      else i1 = p;
+    }
+  const double sd = (double)s16;
+  auto code = [&](float x) -> uint32_t {
+    if (!(sd > 0.0)) return 8u;
+    double q = rint((double)x / sd);
+    q = fmin(7.0, fmax(-7.0, q));
+    return (uint32_t)((int)q + 8);
+  };
+  const uint32_t u0 = code(w[i0]);
+  const uint32_t u1 = code(w[i1]);
+  const int64_t j = t % (K / 4);          // group index inside the row
+  const int c = (int)(t & 3);             // group slot inside its 16-position block
+  uint32_t cw = (u0 << (4 * c)) | (u1 << (16 + 4 * c));
+  uint32_t mw = (uint32_t)(i0 | (i1 << 2)) << (4 * c);
+  cw |= __shfl_xor(cw, 1, 64);
+  mw |= __shfl_xor(mw, 1, 64);
+  cw |= __shfl_xor(cw, 2, 64);
+  mw |= __shfl_xor(mw, 2, 64);
+  if (!valid) return;
+  const int64_t row = t / (K / 4);
+  if (c == 0) {
+    codes[t >> 2] = cw;
+    meta[t >> 2] = (uint16_t)mw;
+  }
+  if ((j & 31) == 0) scales[row * (K / 128) + (j >> 5)] = s16bits;
+  if (mask) mask[t] = (uint32_t)keep[0] | ((uint32_t)keep[1] << 8) | ((uint32_t)keep[2] << 16) |
+                      ((uint32_t)keep[3] << 24);
+}
+
+// Backward pack. Block = 256 threads, tile = 64 rows (n) x 64 columns (k).
+// Phase 1 decodes the forward pack of the tile into LDS; phase 2 gives each thread one
+// column k and one 16-row block, prunes each aligned 4-row group to its top two
+// (|Wc| desc, forward-kept desc, row asc) and emits one codesT word and one metaT half-word.
+constexpr int kBT = 64;
+
+__global__ void __launch_bounds__(256)
+k_pack_bwd(const uint32_t* __restrict__ codes, const uint16_t* __restrict__ meta,
+           const uint16_t* __restrict__ scales, int64_t N, int64_t K, uint32_t* __restrict__ codesT,
+           uint16_t* __restrict__ metaT, uint16_t* __restrict__ scalesT, uint8_t* __restrict__ mask_rc) {
+  __shared__ uint8_t u_s[kBT][kBT + 4];     // forward code per (row, col), 8 where pruned
+  __shared__ uint8_t f_s[kBT][kBT + 4];     // forward-kept bit, later the W^{R,C} support bit
+  __shared__ float sc_s[kBT];               // scale of each row for this column tile
+  const int tid = threadIdx.x;
+  const int64_t k0 = (int64_t)blockIdx.x * kBT;
+  const int64_t n0 = (int64_t)blockIdx.y * kBT;
+  const int rows = (int)min((int64_t)kBT, N - n0);   // multiple of 16 (N % 16 == 0)
+
+  // phase 1: thread -> (row = tid / 4, 16-column block w = tid % 4)
+  {
+    const int row = tid >> 2, w = tid & 3;
+    if (row < rows) {
+      const int64_t n = n0 + row;
+      const uint32_t cw = codes[n * (K / 16) + (k0 >> 4) + w];
+      const uint32_t mw = meta[n * (K / 16) + (k0 >> 4) + w];
+#pragma unroll
+      for (int p = 0; p < 16; ++p) {
+        u_s[row][16 * w + p] = 8;
+        f_s[row][16 * w + p] = 0;
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int i0 = (mw >> (4 * c)) & 3, i1 = (mw >> (4 * c + 2)) & 3;
+        u_s[row][16 * w + 4 * c + i0] = (cw >> (4 * c)) & 0xF;
+        u_s[row][16 * w + 4 * c + i1] = (cw >> (16 + 4 * c)) & 0xF;
+        f_s[row][16 * w + 4 * c + i0] = 1;
+        f_s[row][16 * w + 4 * c + i1] = 1;
+      }
+      if (w == 0) sc_s[row] = h_bits_to_f(scales[n * (K / 128) + (k0 >> 7)]);
+    }
+  }
+  __syncthreads();
+
+  // phase 2: thread -> (column col = tid / 4, 16-row block rb = tid % 4)
+  uint32_t sel16 = 0;
+  const int col = tid >> 2, rb = tid & 3;
+  if (16 * rb < rows) {
+    uint32_t cw = 0, mw = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      float av[4];
+      int fv[4];
+      uint32_t uv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 16 * rb + 4 * c + i;
+        uv[i] = u_s[row][col];
+        fv[i] = f_s[row][col];
+        av[i] = fabsf((float)((int)uv[i] - 8) * sc_s[row]);   // exact: 3-bit x 11-bit significand
+      }
+      int keep[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        int rank = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (q == p) continue;
+          const bool better = av[q] > av[p] || (av[q] == av[p] && (fv[q] > fv[p] || (fv[q] == fv[p] && q < p)));
+          if (better) ++rank;
+        }
+        keep[p] = rank < 2;
+      }
+      int i0 = -1, i1 = -1;
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+        if (keep[p]) {
+          if (i0 < 0) i0 = p;
+          else i1 = p;
+        }
+      cw |= (uv[i0] << (4 * c)) | (uv[i1] << (16 + 4 * c));
+      mw |= (uint32_t)(i0 | (i1 << 2)) << (4 * c);
+      sel16 |= (uint32_t)((keep[0] & fv[0]) | ((keep[1] & fv[1]) << 1) | ((keep[2] & fv[2]) << 2) |
+                          ((keep[3] & fv[3]) << 3)) << (4 * c);
+    }
+    const int64_t k = k0 + col;
+    codesT[k * (N / 16) + (n0 >> 4) + rb] = cw;
+    metaT[k * (N / 16) + (n0 >> 4) + rb] = (uint16_t)mw;
+  }
+  if (mask_rc) {
+    __syncthreads();
+    if (16 * rb < rows) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) f_s[16 * rb + i][col] = (sel16 >> i) & 1;
+    }
+    __syncthreads();
+    // write rows of the tile: thread -> (row = tid / 4, 16 bytes at column 16 * (tid % 4))
+    const int row = tid >> 2, w = tid & 3;
+    if (row < rows) {
+      uint32_t v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        v[q] = (uint32_t)f_s[row][16 * w + 4 * q] | ((uint32_t)f_s[row][16 * w + 4 * q + 1] << 8) |
+               ((uint32_t)f_s[row][16 * w + 4 * q + 2] << 16) | ((uint32_t)f_s[row][16 * w + 4 * q + 3] << 24);
+      uint4* dst = reinterpret_cast<uint4*>(mask_rc + (n0 + row) * K + k0 + 16 * w);
+      *dst = make_uint4(v[0], v[1], v[2], v[3]);
+    }
+  }
+  // scalesT: the first column tile of each 128-group copies the tile's row scales
+  if ((k0 & 127) == 0 && tid < rows) scalesT[(k0 >> 7) * N + n0 + tid] = scales[(n0 + tid) * (K / 128) + (k0 >> 7)];
+}
+
+}  // namespace
+
+extern "C" int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, uint8_t* meta,
+                         uint16_t* scales, uint8_t* mask, void* stream) {
+  int st = slim_check_pack(W, N, K, codes, meta, scales, mask);
+  if (st != SLIM_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  int* d_status = nullptr;
+  if (hipMalloc(&d_status, sizeof(int)) != hipSuccess) return SLIM_EDEVICE;
+  int h_status = 0;
+  int rc = SLIM_OK;
+  const int64_t total4 = N * (K / 4);
+  const int64_t blocks = (total4 + kPackThreads - 1) / kPackThreads;
+  do {
+    if (hipMemsetAsync(d_status, 0, sizeof(int), s) != hipSuccess) { rc = SLIM_EDEVICE; break; }
+    hipLaunchKernelGGL(k_pack, dim3((unsigned)blocks), dim3(kPackThreads), 0, s,
+                       reinterpret_cast<const float4*>(W), total4, K, reinterpret_cast<uint32_t*>(codes),
+                       reinterpret_cast<uint16_t*>(meta), scales, reinterpret_cast<uint32_t*>(mask), d_status);
+    if (hipGetLastError() != hipSuccess) { rc = SLIM_EDEVICE; break; }
+    if (hipMemcpyAsync(&h_status, d_status, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess) { rc = SLIM_EDEVICE; break; }
+    if (h_status & 1) rc = SLIM_ENONFINITE;
+    else if (h_status & 2) rc = SLIM_ERANGE;
+  } while (0);
+  hipFree(d_status);
+  return rc;
+}
+
+extern "C" int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const uint16_t* scales, int64_t N,
+                             int64_t K, uint8_t* codesT, uint8_t* metaT, uint16_t* scalesT, uint8_t* mask_rc,
+                             void* stream) {
+  int st = slim_check_pack_bwd(codes, meta, scales, N, K, codesT, metaT, scalesT, mask_rc);
+  if (st != SLIM_OK) return st;
+  dim3 grid((unsigned)(K / kBT), (unsigned)((N + kBT - 1) / kBT));
+  hipLaunchKernelGGL(k_pack_bwd, grid, dim3(256), 0, (hipStream_t)stream,
+                     reinterpret_cast<const uint32_t*>(codes), reinterpret_cast<const uint16_t*>(meta), scales, N,
+                     K, reinterpret_cast<uint32_t*>(codesT), reinterpret_cast<uint16_t*>(metaT), scalesT, mask_rc);
+  return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
+}

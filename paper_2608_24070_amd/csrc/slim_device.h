@@ -1,0 +1,130 @@
+// slim_device.h - device-side helpers shared by the libslim kernels (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 h16_t __attribute__((ext_vector_type(16)));
+typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef float f16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+#define SLIM_DEV __device__ __forceinline__
+
+SLIM_DEV uint32_t bits_of(h2_t x) { return __builtin_bit_cast(uint32_t, x); }
+SLIM_DEV h2_t h2_of(uint32_t x) { return __builtin_bit_cast(h2_t, x); }
+
+// Two fp16 copies of one fp16 bit pattern.
+SLIM_DEV h2_t splat_h2(uint32_t hbits) { return h2_of((hbits & 0xFFFFu) | (hbits << 16)); }
+
+// One packed code word (16 K positions, four 2:4 groups) -> the eight kept values as the
+// compressed A operand of a sparse MFMA: dword c = (first kept, second kept) of group c.
+// Nibbles are turned into exact fp16 integers with the 1024-magic: (0x6400 | u) is 1024 + u,
+// (0x6400 | 16u) is 1024 + 16u; both become u - 8 exactly. The scale multiply is the only
+// rounding step: (u - 8) * s16 rounded to fp16.
+SLIM_DEV h8_t dequant_word(uint32_t w, h2_t s2) {
+  const h2_t m1032 = {(_Float16)-1032.0f, (_Float16)-1032.0f};
+  const h2_t r16 = {(_Float16)0.0625f, (_Float16)0.0625f};
+  const h2_t m72 = {(_Float16)-72.0f, (_Float16)-72.0f};
+  const uint32_t w8 = w >> 8;
+  h2_t g0 = h2_of((w & 0x000F000Fu) | 0x64006400u) + m1032;
+  h2_t g1 = h2_of((w & 0x00F000F0u) | 0x64006400u) * r16 + m72;
+  h2_t g2 = h2_of((w8 & 0x000F000Fu) | 0x64006400u) + m1032;
+  h2_t g3 = h2_of((w8 & 0x00F000F0u) | 0x64006400u) * r16 + m72;
+  g0 = g0 * s2;
+  g1 = g1 * s2;
+  g2 = g2 * s2;
+  g3 = g3 * s2;
+  h8_t a;
+  a[0] = g0[0]; a[1] = g0[1]; a[2] = g1[0]; a[3] = g1[1];
+  a[4] = g2[0]; a[5] = g2[1]; a[6] = g3[0]; a[7] = g3[1];
+  return a;
+}
+
+// Same without the scale: exact integers q = u - 8.
+SLIM_DEV h8_t dequant_word_int(uint32_t w) {
+  const h2_t m1032 = {(_Float16)-1032.0f, (_Float16)-1032.0f};
+  const h2_t r16 = {(_Float16)0.0625f, (_Float16)0.0625f};
+  const h2_t m72 = {(_Float16)-72.0f, (_Float16)-72.0f};
+  const uint32_t w8 = w >> 8;
+  h2_t g0 = h2_of((w & 0x000F000Fu) | 0x64006400u) + m1032;
+  h2_t g1 = h2_of((w & 0x00F000F0u) | 0x64006400u) * r16 + m72;
+  h2_t g2 = h2_of((w8 & 0x000F000Fu) | 0x64006400u) + m1032;
+  h2_t g3 = h2_of((w8 & 0x00F000F0u) | 0x64006400u) * r16 + m72;
+  h8_t a;
+  a[0] = g0[0]; a[1] = g0[1]; a[2] = g1[0]; a[3] = g1[1];
+  a[4] = g2[0]; a[5] = g2[1]; a[6] = g3[0]; a[7] = g3[1];
+  return a;
+}
+
+// bf16 bits -> fp16 (through fp32; exact for |x| in [2^-14, 65504]).
+SLIM_DEV _Float16 bf16_to_h(uint32_t b) { return (_Float16)__builtin_bit_cast(float, b << 16); }
+
+// Eight 16-bit activations (bf16 or fp16 bits in a uint4) -> h8, optionally times an fp32 factor.
+SLIM_DEV h8_t load8_as_h(u32x4_t v, bool is_bf16) {
+  h8_t r;
+  if (is_bf16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r[2 * i] = (_Float16)__builtin_bit_cast(float, v[i] << 16);
+      r[2 * i + 1] = (_Float16)__builtin_bit_cast(float, v[i] & 0xFFFF0000u);
+    }
+  } else {
+    r = __builtin_bit_cast(h8_t, v);
+  }
+  return r;
+}
+
+SLIM_DEV float h_bits_to_f(uint32_t hb) { return (float)__builtin_bit_cast(_Float16, (uint16_t)hb); }
+
+SLIM_DEV float act_to_f(uint32_t b16, bool is_bf16) {
+  return is_bf16 ? __builtin_bit_cast(float, b16 << 16) : h_bits_to_f(b16);
+}
+
+// ----------------------------------------------------------------------------------------------
+// Sparse MFMA operand mapping on gfx950 (measured with one-hot probes of
+// v_smfmac_f32_{16x16x64,32x32x32}_f16). NC = 16 or 32 output rows; G = 64 / NC lane groups.
+//   A (compressed, 8 x fp16 per lane): lane (row lane % NC, group g = lane / NC) covers 16
+//     consecutive dense reduction positions. Slot c is at position 4*(c/2) + idx_c, where
+//     idx_c is bits [2c+1:2c] of the index VGPR with ABID 0, or bits [2c+17:2c+16] with ABID 1.
+//   B (dense, 16 x fp16 per lane): lane (column lane % NC, group g). Element e pairs with A lane
+//     group (g >> 1) + (e >> 3) * (G / 2), at position 8*(g & 1) + (e & 7) of that group's block.
+//   C/D: the standard MFMA output layouts.
+// One "chunk" is one 128-position quantisation group. Inside a chunk, A lane group g takes the
+// 16-blocks {S*g + s} for steps s = 0..S-1 (S = 2 for 16x16x64, 4 for 32x32x32), so its code
+// words and index half-words for the whole chunk are contiguous. B lane (g) then reads two runs of
+// eight activations at chunk offsets c0 and c0 + 64, with c0 from b_chunk_offset.
+// ----------------------------------------------------------------------------------------------
+template <int NC>
+SLIM_DEV int b_chunk_offset(int lane, int step) {
+  if (NC == 16) {
+    const int qb = lane >> 4;                       // 0..3
+    return 32 * (qb >> 1) + 16 * step + 8 * (qb & 1);
+  } else {
+    const int hb = lane >> 5;                       // 0..1
+    return 16 * step + 8 * hb;
+  }
+}
+
+SLIM_DEV f4_t smfmac16(h8_t a, h16_t b, f4_t c, int idx, int abid) {
+  if (abid == 0) return __builtin_amdgcn_smfmac_f32_16x16x64_f16(a, b, c, idx, 0, 0);
+  return __builtin_amdgcn_smfmac_f32_16x16x64_f16(a, b, c, idx, 0, 1);
+}
+
+SLIM_DEV f16_t smfmac32(h8_t a, h16_t b, f16_t c, int idx, int abid) {
+  if (abid == 0) return __builtin_amdgcn_smfmac_f32_32x32x32_f16(a, b, c, idx, 0, 0);
+  return __builtin_amdgcn_smfmac_f32_32x32x32_f16(a, b, c, idx, 0, 1);
+}
+
+SLIM_DEV h16_t cat16(h8_t lo, h8_t hi) {
+  h16_t r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    r[i] = lo[i];
+    r[8 + i] = hi[i];
+  }
+  return r;
+}

@@ -1,0 +1,43 @@
+// slim_host.h - host-side argument checks and launch planning for libslim (no device code).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/slim.h"
+
+// Completion counters live in a fixed-size region at the start of the workspace.
+#define SLIM_COUNTER_SLOTS 4096
+
+// Argument checks: pure host functions, run before anything is enqueued.
+int slim_check_pack(const float* W, int64_t N, int64_t K, const void* codes, const void* meta,
+                    const void* scales, const void* mask);
+int slim_check_pack_bwd(const void* codes, const void* meta, const void* scales, int64_t N, int64_t K,
+                        const void* codesT, const void* metaT, const void* scalesT, const void* mask_rc);
+
+// Which kernels one call runs and how its workspace is carved up.
+struct SlimPlan {
+  // dense adapter GEMM (T = X L forward, U = dY R^T backward)
+  int ad_tiles_m = 0, ad_tiles_j = 0, ad_split = 1;
+  int64_t ad_slice = 0;               // reduction length per split (multiple of 64)
+  // sparse contraction
+  bool decode = false;                // small-M kernel (16-column MFMA tiles, split reduction)
+  int dec_fm = 1;                     // 16-column fragments per wave in the small-M kernel
+  int sp_rows_tile = 0, sp_cols_tile = 0;  // output tile (rows of W or W^T, columns = M)
+  int64_t sp_row_tiles = 0, sp_col_tiles = 0;
+  int sp_split = 1;                   // reduction splits (small-M kernel only)
+  int64_t sp_chunks_per_split = 0;    // 128-wide chunks per split
+  size_t lds_bytes = 0;               // dynamic LDS of the sparse kernel
+  // workspace layout (byte offsets)
+  size_t off_counters = 0, n_counters = 0, sp_counter_base = 0;
+  size_t off_t = 0, off_tpart = 0, off_ypart = 0, total = 0;
+};
+
+// Forward (bwd == false: rows = N, red = K) or backward (bwd == true: rows = K, red = N) plan.
+int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPlan* plan);
+
+int slim_check_linear(bool bwd, const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const void* codes,
+                      const void* meta, const void* scales, const void* L, const void* R, int64_t r, const void* Y,
+                      const void* ws, size_t ws_bytes, SlimPlan* plan);
+
+inline bool slim_aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }

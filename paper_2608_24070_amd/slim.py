@@ -1,0 +1,245 @@
+"""ctypes binding of libslim (``include/slim.h``): argument marshalling only.
+
+Every computation runs in the HIP kernels of ``libslim.so``; this module only turns torch
+tensors into device pointers, sizes and the current HIP stream. There is no fallback: if the
+library is missing, loading it raises.
+
+Low-level functions carry the C names (``slim_pack``, ``slim_pack_bwd``, ``slim_linear``,
+``slim_linear_bwd_dx``, ...) and take raw integers. The tensor-level helpers ``pack``,
+``pack_bwd``, ``linear`` and ``bwd_dx`` allocate outputs and a cached workspace with torch.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libslim.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "slim.h")
+
+SLIM_OK = 0
+SLIM_F16, SLIM_BF16 = 0, 1
+
+_c_i64 = ctypes.c_int64
+_c_p = ctypes.c_void_p
+_SIGS = {
+    "slim_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "slim_abi_version": (ctypes.c_int, []),
+    "slim_pack": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "slim_pack_bwd": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "slim_linear_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "slim_bwd_dx_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "slim_workspace_init": (ctypes.c_int, [_c_p, ctypes.c_size_t, _c_p]),
+    "slim_linear": (ctypes.c_int, [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i64,
+                                   _c_p, _c_p, ctypes.c_size_t, _c_p]),
+    "slim_linear_bwd_dx": (ctypes.c_int, [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p,
+                                          _c_i64, _c_p, _c_p, ctypes.c_size_t, _c_p]),
+}
+
+_lib = None
+
+
+class SlimError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)}")
+
+
+def lib():
+    """The loaded libslim.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing; build it with `python -m paper_2608_24070_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def header_symbols() -> list[str]:
+    """Entry points declared in include/slim.h."""
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(slim_\w+)\s*\(", text, flags=re.M)))
+
+
+def status_string(status: int) -> str:
+    return lib().slim_status_string(status).decode()
+
+
+def _check(status: int, where: str):
+    if status != SLIM_OK:
+        raise SlimError(status, where)
+
+
+# ------------------------------------------------------------------ raw C entry points
+
+def slim_abi_version() -> int:
+    return lib().slim_abi_version()
+
+
+def slim_status_string(status: int) -> str:
+    return status_string(status)
+
+
+def slim_pack(W, N, K, codes, meta, scales, mask, stream) -> int:
+    return lib().slim_pack(W, N, K, codes, meta, scales, mask, stream)
+
+
+def slim_pack_bwd(codes, meta, scales, N, K, codesT, metaT, scalesT, mask_rc, stream) -> int:
+    return lib().slim_pack_bwd(codes, meta, scales, N, K, codesT, metaT, scalesT, mask_rc, stream)
+
+
+def slim_linear_workspace(M, N, K, r) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().slim_linear_workspace(M, N, K, r, ctypes.byref(out)), "slim_linear_workspace")
+    return out.value
+
+
+def slim_bwd_dx_workspace(M, N, K, r) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().slim_bwd_dx_workspace(M, N, K, r, ctypes.byref(out)), "slim_bwd_dx_workspace")
+    return out.value
+
+
+def slim_workspace_init(ws, nbytes, stream) -> int:
+    return lib().slim_workspace_init(ws, nbytes, stream)
+
+
+def slim_linear(X, xdtype, M, N, K, codes, meta, scales, L, R, r, Y, ws, ws_bytes, stream) -> int:
+    return lib().slim_linear(X, xdtype, M, N, K, codes, meta, scales, L, R, r, Y, ws, ws_bytes, stream)
+
+
+def slim_linear_bwd_dx(dY, dydtype, M, N, K, codesT, metaT, scalesT, L, R, r, dX, ws, ws_bytes, stream) -> int:
+    return lib().slim_linear_bwd_dx(dY, dydtype, M, N, K, codesT, metaT, scalesT, L, R, r, dX, ws, ws_bytes, stream)
+
+
+# ------------------------------------------------------------------ tensor helpers
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return SLIM_BF16
+    if t.dtype == torch.float16:
+        return SLIM_F16
+    raise TypeError(f"activations must be bf16 or fp16, got {t.dtype}")
+
+
+def _on_gpu(*ts):
+    for t in ts:
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise ValueError("tensors must be contiguous and on the GPU")
+
+
+_ws_cache: dict = {}
+
+
+def workspace(nbytes: int, device=None, stream=None):
+    """A zero-initialised workspace of at least nbytes, cached per (device, stream)."""
+    torch = _torch()
+    dev = torch.device(device if device is not None else "cuda")
+    key = (dev, _stream(stream))
+    ws = _ws_cache.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.zeros(max(nbytes, 1 << 16), dtype=torch.uint8, device=dev)
+        _ws_cache[key] = ws
+    return ws
+
+
+def pack(W, with_mask: bool = False, stream=None) -> dict:
+    """slim_pack of an fp32 [N, K] weight. Returns codes, meta, scales (and mask)."""
+    torch = _torch()
+    _on_gpu(W)
+    if W.dtype != torch.float32:
+        raise TypeError("W must be fp32")
+    N, K = W.shape
+    dev = W.device
+    out = {
+        "codes": torch.empty((N, K // 4), dtype=torch.uint8, device=dev),
+        "meta": torch.empty((N, K // 8), dtype=torch.uint8, device=dev),
+        "scales": torch.empty((N, K // 128), dtype=torch.int16, device=dev),
+        "N": N, "K": K,
+    }
+    mask = torch.empty((N, K), dtype=torch.uint8, device=dev) if with_mask else None
+    st = slim_pack(_ptr(W), N, K, _ptr(out["codes"]), _ptr(out["meta"]), _ptr(out["scales"]), _ptr(mask),
+                   _stream(stream))
+    _check(st, "slim_pack")
+    if with_mask:
+        out["mask"] = mask
+    return out
+
+
+def pack_bwd(packed: dict, with_mask: bool = False, stream=None) -> dict:
+    """slim_pack_bwd of a forward pack. Returns codesT, metaT, scalesT (and mask_rc)."""
+    torch = _torch()
+    N, K = packed["N"], packed["K"]
+    dev = packed["codes"].device
+    out = {
+        "codesT": torch.empty((K, N // 4), dtype=torch.uint8, device=dev),
+        "metaT": torch.empty((K, N // 8), dtype=torch.uint8, device=dev),
+        "scalesT": torch.empty((K // 128, N), dtype=torch.int16, device=dev),
+        "N": N, "K": K,
+    }
+    mask = torch.empty((N, K), dtype=torch.uint8, device=dev) if with_mask else None
+    st = slim_pack_bwd(_ptr(packed["codes"]), _ptr(packed["meta"]), _ptr(packed["scales"]), N, K,
+                       _ptr(out["codesT"]), _ptr(out["metaT"]), _ptr(out["scalesT"]), _ptr(mask), _stream(stream))
+    _check(st, "slim_pack_bwd")
+    if with_mask:
+        out["mask_rc"] = mask
+    return out
+
+
+def linear(X, packed: dict, L=None, R=None, out=None, ws=None, stream=None):
+    """Y = X Wc^T + (X L) R through slim_linear. X bf16/fp16 [M, K]; L, R fp16; Y fp32 [M, N]."""
+    torch = _torch()
+    _on_gpu(X, L, R, out)
+    M, K = X.shape
+    N = packed["N"]
+    r = 0 if L is None else L.shape[1]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=X.device)
+    need = slim_linear_workspace(M, N, K, r)
+    if ws is None:
+        ws = workspace(need, X.device, stream)
+    st = slim_linear(_ptr(X), _dtype_code(X), M, N, K, _ptr(packed["codes"]), _ptr(packed["meta"]),
+                     _ptr(packed["scales"]), _ptr(L), _ptr(R), r, _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "slim_linear")
+    return out
+
+
+def bwd_dx(dY, packed_bwd: dict, L=None, R=None, out=None, ws=None, stream=None):
+    """dX = dY W^{R,C} + (dY R^T) L^T through slim_linear_bwd_dx. dX fp32 [M, K]."""
+    torch = _torch()
+    _on_gpu(dY, L, R, out)
+    M, N = dY.shape
+    K = packed_bwd["K"]
+    r = 0 if L is None else L.shape[1]
+    if out is None:
+        out = torch.empty((M, K), dtype=torch.float32, device=dY.device)
+    need = slim_bwd_dx_workspace(M, N, K, r)
+    if ws is None:
+        ws = workspace(need, dY.device, stream)
+    st = slim_linear_bwd_dx(_ptr(dY), _dtype_code(dY), M, N, K, _ptr(packed_bwd["codesT"]),
+                            _ptr(packed_bwd["metaT"]), _ptr(packed_bwd["scalesT"]), _ptr(L), _ptr(R), r,
+                            _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "slim_linear_bwd_dx")
+    return out

@@ -1,0 +1,86 @@
+"""libslim loads, exports every entry point of include/slim.h, and rejects bad arguments on the
+host before touching a GPU (no compute call here needs a device)."""
+import ctypes
+
+import pytest
+
+from paper_2608_24070_amd import slim
+
+A = 1 << 20          # a fake, 16-byte aligned, non-null "device" address (never dereferenced)
+MIS = A + 4          # misaligned
+
+
+def test_library_exports_every_declared_symbol():
+    lib = slim.lib()
+    syms = slim.header_symbols()
+    assert {"slim_pack", "slim_pack_bwd", "slim_linear", "slim_linear_bwd_dx", "slim_linear_workspace",
+            "slim_bwd_dx_workspace", "slim_workspace_init", "slim_status_string", "slim_abi_version"} <= set(syms)
+    for name in syms:
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings():
+    assert slim.slim_abi_version() == 1
+    for code in range(10):
+        assert slim.status_string(code).startswith("SLIM_")
+    assert "unknown" in slim.status_string(99)
+
+
+def test_pack_validation():
+    ok = dict(W=A, N=8, K=128, codes=A, meta=A, scales=A, mask=None, stream=None)
+    def call(**kw):
+        a = dict(ok, **kw)
+        return slim.slim_pack(a["W"], a["N"], a["K"], a["codes"], a["meta"], a["scales"], a["mask"], a["stream"])
+    assert call(W=None) == 1
+    assert call(codes=None) == 1
+    assert call(K=100) == 2
+    assert call(K=64) == 2
+    assert call(N=0) == 2
+    assert call(W=MIS) == 4
+    assert call(mask=MIS) == 4
+
+
+def test_pack_bwd_validation():
+    def call(N=32, K=256, codes=A, codesT=A, mask=None):
+        return slim.slim_pack_bwd(codes, A, A, N, K, codesT, A, A, mask, None)
+    assert call(codes=None) == 1
+    assert call(N=24) == 2          # N % 16
+    assert call(K=200) == 2
+    assert call(codesT=MIS) == 4
+
+
+def test_linear_validation_and_workspace():
+    need = slim.slim_linear_workspace(16, 512, 512, 32)
+    assert need > 0
+    def call(X=A, xdt=1, M=16, N=512, K=512, L=A, R=A, r=32, Y=A, ws=A, wsb=None):
+        return slim.slim_linear(X, xdt, M, N, K, A, A, A, L, R, r, Y, ws, need if wsb is None else wsb, None)
+    assert call(X=None) == 1
+    assert call(L=None) == 1                  # r > 0 needs both factors
+    assert call(r=0) == 1                     # r == 0 needs both NULL
+    assert call(xdt=2) == 3
+    assert call(N=500) == 2
+    assert call(K=500) == 2
+    assert call(r=24) == 2
+    assert call(M=0) == 2
+    assert call(X=MIS) == 4
+    assert call(wsb=need - 1) == 7
+    assert call(ws=None) == 7
+
+
+def test_bwd_workspace_and_shape_rules():
+    assert slim.slim_bwd_dx_workspace(16, 28672, 8192, 512) > 0
+    with pytest.raises(slim.SlimError):
+        slim.slim_bwd_dx_workspace(16, 1040, 512, 0)      # backward needs N % 128
+    def call(N=1024, K=512, r=0):
+        return slim.slim_linear_bwd_dx(A, 1, 4, N, K, A, A, A, None, None, r, A, A, 1 << 30, None)
+    assert call(N=1040) == 2
+
+
+@pytest.mark.parametrize("M,N,K,r", [(1, 4096, 4096, 384), (16, 4096, 4096, 384), (2048, 11008, 4096, 384),
+                                     (8192, 28672, 8192, 512), (4096, 5120, 13824, 512)])
+def test_workspace_sizes_are_modest(M, N, K, r):
+    fwd = slim.slim_linear_workspace(M, N, K, r)
+    bwd = slim.slim_bwd_dx_workspace(M, N, K, r)
+    out_bytes = 4 * M * max(N, K)
+    assert fwd < 64 * 2 ** 20 + out_bytes
+    assert bwd < 64 * 2 ** 20 + out_bytes

@@ -1,0 +1,139 @@
+"""slim_linear and slim_linear_bwd_dx against the fp64 oracle, within the tolerance gate
+(relative Frobenius error <= 2e-3 and max |error| <= 1e-2 * max |Y_ref|)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import slim_oracle as O
+from paper_2608_24070_amd import slim, synth
+from tests.gpu_common import assert_close, dev, dev_bits, host, layer_inputs, oracle_pack_on_device
+
+pytestmark = pytest.mark.gpu
+
+
+def _fwd_case(n, k, r, m, xdtype="bf16", outliers=False, seed=0, rows=None, ms=None, name="layer",
+              use_oracle_pack=False):
+    print(f"fwd n={n} k={k} r={r} m={m} {xdtype} outliers={outliers} seed={seed}", flush=True)
+    W, X, L, R, dx, dL, dR = layer_inputs(n, k, r, m, seed=seed, xdtype=xdtype, outliers=outliers, name=name)
+    if use_oracle_pack:
+        p = oracle_pack_on_device(O.pack(W), n, k)
+    else:
+        p = slim.pack(dev(W))
+    Y = host(slim.linear(dx, p, dL, dR))
+    torch.cuda.synchronize()
+    rows = np.arange(n) if rows is None else rows
+    ms = np.arange(m) if ms is None else ms
+    ref = O.linear(X[ms], O.pack(W[rows]), L, None if R is None else R[:, rows], len(rows), k)
+    return assert_close(Y[np.ix_(ms, rows)], ref, f"fwd n={n} k={k} r={r} m={m}")
+
+
+@pytest.mark.parametrize("m,r,xdtype", [(16, 32, "fp16"), (1, 32, "fp16"), (16, 0, "fp16"), (3, 32, "bf16")])
+def test_tiny(m, r, xdtype):
+    _fwd_case(512, 512, r, m, xdtype=xdtype, name="tiny")
+
+
+@pytest.mark.parametrize("m", [1, 4, 16])
+def test_decode_shape(m):
+    _fwd_case(4096, 4096, 384, m, name="decode")
+
+
+@pytest.mark.parametrize("m", [17, 32, 33, 64])
+def test_small_m_multi_fragment(m):
+    _fwd_case(1024, 2048, 64, m, name="smallm")
+
+
+@pytest.mark.parametrize("m,r", [(65, 32), (200, 16), (256, 0), (300, 48)])
+def test_tile_kernel_ragged(m, r):
+    _fwd_case(768, 1024, r, m, name="ragged")
+
+
+def test_linear_on_oracle_pack():
+    _fwd_case(1024, 1024, 64, 16, use_oracle_pack=True, name="opack")
+    _fwd_case(1024, 1024, 64, 256, use_oracle_pack=True, name="opack")
+
+
+def test_prefill_sampled():
+    rows = np.sort(synth.stream(1, "prows").choice(11008, size=1024, replace=False))
+    ms = np.sort(synth.stream(1, "pms").choice(2048, size=128, replace=False))
+    _fwd_case(11008, 4096, 384, 2048, rows=rows, ms=ms, name="prefill")
+
+
+def test_prefill_fp16_outliers_sampled():
+    rows = np.sort(synth.stream(2, "prows").choice(11008, size=512, replace=False))
+    ms = np.sort(synth.stream(2, "pms").choice(2048, size=64, replace=False))
+    _fwd_case(11008, 4096, 384, 2048, xdtype="fp16", outliers=True, rows=rows, ms=ms, name="prefill")
+
+
+def test_block13b_down_proj_sampled():
+    rows = np.sort(synth.stream(3, "rows").choice(5120, size=512, replace=False))
+    ms = np.sort(synth.stream(3, "ms").choice(4096, size=64, replace=False))
+    _fwd_case(5120, 13824, 512, 4096, rows=rows, ms=ms, name="down")
+
+
+@pytest.mark.parametrize("m", [1, 16, 512, 8192])
+def test_mlp70b_fwd_sampled(m):
+    rows = np.sort(synth.stream(4, "rows").choice(28672, size=512, replace=False))
+    ms = None if m <= 16 else np.sort(synth.stream(4, "ms").choice(m, size=32, replace=False))
+    _fwd_case(28672, 8192, 512, m, rows=rows, ms=ms, name="mlp70b")
+
+
+def test_forward_is_deterministic():
+    W, X, L, R, dx, dL, dR = layer_inputs(4096, 4096, 384, 16, name="det")
+    p = slim.pack(dev(W))
+    a = slim.linear(dx, p, dL, dR).clone()
+    b = slim.linear(dx, p, dL, dR).clone()
+    assert torch.equal(a, b)
+    W, X, L, R, dx, dL, dR = layer_inputs(1024, 1024, 64, 256, name="det2")
+    p = slim.pack(dev(W))
+    assert torch.equal(slim.linear(dx, p, dL, dR).clone(), slim.linear(dx, p, dL, dR).clone())
+
+
+# ------------------------------------------------------------------------------ backward
+
+def _bwd_case(n, k, r, m, seed=0, ks=None, ms=None, name="bwd", dydtype="bf16"):
+    print(f"bwd n={n} k={k} r={r} m={m} seed={seed}", flush=True)
+    W = synth.weights(n, k, seed=seed, name=name + "/W")
+    dybits, dY = synth.activations(m, n, seed=seed, name=name + "/dY", dtype=dydtype)
+    Lb, Rb, L, R = synth.adapter(k, n, max(r, 16), seed=seed, name=name + "/")
+    if r == 0:
+        L = R = dL = dR = None
+    else:
+        Lb, Rb, L, R = Lb[:, :r].copy(), Rb[:r].copy(), L[:, :r], R[:r]
+        dL, dR = dev_bits(Lb, torch.float16), dev_bits(Rb, torch.float16)
+    tdt = torch.bfloat16 if dydtype == "bf16" else torch.float16
+    pb = slim.pack_bwd(slim.pack(dev(W)))
+    dX = host(slim.bwd_dx(dev_bits(dybits, tdt), pb, dL, dR))
+    ms = np.arange(m) if ms is None else ms
+    if ks is None:
+        ref = O.bwd_dx(dY[ms], O.pack_bwd(O.pack(W), n, k), L, R, n, k)
+        return assert_close(dX[ms], ref, f"bwd n={n} k={k} r={r} m={m}")
+    for g in ks:   # one 128-column group at a time: the backward pack is separable by K-group
+        cols = slice(128 * g, 128 * g + 128)
+        ref = O.bwd_dx(dY[ms], O.pack_bwd(O.pack(W[:, cols]), n, 128), None if L is None else L[cols], R, n, 128)
+        assert_close(dX[np.ix_(ms, np.arange(128 * g, 128 * g + 128))], ref, f"bwd group {g}")
+
+
+@pytest.mark.parametrize("m,r", [(16, 32), (1, 0), (5, 32), (64, 32), (200, 32), (256, 0)])
+def test_bwd_small(m, r):
+    _bwd_case(512, 512, r, m, name="bwd_small")
+
+
+def test_bwd_decode_shape():
+    _bwd_case(4096, 4096, 384, 16, name="bwd_decode")
+
+
+@pytest.mark.parametrize("m,seed", [(1, 0), (16, 1), (512, 2), (8192, 0)])
+def test_bwd_mlp70b_sampled(m, seed):
+    ms = None if m <= 16 else np.sort(synth.stream(seed, "bms").choice(m, size=24, replace=False))
+    _bwd_case(28672, 8192, 512, m, seed=seed, ks=(0, 31, 63), ms=ms, name="mlp70b")
+
+
+def test_bwd_is_deterministic():
+    n, k, m = 4096, 4096, 16
+    W = synth.weights(n, k, seed=9)
+    dybits, _ = synth.activations(m, n, seed=9)
+    Lb, Rb, _, _ = synth.adapter(k, n, 64, seed=9)
+    pb = slim.pack_bwd(slim.pack(dev(W)))
+    dy = dev_bits(dybits, torch.bfloat16)
+    dL, dR = dev_bits(Lb, torch.float16), dev_bits(Rb, torch.float16)
+    assert torch.equal(slim.bwd_dx(dy, pb, dL, dR).clone(), slim.bwd_dx(dy, pb, dL, dR).clone())

@@ -1,0 +1,112 @@
+"""slim_pack / slim_pack_bwd against the oracle: bit-exact codes, indices, scales and masks."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import slim_oracle as O
+from paper_2608_24070_amd import slim, synth
+from tests.gpu_common import dev, host, host_pack
+
+pytestmark = pytest.mark.gpu
+
+
+def _tied(n, k, seed):
+    rng = synth.stream(seed, "tied")
+    lv = rng.integers(0, 6, size=(n, k)).astype(np.float32) * np.float32(0.013)
+    sg = np.where(rng.random((n, k)) < 0.5, -1.0, 1.0).astype(np.float32)
+    w = lv * sg
+    w[rng.random((n, k)) < 0.05] = -0.0
+    return w
+
+
+def _check_pack(W, rows=None):
+    p = host_pack(slim.pack(dev(W), with_mask=True))
+    ref_W = W if rows is None else W[rows]
+    ref = O.pack(ref_W)
+    sel = (lambda a: a) if rows is None else (lambda a: a[rows])
+    for key in ("codes", "meta", "scales", "mask"):
+        assert np.array_equal(sel(p[key]), ref[key]), key
+    return p
+
+
+@pytest.mark.parametrize("n,k,seed", [(512, 512, 0), (64, 1024, 1), (4096, 4096, 0), (48, 384, 2)])
+def test_pack_bit_exact(n, k, seed):
+    print(f"pack n={n} k={k} seed={seed}", flush=True)
+    _check_pack(synth.weights(n, k, seed=seed))
+
+
+def test_pack_bit_exact_ties_and_signed_zeros():
+    _check_pack(_tied(128, 512, 3))
+
+
+def test_pack_zero_and_tiny_groups():
+    W = synth.weights(32, 256, seed=4)
+    W[3, :128] = 0.0
+    W[5, 128:] = 1e-8
+    W[7, 7] = -0.0
+    _check_pack(W)
+
+
+@pytest.mark.parametrize("n,k", [(11008, 4096), (28672, 8192)])
+def test_pack_full_size_sampled_rows(n, k):
+    print(f"pack full n={n} k={k}", flush=True)
+    W = synth.weights(n, k, seed=0)
+    rows = np.sort(synth.stream(0, "rows").choice(n, size=384, replace=False))
+    _check_pack(W, rows)
+
+
+def test_pack_is_deterministic():
+    W = dev(synth.weights(1024, 1024, seed=5))
+    a = slim.pack(W, with_mask=True)
+    b = slim.pack(W, with_mask=True)
+    for key in ("codes", "meta", "scales", "mask"):
+        assert torch.equal(a[key], b[key]), key
+
+
+def test_pack_rejects_nonfinite_and_overflow():
+    W = synth.weights(16, 256, seed=6)
+    W[2, 17] = np.nan
+    with pytest.raises(slim.SlimError) as e:
+        slim.pack(dev(W))
+    assert e.value.status == 5
+    W[2, 17] = np.inf
+    with pytest.raises(slim.SlimError) as e:
+        slim.pack(dev(W))
+    assert e.value.status == 5
+    W[2, 17] = 7.0 * 65520.0
+    with pytest.raises(slim.SlimError) as e:
+        slim.pack(dev(W))
+    assert e.value.status == 6
+
+
+@pytest.mark.parametrize("n,k,tied", [(512, 512, False), (64, 384, True), (4096, 4096, False)])
+def test_pack_bwd_bit_exact(n, k, tied):
+    print(f"pack_bwd n={n} k={k}", flush=True)
+    W = _tied(n, k, 7) if tied else synth.weights(n, k, seed=7)
+    p = slim.pack(dev(W))
+    b = host_pack(slim.pack_bwd(p, with_mask=True))
+    ref = O.pack_bwd(O.pack(W), n, k)
+    for key in ("codesT", "metaT", "scalesT", "mask_rc"):
+        assert np.array_equal(b[key], ref[key]), key
+
+
+def test_pack_bwd_full_size_sampled_groups():
+    n, k = 28672, 8192
+    print("pack_bwd full 28672x8192", flush=True)
+    W = synth.weights(n, k, seed=0)
+    b = host_pack(slim.pack_bwd(slim.pack(dev(W)), with_mask=False))
+    for g in (0, 37, 63):
+        blk = W[:, 128 * g:128 * g + 128]
+        ref = O.pack_bwd(O.pack(blk), n, 128)
+        assert np.array_equal(b["codesT"][128 * g:128 * g + 128], ref["codesT"]), g
+        assert np.array_equal(b["metaT"][128 * g:128 * g + 128], ref["metaT"]), g
+        assert np.array_equal(b["scalesT"][g], ref["scalesT"][0]), g
+
+
+def test_double_pruning_statistic_on_device():
+    n, k = 4096, 4096
+    W = synth.weights(n, k, seed=8)
+    p = slim.pack(dev(W), with_mask=True)
+    b = slim.pack_bwd(p, with_mask=True)
+    extra = (p["mask"].sum().item() - b["mask_rc"].sum().item()) / (n * k)
+    assert abs(extra - O.lemma_extra_sparsity(2, 4)) < 1e-3
