@@ -1,0 +1,303 @@
+#!/usr/bin/env python3
+"""Benchmark of the SLiM compressed linear layer on one MI355X.
+
+Default workload: the decode-shaped layer (X bf16 [16 x 4096], W 4096 x 4096 packed 2:4 + int4
+group-128, rank-384 fp16 adapter). One step = one slim_linear call (the adapter GEMM plus the
+fused sparse contraction) on inputs resident in HBM; the weight copies rotate over more than 3x
+the 256 MB MALL, so the weight stream comes from HBM. Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload decode|prefill|block13b|mlp70b|mlp70b_bwd|tiny]
+                  [--m M] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "dense-equiv TFLOP/s (M≥2048) and weight-stream HBM GB/s (M≤16), 2:4+int4+LoRA"
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
+MFMA_F16_PEAK_TFS = 2516.6       # MI355X dense fp16/bf16 MFMA
+PACK_BYTES_PER_WEIGHT = 0.390625  # 4-bit code x 1/2 + 2-bit index x 1/2 + fp16 scale / 128
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="decode",
+                    choices=["decode", "prefill", "block13b", "mlp70b", "mlp70b_bwd", "tiny"])
+    ap.add_argument("--m", type=int, default=None, help="rows of X (tokens); default per workload")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU budget of the oracle baseline")
+    return ap.parse_args()
+
+
+def layer_bytes(M, N, K, r):
+    """Algorithmic bytes of one forward layer call: packed weight + fp16 adapter + bf16 X + fp32 Y."""
+    return N * K * PACK_BYTES_PER_WEIGHT + 2 * r * (K + N) + 2 * M * K + 4 * M * N
+
+
+def layer_flops(M, N, K, r):
+    """Dense-equivalent FLOPs: the 2:4 product counted as dense, plus both adapter products."""
+    return 2 * M * N * K + 2 * M * r * (K + N)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported in this build "
+              "(the layer shards along N across GPUs by design, but no multi-GPU path is built).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_24070_amd import configs, slim, synth
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    wk = args.workload
+    bwd = wk == "mlp70b_bwd"
+    if wk == "decode":
+        layers, M = configs.DECODE.layers, args.m or 16
+    elif wk == "prefill":
+        layers, M = configs.PREFILL.layers, args.m or 2048
+    elif wk == "block13b":
+        layers, M = configs.BLOCK13B.layers, args.m or 4096
+    elif wk in ("mlp70b", "mlp70b_bwd"):
+        layers, M = configs.MLP70B.layers, args.m or 8192
+    else:
+        layers, M = configs.TINY.layers, args.m or 16
+    decode_like = M <= 16
+
+    # ------------------------------------------------------------------ inputs
+    def dev_bits(bits, dtype):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(dtype)
+
+    t0 = time.time()
+    per_layer = []
+    pack_ms = 0.0
+    for i, ly in enumerate(layers):
+        W = torch.from_numpy(synth.weights(ly.n, ly.k, seed=0, name=f"{wk}/{ly.name}/W")).to(dev)
+        Lb, Rb, _, _ = synth.adapter(ly.k, ly.n, ly.r, seed=0, name=f"{wk}/{ly.name}/")
+        torch.cuda.synchronize()
+        tp = time.perf_counter()
+        p = slim.pack(W)
+        if bwd:
+            p = slim.pack_bwd(p)
+        torch.cuda.synchronize()
+        pack_ms += (time.perf_counter() - tp) * 1e3
+        del W
+        per_layer.append({"layer": ly, "pack": p, "L": dev_bits(Lb, torch.float16), "R": dev_bits(Rb, torch.float16)})
+    # activations: q/k/v/gate/up of the block share X; o and down get their own
+    acts = {}
+    for ly in layers:
+        a_len = ly.n if bwd else ly.k
+        key = (ly.name if ly.name in ("o", "down") else "shared", a_len)
+        if key not in acts:
+            bits, _ = synth.activations(M, a_len, seed=0, name=f"{wk}/{key[0]}/X")
+            acts[key] = dev_bits(bits, torch.bfloat16)
+    for pl in per_layer:
+        ly = pl["layer"]
+        a_len = ly.n if bwd else ly.k
+        pl["x"] = acts[(ly.name if ly.name in ("o", "down") else "shared", a_len)]
+        pl["out"] = torch.empty((M, ly.k if bwd else ly.n), dtype=torch.float32, device=dev)
+
+    # rotate distinct copies of the weight side over > 3x the 256 MB MALL (capped at 2 GB)
+    copy_bytes = sum(pl["pack"]["codes" if not bwd else "codesT"].numel() * 1.5625 + pl["L"].numel() * 4
+                     for pl in per_layer)
+    n_copies = int(min(64, max(1, math.ceil(3 * 256e6 / copy_bytes)), max(1, 2e9 // copy_bytes)))
+    copies = []
+    for c in range(n_copies):
+        cp = []
+        for pl in per_layer:
+            if c == 0:
+                cp.append({"pack": pl["pack"], "L": pl["L"], "R": pl["R"]})
+            else:
+                cp.append({"pack": {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in pl["pack"].items()},
+                           "L": pl["L"].clone(), "R": pl["R"].clone()})
+        copies.append(cp)
+    ws_need = max((slim.slim_bwd_dx_workspace if bwd else slim.slim_linear_workspace)(
+        M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
+    ws = torch.zeros(ws_need + 256, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+
+    def step(i):
+        cp = copies[i % n_copies]
+        for pl, c in zip(per_layer, cp):
+            if bwd:
+                slim.bwd_dx(pl["x"], c["pack"], c["L"], c["R"], out=pl["out"], ws=ws)
+            else:
+                slim.linear(pl["x"], c["pack"], c["L"], c["R"], out=pl["out"], ws=ws)
+
+    # ------------------------------------------------------------------ timed region
+    # The stream is first given a bounded busy kernel (torch.cuda._sleep) long enough for the host
+    # to enqueue every timed step behind it; the GPU then runs the K steps back to back and the two
+    # events bracket GPU time only, not Python launch overhead.
+    stream = torch.cuda.current_stream()
+    cyc_per_ms = sleep_calibration(torch)
+
+    def backlog(ms):
+        torch.cuda._sleep(int(cyc_per_ms * ms))
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    # host enqueue cost of one step, to size the backlog
+    t = time.perf_counter()
+    for i in range(5):
+        step(i)
+    host_ms = (time.perf_counter() - t) / 5 * 1e3
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    backlog(min(2000.0, 20.0 + 2.0 * host_ms * args.steps))
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    print(f"[bench] {wk} M={M}: {ms_per_step * 1e3:.2f} us/step over {args.steps} steps "
+          f"({n_copies} weight copies, host enqueue {host_ms * 1e3:.0f} us/step, setup {setup_s:.1f}s)",
+          file=sys.stderr, flush=True)
+
+    # Per-kernel durations: the library brackets each launch with two hipEvents on the launch
+    # stream (slim_timing_*), again behind a backlog so that they time the GPU, not the host.
+    slim.slim_timing_reset()
+    slim.slim_timing_enable(True)
+    backlog(min(2000.0, 20.0 + 3.0 * host_ms * args.steps))
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    kt = slim.slim_timing_read()
+    slim.slim_timing_enable(False)
+    timing_mode = "hip events around each launch, stream backlogged"
+    kernels = {k: {"launches": n, "avg_us": 1e3 * ms / max(n, 1)} for k, (n, ms) in kt.items()}
+    dominant = max(kt.items(), key=lambda kv: kv[1][1])[0]
+
+    # ------------------------------------------------------------------ figures
+    tot_bytes = sum(layer_bytes(M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
+    tot_flops = sum(layer_flops(M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
+    launches_per_step = kt[dominant][0] / args.steps
+    if decode_like:
+        unit = "GB/s"
+        value = tot_bytes / (ms_per_step * 1e-3) / 1e9
+        # dominant kernel (the sparse contraction): packed weight + R + X in, Y out, per launch
+        dk_bytes = sum(pl["layer"].n * pl["layer"].k * PACK_BYTES_PER_WEIGHT + 2 * pl["layer"].r * pl["layer"].n
+                       + 2 * M * pl["layer"].k + 4 * M * pl["layer"].n for pl in per_layer) / launches_per_step
+        achieved = dk_bytes / (kernels[dominant]["avg_us"] * 1e-6) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None}
+    else:
+        unit = "TFLOP/s"
+        value = tot_flops / (ms_per_step * 1e-3) / 1e12
+        # dominant kernel (the sparse contraction): dense-equivalent 2MNK plus the adapter's 2MrN
+        dk_flops = sum(2 * M * pl["layer"].n * pl["layer"].k + 2 * M * pl["layer"].r *
+                       (pl["layer"].k if bwd else pl["layer"].n) for pl in per_layer) / launches_per_step
+        achieved = dk_flops / (kernels[dominant]["avg_us"] * 1e-6) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_F16_PEAK_TFS, "unit": "TFLOP/s",
+                    "frac": round(achieved / MFMA_F16_PEAK_TFS, 4), "traffic": None}
+    roofline["kernel"] = dominant
+    roofline["timing"] = timing_mode
+
+    # ------------------------------------------------------------------ oracle baseline
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wk, per_layer, M, bwd, decode_like, args.cpu_seconds)
+
+    ly0 = layers[0]
+    shape = ", ".join(f"{ly.name} {ly.n}x{ly.k} r{ly.r}" for ly in layers)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": unit,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wk}: M={M}, {shape}, bf16 {'dY' if bwd else 'X'}, "
+                        f"{'dX' if bwd else 'Y'} fp32, 2:4 + int4 group-128 weights",
+            "M": M, "layers": len(layers), "N": ly0.n, "K": ly0.k, "r": ly0.r,
+            "bytes_per_step": int(tot_bytes), "dense_equiv_flops_per_step": int(tot_flops),
+            "weight_copies_rotated": n_copies, "pack_ms_one_time": round(pack_ms, 2),
+        },
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+def sleep_calibration(torch):
+    """GPU clock cycles per millisecond of torch.cuda._sleep, measured with events."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(1000)
+    e0.record()
+    torch.cuda._sleep(10_000_000)
+    e1.record()
+    torch.cuda.synchronize()
+    return 10_000_000 / max(e0.elapsed_time(e1), 1e-3)
+
+
+def cpu_baseline(wk, per_layer, M, bwd, decode_like, budget_s):
+    """Time the CPU oracle (unchanged) on a bounded sample of the same workload, on this host."""
+    from oracle import slim_oracle as O
+    from paper_2608_24070_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    ly = per_layer[0]["layer"]
+    n_rows = min(ly.n, 512)
+    rows = np.arange(n_rows)
+    m_rows = min(M, 64)
+    W = synth.weights(ly.n, ly.k, seed=0, name=f"{wk}/{ly.name}/W")[:n_rows] if not bwd else None
+    _, _, L, R = synth.adapter(ly.k, ly.n, ly.r, seed=0, name=f"{wk}/{ly.name}/")
+    if bwd:
+        # one 128-column group of the backward: all N rows, 128 input features
+        Wblk = synth.weights(ly.n, ly.k, seed=0, name=f"{wk}/{ly.name}/W")[:, :128]
+        pb = O.pack_bwd(O.pack(Wblk), ly.n, 128)
+        _, dY = synth.activations(m_rows, ly.n, seed=0, name="cpu/dY")
+        run = lambda: O.bwd_dx(dY, pb, L[:128], R, ly.n, 128)
+        flops = 2 * m_rows * ly.n * 128 + 2 * m_rows * ly.r * (ly.n + 128)
+        nbytes = ly.n * 128 * PACK_BYTES_PER_WEIGHT + 2 * ly.r * (ly.n + 128) + 2 * m_rows * ly.n + 4 * m_rows * 128
+        sample = f"bwd dX for {m_rows} rows x one 128-wide K group (all {ly.n} N), oracle pack excluded"
+    else:
+        p = O.pack(W)
+        _, X = synth.activations(m_rows, ly.k, seed=0, name="cpu/X")
+        run = lambda: O.linear(X, p, L, R[:, rows], n_rows, ly.k)
+        flops = layer_flops(m_rows, n_rows, ly.k, ly.r)
+        nbytes = layer_bytes(m_rows, n_rows, ly.k, ly.r)
+        sample = f"forward for {m_rows} rows of X x {n_rows} of {ly.n} output features, oracle pack excluded"
+    times = []
+    t_end = time.perf_counter() + budget_s
+    while time.perf_counter() < t_end or not times:
+        t = time.perf_counter()
+        run()
+        times.append(time.perf_counter() - t)
+        if len(times) >= 50:
+            break
+    med = float(np.median(times))
+    if decode_like:
+        return {"value": round(nbytes / med / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+                "sample": sample + f"; median of {len(times)} calls ({med * 1e3:.1f} ms each)"}
+    return {"value": round(flops / med / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": sample + f"; median of {len(times)} calls ({med * 1e3:.1f} ms each)"}
+
+
+if __name__ == "__main__":
+    main()

@@ -180,6 +180,18 @@ int slim_linear_bwd_dx(const void* dY, int dydtype, int64_t M, int64_t N, int64_
                        const uint16_t* L, const uint16_t* R, int64_t r, float* dX, void* ws,
                        size_t ws_bytes, void* stream);
 
+/*
+ * Per-kernel timing for benchmarks (host-side bookkeeping; not part of the layer's math).
+ * slim_timing_enable(1) makes every later kernel launch of this library record a hipEvent
+ * before and after itself on the caller's stream. slim_timing_read waits for the recorded
+ * events and writes one line per kernel name, "name launches total_ms\n", into buf (host);
+ * it returns 0, or the buffer size needed when buf is NULL or too small. slim_timing_reset
+ * clears the totals. Thread-safe; timing adds two event records per launch while enabled.
+ */
+int slim_timing_enable(int on);
+int slim_timing_reset(void);
+int slim_timing_read(char* buf, size_t buf_len);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,128 +1,144 @@
-// adapter_gemm.hip - the first, reducing product of the low-rank adapter path:
+// adapter_gemm.hip - the adapter's first, reducing product for large M:
 //   forward   T = X L        (X [M, K] activations, L [K, r] fp16, "NN")
 //   backward  U = dY R^T     (dY [M, N],           R [r, N] fp16, "NT")
-// Output fp32 [M, r]. 64 x 64 output tiles on 16x16x32 fp16 MFMA; the reduction may be split
-// across blocks, in which case the last block to finish a tile sums the partial tiles in a
-// fixed order (deterministic) and resets the tile's counter to zero.
+// Result fp16 [M, r] (it only feeds the fp16 MFMA of the second product). 64 x 64 output tiles
+// on 16x16x32 fp16 MFMA, 64-wide reduction stages double-buffered in LDS and staged through
+// registers one stage ahead. The reduction may be split across blocks; the last block of a tile
+// sums the partials in split order (deterministic) through device-scope accesses.
 #include "slim_device.h"
 #include "slim_launch.h"
+#include "slim_timing.h"
 
 namespace {
 
-constexpr int kT = 64;      // tile edge (rows of A = m, columns = adapter rank j)
-constexpr int kBK = 64;     // reduction per LDS stage
+constexpr int kT = 64;      // output tile edge (m and j)
+constexpr int kBK = 64;     // reduction per stage
 constexpr int kLd = kBK + 8;
 
 template <bool NT>
 __global__ void __launch_bounds__(256)
 k_adapter_gemm(const uint16_t* __restrict__ A, int a_bf16, int64_t M, int64_t Kd, const uint16_t* __restrict__ Bsrc,
-               int64_t r, int64_t slice, int split, float* __restrict__ out, float* __restrict__ part,
+               int64_t r, int64_t slice, int split, uint16_t* __restrict__ out, float* __restrict__ part,
                uint32_t* __restrict__ counters) {
-  __shared__ __attribute__((aligned(16))) _Float16 As[kT][kLd];
-  __shared__ __attribute__((aligned(16))) _Float16 Bt[kT][kLd];   // [j][k]
+  __shared__ __attribute__((aligned(16))) _Float16 As[2][kT][kLd];
+  __shared__ __attribute__((aligned(16))) _Float16 Bs[2][kT][kLd];   // NT: [j][k]; NN: [k][j]
   __shared__ int last_flag;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wj = wave >> 1;
+  const int g = lane >> 4;
   const int64_t m0 = (int64_t)blockIdx.x * kT, j0 = (int64_t)blockIdx.y * kT;
   const int s = blockIdx.z;
   const int64_t kbeg = (int64_t)s * slice, kend = min(Kd, kbeg + slice);
-  f4_t acc[2][2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = f4_t{0.f, 0.f, 0.f, 0.f};
+  const int nst = (int)((kend - kbeg + kBK - 1) / kBK);
+  const bool bf16 = a_bf16 != 0;
 
-  for (int64_t k = kbeg; k < kend; k += kBK) {
-    // A tile: 64 rows x 64 k = 512 vectors of 8
+  u32x4_t ar[2], br[2];
+  auto load = [&](int t) {
+    const int64_t k = kbeg + (int64_t)t * kBK;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int idx = tid + 256 * i, row = idx >> 3, kc = idx & 7;
-      const int64_t gm = m0 + row, gk = k + 8 * kc;
-      u32x4_t v = {0u, 0u, 0u, 0u};
-      if (gm < M && gk < kend) v = *reinterpret_cast<const u32x4_t*>(A + gm * Kd + gk);
-      *reinterpret_cast<h8_t*>(&As[row][8 * kc]) = load8_as_h(v, a_bf16 != 0);
-    }
-    // B tile, stored transposed as Bt[j][k]
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int idx = tid + 256 * i;
+      const int q = tid + 256 * i;
+      {  // A tile: 64 rows of m x 8 vectors
+        const int row = q >> 3, kc = q & 7;
+        const int64_t gm = m0 + row, gk = k + 8 * kc;
+        ar[i] = (gm < M && gk < kend) ? *reinterpret_cast<const u32x4_t*>(A + gm * Kd + gk) : u32x4_t{0u, 0u, 0u, 0u};
+      }
       if (NT) {  // R [r, Kd]: row j contiguous along k
-        const int jr = idx >> 3, kc = idx & 7;
+        const int jr = q >> 3, kc = q & 7;
         const int64_t gj = j0 + jr, gk = k + 8 * kc;
-        u32x4_t v = {0u, 0u, 0u, 0u};
-        if (gj < r && gk < kend) v = *reinterpret_cast<const u32x4_t*>(Bsrc + gj * Kd + gk);
-        *reinterpret_cast<u32x4_t*>(&Bt[jr][8 * kc]) = v;
-      } else {   // L [Kd, r]: row k contiguous along j -> transpose on the way into LDS
-        const int kr = idx >> 3, jc = idx & 7;
+        br[i] = (gj < r && gk < kend) ? *reinterpret_cast<const u32x4_t*>(Bsrc + gj * Kd + gk) : u32x4_t{0u, 0u, 0u, 0u};
+      } else {   // L [Kd, r]: row k contiguous along j
+        const int kr = q >> 3, jc = q & 7;
         const int64_t gk = k + kr, gj = j0 + 8 * jc;
-        u32x4_t v = {0u, 0u, 0u, 0u};
-        if (gk < kend && gj < r) v = *reinterpret_cast<const u32x4_t*>(Bsrc + gk * r + gj);
-        const h8_t hv = __builtin_bit_cast(h8_t, v);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) Bt[8 * jc + e][kr] = hv[e];
+        br[i] = (gk < kend && gj < r) ? *reinterpret_cast<const u32x4_t*>(Bsrc + gk * r + gj) : u32x4_t{0u, 0u, 0u, 0u};
       }
     }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = tid + 256 * i;
+      *reinterpret_cast<h8_t*>(&As[buf][q >> 3][8 * (q & 7)]) = load8_as_h(ar[i], bf16);
+      *reinterpret_cast<u32x4_t*>(&Bs[buf][q >> 3][8 * (q & 7)]) = br[i];
+    }
+  };
+
+  f4_t acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) acc[x][y] = f4_t{0.f, 0.f, 0.f, 0.f};
+
+  if (nst > 0) {
+    load(0);
+    store(0);
     __syncthreads();
+    if (nst > 1) load(1);
+  }
+  for (int t = 0; t < nst; ++t) {
+    const int buf = t & 1;
 #pragma unroll
     for (int kk = 0; kk < kBK; kk += 32) {
       h8_t af[2], bf[2];
 #pragma unroll
       for (int f = 0; f < 2; ++f) {
-        af[f] = *reinterpret_cast<const h8_t*>(&As[32 * wm + 16 * f + (lane & 15)][kk + 8 * (lane >> 4)]);
-        bf[f] = *reinterpret_cast<const h8_t*>(&Bt[32 * wj + 16 * f + (lane & 15)][kk + 8 * (lane >> 4)]);
+        af[f] = *reinterpret_cast<const h8_t*>(&As[buf][32 * wm + 16 * f + (lane & 15)][kk + 8 * g]);
+        const int jc = 32 * wj + 16 * f + (lane & 15);
+        if (NT) {
+          bf[f] = *reinterpret_cast<const h8_t*>(&Bs[buf][jc][kk + 8 * g]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) bf[f][e] = Bs[buf][kk + 8 * g + e][jc];
+        }
       }
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int x = 0; x < 2; ++x)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[a], bf[b], acc[a][b], 0, 0, 0);
+        for (int y = 0; y < 2; ++y) acc[x][y] = mfma16(af[x], bf[y], acc[x][y]);
     }
+    if (t + 1 < nst) store(buf ^ 1);
     __syncthreads();
+    if (t + 2 < nst) load(t + 2);
   }
 
   const int tile = blockIdx.x * gridDim.y + blockIdx.y;
   if (split > 1) {
-    // partial tile in register order: fully coalesced
     float* dst = part + ((int64_t)s * gridDim.x * gridDim.y + tile) * (kT * kT);
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int x = 0; x < 2; ++x)
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
+      for (int y = 0; y < 2; ++y)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) dst[(((wave * 2 + a) * 2 + b) * 4 + v) * 64 + lane] = acc[a][b][v];
-    __threadfence();
+        for (int v = 0; v < 4; ++v) st_dev(dst + (((wave * 2 + x) * 2 + y) * 4 + v) * 64 + lane, acc[x][y][v]);
+    drain_stores();
     __syncthreads();
-    if (tid == 0) {
-      const uint32_t done = atomicAdd(&counters[tile], 1u);
-      last_flag = (done == (uint32_t)(split - 1));
-    }
+    if (tid == 0) last_flag = counter_arrive(&counters[tile]) == (uint32_t)(split - 1);
     __syncthreads();
     if (!last_flag) return;
-    __threadfence();
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int x = 0; x < 2; ++x)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) acc[a][b] = f4_t{0.f, 0.f, 0.f, 0.f};
+      for (int y = 0; y < 2; ++y) acc[x][y] = f4_t{0.f, 0.f, 0.f, 0.f};
     for (int ss = 0; ss < split; ++ss) {
       const float* src = part + ((int64_t)ss * gridDim.x * gridDim.y + tile) * (kT * kT);
+      float pv[16];
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int e = 0; e < 16; ++e) pv[e] = ld_dev(src + (wave * 16 + e) * 64 + lane);
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) acc[a][b][v] += src[(((wave * 2 + a) * 2 + b) * 4 + v) * 64 + lane];
+      for (int e = 0; e < 16; ++e) acc[e >> 3][(e >> 2) & 1][e & 3] += pv[e];
     }
-    if (tid == 0) counters[tile] = 0u;
+    if (tid == 0) counter_reset(&counters[tile]);
   }
   // D[i][j] of a 16x16 fragment sits at lane (j + 16 * (i / 4)), element i % 4
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int x = 0; x < 2; ++x)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int64_t gj = j0 + 32 * wj + 16 * b + (lane & 15);
+    for (int y = 0; y < 2; ++y) {
+      const int64_t gj = j0 + 32 * wj + 16 * y + (lane & 15);
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int64_t gm = m0 + 32 * wm + 16 * a + 4 * (lane >> 4) + v;
-        if (gm < M && gj < r) out[gm * r + gj] = acc[a][b][v];
+        const int64_t gm = m0 + 32 * wm + 16 * x + 4 * g + v;
+        if (gm < M && gj < r) out[gm * r + gj] = __builtin_bit_cast(uint16_t, (_Float16)acc[x][y][v]);
       }
     }
 }
@@ -132,9 +148,10 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int a_bf16, int64_t M, int64_t Kd
 int slim_launch_adapter_gemm(bool nt, const uint16_t* A, int a_bf16, int64_t M, int64_t Kd, const uint16_t* B,
                              int64_t r, const SlimPlan& p, char* ws, hipStream_t s) {
   dim3 grid((unsigned)p.ad_tiles_m, (unsigned)p.ad_tiles_j, (unsigned)p.ad_split);
-  float* out = reinterpret_cast<float*>(ws + p.off_t);
+  uint16_t* out = reinterpret_cast<uint16_t*>(ws + p.off_t);
   float* part = reinterpret_cast<float*>(ws + p.off_tpart);
   uint32_t* counters = reinterpret_cast<uint32_t*>(ws + p.off_counters);
+  SlimKernelTimer timer(nt ? "adapter_gemm_nt" : "adapter_gemm_nn", s);
   if (nt)
     hipLaunchKernelGGL(k_adapter_gemm<true>, grid, dim3(256), 0, s, A, a_bf16, M, Kd, B, r, p.ad_slice, p.ad_split,
                        out, part, counters);

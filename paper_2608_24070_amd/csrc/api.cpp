@@ -7,6 +7,7 @@
 namespace {
 constexpr int64_t kMaxDim = int64_t(1) << 31;
 constexpr size_t kCounterSlots = SLIM_COUNTER_SLOTS;
+constexpr int64_t kDecodeAdSlice = SLIM_DECODE_AD_SLICE;
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -57,65 +58,76 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
   if (N % 16 || K % 128 || r < 0 || r % 16 || r >= kMaxDim) return SLIM_ESHAPE;
   if (bwd && N % 128) return SLIM_ESHAPE;
   const int64_t rows = bwd ? K : N, red = bwd ? N : K;
-  SlimPlan q;
-  // adapter GEMM: 64 x 64 output tiles of [M x r], split along the reduction until ~256 blocks
-  if (r > 0) {
-    q.ad_tiles_m = (int)cdiv(M, 64);
-    q.ad_tiles_j = (int)cdiv(r, 64);
-    const int64_t tiles = (int64_t)q.ad_tiles_m * q.ad_tiles_j;
-    int64_t split = std::max<int64_t>(1, std::min<int64_t>(256 / tiles, red / 256));
-    int64_t slice = cdiv(cdiv(red, split), 64) * 64;
-    q.ad_split = (int)cdiv(red, slice);
-    q.ad_slice = slice;
-  }
-  // sparse contraction
   const int64_t nchunks = red / 128;
+  SlimPlan q;
+  size_t ad_counters = 0, tpart_bytes = 0, ypart_bytes = 0;
   if (M <= 64) {
+    // small M: one launch of split-reduction sparse units plus adapter first-product units,
+    // then the adapter's second product
     q.decode = true;
     q.dec_fm = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+    const int64_t mc = 16 * q.dec_fm;
     q.sp_rows_tile = 64;
-    q.sp_cols_tile = 16 * q.dec_fm;
+    q.sp_cols_tile = (int)mc;
     q.sp_row_tiles = cdiv(rows, 64);
     q.sp_col_tiles = 1;
-    // staged activations [16*fm x (cps*128 + 8)] fp16 must fit in 56 KB of LDS (64 KB with the
-    // kernel's static LDS)
-    const int64_t max_cps = std::max<int64_t>(1, (57344 / (32 * q.dec_fm) - 8) / 128);
-    int64_t want = std::max<int64_t>(1, 512 / q.sp_row_tiles);           // ~512 blocks in flight
-    int64_t cps = std::min<int64_t>(max_cps, std::max<int64_t>(1, cdiv(nchunks, want)));
+    // staged activations [mc x (cps*128 + 8)] fp16 within 56 KB of LDS
+    const int64_t max_cps = std::max<int64_t>(1, (57344 / (2 * mc) - 8) / 128);
+    const int64_t want = std::max<int64_t>(1, 512 / q.sp_row_tiles);    // ~512 sparse blocks
+    const int64_t cps = std::min<int64_t>(max_cps, std::max<int64_t>(1, cdiv(nchunks, want)));
     q.sp_chunks_per_split = cps;
     q.sp_split = (int)cdiv(nchunks, cps);
-    if (q.sp_split > 1 && q.sp_row_tiles > kCounterSlots / 2) {   // too many tiles to count: no split
-      q.sp_chunks_per_split = nchunks;
-      q.sp_split = 1;
+    if (q.sp_split > 1 && q.sp_row_tiles > (int64_t)(kCounterSlots / 2)) return SLIM_EUNSUPPORTED;
+    if (r > 0) {
+      q.ad_jblocks = cdiv(r, 64);
+      q.ad_slice = kDecodeAdSlice;
+      q.ad_split = (int)cdiv(red, kDecodeAdSlice);
+      if (q.ad_split > 1) {
+        ad_counters = (size_t)q.ad_jblocks;
+        tpart_bytes = (size_t)q.ad_jblocks * q.ad_split * 4 * q.dec_fm * 256 * 4;
+      }
     }
-    q.lds_bytes = (size_t)(16 * q.dec_fm) * (size_t)(cps * 128 + 8) * 2;
+    if (q.sp_split > 1) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 64 * mc * 4;
+    const size_t lds_w = (size_t)mc * (size_t)(cps * 128 + 8) * 2;
+    const size_t lds_a = (r > 0 && !bwd) ? (size_t)kDecodeAdSlice * (64 + 8) * 2 : 0;
+    q.lds_bytes = std::max(lds_w, lds_a);
   } else {
+    // large M: dense adapter GEMM (64 x 64 tiles) then 256 x 128 sparse tiles
     q.decode = false;
-    q.sp_rows_tile = bwd ? 128 : 256;
+    q.sp_rows_tile = 256;
     q.sp_cols_tile = 128;
-    q.sp_row_tiles = cdiv(rows, q.sp_rows_tile);
-    q.sp_col_tiles = cdiv(M, q.sp_cols_tile);
+    q.sp_row_tiles = cdiv(rows, 256);
+    q.sp_col_tiles = cdiv(M, 128);
     q.sp_split = 1;
     q.sp_chunks_per_split = nchunks;
-    q.lds_bytes = 2 * (size_t)q.sp_cols_tile * (128 + 8) * 2;
+    if (r > 0) {
+      q.ad_tiles_m = (int)cdiv(M, 64);
+      q.ad_tiles_j = (int)cdiv(r, 64);
+      const int64_t tiles = (int64_t)q.ad_tiles_m * q.ad_tiles_j;
+      const int64_t split = std::max<int64_t>(1, std::min<int64_t>(cdiv(256, tiles), red / 512));
+      const int64_t slice = cdiv(cdiv(red, split), 64) * 64;
+      q.ad_split = (int)cdiv(red, slice);
+      q.ad_slice = slice;
+      if (q.ad_split > 1) {
+        if (tiles > (int64_t)kCounterSlots) return SLIM_EUNSUPPORTED;
+        ad_counters = (size_t)tiles;
+        tpart_bytes = (size_t)q.ad_split * tiles * 64 * 64 * 4;
+      }
+    }
   }
-  // workspace: [counters][T or U: M x r fp32][adapter partials][sparse partials]
-  const size_t ad_counters = r > 0 && q.ad_split > 1 ? (size_t)q.ad_tiles_m * q.ad_tiles_j : 0;
-  const size_t sp_counters = q.sp_split > 1 ? (size_t)(q.sp_row_tiles * q.sp_col_tiles) : 0;
-  q.n_counters = ad_counters + sp_counters;
+  // workspace: [counters][adapter intermediate fp16 M x r][adapter partials][sparse partials]
+  q.n_counters = ad_counters + (q.sp_split > 1 ? (size_t)q.sp_row_tiles : 0);
   q.sp_counter_base = ad_counters;
   q.off_counters = 0;
   if (q.n_counters > kCounterSlots) return SLIM_EUNSUPPORTED;
   // the counter region has a fixed size so that it stays at zero across calls with other sizes
   size_t off = kCounterSlots * 4;
   q.off_t = off;
-  off = round256(off + (size_t)M * (size_t)r * 4);
+  off = round256(off + (size_t)M * (size_t)r * 2);
   q.off_tpart = off;
-  if (r > 0 && q.ad_split > 1) off = round256(off + (size_t)q.ad_split * q.ad_tiles_m * q.ad_tiles_j * 64 * 64 * 4);
+  off = round256(off + tpart_bytes);
   q.off_ypart = off;
-  if (q.sp_split > 1)
-    off = round256(off + (size_t)q.sp_split * (size_t)(q.sp_row_tiles * q.sp_col_tiles) * q.sp_rows_tile *
-                             q.sp_cols_tile * 4);
+  off = round256(off + ypart_bytes);
   q.total = off;
   *p = q;
   return SLIM_OK;

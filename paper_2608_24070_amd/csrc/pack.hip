@@ -2,6 +2,7 @@
 // double-pruned backward pack (2:4 along N of the packed forward weight).
 #include "slim_device.h"
 #include "slim_host.h"
+#include "slim_timing.h"
 
 namespace {
 
@@ -216,7 +217,7 @@ extern "C" int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, u
     if (h_status & 1) rc = SLIM_ENONFINITE;
     else if (h_status & 2) rc = SLIM_ERANGE;
   } while (0);
-  hipFree(d_status);
+  (void)hipFree(d_status);
   return rc;
 }
 
@@ -226,6 +227,7 @@ extern "C" int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const ui
   int st = slim_check_pack_bwd(codes, meta, scales, N, K, codesT, metaT, scalesT, mask_rc);
   if (st != SLIM_OK) return st;
   dim3 grid((unsigned)(K / kBT), (unsigned)((N + kBT - 1) / kBT));
+  SlimKernelTimer timer("pack_bwd", (hipStream_t)stream);
   hipLaunchKernelGGL(k_pack_bwd, grid, dim3(256), 0, (hipStream_t)stream,
                      reinterpret_cast<const uint32_t*>(codes), reinterpret_cast<const uint16_t*>(meta), scales, N,
                      K, reinterpret_cast<uint32_t*>(codesT), reinterpret_cast<uint16_t*>(metaT), scalesT, mask_rc);

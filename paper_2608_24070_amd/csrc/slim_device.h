@@ -119,6 +119,44 @@ SLIM_DEV f16_t smfmac32(h8_t a, h16_t b, f16_t c, int idx, int abid) {
   return __builtin_amdgcn_smfmac_f32_32x32x32_f16(a, b, c, idx, 0, 1);
 }
 
+// ----------------------------------------------------------------------------------------------
+// Cross-block hand-off of partial tiles. The partials are stored and loaded with device-scope
+// relaxed atomic accesses (sc1), which are coherent across the XCDs' separate L2s by themselves,
+// so no L2-wide write-back or invalidate (what a device-scope fence costs) is needed. Before a
+// block bumps the tile counter, s_waitcnt(0) makes sure its partial stores have completed.
+// ----------------------------------------------------------------------------------------------
+SLIM_DEV void st_dev(float* p, float v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+SLIM_DEV float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+SLIM_DEV void drain_stores() { __builtin_amdgcn_s_waitcnt(0); }
+SLIM_DEV uint32_t counter_arrive(uint32_t* c) {
+  return __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+SLIM_DEV void counter_reset(uint32_t* c) { __hip_atomic_store(c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+
+SLIM_DEV f4_t mfma16(h8_t a, h8_t b, f4_t c) { return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0); }
+SLIM_DEV f16_t mfma32(h8_t a, h8_t b, f16_t c) { return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0); }
+
+SLIM_DEV h8_t zero_h8() {
+  h8_t z;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) z[e] = (_Float16)0.0f;
+  return z;
+}
+
+SLIM_DEV h8_t mul_h8(h8_t x, h8_t s) {
+  h8_t r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    h2_t a = {x[2 * i], x[2 * i + 1]}, b = {s[2 * i], s[2 * i + 1]};
+    a = a * b;
+    r[2 * i] = a[0];
+    r[2 * i + 1] = a[1];
+  }
+  return r;
+}
+
 SLIM_DEV h16_t cat16(h8_t lo, h8_t hi) {
   h16_t r;
 #pragma unroll

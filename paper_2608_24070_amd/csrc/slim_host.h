@@ -4,10 +4,12 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/slim.h"
+#include "slim.h"
 
 // Completion counters live in a fixed-size region at the start of the workspace.
 #define SLIM_COUNTER_SLOTS 4096
+// Reduction positions per adapter first-product unit of the small-M path.
+#define SLIM_DECODE_AD_SLICE 256
 
 // Argument checks: pure host functions, run before anything is enqueued.
 int slim_check_pack(const float* W, int64_t N, int64_t K, const void* codes, const void* meta,
@@ -19,7 +21,8 @@ int slim_check_pack_bwd(const void* codes, const void* meta, const void* scales,
 struct SlimPlan {
   // dense adapter GEMM (T = X L forward, U = dY R^T backward)
   int ad_tiles_m = 0, ad_tiles_j = 0, ad_split = 1;
-  int64_t ad_slice = 0;               // reduction length per split (multiple of 64)
+  int64_t ad_slice = 0;               // reduction length per split
+  int64_t ad_jblocks = 0;             // small-M path: 64-wide blocks of the adapter rank
   // sparse contraction
   bool decode = false;                // small-M kernel (16-column MFMA tiles, split reduction)
   int dec_fm = 1;                     // 16-column fragments per wave in the small-M kernel

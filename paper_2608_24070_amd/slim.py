@@ -35,6 +35,9 @@ _SIGS = {
                                    _c_p, _c_p, ctypes.c_size_t, _c_p]),
     "slim_linear_bwd_dx": (ctypes.c_int, [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p,
                                           _c_i64, _c_p, _c_p, ctypes.c_size_t, _c_p]),
+    "slim_timing_enable": (ctypes.c_int, [ctypes.c_int]),
+    "slim_timing_reset": (ctypes.c_int, []),
+    "slim_timing_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_size_t]),
 }
 
 _lib = None
@@ -116,6 +119,26 @@ def slim_linear(X, xdtype, M, N, K, codes, meta, scales, L, R, r, Y, ws, ws_byte
 
 def slim_linear_bwd_dx(dY, dydtype, M, N, K, codesT, metaT, scalesT, L, R, r, dX, ws, ws_bytes, stream) -> int:
     return lib().slim_linear_bwd_dx(dY, dydtype, M, N, K, codesT, metaT, scalesT, L, R, r, dX, ws, ws_bytes, stream)
+
+
+def slim_timing_enable(on: bool) -> int:
+    return lib().slim_timing_enable(1 if on else 0)
+
+
+def slim_timing_reset() -> int:
+    return lib().slim_timing_reset()
+
+
+def slim_timing_read() -> dict:
+    """{kernel name: (launches, total_ms)} since the last reset (waits for recorded events)."""
+    need = lib().slim_timing_read(None, 0)
+    buf = ctypes.create_string_buffer(max(need, 1) + 256)
+    lib().slim_timing_read(buf, len(buf))
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, n, ms = line.split()
+        out[name] = (int(n), float(ms))
+    return out
 
 
 # ------------------------------------------------------------------ tensor helpers

@@ -14,7 +14,8 @@ def test_library_exports_every_declared_symbol():
     lib = slim.lib()
     syms = slim.header_symbols()
     assert {"slim_pack", "slim_pack_bwd", "slim_linear", "slim_linear_bwd_dx", "slim_linear_workspace",
-            "slim_bwd_dx_workspace", "slim_workspace_init", "slim_status_string", "slim_abi_version"} <= set(syms)
+            "slim_bwd_dx_workspace", "slim_workspace_init", "slim_status_string", "slim_abi_version",
+            "slim_timing_enable", "slim_timing_reset", "slim_timing_read"} <= set(syms)
     for name in syms:
         assert hasattr(lib, name), name
 
