@@ -94,7 +94,8 @@ def main():
         torch.cuda.synchronize()
         pack_ms += (time.perf_counter() - tp) * 1e3
         del W
-        per_layer.append({"layer": ly, "pack": p, "L": dev_bits(Lb, torch.float16), "R": dev_bits(Rb, torch.float16)})
+        ad = slim.pack_adapter(dev_bits(Lb, torch.float16), dev_bits(Rb, torch.float16))
+        per_layer.append({"layer": ly, "pack": p, "L": ad["L"], "R": ad["R"], "Lt": ad["Lt"], "Rt": ad["Rt"]})
     # activations: q/k/v/gate/up of the block share X; o and down get their own
     acts = {}
     for ly in layers:
@@ -117,11 +118,15 @@ def main():
     for c in range(n_copies):
         cp = []
         for pl in per_layer:
+            if bwd:
+                ad = {"L": pl["L"], "R": pl["R"]}
+            else:
+                ad = {"Lt": pl["Lt"], "Rt": pl["Rt"]}
             if c == 0:
-                cp.append({"pack": pl["pack"], "L": pl["L"], "R": pl["R"]})
+                cp.append({"pack": pl["pack"], "ad": ad})
             else:
                 cp.append({"pack": {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in pl["pack"].items()},
-                           "L": pl["L"].clone(), "R": pl["R"].clone()})
+                           "ad": {k: v.clone() for k, v in ad.items()}})
         copies.append(cp)
     ws_need = max((slim.slim_bwd_dx_workspace if bwd else slim.slim_linear_workspace)(
         M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
@@ -133,9 +138,9 @@ def main():
         cp = copies[i % n_copies]
         for pl, c in zip(per_layer, cp):
             if bwd:
-                slim.bwd_dx(pl["x"], c["pack"], c["L"], c["R"], out=pl["out"], ws=ws)
+                slim.bwd_dx(pl["x"], c["pack"], c["ad"]["L"], c["ad"]["R"], out=pl["out"], ws=ws)
             else:
-                slim.linear(pl["x"], c["pack"], c["L"], c["R"], out=pl["out"], ws=ws)
+                slim.linear(pl["x"], c["pack"], c["ad"], out=pl["out"], ws=ws)
 
     # ------------------------------------------------------------------ timed region
     # The stream is first given a bounded busy kernel (torch.cuda._sleep) long enough for the host

@@ -123,6 +123,20 @@ int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const uint16_t* sca
                   void* stream);
 
 /*
+ * slim_pack_adapter - one-time layout of the adapter factors for slim_linear.
+ * Thesis: the rank-r adapter W ~ W^C + L R (SLiM "SLiM-LoRA low-rank adapters"); like the weight
+ * pack, this runs once per layer. The forward consumes both factors along their rank
+ * dimension, so it takes them transposed; the backward (slim_linear_bwd_dx) takes L and R as given.
+ *
+ *   L    fp16 [K, r], device.     R    fp16 [r, N], device.
+ *   K, N >= 1; r >= 16, r % 16 == 0.
+ *   Lt   out, fp16 [r, K] = L^T.  Rt   out, fp16 [N, r] = R^T.
+ * Asynchronous on `stream`; a pure data movement (bit-exact).
+ */
+int slim_pack_adapter(const uint16_t* L, const uint16_t* R, int64_t K, int64_t N, int64_t r, uint16_t* Lt,
+                      uint16_t* Rt, void* stream);
+
+/*
  * slim_linear_workspace - bytes of device workspace slim_linear needs for these sizes
  * (written to *bytes, host pointer). Depends only on the sizes. Pure host function.
  */
@@ -145,20 +159,21 @@ int slim_workspace_init(void* ws, size_t ws_bytes, void* stream);
  * with the adapter as a parallel path; the adapter product is fused into the same kernels.
  *
  *   X       [M, K] in `xdtype` (SLIM_BF16 or SLIM_F16), device.
- *   M, N, K M >= 1, N >= 1, K % 128 == 0.
+ *   M, N, K M >= 1, N >= 16, N % 16 == 0, K % 128 == 0.
  *   codes, meta, scales   forward pack of W (slim_pack).
- *   L, R    fp16 [K, r] and [r, N]; both NULL when r == 0. r % 16 == 0.
+ *   Lt, Rt  the adapter from slim_pack_adapter: fp16 [r, K] = L^T and [N, r] = R^T; both NULL when
+ *           r == 0. r % 16 == 0.
  *   Y       out, fp32 [M, N]. Must not alias any input.
  *   ws      device workspace of at least slim_linear_workspace(M, N, K, r) bytes, zeroed once
  *           with slim_workspace_init before its first use. Two calls that overlap in time must
  *           not share a workspace.
  * Operand precision: bf16 activations are converted to fp16 (exact for |x| in
  * [2^-14, 65504]); dequantised weights are (u-8)*s16 rounded to fp16; the adapter intermediate
- * X*L is kept in fp32 and rounded to fp16 for the second product. Deterministic: identical
- * inputs give identical bits.
+ * X*L is accumulated in fp32 and rounded to fp16 for the second product. Deterministic:
+ * identical inputs give identical bits.
  */
 int slim_linear(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const uint8_t* codes,
-                const uint8_t* meta, const uint16_t* scales, const uint16_t* L, const uint16_t* R,
+                const uint8_t* meta, const uint16_t* scales, const uint16_t* Lt, const uint16_t* Rt,
                 int64_t r, float* Y, void* ws, size_t ws_bytes, void* stream);
 
 /*

@@ -1,6 +1,7 @@
 // adapter_gemm.hip - the adapter's first, reducing product for large M:
-//   forward   T = X L        (X [M, K] activations, L [K, r] fp16, "NN")
-//   backward  U = dY R^T     (dY [M, N],           R [r, N] fp16, "NT")
+//   tm = act Q^T with act [M, red] (bf16/fp16) and Q [r, red] fp16 row-major:
+//   forward  T = X L      (Q = L^T, from slim_pack_adapter)
+//   backward U = dY R^T   (Q = R as given)
 // Result fp16 [M, r] (it only feeds the fp16 MFMA of the second product). 64 x 64 output tiles
 // on 16x16x32 fp16 MFMA, 64-wide reduction stages double-buffered in LDS and staged through
 // registers one stage ahead. The reduction may be split across blocks; the last block of a tile
@@ -15,13 +16,12 @@ constexpr int kT = 64;      // output tile edge (m and j)
 constexpr int kBK = 64;     // reduction per stage
 constexpr int kLd = kBK + 8;
 
-template <bool NT>
 __global__ void __launch_bounds__(256)
 k_adapter_gemm(const uint16_t* __restrict__ A, int a_bf16, int64_t M, int64_t Kd, const uint16_t* __restrict__ Bsrc,
                int64_t r, int64_t slice, int split, uint16_t* __restrict__ out, float* __restrict__ part,
                uint32_t* __restrict__ counters) {
   __shared__ __attribute__((aligned(16))) _Float16 As[2][kT][kLd];
-  __shared__ __attribute__((aligned(16))) _Float16 Bs[2][kT][kLd];   // NT: [j][k]; NN: [k][j]
+  __shared__ __attribute__((aligned(16))) _Float16 Bs[2][kT][kLd];   // [j][k]
   __shared__ int last_flag;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wj = wave >> 1;
@@ -32,7 +32,10 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int a_bf16, int64_t M, int64_t Kd
   const int nst = (int)((kend - kbeg + kBK - 1) / kBK);
   const bool bf16 = a_bf16 != 0;
 
+  // loads are unconditional from clamped addresses; out-of-range elements are zeroed when stored
+  // to LDS (a conditional load would make the compiler wait for it at the branch join)
   u32x4_t ar[2], br[2];
+  bool aok[2], bok[2];
   auto load = [&](int t) {
     const int64_t k = kbeg + (int64_t)t * kBK;
 #pragma unroll
@@ -41,16 +44,14 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int a_bf16, int64_t M, int64_t Kd
       {  // A tile: 64 rows of m x 8 vectors
         const int row = q >> 3, kc = q & 7;
         const int64_t gm = m0 + row, gk = k + 8 * kc;
-        ar[i] = (gm < M && gk < kend) ? *reinterpret_cast<const u32x4_t*>(A + gm * Kd + gk) : u32x4_t{0u, 0u, 0u, 0u};
+        aok[i] = gm < M && gk < kend;
+        ar[i] = *reinterpret_cast<const u32x4_t*>(A + (gm < M ? gm : M - 1) * Kd + (gk < kend ? gk : kend - 8));
       }
-      if (NT) {  // R [r, Kd]: row j contiguous along k
+      {  // Q [r, Kd]: row j contiguous along k
         const int jr = q >> 3, kc = q & 7;
         const int64_t gj = j0 + jr, gk = k + 8 * kc;
-        br[i] = (gj < r && gk < kend) ? *reinterpret_cast<const u32x4_t*>(Bsrc + gj * Kd + gk) : u32x4_t{0u, 0u, 0u, 0u};
-      } else {   // L [Kd, r]: row k contiguous along j
-        const int kr = q >> 3, jc = q & 7;
-        const int64_t gk = k + kr, gj = j0 + 8 * jc;
-        br[i] = (gk < kend && gj < r) ? *reinterpret_cast<const u32x4_t*>(Bsrc + gk * r + gj) : u32x4_t{0u, 0u, 0u, 0u};
+        bok[i] = gj < r && gk < kend;
+        br[i] = *reinterpret_cast<const u32x4_t*>(Bsrc + (gj < r ? gj : r - 1) * Kd + (gk < kend ? gk : kend - 8));
       }
     }
   };
@@ -58,8 +59,8 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int a_bf16, int64_t M, int64_t Kd
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int q = tid + 256 * i;
-      *reinterpret_cast<h8_t*>(&As[buf][q >> 3][8 * (q & 7)]) = load8_as_h(ar[i], bf16);
-      *reinterpret_cast<u32x4_t*>(&Bs[buf][q >> 3][8 * (q & 7)]) = br[i];
+      *reinterpret_cast<h8_t*>(&As[buf][q >> 3][8 * (q & 7)]) = aok[i] ? load8_as_h(ar[i], bf16) : zero_h8();
+      *reinterpret_cast<u32x4_t*>(&Bs[buf][q >> 3][8 * (q & 7)]) = bok[i] ? br[i] : u32x4_t{0u, 0u, 0u, 0u};
     }
   };
 
@@ -83,13 +84,7 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int a_bf16, int64_t M, int64_t Kd
 #pragma unroll
       for (int f = 0; f < 2; ++f) {
         af[f] = *reinterpret_cast<const h8_t*>(&As[buf][32 * wm + 16 * f + (lane & 15)][kk + 8 * g]);
-        const int jc = 32 * wj + 16 * f + (lane & 15);
-        if (NT) {
-          bf[f] = *reinterpret_cast<const h8_t*>(&Bs[buf][jc][kk + 8 * g]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) bf[f][e] = Bs[buf][kk + 8 * g + e][jc];
-        }
+        bf[f] = *reinterpret_cast<const h8_t*>(&Bs[buf][32 * wj + 16 * f + (lane & 15)][kk + 8 * g]);
       }
 #pragma unroll
       for (int x = 0; x < 2; ++x)
@@ -145,18 +140,14 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int a_bf16, int64_t M, int64_t Kd
 
 }  // namespace
 
-int slim_launch_adapter_gemm(bool nt, const uint16_t* A, int a_bf16, int64_t M, int64_t Kd, const uint16_t* B,
-                             int64_t r, const SlimPlan& p, char* ws, hipStream_t s) {
+int slim_launch_adapter_gemm(const uint16_t* A, int a_bf16, int64_t M, int64_t Kd, const uint16_t* Q, int64_t r,
+                             const SlimPlan& p, char* ws, hipStream_t s) {
   dim3 grid((unsigned)p.ad_tiles_m, (unsigned)p.ad_tiles_j, (unsigned)p.ad_split);
   uint16_t* out = reinterpret_cast<uint16_t*>(ws + p.off_t);
   float* part = reinterpret_cast<float*>(ws + p.off_tpart);
   uint32_t* counters = reinterpret_cast<uint32_t*>(ws + p.off_counters);
-  SlimKernelTimer timer(nt ? "adapter_gemm_nt" : "adapter_gemm_nn", s);
-  if (nt)
-    hipLaunchKernelGGL(k_adapter_gemm<true>, grid, dim3(256), 0, s, A, a_bf16, M, Kd, B, r, p.ad_slice, p.ad_split,
-                       out, part, counters);
-  else
-    hipLaunchKernelGGL(k_adapter_gemm<false>, grid, dim3(256), 0, s, A, a_bf16, M, Kd, B, r, p.ad_slice, p.ad_split,
-                       out, part, counters);
+  SlimKernelTimer timer("adapter_gemm", s);
+  hipLaunchKernelGGL(k_adapter_gemm, grid, dim3(256), 0, s, A, a_bf16, M, Kd, Q, r, p.ad_slice, p.ad_split, out, part,
+                     counters);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }

@@ -61,22 +61,21 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
   const int64_t nchunks = red / 128;
   SlimPlan q;
   size_t ad_counters = 0, tpart_bytes = 0, ypart_bytes = 0;
-  if (M <= 64) {
+  if (M <= 32) {
     // small M: one launch of split-reduction sparse units plus adapter first-product units,
     // then the adapter's second product
     q.decode = true;
-    q.dec_fm = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+    q.dec_fm = M <= 16 ? 1 : 2;
     const int64_t mc = 16 * q.dec_fm;
     q.sp_rows_tile = 64;
     q.sp_cols_tile = (int)mc;
     q.sp_row_tiles = cdiv(rows, 64);
     q.sp_col_tiles = 1;
-    // staged activations [mc x (cps*128 + 8)] fp16 within 56 KB of LDS
-    const int64_t max_cps = std::max<int64_t>(1, (57344 / (2 * mc) - 8) / 128);
-    const int64_t want = std::max<int64_t>(1, 512 / q.sp_row_tiles);    // ~512 sparse blocks
-    const int64_t cps = std::min<int64_t>(max_cps, std::max<int64_t>(1, cdiv(nchunks, want)));
-    q.sp_chunks_per_split = cps;
-    q.sp_split = (int)cdiv(nchunks, cps);
+    // a sparse unit covers 4 * G quantisation groups of the reduction; two groups per lane group
+    // when that still gives every CU a unit
+    q.dec_g = (q.dec_fm == 1 && q.sp_row_tiles * cdiv(nchunks, 8) >= 256) ? 2 : 1;
+    q.sp_chunks_per_split = 4 * q.dec_g;
+    q.sp_split = (int)cdiv(nchunks, q.sp_chunks_per_split);
     if (q.sp_split > 1 && q.sp_row_tiles > (int64_t)(kCounterSlots / 2)) return SLIM_EUNSUPPORTED;
     if (r > 0) {
       q.ad_jblocks = cdiv(r, 64);
@@ -87,10 +86,8 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
         tpart_bytes = (size_t)q.ad_jblocks * q.ad_split * 4 * q.dec_fm * 256 * 4;
       }
     }
-    if (q.sp_split > 1) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 64 * mc * 4;
-    const size_t lds_w = (size_t)mc * (size_t)(cps * 128 + 8) * 2;
-    const size_t lds_a = (r > 0 && !bwd) ? (size_t)kDecodeAdSlice * (64 + 8) * 2 : 0;
-    q.lds_bytes = std::max(lds_w, lds_a);
+    if (q.sp_split > 1) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 4 * q.dec_fm * 256 * 4;
+    q.lds_bytes = 0;
   } else {
     // large M: dense adapter GEMM (64 x 64 tiles) then 256 x 128 sparse tiles
     q.decode = false;

@@ -193,7 +193,41 @@ k_pack_bwd(const uint32_t* __restrict__ codes, const uint16_t* __restrict__ meta
   if ((k0 & 127) == 0 && tid < rows) scalesT[(k0 >> 7) * N + n0 + tid] = scales[(n0 + tid) * (K / 128) + (k0 >> 7)];
 }
 
+// fp16 transpose out[c][r] = in[r][c] of a row-major [R x C] matrix, through a 64 x 64 LDS tile.
+__global__ void __launch_bounds__(256)
+k_transpose16(const uint16_t* __restrict__ in, int64_t R, int64_t C, uint16_t* __restrict__ out) {
+  __shared__ uint16_t t[64][66];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int rr = ty + 4 * i;
+    if (r0 + rr < R && c0 + tx < C) t[rr][tx] = in[(r0 + rr) * C + c0 + tx];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int cc = ty + 4 * i;
+    if (c0 + cc < C && r0 + tx < R) out[(c0 + cc) * R + r0 + tx] = t[tx][cc];
+  }
+}
+
 }  // namespace
+
+extern "C" int slim_pack_adapter(const uint16_t* L, const uint16_t* R, int64_t K, int64_t N, int64_t r, uint16_t* Lt,
+                                 uint16_t* Rt, void* stream) {
+  if (!L || !R || !Lt || !Rt) return SLIM_EINVAL;
+  if (K < 1 || N < 1 || r < 16 || r % 16 || K >= (int64_t(1) << 31) || N >= (int64_t(1) << 31) || r >= 65536)
+    return SLIM_ESHAPE;
+  if (!slim_aligned16(L) || !slim_aligned16(R) || !slim_aligned16(Lt) || !slim_aligned16(Rt)) return SLIM_EALIGN;
+  hipStream_t s = (hipStream_t)stream;
+  SlimKernelTimer timer("pack_adapter", s);
+  hipLaunchKernelGGL(k_transpose16, dim3((unsigned)((r + 63) / 64), (unsigned)((K + 63) / 64)), dim3(256), 0, s, L, K, r,
+                     Lt);
+  hipLaunchKernelGGL(k_transpose16, dim3((unsigned)((N + 63) / 64), (unsigned)((r + 63) / 64)), dim3(256), 0, s, R, r, N,
+                     Rt);
+  return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
+}
 
 extern "C" int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, uint8_t* meta,
                          uint16_t* scales, uint8_t* mask, void* stream) {

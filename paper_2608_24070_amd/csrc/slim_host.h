@@ -26,11 +26,12 @@ struct SlimPlan {
   // sparse contraction
   bool decode = false;                // small-M kernel (16-column MFMA tiles, split reduction)
   int dec_fm = 1;                     // 16-column fragments per wave in the small-M kernel
+  int dec_g = 1;                      // quantisation groups per lane group in a small-M sparse unit
   int sp_rows_tile = 0, sp_cols_tile = 0;  // output tile (rows of W or W^T, columns = M)
   int64_t sp_row_tiles = 0, sp_col_tiles = 0;
   int sp_split = 1;                   // reduction splits (small-M kernel only)
   int64_t sp_chunks_per_split = 0;    // 128-wide chunks per split
-  size_t lds_bytes = 0;               // dynamic LDS of the sparse kernel
+  size_t lds_bytes = 0;               // dynamic LDS (unused: the kernels size their LDS statically)
   // workspace layout (byte offsets)
   size_t off_counters = 0, n_counters = 0, sp_counter_base = 0;
   size_t off_t = 0, off_tpart = 0, off_ypart = 0, total = 0;

@@ -5,6 +5,6 @@
 
 #include "slim_host.h"
 
-// T = A B (nt == false: B is [Kd, r]) or T = A B^T (nt == true: B is [r, Kd]); fp16 result at ws + p.off_t.
-int slim_launch_adapter_gemm(bool nt, const uint16_t* A, int a_bf16, int64_t M, int64_t Kd, const uint16_t* B,
-                             int64_t r, const SlimPlan& p, char* ws, hipStream_t s);
+// tm = A Q^T: A [M, Kd] activations, Q [r, Kd] fp16 row-major; fp16 result [M, r] at ws + p.off_t.
+int slim_launch_adapter_gemm(const uint16_t* A, int a_bf16, int64_t M, int64_t Kd, const uint16_t* Q, int64_t r,
+                             const SlimPlan& p, char* ws, hipStream_t s);

@@ -4,10 +4,13 @@
 //   forward   Y[m, n]  = sum_k X[m, k] Wc[n, k]          + sum_j T[m, j] R[j, n],   T = X L
 //   backward  dX[m, k] = sum_n dY[m, n] W^{R,C}[n, k]    + sum_j U[m, j] L[k, j],   U = dY R^T
 //
-// Both are "out[m, row] = sum_red act[m, red] A[row, red] + sum_j tm[m, j] ap(row, j)" with A the
-// packed sparse operand (rows = N, red = K forward; rows = K, red = N backward). Packed code
-// words feed the sparse MFMA's compressed A operand directly; activations are the dense B
-// operand as fp16. Accumulators hold out^T tiles (rows x m).
+// Both have the form
+//   out[m, row] = sum_red act[m, red] A[row, red] + sum_j tm[m, j] P[row, j],  tm[m, j] = sum_red act[m, red] Q[j, red]
+// with A the packed sparse operand (rows = N, red = K forward; rows = K, red = N backward) and the
+// adapter factors in row-major [r x red] (Q) and [rows x r] (P) form: forward Q = L^T and P = R^T
+// (from slim_pack_adapter), backward Q = R and P = L as given. Packed code words feed the sparse
+// MFMA's compressed A operand directly; activations are the dense B operand as fp16; the
+// accumulators hold out^T tiles (rows x m).
 //
 // Scales: forward, s16[n, k/128] varies along the output row and is applied while dequantising
 // (fp16 product). Backward, s16[n, k/128] varies along the reduction n, so it multiplies the
@@ -15,15 +18,17 @@
 // enter the MFMA as exact integers.
 //
 // Two paths, chosen by the number of activation rows M:
-//  * small M (<= 64, decode): k_decode splits the reduction across blocks so that every CU
-//    streams a slice of the packed weight; the same launch also computes the adapter's first
-//    product (X L, or dY R^T) as extra blocks (the two products share the activations, as in
-//    SLoPe's concatenated adapter). Split partials are reduced by the last block of each tile
-//    in a fixed order. k_adapter_out then adds the adapter's second product.
-//  * large M (prefill/training): the adapter's first product runs as a dense GEMM
-//    (adapter_gemm.hip), then k_tile computes 256 x 128 output tiles on 32x32x32 sparse MFMA
-//    with a double-buffered LDS activation tile and adds the second adapter product in its
-//    epilogue.
+//  * small M (<= 32, decode): k_decode splits the reduction across blocks so that every CU
+//    streams a slice of the packed weight; the same launch computes the adapter's first product
+//    in extra blocks (the two products share the activations, as in SLoPe's concatenated
+//    adapter). Split partials are summed by the last block of each tile in a fixed order.
+//    k_adapter_out then adds the adapter's second product.
+//  * large M: the adapter's first product runs as a dense GEMM (adapter_gemm.hip); k_tile then
+//    computes 256 x 128 output tiles on 32x32x32 sparse MFMA with a double-buffered LDS
+//    activation tile and adds the second adapter product in its epilogue.
+// Every global load is issued unconditionally from a clamped, valid address and masked when
+// used: a load under a branch makes the compiler wait for it at the join, which serialises
+// what should be one round of memory traffic.
 #include "slim_device.h"
 #include "slim_launch.h"
 #include "slim_timing.h"
@@ -38,16 +43,14 @@ struct LayerArgs {
   int act_bf16;
   int64_t M, rows, red;
   int64_t r;
-  const uint16_t* ad_in;   // first adapter factor: forward L [red, r]; backward R [r, red]
-  const uint16_t* ad_out;  // second adapter factor: forward R [r, rows]; backward L [rows, r]
-  uint16_t* tm;            // fp16 [M, r] adapter intermediate (T forward, U backward)
+  const uint16_t* ad_q;    // adapter first factor, row-major [r, red]
+  const uint16_t* ad_p;    // adapter second factor, row-major [rows, r]
+  uint16_t* tm;            // fp16 [M, r] adapter intermediate
   float* out;              // [M, rows]
   // small-M path
   int split;               // reduction splits of the sparse product
-  int64_t cps;             // 128-wide chunks per split
   int64_t row_tiles;       // 64-row tiles
   int ad_split;            // reduction splits of the adapter's first product
-  int64_t ad_slice;        // reduction positions per adapter split
   int64_t ad_jblocks;      // 64-wide column blocks of the adapter rank
   float* part;             // sparse split partials
   float* tpart;            // adapter split partials
@@ -55,12 +58,8 @@ struct LayerArgs {
   uint32_t* tcounters;     // per adapter column block
 };
 
-constexpr int kMaxChunks = 16;   // the plan keeps cps <= 13 and FM * cps <= 16
-
 SLIM_DEV u32x4_t zero_u4() { return u32x4_t{0u, 0u, 0u, 0u}; }
-
-// fp16 eight-vector from 16-bit activation bits (bf16 -> fp16 through fp32).
-SLIM_DEV h8_t act8(u32x4_t v, bool bf16) { return load8_as_h(v, bf16); }
+SLIM_DEV int64_t clamp_hi(int64_t x, int64_t hi) { return x < hi ? x : hi; }
 
 // bits of eight fp16 scales times eight activations (backward fold), rounded once to fp16.
 SLIM_DEV h8_t act8_scaled(u32x4_t v, u32x4_t sv, bool bf16) {
@@ -73,115 +72,125 @@ SLIM_DEV h8_t act8_scaled(u32x4_t v, u32x4_t sv, bool bf16) {
   return h;
 }
 
+// Reduce split partials of one tile: every block stores its FM x 4 accumulator values per lane
+// (device scope), the last one to arrive sums all S partials in split order.
+template <int FM>
+SLIM_DEV bool split_reduce(f4_t* acc, float* part_tile, int S, int s, uint32_t* counter, int* last_flag) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int kPer = FM * 256;                    // floats per wave per split
+  float* dst = part_tile + ((int64_t)s * 4 + wave) * kPer;
+#pragma unroll
+  for (int f = 0; f < FM; ++f)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) st_dev(dst + (f * 4 + v) * 64 + lane, acc[f][v]);
+  drain_stores();
+  __syncthreads();
+  if (tid == 0) *last_flag = counter_arrive(counter) == (uint32_t)(S - 1);
+  __syncthreads();
+  if (!*last_flag) return false;
+#pragma unroll
+  for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+  const float* src = part_tile + (int64_t)wave * kPer;
+  for (int s0 = 0; s0 < S; s0 += 8) {
+    float pv[8][FM * 4];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int ss = s0 + j < S ? s0 + j : S - 1;
+#pragma unroll
+      for (int e = 0; e < FM * 4; ++e) pv[j][e] = ld_dev(src + (int64_t)ss * 4 * kPer + e * 64 + lane);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (s0 + j < S)
+#pragma unroll
+        for (int e = 0; e < FM * 4; ++e) acc[e >> 2][e & 3] += pv[j][e];
+  }
+  if (tid == 0) counter_reset(counter);
+  return true;
+}
+
 // ============================================================ small-M: sparse split units
-template <bool BWD, int FM>
+// Unit = 64 rows (16 per wave) x one slice of 4G quantisation groups. Lane group qa (lane / 16)
+// of the 16x16x64 sparse MFMA owns G whole groups, so its code words (32 B per group), index
+// words (16 B) and scales are contiguous: 4G loads per lane for the whole slice.
+template <bool BWD, int FM, int G>
 SLIM_DEV void decode_sparse_unit(const LayerArgs& a, int64_t u, _Float16* xs, int* last_flag) {
   constexpr int MC = 16 * FM;
+  constexpr int SL = 512 * G;              // reduction positions per slice
+  constexpr int LDX = SL + 8;
+  constexpr int VPR = SL / 8;              // 16-byte activation vectors per row of the slice
+  constexpr int XV = MC * VPR / 256;       // ... per thread
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int S = a.split;
   const int64_t rt = u / S;
   const int s = (int)(u - rt * S);
   const int64_t row0 = rt * 64;
-  const int64_t c_beg = (int64_t)s * a.cps;
-  const int nch = (int)min(a.cps, a.red / 128 - c_beg);
-  const int ldx = (int)a.cps * 128 + 8;
-  const int64_t red0 = c_beg * 128;
+  const int64_t nchunks = a.red / 128;
+  const int64_t c0 = (int64_t)s * 4 * G;
+  const int64_t red0 = c0 * 128;
   const bool bf16 = a.act_bf16 != 0;
 
-  // 1. packed words of every chunk of the slice, and the activation slice: one round of loads
-  const int64_t arow = row0 + 16 * wave + (lane & 15);
-  const int64_t lrow = arow < a.rows ? arow : a.rows - 1;
+  const int64_t lrow = clamp_hi(row0 + 16 * wave + (lane & 15), a.rows - 1);
   const int qa = lane >> 4;
-  const uint32_t* cp = a.codes + lrow * (a.red / 16) + c_beg * 8 + 2 * qa;
-  const uint32_t* mp = a.meta + lrow * (a.red / 32) + c_beg * 4 + qa;
-  const uint16_t* sp = a.scales + lrow * (a.red / 128) + c_beg;
-  u32x2_t cw[kMaxChunks];
-  uint32_t mw[kMaxChunks], sw[kMaxChunks];
+  const int64_t cl = c0 + (int64_t)qa * G;      // first chunk (group) of this lane group
+  u32x4_t cw[2 * G], mw[G];
+  uint32_t sw[G];
 #pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i) {
-    if (i < nch) {
-      cw[i] = *reinterpret_cast<const u32x2_t*>(cp + 8 * i);
-      mw[i] = mp[4 * i];
-      sw[i] = BWD ? 0u : (uint32_t)sp[i];
-    }
+  for (int gi = 0; gi < G; ++gi) {
+    const int64_t ch = clamp_hi(cl + gi, nchunks - 1);
+    const uint32_t* cp = a.codes + lrow * (a.red / 16) + ch * 8;
+    cw[2 * gi] = *reinterpret_cast<const u32x4_t*>(cp);
+    cw[2 * gi + 1] = *reinterpret_cast<const u32x4_t*>(cp + 4);
+    mw[gi] = *reinterpret_cast<const u32x4_t*>(a.meta + lrow * (a.red / 32) + ch * 4);
+    sw[gi] = BWD ? 0u : (uint32_t)a.scales[lrow * (a.red / 128) + ch];
   }
-  const int vpr = nch * 16;          // 16-byte activation vectors per row of the slice
-  const int nvec = MC * vpr;         // at most 256 * kMaxChunks
   const int64_t sgroup = row0 / 128;
-  u32x4_t xv[kMaxChunks], sv[kMaxChunks];
+  u32x4_t xv[XV], sv[XV];
 #pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i) {
-    const int q = tid + 256 * i;
-    if (q < nvec) {
-      const int m = q / vpr, vc = q - m * vpr;
-      xv[i] = m < a.M ? *reinterpret_cast<const u32x4_t*>(a.act + m * a.red + red0 + 8 * vc) : zero_u4();
-      if (BWD) sv[i] = *reinterpret_cast<const u32x4_t*>(a.scales + sgroup * a.red + red0 + 8 * vc);
-    }
+  for (int i = 0; i < XV; ++i) {
+    const int q = tid + 256 * i, m = q / VPR, vc = q % VPR;
+    const int64_t pos = clamp_hi(red0 + 8 * vc, a.red - 8);
+    xv[i] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(m, a.M - 1) * a.red + pos);
+    if (BWD) sv[i] = *reinterpret_cast<const u32x4_t*>(a.scales + sgroup * a.red + pos);
   }
 #pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i) {
-    const int q = tid + 256 * i;
-    if (q < nvec) {
-      const int m = q / vpr, vc = q - m * vpr;
-      *reinterpret_cast<h8_t*>(&xs[m * ldx + 8 * vc]) = BWD ? act8_scaled(xv[i], sv[i], bf16) : act8(xv[i], bf16);
-    }
+  for (int i = 0; i < XV; ++i) {
+    const int q = tid + 256 * i, m = q / VPR, vc = q % VPR;
+    const bool ok = m < a.M && red0 + 8 * vc < a.red;
+    const h8_t h = BWD ? act8_scaled(xv[i], sv[i], bf16) : load8_as_h(xv[i], bf16);
+    *reinterpret_cast<h8_t*>(&xs[m * LDX + 8 * vc]) = ok ? h : zero_h8();
   }
   __syncthreads();
 
-  // 2. contraction: 16 rows per wave, FM 16-column fragments, two 16x16x64 steps per chunk
   f4_t acc[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+  const int qb = lane >> 4;
+  const int pbase = 128 * G * (qb >> 1) + 8 * (qb & 1);
 #pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i) {
-    if (i < nch) {
-      const h2_t s2 = splat_h2(sw[i]);
+  for (int gi = 0; gi < G; ++gi) {
+    const bool gok = cl + gi < nchunks;
+    const h2_t s2 = splat_h2(sw[gi]);
 #pragma unroll
-      for (int st = 0; st < 2; ++st) {
-        const h8_t av = BWD ? dequant_word_int(cw[i][st]) : dequant_word(cw[i][st], s2);
-        const int off = i * 128 + b_chunk_offset<16>(lane, st);
+    for (int t4 = 0; t4 < 8; ++t4) {
+      const uint32_t word = cw[2 * gi + (t4 >> 2)][t4 & 3];
+      h8_t av = BWD ? dequant_word_int(word) : dequant_word(word, s2);
+      av = gok ? av : zero_h8();
+      const int idx = (int)mw[gi][t4 >> 1];
+      const int p0 = pbase + 16 * (8 * gi + t4);
 #pragma unroll
-        for (int f = 0; f < FM; ++f) {
-          const _Float16* xr = xs + (16 * f + (lane & 15)) * ldx + off;
-          acc[f] = smfmac16(av, cat16(*reinterpret_cast<const h8_t*>(xr), *reinterpret_cast<const h8_t*>(xr + 64)),
-                            acc[f], (int)mw[i], st);
-        }
+      for (int f = 0; f < FM; ++f) {
+        const _Float16* xr = xs + (16 * f + (lane & 15)) * LDX + p0;
+        acc[f] = smfmac16(av, cat16(*reinterpret_cast<const h8_t*>(xr), *reinterpret_cast<const h8_t*>(xr + 256 * G)),
+                          acc[f], idx, t4 & 1);
       }
     }
   }
 
-  // 3. split reduction: the last block of the row tile sums the partials in split order
-  if (S > 1) {
-    float* dst = a.part + ((rt * S + s) * 4 + wave) * (FM * 256);
-#pragma unroll
-    for (int f = 0; f < FM; ++f)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) st_dev(dst + (f * 4 + v) * 64 + lane, acc[f][v]);
-    drain_stores();
-    __syncthreads();
-    if (tid == 0) *last_flag = counter_arrive(&a.counters[rt]) == (uint32_t)(S - 1);
-    __syncthreads();
-    if (!*last_flag) return;
-#pragma unroll
-    for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-    const float* src = a.part + (rt * S * 4 + wave) * (FM * 256);
-    for (int s0 = 0; s0 < S; s0 += 8) {
-      float pv[8][FM * 4];
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (s0 + j < S)
-#pragma unroll
-          for (int e = 0; e < FM * 4; ++e) pv[j][e] = ld_dev(src + (int64_t)(s0 + j) * (4 * FM * 256) + e * 64 + lane);
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (s0 + j < S)
-#pragma unroll
-          for (int e = 0; e < FM * 4; ++e) acc[e >> 2][e & 3] += pv[j][e];
-    }
-    if (tid == 0) counter_reset(&a.counters[rt]);
-  }
+  if (S > 1 && !split_reduce<FM>(acc, a.part + rt * (int64_t)S * 4 * FM * 256, S, s, &a.counters[rt], last_flag))
+    return;
 
-  // 4. store out^T fragment: lane (col + 16 * (row / 4)), element row % 4 -> 4 consecutive rows
+  // out^T fragment: lane (col + 16 * (row / 4)), element row % 4 -> 4 consecutive rows
   const int64_t rr = row0 + 16 * wave + 4 * (lane >> 4);
   if (rr < a.rows) {
 #pragma unroll
@@ -193,181 +202,113 @@ SLIM_DEV void decode_sparse_unit(const LayerArgs& a, int64_t u, _Float16* xs, in
 }
 
 // ============================================================ small-M: adapter first-product units
-// tm[m, j] = sum_red act[m, red] B(red, j) with B = L[red, j] (forward) or R[j, red] (backward).
-// Unit = 64 adapter columns (one 16-column fragment per wave) x one reduction slice.
+// tm[m, j] = sum_red act[m, red] Q[j, red]. Unit = 64 adapter columns (16 per wave) x one slice
+// of 256 reduction positions; both operands are read straight from global memory.
 constexpr int kAdSlice = SLIM_DECODE_AD_SLICE;
-constexpr int kLdL = 64 + 8;
 
-template <bool BWD, int FM>
-SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, _Float16* ls, int* last_flag) {
+template <int FM>
+SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, int* last_flag) {
   constexpr int kSteps = kAdSlice / 32;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int SA = a.ad_split;
   const int64_t jb = v / SA;
   const int sa = (int)(v - jb * SA);
-  const int64_t j0 = jb * 64;
   const int64_t r0 = (int64_t)sa * kAdSlice;
-  const int nst = (int)min((int64_t)kSteps, (a.red - r0) / 32);
   const bool bf16 = a.act_bf16 != 0;
   const int g = lane >> 4;
-  const int64_t jcol = j0 + 16 * wave + (lane & 15);
+  const int64_t jcol = jb * 64 + 16 * wave + (lane & 15);
+  const int64_t jl = clamp_hi(jcol, a.r - 1);
 
-  // activation fragments (A operand: rows m) and adapter-factor fragments (B operand: columns j)
-  h8_t af[kSteps][FM];
-  u32x4_t bq[kSteps];
+  u32x4_t aq[kSteps][FM], bq[kSteps];
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
-    if (t < nst) {
-      const int64_t rk = r0 + 32 * t + 8 * g;
+    const int64_t rk = clamp_hi(r0 + 32 * t + 8 * g, a.red - 8);
 #pragma unroll
-      for (int f = 0; f < FM; ++f) {
-        const int64_t m = 16 * f + (lane & 15);
-        af[t][f] = m < a.M ? act8(*reinterpret_cast<const u32x4_t*>(a.act + m * a.red + rk), bf16) : zero_h8();
-      }
-      if (BWD) bq[t] = jcol < a.r ? *reinterpret_cast<const u32x4_t*>(a.ad_in + jcol * a.red + rk) : zero_u4();
-    }
-  }
-  if (!BWD) {
-    // L[red, j] rows are contiguous along j: stage the [slice x 64] tile in LDS, read columns
-    u32x4_t lv[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int q = tid + 256 * i, kr = q >> 3, jc = q & 7;
-      const int64_t gk = r0 + kr, gj = j0 + 8 * jc;
-      lv[i] = (kr < 32 * nst && gj < a.r) ? *reinterpret_cast<const u32x4_t*>(a.ad_in + gk * a.r + gj) : zero_u4();
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int q = tid + 256 * i, kr = q >> 3, jc = q & 7;
-      *reinterpret_cast<u32x4_t*>(&ls[kr * kLdL + 8 * jc]) = lv[i];
-    }
-    __syncthreads();
+    for (int f = 0; f < FM; ++f)
+      aq[t][f] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.red + rk);
+    bq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_q + jl * a.red + rk);
   }
   f4_t acc[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
-    if (t < nst) {
-      h8_t bv;
-      if (BWD) {
-        bv = __builtin_bit_cast(h8_t, bq[t]);
-      } else {
-        const int col = 16 * wave + (lane & 15);
+    const bool kok = r0 + 32 * t + 8 * g < a.red;
+    const h8_t bv = (kok && jcol < a.r) ? __builtin_bit_cast(h8_t, bq[t]) : zero_h8();
 #pragma unroll
-        for (int e = 0; e < 8; ++e) bv[e] = ls[(32 * t + 8 * g + e) * kLdL + col];
-      }
-#pragma unroll
-      for (int f = 0; f < FM; ++f) acc[f] = mfma16(af[t][f], bv, acc[f]);
+    for (int f = 0; f < FM; ++f) {
+      const h8_t av = (16 * f + (lane & 15) < a.M) ? load8_as_h(aq[t][f], bf16) : zero_h8();
+      acc[f] = mfma16(av, bv, acc[f]);
     }
   }
-  // D[m][j] fragment: lane (j + 16 * (m / 4)), element m % 4
-  auto store_tm = [&](const f4_t* res) {
-#pragma unroll
-    for (int f = 0; f < FM; ++f)
-#pragma unroll
-      for (int vv = 0; vv < 4; ++vv) {
-        const int64_t m = 16 * f + 4 * g + vv;
-        if (m < a.M && jcol < a.r) a.tm[m * a.r + jcol] = __builtin_bit_cast(uint16_t, (_Float16)res[f][vv]);
-      }
-  };
-  if (SA == 1) {
-    store_tm(acc);
+  if (SA > 1 && !split_reduce<FM>(acc, a.tpart + jb * (int64_t)SA * 4 * FM * 256, SA, sa, &a.tcounters[jb], last_flag))
     return;
-  }
-  float* dst = a.tpart + ((jb * SA + sa) * 4 + wave) * (FM * 256);
+  // D[m][j] fragment: lane (j + 16 * (m / 4)), element m % 4
 #pragma unroll
   for (int f = 0; f < FM; ++f)
 #pragma unroll
-    for (int vv = 0; vv < 4; ++vv) st_dev(dst + (f * 4 + vv) * 64 + lane, acc[f][vv]);
-  drain_stores();
-  __syncthreads();
-  if (tid == 0) *last_flag = counter_arrive(&a.tcounters[jb]) == (uint32_t)(SA - 1);
-  __syncthreads();
-  if (!*last_flag) return;
-#pragma unroll
-  for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-  const float* src = a.tpart + (jb * SA * 4 + wave) * (FM * 256);
-  for (int s0 = 0; s0 < SA; s0 += 8) {
-    float pv[8][FM * 4];
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (s0 + j < SA)
-#pragma unroll
-        for (int e = 0; e < FM * 4; ++e) pv[j][e] = ld_dev(src + (int64_t)(s0 + j) * (4 * FM * 256) + e * 64 + lane);
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (s0 + j < SA)
-#pragma unroll
-        for (int e = 0; e < FM * 4; ++e) acc[e >> 2][e & 3] += pv[j][e];
-  }
-  if (tid == 0) counter_reset(&a.tcounters[jb]);
-  store_tm(acc);
+    for (int vv = 0; vv < 4; ++vv) {
+      const int64_t m = 16 * f + 4 * g + vv;
+      if (m < a.M && jcol < a.r) a.tm[m * a.r + jcol] = __builtin_bit_cast(uint16_t, (_Float16)acc[f][vv]);
+    }
 }
 
 // Blocks [0, row_tiles * split) are sparse units; the rest are adapter units.
-template <bool BWD, int FM>
+template <bool BWD, int FM, int G>
 __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
-  extern __shared__ __attribute__((aligned(16))) _Float16 lds[];
+  __shared__ __attribute__((aligned(16))) _Float16 xs[16 * FM * (512 * G + 8)];
   __shared__ int last_flag;
   const int64_t nW = a.row_tiles * a.split;
   const int64_t b = blockIdx.x;
-  if (b < nW) decode_sparse_unit<BWD, FM>(a, b, lds, &last_flag);
-  else decode_adapter_unit<BWD, FM>(a, b - nW, lds, &last_flag);
+  if (b < nW) decode_sparse_unit<BWD, FM, G>(a, b, xs, &last_flag);
+  else decode_adapter_unit<FM>(a, b - nW, &last_flag);
 }
 
 // ============================================================ small-M: adapter second product
-// out[m, row] += sum_j tm[m, j] ap(row, j), ap = R[j, row] (forward) or L[row, j] (backward).
-// One wave per 16 output rows; all fragment loads are issued before the first MFMA.
-template <bool BWD, int FM>
+// out[m, row] += sum_j tm[m, j] P[row, j]. One wave per 16 output rows; all operand loads of a
+// 512-rank round are issued before the first MFMA.
+template <int FM>
 __global__ void __launch_bounds__(64) k_adapter_out(LayerArgs a) {
-  constexpr int kMaxSteps = 8;                     // 256 adapter ranks per round of loads
+  constexpr int kSteps = FM == 1 ? 16 : 8;
   const int lane = threadIdx.x, g = lane >> 4;
   const int64_t row0 = (int64_t)blockIdx.x * 16;
-  const int64_t row = row0 + (lane & 15);
-  const int64_t lrow = row < a.rows ? row : a.rows - 1;
+  const int64_t lrow = clamp_hi(row0 + (lane & 15), a.rows - 1);
+  const int64_t rr = row0 + 4 * g;
+  f4_t yv[FM];
+#pragma unroll
+  for (int f = 0; f < FM; ++f) {
+    const int64_t m = clamp_hi(16 * f + (lane & 15), a.M - 1);
+    yv[f] = *reinterpret_cast<const f4_t*>(a.out + m * a.rows + clamp_hi(rr, a.rows - 4));
+  }
   f4_t acc[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-  for (int64_t jbase = 0; jbase < a.r; jbase += 32 * kMaxSteps) {
-    h8_t av[kMaxSteps], bv[kMaxSteps][FM];
+  for (int64_t jbase = 0; jbase < a.r; jbase += 32 * kSteps) {
+    u32x4_t aq[kSteps], bq[kSteps][FM];
 #pragma unroll
-    for (int t = 0; t < kMaxSteps; ++t) {
-      const int64_t jj = jbase + 32 * t + 8 * g;
-      if (jj < a.r) {
-        if (BWD) {
-          av[t] = __builtin_bit_cast(h8_t, *reinterpret_cast<const u32x4_t*>(a.ad_out + lrow * a.r + jj));
-        } else {
+    for (int t = 0; t < kSteps; ++t) {
+      const int64_t jj = clamp_hi(jbase + 32 * t + 8 * g, a.r - 8);
+      aq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_p + lrow * a.r + jj);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) av[t][e] = __builtin_bit_cast(_Float16, a.ad_out[(jj + e) * a.rows + lrow]);
-        }
-#pragma unroll
-        for (int f = 0; f < FM; ++f) {
-          const int64_t m = 16 * f + (lane & 15);
-          bv[t][f] = m < a.M ? __builtin_bit_cast(h8_t, *reinterpret_cast<const u32x4_t*>(a.tm + m * a.r + jj))
-                             : zero_h8();
-        }
-      } else {
-        av[t] = zero_h8();
-#pragma unroll
-        for (int f = 0; f < FM; ++f) bv[t][f] = zero_h8();
-      }
+      for (int f = 0; f < FM; ++f)
+        bq[t][f] = *reinterpret_cast<const u32x4_t*>(a.tm + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.r + jj);
     }
 #pragma unroll
-    for (int t = 0; t < kMaxSteps; ++t)
-      if (jbase + 32 * t < a.r)
+    for (int t = 0; t < kSteps; ++t) {
+      const bool jok = jbase + 32 * t + 8 * g < a.r;
+      const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[t]) : zero_h8();
 #pragma unroll
-        for (int f = 0; f < FM; ++f) acc[f] = mfma16(av[t], bv[t][f], acc[f]);
+      for (int f = 0; f < FM; ++f) {
+        const h8_t bv = (16 * f + (lane & 15) < a.M) ? __builtin_bit_cast(h8_t, bq[t][f]) : zero_h8();
+        acc[f] = mfma16(av, bv, acc[f]);
+      }
+    }
   }
-  const int64_t rr = row0 + 4 * g;
   if (rr < a.rows) {
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
       const int64_t m = 16 * f + (lane & 15);
-      if (m < a.M) {
-        f4_t* p = reinterpret_cast<f4_t*>(a.out + m * a.rows + rr);
-        *p = *p + acc[f];
-      }
+      if (m < a.M) *reinterpret_cast<f4_t*>(a.out + m * a.rows + rr) = yv[f] + acc[f];
     }
   }
 }
@@ -414,8 +355,7 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
   const uint16_t* sp[4];
 #pragma unroll
   for (int fn = 0; fn < 4; ++fn) {
-    int64_t arow = wrow0 + 32 * fn + (lane & 31);
-    if (arow >= a.rows) arow = a.rows - 1;
+    const int64_t arow = clamp_hi(wrow0 + 32 * fn + (lane & 31), a.rows - 1);
     cp[fn] = a.codes + arow * (a.red / 16) + 4 * ha;
     mp[fn] = a.meta + arow * (a.red / 32) + 2 * ha;
     sp[fn] = a.scales + arow * (a.red / 128);
@@ -427,14 +367,12 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
 #pragma unroll
     for (int i = 0; i < kTXV; ++i) {
       const int q = tid + kTThreads * i, m = q >> 4, vc = q & 15;
-      const int64_t gm = m0 + m;
-      xr[i] = gm < a.M ? *reinterpret_cast<const u32x4_t*>(a.act + gm * a.red + c * 128 + 8 * vc) : zero_u4();
+      xr[i] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(m0 + m, a.M - 1) * a.red + c * 128 + 8 * vc);
     }
-    if (BWD && tid < 32) {
+    if (BWD) {
       // backward: scale row s16[n, g] of each row half's 128-row group, for this chunk
-      const int h = tid >> 4, vc = tid & 15;
-      int64_t gr = row0 + 128 * h;
-      if (gr >= a.rows) gr = a.rows - 1;
+      const int h = (tid >> 4) & 1, vc = tid & 15;
+      const int64_t gr = clamp_hi(row0 + 128 * h, a.rows - 1);
       sr = *reinterpret_cast<const u32x4_t*>(a.scales + (gr / 128) * a.red + c * 128 + 8 * vc);
     }
   };
@@ -442,7 +380,7 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
 #pragma unroll
     for (int i = 0; i < kTXV; ++i) {
       const int q = tid + kTThreads * i, m = q >> 4, vc = q & 15;
-      *reinterpret_cast<h8_t*>(&xs[buf][m][8 * vc]) = act8(xr[i], bf16);
+      *reinterpret_cast<h8_t*>(&xs[buf][m][8 * vc]) = m0 + m < a.M ? load8_as_h(xr[i], bf16) : zero_h8();
     }
     if (BWD && tid < 32) *reinterpret_cast<u32x4_t*>(&ss[buf][tid >> 4][8 * (tid & 15)]) = sr;
   };
@@ -498,65 +436,36 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
     }
   }
 
-  // adapter second product: out^T[row, m] += sum_j ap(row, j) tm[m, j], 32 ranks per round,
-  // on 32x32x16 fp16 MFMA. Forward ap = R^T, staged through LDS transposed.
+  // adapter second product: out^T[row, m] += sum_j P[row, j] tm[m, j], on 32x32x16 fp16 MFMA;
+  // both operands are row-major along j, 64 ranks per round of loads
   if (a.r > 0) {
-    constexpr int kAtLd = 40;
-    _Float16(*at)[kAtLd] = reinterpret_cast<_Float16(*)[kAtLd]>(&xs[0][0][0]);   // [256][40]
-    static_assert(kTR * kAtLd <= 2 * kTC * kTLd, "adapter slab must fit in the activation buffers");
-    for (int64_t jb = 0; jb < a.r; jb += 32) {
-      h8_t bv[2][2];       // [kk][fm]: tm[m][jb + 16 kk + 8 ha .. +7]
-      h8_t av[2][4];       // [kk][fn]
+    for (int64_t jb = 0; jb < a.r; jb += 64) {
+      u32x4_t aq[4][4], bq[4][2];     // [kk][fn], [kk][fm]
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const int64_t jj = jb + 16 * kk + 8 * ha;
+      for (int kk = 0; kk < 4; ++kk) {
+        const int64_t jj = clamp_hi(jb + 16 * kk + 8 * ha, a.r - 8);
 #pragma unroll
-        for (int fm = 0; fm < 2; ++fm) {
-          const int64_t m = m0 + 64 * wc + 32 * fm + (lane & 31);
-          bv[kk][fm] = (m < a.M && jj < a.r)
-                           ? __builtin_bit_cast(h8_t, *reinterpret_cast<const u32x4_t*>(a.tm + m * a.r + jj))
-                           : zero_h8();
-        }
-        if (BWD) {
+        for (int fn = 0; fn < 4; ++fn)
+          aq[kk][fn] =
+              *reinterpret_cast<const u32x4_t*>(a.ad_p + clamp_hi(wrow0 + 32 * fn + (lane & 31), a.rows - 1) * a.r + jj);
 #pragma unroll
-          for (int fn = 0; fn < 4; ++fn) {
-            int64_t rw = wrow0 + 32 * fn + (lane & 31);
-            if (rw >= a.rows) rw = a.rows - 1;
-            av[kk][fn] = jj < a.r ? __builtin_bit_cast(h8_t, *reinterpret_cast<const u32x4_t*>(a.ad_out + rw * a.r + jj))
-                                  : zero_h8();
+        for (int fm = 0; fm < 2; ++fm)
+          bq[kk][fm] =
+              *reinterpret_cast<const u32x4_t*>(a.tm + clamp_hi(m0 + 64 * wc + 32 * fm + (lane & 31), a.M - 1) * a.r + jj);
+      }
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const bool jok = jb + 16 * kk + 8 * ha < a.r;
+#pragma unroll
+        for (int fn = 0; fn < 4; ++fn) {
+          const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[kk][fn]) : zero_h8();
+#pragma unroll
+          for (int fm = 0; fm < 2; ++fm) {
+            const h8_t bv = (m0 + 64 * wc + 32 * fm + (lane & 31) < a.M) ? __builtin_bit_cast(h8_t, bq[kk][fm]) : zero_h8();
+            acc[fn][fm] = mfma32(av, bv, acc[fn][fm]);
           }
         }
       }
-      if (!BWD) {
-        // R[jb .. jb+31][row0 .. row0+255] -> at[row][j]
-        u32x4_t rv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int q = tid + kTThreads * i, jr = q >> 5, nc = q & 31;
-          const int64_t gj = jb + jr, gn = row0 + 8 * nc;
-          rv[i] = (gj < a.r && gn < a.rows) ? *reinterpret_cast<const u32x4_t*>(a.ad_out + gj * a.rows + gn) : zero_u4();
-        }
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int q = tid + kTThreads * i, jr = q >> 5, nc = q & 31;
-          const h8_t hv = __builtin_bit_cast(h8_t, rv[i]);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) at[8 * nc + e][jr] = hv[e];
-        }
-        __syncthreads();
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-          for (int fn = 0; fn < 4; ++fn)
-            av[kk][fn] = *reinterpret_cast<const h8_t*>(&at[128 * wr + 32 * fn + (lane & 31)][16 * kk + 8 * ha]);
-      }
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-        for (int fn = 0; fn < 4; ++fn)
-#pragma unroll
-          for (int fm = 0; fm < 2; ++fm) acc[fn][fm] = mfma32(av[kk][fn], bv[kk][fm], acc[fn][fm]);
     }
   }
 
@@ -579,33 +488,36 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
 }
 
 // ------------------------------------------------------------------------------ launch
+template <bool BWD, int FM, int G>
+void launch_decode(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
+  dim3 grid((unsigned)(p.sp_row_tiles * p.sp_split + (a.r > 0 ? p.ad_jblocks * p.ad_split : 0)));
+  hipLaunchKernelGGL((k_decode<BWD, FM, G>), grid, dim3(256), 0, s, a);
+}
+
 template <bool BWD>
 int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int act_bf16, char* ws, hipStream_t s) {
   if (p.decode) {
     {
       SlimKernelTimer timer(BWD ? "decode_bwd" : "decode_fwd", s);
-      dim3 grid((unsigned)(p.sp_row_tiles * p.sp_split + (a.r > 0 ? p.ad_jblocks * p.ad_split : 0)));
-      switch (p.dec_fm) {
-        case 1: hipLaunchKernelGGL((k_decode<BWD, 1>), grid, dim3(256), p.lds_bytes, s, a); break;
-        case 2: hipLaunchKernelGGL((k_decode<BWD, 2>), grid, dim3(256), p.lds_bytes, s, a); break;
-        default: hipLaunchKernelGGL((k_decode<BWD, 4>), grid, dim3(256), p.lds_bytes, s, a); break;
+      if (p.dec_fm == 1) {
+        if (p.dec_g == 1) launch_decode<BWD, 1, 1>(a, p, s);
+        else launch_decode<BWD, 1, 2>(a, p, s);
+      } else {
+        launch_decode<BWD, 2, 1>(a, p, s);
       }
       if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
     }
     if (a.r > 0) {
       SlimKernelTimer timer(BWD ? "adapter_out_bwd" : "adapter_out_fwd", s);
       dim3 grid((unsigned)((a.rows + 15) / 16));
-      switch (p.dec_fm) {
-        case 1: hipLaunchKernelGGL((k_adapter_out<BWD, 1>), grid, dim3(64), 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_adapter_out<BWD, 2>), grid, dim3(64), 0, s, a); break;
-        default: hipLaunchKernelGGL((k_adapter_out<BWD, 4>), grid, dim3(64), 0, s, a); break;
-      }
+      if (p.dec_fm == 1) hipLaunchKernelGGL((k_adapter_out<1>), grid, dim3(64), 0, s, a);
+      else hipLaunchKernelGGL((k_adapter_out<2>), grid, dim3(64), 0, s, a);
       if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
     }
     return SLIM_OK;
   }
   if (a.r > 0) {
-    int st = slim_launch_adapter_gemm(BWD, act, act_bf16, a.M, a.red, a.ad_in, a.r, p, ws, s);
+    int st = slim_launch_adapter_gemm(act, act_bf16, a.M, a.red, a.ad_q, a.r, p, ws, s);
     if (st != SLIM_OK) return st;
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
@@ -615,8 +527,8 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
 }
 
 LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int64_t M, int64_t rows, int64_t red,
-                    const uint8_t* codes, const uint8_t* meta, const uint16_t* scales, const uint16_t* ad_in,
-                    const uint16_t* ad_out, int64_t r, float* out) {
+                    const uint8_t* codes, const uint8_t* meta, const uint16_t* scales, const uint16_t* ad_q,
+                    const uint16_t* ad_p, int64_t r, float* out) {
   LayerArgs a;
   a.codes = reinterpret_cast<const uint32_t*>(codes);
   a.meta = reinterpret_cast<const uint32_t*>(meta);
@@ -627,15 +539,13 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.rows = rows;
   a.red = red;
   a.r = r;
-  a.ad_in = ad_in;
-  a.ad_out = ad_out;
+  a.ad_q = ad_q;
+  a.ad_p = ad_p;
   a.tm = reinterpret_cast<uint16_t*>(ws + p.off_t);
   a.out = out;
   a.split = p.sp_split;
-  a.cps = p.sp_chunks_per_split;
   a.row_tiles = p.sp_row_tiles;
   a.ad_split = p.ad_split;
-  a.ad_slice = p.ad_slice;
   a.ad_jblocks = p.ad_jblocks;
   a.part = reinterpret_cast<float*>(ws + p.off_ypart);
   a.tpart = reinterpret_cast<float*>(ws + p.off_tpart);
@@ -653,13 +563,13 @@ extern "C" int slim_workspace_init(void* ws, size_t ws_bytes, void* stream) {
 }
 
 extern "C" int slim_linear(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const uint8_t* codes,
-                           const uint8_t* meta, const uint16_t* scales, const uint16_t* L, const uint16_t* R,
+                           const uint8_t* meta, const uint16_t* scales, const uint16_t* Lt, const uint16_t* Rt,
                            int64_t r, float* Y, void* ws, size_t ws_bytes, void* stream) {
   SlimPlan p;
-  int st = slim_check_linear(false, X, xdtype, M, N, K, codes, meta, scales, L, R, r, Y, ws, ws_bytes, &p);
+  int st = slim_check_linear(false, X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, ws, ws_bytes, &p);
   if (st != SLIM_OK) return st;
   char* w = reinterpret_cast<char*>(ws);
-  const LayerArgs a = make_args(p, w, X, xdtype, M, N, K, codes, meta, scales, L, R, r, Y);
+  const LayerArgs a = make_args(p, w, X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y);
   return launch_layer<false>(a, p, reinterpret_cast<const uint16_t*>(X), xdtype == SLIM_BF16, w, (hipStream_t)stream);
 }
 

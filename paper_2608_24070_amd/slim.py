@@ -28,6 +28,7 @@ _SIGS = {
     "slim_abi_version": (ctypes.c_int, []),
     "slim_pack": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "slim_pack_bwd": (ctypes.c_int, [_c_p, _c_p, _c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "slim_pack_adapter": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
     "slim_linear_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
     "slim_bwd_dx_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
     "slim_workspace_init": (ctypes.c_int, [_c_p, ctypes.c_size_t, _c_p]),
@@ -97,6 +98,10 @@ def slim_pack_bwd(codes, meta, scales, N, K, codesT, metaT, scalesT, mask_rc, st
     return lib().slim_pack_bwd(codes, meta, scales, N, K, codesT, metaT, scalesT, mask_rc, stream)
 
 
+def slim_pack_adapter(L, R, K, N, r, Lt, Rt, stream) -> int:
+    return lib().slim_pack_adapter(L, R, K, N, r, Lt, Rt, stream)
+
+
 def slim_linear_workspace(M, N, K, r) -> int:
     out = ctypes.c_size_t(0)
     _check(lib().slim_linear_workspace(M, N, K, r, ctypes.byref(out)), "slim_linear_workspace")
@@ -113,8 +118,8 @@ def slim_workspace_init(ws, nbytes, stream) -> int:
     return lib().slim_workspace_init(ws, nbytes, stream)
 
 
-def slim_linear(X, xdtype, M, N, K, codes, meta, scales, L, R, r, Y, ws, ws_bytes, stream) -> int:
-    return lib().slim_linear(X, xdtype, M, N, K, codes, meta, scales, L, R, r, Y, ws, ws_bytes, stream)
+def slim_linear(X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, ws, ws_bytes, stream) -> int:
+    return lib().slim_linear(X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, ws, ws_bytes, stream)
 
 
 def slim_linear_bwd_dx(dY, dydtype, M, N, K, codesT, metaT, scalesT, L, R, r, dX, ws, ws_bytes, stream) -> int:
@@ -231,20 +236,37 @@ def pack_bwd(packed: dict, with_mask: bool = False, stream=None) -> dict:
     return out
 
 
-def linear(X, packed: dict, L=None, R=None, out=None, ws=None, stream=None):
-    """Y = X Wc^T + (X L) R through slim_linear. X bf16/fp16 [M, K]; L, R fp16; Y fp32 [M, N]."""
+def pack_adapter(L, R, stream=None) -> dict:
+    """slim_pack_adapter of fp16 L [K, r] and R [r, N]: returns {"Lt", "Rt", "L", "R"} (the forward
+    takes Lt, Rt; the backward takes L, R)."""
     torch = _torch()
-    _on_gpu(X, L, R, out)
+    _on_gpu(L, R)
+    K, r = L.shape
+    N = R.shape[1]
+    out = {"Lt": torch.empty((r, K), dtype=torch.float16, device=L.device),
+           "Rt": torch.empty((N, r), dtype=torch.float16, device=L.device), "L": L, "R": R}
+    _check(slim_pack_adapter(_ptr(L), _ptr(R), K, N, r, _ptr(out["Lt"]), _ptr(out["Rt"]), _stream(stream)),
+           "slim_pack_adapter")
+    return out
+
+
+def linear(X, packed: dict, adapter: dict | None = None, out=None, ws=None, stream=None):
+    """Y = X Wc^T + (X L) R through slim_linear. X bf16/fp16 [M, K]; adapter from pack_adapter (or None);
+    Y fp32 [M, N]."""
+    torch = _torch()
+    Lt = None if adapter is None else adapter["Lt"]
+    Rt = None if adapter is None else adapter["Rt"]
+    _on_gpu(X, Lt, Rt, out)
     M, K = X.shape
     N = packed["N"]
-    r = 0 if L is None else L.shape[1]
+    r = 0 if Lt is None else Lt.shape[0]
     if out is None:
         out = torch.empty((M, N), dtype=torch.float32, device=X.device)
     need = slim_linear_workspace(M, N, K, r)
     if ws is None:
         ws = workspace(need, X.device, stream)
     st = slim_linear(_ptr(X), _dtype_code(X), M, N, K, _ptr(packed["codes"]), _ptr(packed["meta"]),
-                     _ptr(packed["scales"]), _ptr(L), _ptr(R), r, _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
+                     _ptr(packed["scales"]), _ptr(Lt), _ptr(Rt), r, _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "slim_linear")
     return out
 

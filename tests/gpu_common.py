@@ -50,9 +50,8 @@ def layer_inputs(n, k, r, m, seed=0, xdtype="bf16", outliers=False, name="layer"
         Lb, Rb, L, R = Lb[:, :r].copy(), Rb[:r].copy(), L[:, :r], R[:r]
     tdt = torch.bfloat16 if xdtype == "bf16" else torch.float16
     dx = dev_bits(xbits, tdt)
-    dL = None if Lb is None else dev_bits(Lb, torch.float16)
-    dR = None if Rb is None else dev_bits(Rb, torch.float16)
-    return W, X, L, R, dx, dL, dR
+    ad = None if Lb is None else slim.pack_adapter(dev_bits(Lb, torch.float16), dev_bits(Rb, torch.float16))
+    return W, X, L, R, dx, ad
 
 
 def assert_close(Y, Yref, what=""):

@@ -15,7 +15,7 @@ def test_library_exports_every_declared_symbol():
     syms = slim.header_symbols()
     assert {"slim_pack", "slim_pack_bwd", "slim_linear", "slim_linear_bwd_dx", "slim_linear_workspace",
             "slim_bwd_dx_workspace", "slim_workspace_init", "slim_status_string", "slim_abi_version",
-            "slim_timing_enable", "slim_timing_reset", "slim_timing_read"} <= set(syms)
+            "slim_timing_enable", "slim_timing_reset", "slim_timing_read", "slim_pack_adapter"} <= set(syms)
     for name in syms:
         assert hasattr(lib, name), name
 
@@ -48,6 +48,12 @@ def test_pack_bwd_validation():
     assert call(N=24) == 2          # N % 16
     assert call(K=200) == 2
     assert call(codesT=MIS) == 4
+
+
+def test_pack_adapter_validation():
+    assert slim.slim_pack_adapter(None, A, 128, 64, 16, A, A, None) == 1
+    assert slim.slim_pack_adapter(A, A, 128, 64, 24, A, A, None) == 2
+    assert slim.slim_pack_adapter(A, A, 128, 64, 16, MIS, A, None) == 4
 
 
 def test_linear_validation_and_workspace():

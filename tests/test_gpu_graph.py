@@ -14,19 +14,19 @@ pytestmark = pytest.mark.gpu
 @pytest.mark.parametrize("n,k,r,m", [(4096, 4096, 384, 16), (1024, 2048, 64, 48), (1024, 1024, 64, 256)])
 def test_forward_graph_replays(n, k, r, m):
     print(f"graph fwd n={n} k={k} r={r} m={m}", flush=True)
-    W, X, L, R, dx, dL, dR = layer_inputs(n, k, r, m, name="graph")
+    W, X, L, R, dx, ad = layer_inputs(n, k, r, m, name="graph")
     p = slim.pack(dev(W))
     ws = torch.zeros(slim.slim_linear_workspace(m, n, k, r), dtype=torch.uint8, device="cuda")
-    eager = slim.linear(dx, p, dL, dR, ws=ws).clone()
+    eager = slim.linear(dx, p, ad, ws=ws).clone()
     out = torch.empty_like(eager)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        slim.linear(dx, p, dL, dR, out=out, ws=ws)
+        slim.linear(dx, p, ad, out=out, ws=ws)
     noise = torch.randn(1 << 20, device="cuda")
     for rep in range(4):
         out.fill_(float("nan"))
-        slim.linear(dx, p, dL, dR, ws=ws)         # eager call sharing the workspace in between
+        slim.linear(dx, p, ad, ws=ws)         # eager call sharing the workspace in between
         noise.mul_(1.0001).sum()
         g.replay()
         torch.cuda.synchronize()

@@ -14,12 +14,12 @@ pytestmark = pytest.mark.gpu
 def _fwd_case(n, k, r, m, xdtype="bf16", outliers=False, seed=0, rows=None, ms=None, name="layer",
               use_oracle_pack=False):
     print(f"fwd n={n} k={k} r={r} m={m} {xdtype} outliers={outliers} seed={seed}", flush=True)
-    W, X, L, R, dx, dL, dR = layer_inputs(n, k, r, m, seed=seed, xdtype=xdtype, outliers=outliers, name=name)
+    W, X, L, R, dx, ad = layer_inputs(n, k, r, m, seed=seed, xdtype=xdtype, outliers=outliers, name=name)
     if use_oracle_pack:
         p = oracle_pack_on_device(O.pack(W), n, k)
     else:
         p = slim.pack(dev(W))
-    Y = host(slim.linear(dx, p, dL, dR))
+    Y = host(slim.linear(dx, p, ad))
     torch.cuda.synchronize()
     rows = np.arange(n) if rows is None else rows
     ms = np.arange(m) if ms is None else ms
@@ -42,7 +42,7 @@ def test_small_m_multi_fragment(m):
     _fwd_case(1024, 2048, 64, m, name="smallm")
 
 
-@pytest.mark.parametrize("m,r", [(65, 32), (200, 16), (256, 0), (300, 48)])
+@pytest.mark.parametrize("m,r", [(65, 32), (200, 16), (256, 0), (300, 48), (40, 80)])
 def test_tile_kernel_ragged(m, r):
     _fwd_case(768, 1024, r, m, name="ragged")
 
@@ -78,14 +78,22 @@ def test_mlp70b_fwd_sampled(m):
 
 
 def test_forward_is_deterministic():
-    W, X, L, R, dx, dL, dR = layer_inputs(4096, 4096, 384, 16, name="det")
+    W, X, L, R, dx, ad = layer_inputs(4096, 4096, 384, 16, name="det")
     p = slim.pack(dev(W))
-    a = slim.linear(dx, p, dL, dR).clone()
-    b = slim.linear(dx, p, dL, dR).clone()
+    a = slim.linear(dx, p, ad).clone()
+    b = slim.linear(dx, p, ad).clone()
     assert torch.equal(a, b)
-    W, X, L, R, dx, dL, dR = layer_inputs(1024, 1024, 64, 256, name="det2")
+    W, X, L, R, dx, ad = layer_inputs(1024, 1024, 64, 256, name="det2")
     p = slim.pack(dev(W))
-    assert torch.equal(slim.linear(dx, p, dL, dR).clone(), slim.linear(dx, p, dL, dR).clone())
+    assert torch.equal(slim.linear(dx, p, ad).clone(), slim.linear(dx, p, ad).clone())
+
+
+@pytest.mark.parametrize("k,n,r", [(512, 512, 32), (4096, 11008, 384), (13824, 5120, 512), (200, 72, 16)])
+def test_pack_adapter_is_exact_transpose(k, n, r):
+    Lb, Rb, _, _ = synth.adapter(k, n, r, seed=5, name="tp/")
+    ad = slim.pack_adapter(dev_bits(Lb, torch.float16), dev_bits(Rb, torch.float16))
+    assert np.array_equal(host(ad["Lt"]).view(np.uint16), Lb.T)
+    assert np.array_equal(host(ad["Rt"]).view(np.uint16), Rb.T)
 
 
 # ------------------------------------------------------------------------------ backward
