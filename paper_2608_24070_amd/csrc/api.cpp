@@ -76,7 +76,6 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     q.dec_g = (q.dec_fm == 1 && q.sp_row_tiles * cdiv(nchunks, 8) >= 256) ? 2 : 1;
     q.sp_chunks_per_split = 4 * q.dec_g;
     q.sp_split = (int)cdiv(nchunks, q.sp_chunks_per_split);
-    if (q.sp_split > 1 && q.sp_row_tiles > (int64_t)(kCounterSlots / 2)) return SLIM_EUNSUPPORTED;
     if (r > 0) {
       q.ad_jblocks = cdiv(r, 64);
       q.ad_slice = kDecodeAdSlice;
@@ -86,7 +85,7 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
         tpart_bytes = (size_t)q.ad_jblocks * q.ad_split * 4 * q.dec_fm * 256 * 4;
       }
     }
-    if (q.sp_split > 1) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 4 * q.dec_fm * 256 * 4;
+    if (q.sp_split > 1 || r > 0) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 4 * q.dec_fm * 256 * 4;
     q.lds_bytes = 0;
   } else {
     // large M: dense adapter GEMM (64 x 64 tiles) then 256 x 128 sparse tiles
@@ -113,8 +112,7 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     }
   }
   // workspace: [counters][adapter intermediate fp16 M x r][adapter partials][sparse partials]
-  q.n_counters = ad_counters + (q.sp_split > 1 ? (size_t)q.sp_row_tiles : 0);
-  q.sp_counter_base = ad_counters;
+  q.n_counters = ad_counters;
   q.off_counters = 0;
   if (q.n_counters > kCounterSlots) return SLIM_EUNSUPPORTED;
   // the counter region has a fixed size so that it stays at zero across calls with other sizes

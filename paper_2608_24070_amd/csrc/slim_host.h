@@ -33,7 +33,7 @@ struct SlimPlan {
   int64_t sp_chunks_per_split = 0;    // 128-wide chunks per split
   size_t lds_bytes = 0;               // dynamic LDS (unused: the kernels size their LDS statically)
   // workspace layout (byte offsets)
-  size_t off_counters = 0, n_counters = 0, sp_counter_base = 0;
+  size_t off_counters = 0, n_counters = 0;
   size_t off_t = 0, off_tpart = 0, off_ypart = 0, total = 0;
 };
 

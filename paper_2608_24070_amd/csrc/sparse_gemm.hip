@@ -21,8 +21,8 @@
 //  * small M (<= 32, decode): k_decode splits the reduction across blocks so that every CU
 //    streams a slice of the packed weight; the same launch computes the adapter's first product
 //    in extra blocks (the two products share the activations, as in SLoPe's concatenated
-//    adapter). Split partials are summed by the last block of each tile in a fixed order.
-//    k_adapter_out then adds the adapter's second product.
+//    adapter). Sparse units only store their partials; k_finish sums them in a fixed order and
+//    adds the adapter's second product, so no sparse unit waits on another.
 //  * large M: the adapter's first product runs as a dense GEMM (adapter_gemm.hip); k_tile then
 //    computes 256 x 128 output tiles on 32x32x32 sparse MFMA with a double-buffered LDS
 //    activation tile and adds the second adapter product in its epilogue.
@@ -54,8 +54,8 @@ struct LayerArgs {
   int64_t ad_jblocks;      // 64-wide column blocks of the adapter rank
   float* part;             // sparse split partials
   float* tpart;            // adapter split partials
-  uint32_t* counters;      // per 64-row tile
   uint32_t* tcounters;     // per adapter column block
+  int finish;              // sparse partials go to k_finish (split > 1 or an adapter)
 };
 
 SLIM_DEV u32x4_t zero_u4() { return u32x4_t{0u, 0u, 0u, 0u}; }
@@ -187,8 +187,14 @@ SLIM_DEV void decode_sparse_unit(const LayerArgs& a, int64_t u, _Float16* xs, in
     }
   }
 
-  if (S > 1 && !split_reduce<FM>(acc, a.part + rt * (int64_t)S * 4 * FM * 256, S, s, &a.counters[rt], last_flag))
+  (void)last_flag;
+  if (a.finish) {
+    // k_finish sums the split partials (and adds the adapter); the kernel boundary orders them
+    float* dst = a.part + ((rt * S + s) * 4 + wave) * (int64_t)(FM * 256);
+#pragma unroll
+    for (int f = 0; f < FM; ++f) *reinterpret_cast<f4_t*>(dst + f * 256 + 4 * lane) = acc[f];
     return;
+  }
 
   // out^T fragment: lane (col + 16 * (row / 4)), element row % 4 -> 4 consecutive rows
   const int64_t rr = row0 + 16 * wave + 4 * (lane >> 4);
@@ -253,36 +259,52 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, int* last_flag)
     }
 }
 
-// Blocks [0, row_tiles * split) are sparse units; the rest are adapter units.
+// Blocks [0, jblocks * ad_split) are adapter units (dispatched first: their reduction is the
+// longer path); the rest are sparse units.
 template <bool BWD, int FM, int G>
 __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
   __shared__ __attribute__((aligned(16))) _Float16 xs[16 * FM * (512 * G + 8)];
   __shared__ int last_flag;
-  const int64_t nW = a.row_tiles * a.split;
+  const int64_t nA = a.r > 0 ? a.ad_jblocks * a.ad_split : 0;
   const int64_t b = blockIdx.x;
-  if (b < nW) decode_sparse_unit<BWD, FM, G>(a, b, xs, &last_flag);
-  else decode_adapter_unit<FM>(a, b - nW, &last_flag);
+  if (b < nA) decode_adapter_unit<FM>(a, b, &last_flag);
+  else decode_sparse_unit<BWD, FM, G>(a, b - nA, xs, &last_flag);
 }
 
-// ============================================================ small-M: adapter second product
-// out[m, row] += sum_j tm[m, j] P[row, j]. One wave per 16 output rows; all operand loads of a
-// 512-rank round are issued before the first MFMA.
+// ============================================================ small-M: finish
+// out[m, row] = sum_s part_s[m, row] + sum_j tm[m, j] P[row, j]. One wave per 16 output rows; the
+// split partials are summed in split order (deterministic) and the adapter's second product is
+// accumulated on top with 16x16x32 fp16 MFMA. The partials share the MFMA output layout, so each
+// lane reads its own four values per split and fragment.
 template <int FM>
-__global__ void __launch_bounds__(64) k_adapter_out(LayerArgs a) {
+__global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
   constexpr int kSteps = FM == 1 ? 16 : 8;
   const int lane = threadIdx.x, g = lane >> 4;
   const int64_t row0 = (int64_t)blockIdx.x * 16;
   const int64_t lrow = clamp_hi(row0 + (lane & 15), a.rows - 1);
   const int64_t rr = row0 + 4 * g;
-  f4_t yv[FM];
-#pragma unroll
-  for (int f = 0; f < FM; ++f) {
-    const int64_t m = clamp_hi(16 * f + (lane & 15), a.M - 1);
-    yv[f] = *reinterpret_cast<const f4_t*>(a.out + m * a.rows + clamp_hi(rr, a.rows - 4));
-  }
+  const int64_t rt = row0 / 64;
+  const int w16 = (int)((row0 % 64) / 16);
+  const int S = a.split;
   f4_t acc[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+  const float* src = a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256);
+  for (int s0 = 0; s0 < S; s0 += 8) {
+    f4_t pv[8][FM];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int ss = s0 + j < S ? s0 + j : S - 1;
+#pragma unroll
+      for (int f = 0; f < FM; ++f)
+        pv[j][f] = *reinterpret_cast<const f4_t*>(src + (int64_t)ss * 4 * FM * 256 + f * 256 + 4 * lane);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (s0 + j < S)
+#pragma unroll
+        for (int f = 0; f < FM; ++f) acc[f] = acc[f] + pv[j][f];
+  }
   for (int64_t jbase = 0; jbase < a.r; jbase += 32 * kSteps) {
     u32x4_t aq[kSteps], bq[kSteps][FM];
 #pragma unroll
@@ -308,7 +330,7 @@ __global__ void __launch_bounds__(64) k_adapter_out(LayerArgs a) {
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
       const int64_t m = 16 * f + (lane & 15);
-      if (m < a.M) *reinterpret_cast<f4_t*>(a.out + m * a.rows + rr) = yv[f] + acc[f];
+      if (m < a.M) *reinterpret_cast<f4_t*>(a.out + m * a.rows + rr) = acc[f];
     }
   }
 }
@@ -507,11 +529,11 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
       }
       if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
     }
-    if (a.r > 0) {
-      SlimKernelTimer timer(BWD ? "adapter_out_bwd" : "adapter_out_fwd", s);
+    if (a.finish) {
+      SlimKernelTimer timer(BWD ? "finish_bwd" : "finish_fwd", s);
       dim3 grid((unsigned)((a.rows + 15) / 16));
-      if (p.dec_fm == 1) hipLaunchKernelGGL((k_adapter_out<1>), grid, dim3(64), 0, s, a);
-      else hipLaunchKernelGGL((k_adapter_out<2>), grid, dim3(64), 0, s, a);
+      if (p.dec_fm == 1) hipLaunchKernelGGL((k_finish<1>), grid, dim3(64), 0, s, a);
+      else hipLaunchKernelGGL((k_finish<2>), grid, dim3(64), 0, s, a);
       if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
     }
     return SLIM_OK;
@@ -549,8 +571,8 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.ad_jblocks = p.ad_jblocks;
   a.part = reinterpret_cast<float*>(ws + p.off_ypart);
   a.tpart = reinterpret_cast<float*>(ws + p.off_tpart);
-  a.counters = reinterpret_cast<uint32_t*>(ws + p.off_counters) + p.sp_counter_base;
   a.tcounters = reinterpret_cast<uint32_t*>(ws + p.off_counters);
+  a.finish = p.decode && (p.sp_split > 1 || r > 0);
   return a;
 }
 
