@@ -8,10 +8,16 @@ the 256 MB MALL, so the weight stream comes from HBM. Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload decode|prefill|block13b|mlp70b|mlp70b_bwd|tiny]
                   [--m M] [--no-cpu-baseline]
+  python bench.py --copy-probe MB     # plain device copy of MB megabytes (counter calibration)
+
+The roofline's "traffic" field comes from the hardware-counter summary committed under profiles/
+for the same kernel and workload; it is null when no summary matches, or when the kernel sources
+have changed since the counters were taken (the summary records their hash).
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -36,12 +42,85 @@ def parse():
     ap.add_argument("--m", type=int, default=None, help="rows of X (tokens); default per workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU budget of the oracle baseline")
+    ap.add_argument("--copy-probe", type=float, default=None, metavar="MB",
+                    help="only run a plain device-to-device copy of MB megabytes (HBM counter calibration)")
     return ap.parse_args()
+
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCES = ("include/slim.h", "paper_2608_24070_amd/csrc/api.cpp", "paper_2608_24070_amd/csrc/slim_host.h",
+                  "paper_2608_24070_amd/csrc/slim_device.h", "paper_2608_24070_amd/csrc/sparse_gemm.hip",
+                  "paper_2608_24070_amd/csrc/adapter_gemm.hip", "paper_2608_24070_amd/csrc/pack.hip")
+
+
+def kernel_source_hash():
+    """sha256 over the sources that decide what the measured kernels do (first 16 hex digits)."""
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(rel.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(kernel, workload_key):
+    """HBM bytes per launch of `kernel` on `workload_key` from the committed counter summary.
+
+    profiles/hbm_traffic.txt holds lines
+        traffic <kernel> <workload> <fetch_bytes> <write_bytes> <source_hash>
+    with FETCH_SIZE and WRITE_SIZE already scaled by the copy-kernel calibration. Returns None if
+    no line matches or the sources have changed since.
+    """
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    cur = kernel_source_hash()
+    with open(path) as f:
+        for line in f:
+            t = line.split()
+            if len(t) == 6 and t[0] == "traffic" and t[1] == kernel and t[2] == workload_key and t[5] == cur:
+                return float(t[3]) + float(t[4])
+    return None
+
+
+def copy_probe(mb):
+    """A plain device copy of `mb` MB, 10 times: the known-size kernel the HBM counters are scaled by."""
+    import torch
+    n = int(mb * 1e6) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(10):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 10
+    print(json.dumps({"copy_probe_bytes_each_way": n * 4, "launches": 11, "avg_ms": round(ms, 4),
+                      "read_plus_write_GBps": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}))
 
 
 def layer_bytes(M, N, K, r):
     """Algorithmic bytes of one forward layer call: packed weight + fp16 adapter + bf16 X + fp32 Y."""
     return N * K * PACK_BYTES_PER_WEIGHT + 2 * r * (K + N) + 2 * M * K + 4 * M * N
+
+
+def kernel_bytes(kernel, M, N, K, r, bwd):
+    """Algorithmic HBM bytes of one launch of a library kernel on one layer: the operands it must
+    read and the results it must produce, once each (split partials and re-reads not counted).
+    Forward: rows = N, reduction = K; backward: rows = K, reduction = N."""
+    rows, red = (K, N) if bwd else (N, K)
+    weight = N * K * PACK_BYTES_PER_WEIGHT
+    if kernel.startswith("decode"):      # packed weight + adapter first factor + activations -> Y, T
+        return weight + 2 * r * red + 2 * M * red + 4 * M * rows + 2 * M * r
+    if kernel.startswith("finish"):      # adapter second factor + T -> Y
+        return 2 * r * rows + 2 * M * r + 4 * M * rows
+    if kernel.startswith("tile"):        # packed weight + activations + second factor + T -> Y
+        return weight + 2 * M * red + 2 * r * rows + 2 * M * r + 4 * M * rows
+    if kernel.startswith("adapter_gemm"):
+        return 2 * M * red + 2 * r * red + 2 * M * r
+    return 0
 
 
 def layer_flops(M, N, K, r):
@@ -51,6 +130,9 @@ def layer_flops(M, N, K, r):
 
 def main():
     args = parse()
+    if args.copy_probe is not None:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported in this build "
               "(the layer shards along N across GPUs by design, but no multi-GPU path is built).",
@@ -173,8 +255,8 @@ def main():
           f"({n_copies} weight copies, host enqueue {host_ms * 1e3:.0f} us/step, setup {setup_s:.1f}s)",
           file=sys.stderr, flush=True)
 
-    # Per-kernel durations: the library brackets each launch with two hipEvents on the launch
-    # stream (slim_timing_*), again behind a backlog so that they time the GPU, not the host.
+    # Per-kernel durations: each library launch records a start and a stop event as part of its own
+    # dispatch (slim_timing_*, hipExtLaunchKernel), so they carry the kernel's begin and end times.
     slim.slim_timing_reset()
     slim.slim_timing_enable(True)
     backlog(min(2000.0, 20.0 + 3.0 * host_ms * args.steps))
@@ -183,7 +265,7 @@ def main():
     torch.cuda.synchronize()
     kt = slim.slim_timing_read()
     slim.slim_timing_enable(False)
-    timing_mode = "hip events around each launch, stream backlogged"
+    timing_mode = "hip events recorded by each kernel dispatch (hipExtLaunchKernel), stream backlogged"
     kernels = {k: {"launches": n, "avg_us": 1e3 * ms / max(n, 1)} for k, (n, ms) in kt.items()}
     dominant = max(kt.items(), key=lambda kv: kv[1][1])[0]
 
@@ -191,24 +273,27 @@ def main():
     tot_bytes = sum(layer_bytes(M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
     tot_flops = sum(layer_flops(M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
     launches_per_step = kt[dominant][0] / args.steps
+    wkey = f"{wk}_m{M}"
     if decode_like:
         unit = "GB/s"
         value = tot_bytes / (ms_per_step * 1e-3) / 1e9
-        # dominant kernel (the sparse contraction): packed weight + R + X in, Y out, per launch
-        dk_bytes = sum(pl["layer"].n * pl["layer"].k * PACK_BYTES_PER_WEIGHT + 2 * pl["layer"].r * pl["layer"].n
-                       + 2 * M * pl["layer"].k + 4 * M * pl["layer"].n for pl in per_layer) / launches_per_step
+        dk_bytes = sum(kernel_bytes(dominant, M, pl["layer"].n, pl["layer"].k, pl["layer"].r, bwd)
+                       for pl in per_layer) / launches_per_step
         achieved = dk_bytes / (kernels[dominant]["avg_us"] * 1e-6) / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None}
+                    "frac": round(achieved / HBM_PEAK_GBS, 4)}
     else:
         unit = "TFLOP/s"
         value = tot_flops / (ms_per_step * 1e-3) / 1e12
-        # dominant kernel (the sparse contraction): dense-equivalent 2MNK plus the adapter's 2MrN
+        # dominant kernel (the sparse contraction): dense-equivalent 2MNK plus the adapter's second product
         dk_flops = sum(2 * M * pl["layer"].n * pl["layer"].k + 2 * M * pl["layer"].r *
                        (pl["layer"].k if bwd else pl["layer"].n) for pl in per_layer) / launches_per_step
         achieved = dk_flops / (kernels[dominant]["avg_us"] * 1e-6) / 1e12
         roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_F16_PEAK_TFS, "unit": "TFLOP/s",
-                    "frac": round(achieved / MFMA_F16_PEAK_TFS, 4), "traffic": None}
+                    "frac": round(achieved / MFMA_F16_PEAK_TFS, 4)}
+    traffic = counter_traffic(dominant, wkey)
+    roofline["traffic"] = None if traffic is None else round(traffic / 1e6, 3)
+    roofline["traffic_unit"] = "MB per launch (HBM fetch + write, copy-calibrated counters)"
     roofline["kernel"] = dominant
     roofline["timing"] = timing_mode
 
@@ -238,6 +323,7 @@ def main():
             "M": M, "layers": len(layers), "N": ly0.n, "K": ly0.k, "r": ly0.r,
             "bytes_per_step": int(tot_bytes), "dense_equiv_flops_per_step": int(tot_flops),
             "weight_copies_rotated": n_copies, "pack_ms_one_time": round(pack_ms, 2),
+            "kernel_source_hash": kernel_source_hash(),
         },
         "kernels": kernels,
         "roofline": roofline,

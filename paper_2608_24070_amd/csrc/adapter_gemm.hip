@@ -147,7 +147,7 @@ int slim_launch_adapter_gemm(const uint16_t* A, int a_bf16, int64_t M, int64_t K
   float* part = reinterpret_cast<float*>(ws + p.off_tpart);
   uint32_t* counters = reinterpret_cast<uint32_t*>(ws + p.off_counters);
   SlimKernelTimer timer("adapter_gemm", s);
-  hipLaunchKernelGGL(k_adapter_gemm, grid, dim3(256), 0, s, A, a_bf16, M, Kd, Q, r, p.ad_slice, p.ad_split, out, part,
-                     counters);
+  SLIM_LAUNCH(timer, k_adapter_gemm, grid, dim3(256), s, A, a_bf16, M, Kd, Q, r, p.ad_slice, p.ad_split, out, part,
+              counters);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }

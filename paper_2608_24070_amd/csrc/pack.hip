@@ -221,11 +221,16 @@ extern "C" int slim_pack_adapter(const uint16_t* L, const uint16_t* R, int64_t K
     return SLIM_ESHAPE;
   if (!slim_aligned16(L) || !slim_aligned16(R) || !slim_aligned16(Lt) || !slim_aligned16(Rt)) return SLIM_EALIGN;
   hipStream_t s = (hipStream_t)stream;
-  SlimKernelTimer timer("pack_adapter", s);
-  hipLaunchKernelGGL(k_transpose16, dim3((unsigned)((r + 63) / 64), (unsigned)((K + 63) / 64)), dim3(256), 0, s, L, K, r,
-                     Lt);
-  hipLaunchKernelGGL(k_transpose16, dim3((unsigned)((N + 63) / 64), (unsigned)((r + 63) / 64)), dim3(256), 0, s, R, r, N,
-                     Rt);
+  {
+    SlimKernelTimer timer("pack_adapter", s);
+    SLIM_LAUNCH(timer, k_transpose16, dim3((unsigned)((r + 63) / 64), (unsigned)((K + 63) / 64)), dim3(256), s, L, K, r,
+                Lt);
+  }
+  {
+    SlimKernelTimer timer("pack_adapter", s);
+    SLIM_LAUNCH(timer, k_transpose16, dim3((unsigned)((N + 63) / 64), (unsigned)((r + 63) / 64)), dim3(256), s, R, r, N,
+                Rt);
+  }
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }
 
@@ -242,9 +247,12 @@ extern "C" int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, u
   const int64_t blocks = (total4 + kPackThreads - 1) / kPackThreads;
   do {
     if (hipMemsetAsync(d_status, 0, sizeof(int), s) != hipSuccess) { rc = SLIM_EDEVICE; break; }
-    hipLaunchKernelGGL(k_pack, dim3((unsigned)blocks), dim3(kPackThreads), 0, s,
-                       reinterpret_cast<const float4*>(W), total4, K, reinterpret_cast<uint32_t*>(codes),
-                       reinterpret_cast<uint16_t*>(meta), scales, reinterpret_cast<uint32_t*>(mask), d_status);
+    {
+      SlimKernelTimer timer("pack", s);
+      SLIM_LAUNCH(timer, k_pack, dim3((unsigned)blocks), dim3(kPackThreads), s, reinterpret_cast<const float4*>(W),
+                  total4, K, reinterpret_cast<uint32_t*>(codes), reinterpret_cast<uint16_t*>(meta), scales,
+                  reinterpret_cast<uint32_t*>(mask), d_status);
+    }
     if (hipGetLastError() != hipSuccess) { rc = SLIM_EDEVICE; break; }
     if (hipMemcpyAsync(&h_status, d_status, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess) { rc = SLIM_EDEVICE; break; }
@@ -262,8 +270,8 @@ extern "C" int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const ui
   if (st != SLIM_OK) return st;
   dim3 grid((unsigned)(K / kBT), (unsigned)((N + kBT - 1) / kBT));
   SlimKernelTimer timer("pack_bwd", (hipStream_t)stream);
-  hipLaunchKernelGGL(k_pack_bwd, grid, dim3(256), 0, (hipStream_t)stream,
-                     reinterpret_cast<const uint32_t*>(codes), reinterpret_cast<const uint16_t*>(meta), scales, N,
-                     K, reinterpret_cast<uint32_t*>(codesT), reinterpret_cast<uint16_t*>(metaT), scalesT, mask_rc);
+  SLIM_LAUNCH(timer, k_pack_bwd, grid, dim3(256), (hipStream_t)stream, reinterpret_cast<const uint32_t*>(codes),
+              reinterpret_cast<const uint16_t*>(meta), scales, N, K, reinterpret_cast<uint32_t*>(codesT),
+              reinterpret_cast<uint16_t*>(metaT), scalesT, mask_rc);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }

@@ -512,28 +512,30 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
 // ------------------------------------------------------------------------------ launch
 template <bool BWD, int FM, int G>
 void launch_decode(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
+  SlimKernelTimer timer(BWD ? "decode_bwd" : "decode_fwd", s);
   dim3 grid((unsigned)(p.sp_row_tiles * p.sp_split + (a.r > 0 ? p.ad_jblocks * p.ad_split : 0)));
-  hipLaunchKernelGGL((k_decode<BWD, FM, G>), grid, dim3(256), 0, s, a);
+  SLIM_LAUNCH(timer, (k_decode<BWD, FM, G>), grid, dim3(256), s, a);
+}
+
+template <int FM>
+void launch_finish(const LayerArgs& a, bool bwd, hipStream_t s) {
+  SlimKernelTimer timer(bwd ? "finish_bwd" : "finish_fwd", s);
+  SLIM_LAUNCH(timer, (k_finish<FM>), dim3((unsigned)((a.rows + 15) / 16)), dim3(64), s, a);
 }
 
 template <bool BWD>
 int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int act_bf16, char* ws, hipStream_t s) {
   if (p.decode) {
-    {
-      SlimKernelTimer timer(BWD ? "decode_bwd" : "decode_fwd", s);
-      if (p.dec_fm == 1) {
-        if (p.dec_g == 1) launch_decode<BWD, 1, 1>(a, p, s);
-        else launch_decode<BWD, 1, 2>(a, p, s);
-      } else {
-        launch_decode<BWD, 2, 1>(a, p, s);
-      }
-      if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
+    if (p.dec_fm == 1) {
+      if (p.dec_g == 1) launch_decode<BWD, 1, 1>(a, p, s);
+      else launch_decode<BWD, 1, 2>(a, p, s);
+    } else {
+      launch_decode<BWD, 2, 1>(a, p, s);
     }
+    if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
     if (a.finish) {
-      SlimKernelTimer timer(BWD ? "finish_bwd" : "finish_fwd", s);
-      dim3 grid((unsigned)((a.rows + 15) / 16));
-      if (p.dec_fm == 1) hipLaunchKernelGGL((k_finish<1>), grid, dim3(64), 0, s, a);
-      else hipLaunchKernelGGL((k_finish<2>), grid, dim3(64), 0, s, a);
+      if (p.dec_fm == 1) launch_finish<1>(a, BWD, s);
+      else launch_finish<2>(a, BWD, s);
       if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
     }
     return SLIM_OK;
@@ -544,7 +546,7 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
   dim3 grid((unsigned)p.sp_row_tiles, (unsigned)p.sp_col_tiles);
-  hipLaunchKernelGGL((k_tile<BWD>), grid, dim3(kTThreads), 0, s, a);
+  SLIM_LAUNCH(timer, (k_tile<BWD>), grid, dim3(kTThreads), s, a);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }
 

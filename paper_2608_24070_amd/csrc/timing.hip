@@ -1,7 +1,7 @@
 // timing.hip - optional per-kernel timing with HIP events (host code only).
-// When enabled, each kernel launched by the library is bracketed by two hipEvents recorded on
-// the caller's stream; slim_timing_read waits for them and reports launches and summed
-// milliseconds per kernel name. Off by default; costs nothing when off.
+// When enabled, each kernel launched by the library records a start and a stop event as part of
+// its own dispatch (hipExtLaunchKernel); slim_timing_read waits for them and reports launches and
+// summed milliseconds per kernel name. Off by default; costs nothing when off.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -49,21 +49,25 @@ void drain_locked() {
 }
 }  // namespace
 
-SlimKernelTimer::SlimKernelTimer(const char* name, hipStream_t s) : name_(name), s_(s) {
+SlimKernelTimer::SlimKernelTimer(const char* name, hipStream_t s) : name_(name) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on) return;
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-  if (hipStreamIsCapturing(s_, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return;  // never inside a graph
-  a_ = take_event();
-  b_ = take_event();
-  if (a_ && b_ && hipEventRecord((hipEvent_t)a_, s_) == hipSuccess) active_ = true;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return;  // never inside a graph
+  hipEvent_t a = take_event(), b = take_event();
+  if (a && b) {
+    a_ = a;
+    b_ = b;
+  } else {
+    if (a) g_pool.push_back(a);
+    if (b) g_pool.push_back(b);
+  }
 }
 
-void SlimKernelTimer::stop() {
-  if (!active_) return;
+SlimKernelTimer::~SlimKernelTimer() {
+  if (!a_) return;
   std::lock_guard<std::mutex> lk(g_mu);
-  if (hipEventRecord((hipEvent_t)b_, s_) == hipSuccess) g_pending.push_back({name_, (hipEvent_t)a_, (hipEvent_t)b_});
-  active_ = false;
+  g_pending.push_back({name_, (hipEvent_t)a_, (hipEvent_t)b_});
   if (g_pending.size() > 4096) drain_locked();
 }
 
