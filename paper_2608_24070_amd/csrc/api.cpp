@@ -112,6 +112,7 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     }
   }
   // workspace: [counters][adapter intermediate fp16 M x r][adapter partials][sparse partials]
+  // [fp16 activations (large M)]
   q.n_counters = ad_counters;
   q.off_counters = 0;
   if (q.n_counters > kCounterSlots) return SLIM_EUNSUPPORTED;
@@ -123,6 +124,9 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
   off = round256(off + tpart_bytes);
   q.off_ypart = off;
   off = round256(off + ypart_bytes);
+  // large M: fp16 copy of bf16 activations for the tile kernel's direct-to-LDS loads
+  q.off_x16 = off;
+  if (!q.decode) off = round256(off + (size_t)M * (size_t)red * 2);
   q.total = off;
   *p = q;
   return SLIM_OK;

@@ -29,6 +29,8 @@
 // Every global load is issued unconditionally from a clamped, valid address and masked when
 // used: a load under a branch makes the compiler wait for it at the join, which serialises
 // what should be one round of memory traffic.
+#include <type_traits>
+
 #include "slim_device.h"
 #include "slim_launch.h"
 #include "slim_timing.h"
@@ -41,6 +43,7 @@ struct LayerArgs {
   const uint16_t* scales;  // forward [rows, red/128]; backward scalesT [rows/128, red]
   const uint16_t* act;     // [M, red] activations (bf16 or fp16 bits)
   int act_bf16;
+  const uint16_t* act16;   // [M, red] fp16 activations for the large-M path (act, or a converted copy)
   int64_t M, rows, red;
   int64_t r;
   const uint16_t* ad_q;    // adapter first factor, row-major [r, red]
@@ -337,11 +340,25 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
 
 // ============================================================ large-M tile kernel
 // Block = 4 waves; wave (wr, wc) owns rows [row0 + 128 wr, +128) as 4 fragments of 32 and columns
-// [m0 + 64 wc, +64) as 2 fragments of 32 (a 128 x 64 accumulator on 32x32x32 sparse MFMA). Per
-// 128-wide chunk: activations [128 x 128] in a double-buffered LDS tile (staged through
-// registers one chunk ahead), packed words in registers two chunks ahead.
-constexpr int kTR = 256, kTC = 128, kTLd = 136, kTThreads = 256;
-constexpr int kTXV = kTC * 16 / kTThreads;      // 16-byte activation vectors per thread per chunk
+// [m0 + 64 wc, +64) as 2 fragments of 32 (a 128 x 64 accumulator on 32x32x32 sparse MFMA).
+// Per 128-wide reduction chunk the fp16 activation tile [128 x 128] goes straight from memory to
+// LDS (16-byte direct loads) into a ring of three buffers, two chunks ahead; the packed words
+// go to registers two chunks ahead. LDS rows are 256 B with the 16-byte column
+// index XOR-swizzled by the row, so the B-fragment reads (32 rows at one column) hit distinct
+// banks. The backward also brings each wave's scale row (its 128-row group) into LDS.
+constexpr int kTR = 256, kTC = 128, kTThreads = 256, kStages = 3;
+// VMEM instructions per thread per chunk: 8 activation loads and 12 packed-word loads (codes,
+// index words, scales); the backward has no scale words but one scale-row load. Chunk c's loads
+// are issued in the body of chunk c - (kStages - 1); at least kStages - 2 whole bodies of loads
+// follow them (more in the prologue, which issues them in the same order), so they are complete
+// once at most that many are outstanding: the count the loop waits for before its barrier.
+constexpr int kTileVmemFwd = 8 + 12, kTileVmemBwd = 8 + 8 + 1;
+constexpr int kTileWaitFwd = (kStages - 2) * kTileVmemFwd, kTileWaitBwd = (kStages - 2) * kTileVmemBwd;
+
+// s_waitcnt immediate (gfx9 layout) waiting for at most n outstanding vector-memory operations:
+// vmcnt bits [3:0] and [15:14]; expcnt [6:4] and lgkmcnt [11:8] left at their maxima (no wait)
+constexpr unsigned vmcnt_wait(int n) { return (unsigned)(n & 15) | ((unsigned)(n >> 4) << 14) | 0x0F70u; }
+static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && kTileWaitFwd < 64, "s_waitcnt encoding");
 
 struct TileA {
   u32x4_t cw[4];
@@ -361,16 +378,20 @@ SLIM_DEV void tile_load_a(const uint32_t* const* cp, const uint32_t* const* mp, 
 }
 
 template <bool BWD>
-__global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
-  __shared__ __attribute__((aligned(16))) _Float16 xs[2][kTC][kTLd];
-  __shared__ __attribute__((aligned(16))) _Float16 ss[2][2][128];    // backward: scale row per row half
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+SLIM_DEV void tile_body(const LayerArgs& a) {
+  // one array per stage (the stage of chunk c is c % 3, a constant in the loop unrolled by three),
+  // so that reads of one stage are not ordered behind loads still landing in another
+  __shared__ __attribute__((aligned(16))) _Float16 xs0[kTC][128], xs1[kTC][128], xs2[kTC][128];
+  __shared__ __attribute__((aligned(16))) _Float16 ss0[BWD ? 4 : 1][512], ss1[BWD ? 4 : 1][512], ss2[BWD ? 4 : 1][512];
+  auto xs_at = [&](int stg) -> _Float16(*)[128] { return stg == 0 ? xs0 : (stg == 1 ? xs1 : xs2); };
+  auto ss_at = [&](int stg) -> _Float16(*)[512] { return stg == 0 ? ss0 : (stg == 1 ? ss1 : ss2); };
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr = wave & 1, wc = wave >> 1;
   const int ha = lane >> 5;
   const int64_t row0 = (int64_t)blockIdx.x * kTR, m0 = (int64_t)blockIdx.y * kTC;
   const int64_t wrow0 = row0 + 128 * wr;
   const int64_t nch = a.red / 128;
-  const bool bf16 = a.act_bf16 != 0;
 
   const uint32_t* cp[4];
   const uint32_t* mp[4];
@@ -383,28 +404,24 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
     sp[fn] = a.scales + arow * (a.red / 128);
   }
 
-  u32x4_t xr[kTXV];
-  u32x4_t sr = zero_u4();
-  auto load_x = [&](int64_t c) {
+  // activation chunk c -> stage c % kStages: wave w writes rows 32 w .. 32 w + 31, four per load
+  // (lane L: row + L / 16, LDS column slot L % 16 holding column (L % 16) ^ (row % 16))
+  const int lrow = lane >> 4, lslot = lane & 15;
+  auto dma_x = [&](int64_t c, int stg) {
+    const int64_t cc = clamp_hi(c, nch - 1);
 #pragma unroll
-    for (int i = 0; i < kTXV; ++i) {
-      const int q = tid + kTThreads * i, m = q >> 4, vc = q & 15;
-      xr[i] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(m0 + m, a.M - 1) * a.red + c * 128 + 8 * vc);
+    for (int i = 0; i < 8; ++i) {
+      const int row = 32 * wave + 4 * i + lrow;
+      const uint16_t* src =
+          a.act16 + clamp_hi(m0 + row, a.M - 1) * a.red + cc * 128 + 8 * (lslot ^ (row & 15));
+      __builtin_amdgcn_global_load_lds(src, &xs_at(stg)[32 * wave + 4 * i][0], 16, 0, 0);
     }
     if (BWD) {
-      // backward: scale row s16[n, g] of each row half's 128-row group, for this chunk
-      const int h = (tid >> 4) & 1, vc = tid & 15;
-      const int64_t gr = clamp_hi(row0 + 128 * h, a.rows - 1);
-      sr = *reinterpret_cast<const u32x4_t*>(a.scales + (gr / 128) * a.red + c * 128 + 8 * vc);
+      // the wave's scale row s16[n, g] for this chunk (g = its 128-row group), four copies
+      const int64_t g = clamp_hi(wrow0, a.rows - 1) / 128;
+      const uint16_t* src = a.scales + g * a.red + cc * 128 + 8 * lslot;
+      __builtin_amdgcn_global_load_lds(src, &ss_at(stg)[wave][0], 16, 0, 0);
     }
-  };
-  auto store_x = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < kTXV; ++i) {
-      const int q = tid + kTThreads * i, m = q >> 4, vc = q & 15;
-      *reinterpret_cast<h8_t*>(&xs[buf][m][8 * vc]) = m0 + m < a.M ? load8_as_h(xr[i], bf16) : zero_h8();
-    }
-    if (BWD && tid < 32) *reinterpret_cast<u32x4_t*>(&ss[buf][tid >> 4][8 * (tid & 15)]) = sr;
   };
 
   f16_t acc[4][2];
@@ -415,16 +432,34 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[fn][fm][v] = 0.f;
 
-  TileA cur, nxt;
-  tile_load_a<BWD>(cp, mp, sp, 0, cur);
-  load_x(0);
-  if (nch > 1) tile_load_a<BWD>(cp, mp, sp, 1, nxt);
-  store_x(0);
-  __syncthreads();
-  if (nch > 1) load_x(1);
+  // packed words: a ring of three register sets, chunk c in set c % 3, two chunks ahead; the
+  // loop is unrolled by three so that the sets rotate without copies
+  // (issued in the order the loop issues them, so the loop entry matches its back edge)
+  TileA w[3];
+  dma_x(0, 0);
+  tile_load_a<BWD>(cp, mp, sp, 0, w[0]);
+  dma_x(1, 1);
+  tile_load_a<BWD>(cp, mp, sp, clamp_hi(1, nch - 1), w[1]);
 
-  for (int64_t c = 0; c < nch; ++c) {
-    const int buf = (int)(c & 1);
+  // one chunk: wait for its activations, refill the ring two chunks ahead, multiply
+  auto chunk = [&](int64_t c, auto zc) {
+    constexpr int z = decltype(zc)::value;
+    const int stg = z;                      // c % 3 (c0 is a multiple of 3)
+    // chunk c's activations (and packed words) have landed once at most kStages - 2 chunks of later
+    // loads are outstanding.
+    // The barrier is issued as a bare instruction: the builtin would also make this wave wait
+    // for every direct-to-LDS load in flight, including the ones for the next two chunks.
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait(BWD ? kTileWaitBwd : kTileWaitFwd));
+    asm volatile("s_barrier" ::: "memory");
+    dma_x(c + kStages - 1, (z + 2) % 3);    // into the stage read in iteration c - 1
+    tile_load_a<BWD>(cp, mp, sp, clamp_hi(c + 2, nch - 1), w[(z + 2) % 3]);
+    // pin this chunk's packed words here: work on them cannot be scheduled into earlier chunks
+    // (which would make those wait for loads that are meant to stay in flight)
+    TileA& cur = w[z];
+#pragma unroll
+    for (int fn = 0; fn < 4; ++fn) {
+      asm volatile("" : "+v"(cur.cw[fn]), "+v"(cur.mw[fn]), "+v"(cur.sw[fn]));
+    }
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
       h8_t av[4];
@@ -432,14 +467,17 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
 #pragma unroll
       for (int fn = 0; fn < 4; ++fn)
         av[fn] = BWD ? dequant_word_int(cur.cw[fn][st]) : dequant_word(cur.cw[fn][st], splat_h2(cur.sw[fn]));
-      const int off = b_chunk_offset<32>(lane, st);
+      // B operand: columns (16-byte units) 2 st + ha and 2 st + ha + 8 of the chunk
+      const int c16 = 2 * st + ha;
 #pragma unroll
       for (int fm = 0; fm < 2; ++fm) {
-        const _Float16* p = &xs[buf][64 * wc + 32 * fm + (lane & 31)][off];
-        h8_t lo = *reinterpret_cast<const h8_t*>(p), hi = *reinterpret_cast<const h8_t*>(p + 64);
+        const int row = 64 * wc + 32 * fm + (lane & 31);
+        const _Float16* rp = &xs_at(stg)[row][0];
+        h8_t lo = *reinterpret_cast<const h8_t*>(rp + 8 * (c16 ^ (row & 15)));
+        h8_t hi = *reinterpret_cast<const h8_t*>(rp + 8 * ((c16 + 8) ^ (row & 15)));
         if (BWD) {
-          lo = mul_h8(lo, *reinterpret_cast<const h8_t*>(&ss[buf][wr][off]));
-          hi = mul_h8(hi, *reinterpret_cast<const h8_t*>(&ss[buf][wr][off + 64]));
+          lo = mul_h8(lo, *reinterpret_cast<const h8_t*>(&ss_at(stg)[wave][8 * c16]));
+          hi = mul_h8(hi, *reinterpret_cast<const h8_t*>(&ss_at(stg)[wave][8 * c16 + 64]));
         }
         bv[fm] = cat16(lo, hi);
       }
@@ -449,14 +487,19 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
         for (int fm = 0; fm < 2; ++fm)
           acc[fn][fm] = smfmac32(av[fn], bv[fm], acc[fn][fm], (int)cur.mw[fn][st >> 1], st & 1);
     }
-    if (c + 1 < nch) store_x(buf ^ 1);       // activations of chunk c+1 (loaded one chunk ago)
-    __syncthreads();
-    cur = nxt;
-    if (c + 2 < nch) {
-      tile_load_a<BWD>(cp, mp, sp, c + 2, nxt);
-      load_x(c + 2);
-    }
+  };
+  // full groups of three without guards (a load under a branch costs a full wait at the join),
+  // then at most two chunks
+  int64_t c0 = 0;
+  for (; c0 + 3 <= nch; c0 += 3) {
+    chunk(c0, std::integral_constant<int, 0>{});
+    chunk(c0 + 1, std::integral_constant<int, 1>{});
+    chunk(c0 + 2, std::integral_constant<int, 2>{});
   }
+  if (c0 < nch) chunk(c0, std::integral_constant<int, 0>{});
+  if (c0 + 1 < nch) chunk(c0 + 1, std::integral_constant<int, 1>{});
+  // the ring's last loads (repeats of the final chunk) must land before the block's LDS is released
+  __builtin_amdgcn_s_waitcnt(0);
 
   // adapter second product: out^T[row, m] += sum_j P[row, j] tm[m, j], on 32x32x16 fp16 MFMA;
   // both operands are row-major along j, 64 ranks per round of loads
@@ -509,6 +552,18 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
   }
 }
 
+template <bool BWD>
+__global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
+  tile_body<BWD>(a);
+}
+
+// bf16 -> fp16 (round to nearest even), 8 values per thread
+__global__ void __launch_bounds__(256) k_bf16_to_f16(const u32x4_t* __restrict__ src, u32x4_t* __restrict__ dst,
+                                                     int64_t n8) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n8) dst[i] = __builtin_bit_cast(u32x4_t, load8_as_h(src[i], true));
+}
+
 // ------------------------------------------------------------------------------ launch
 template <bool BWD, int FM, int G>
 void launch_decode(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
@@ -540,6 +595,14 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
     }
     return SLIM_OK;
   }
+  if (act_bf16) {
+    // the tile kernel streams fp16 activations straight into LDS: convert them once
+    SlimKernelTimer timer("to_f16", s);
+    const int64_t n8 = a.M * a.red / 8;
+    SLIM_LAUNCH(timer, k_bf16_to_f16, dim3((unsigned)((n8 + 255) / 256)), dim3(256), s,
+                reinterpret_cast<const u32x4_t*>(act), reinterpret_cast<u32x4_t*>(const_cast<uint16_t*>(a.act16)), n8);
+    if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
+  }
   if (a.r > 0) {
     int st = slim_launch_adapter_gemm(act, act_bf16, a.M, a.red, a.ad_q, a.r, p, ws, s);
     if (st != SLIM_OK) return st;
@@ -566,6 +629,7 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.ad_q = ad_q;
   a.ad_p = ad_p;
   a.tm = reinterpret_cast<uint16_t*>(ws + p.off_t);
+  a.act16 = (!p.decode && dtype == SLIM_BF16) ? reinterpret_cast<const uint16_t*>(ws + p.off_x16) : a.act;
   a.out = out;
   a.split = p.sp_split;
   a.row_tiles = p.sp_row_tiles;
