@@ -88,12 +88,12 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     if (q.sp_split > 1 || r > 0) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 4 * q.dec_fm * 256 * 4;
     q.lds_bytes = 0;
   } else {
-    // large M: dense adapter GEMM (64 x 64 tiles) then 256 x 128 sparse tiles
+    // large M: dense adapter GEMM (64 x 64 tiles) then 512 x 96 sparse tiles
     q.decode = false;
-    q.sp_rows_tile = 256;
-    q.sp_cols_tile = 128;
-    q.sp_row_tiles = cdiv(rows, 256);
-    q.sp_col_tiles = cdiv(M, 128);
+    q.sp_rows_tile = 512;
+    q.sp_cols_tile = 96;
+    q.sp_row_tiles = cdiv(rows, 512);
+    q.sp_col_tiles = cdiv(M, 96);
     q.sp_split = 1;
     q.sp_chunks_per_split = nchunks;
     if (r > 0) {

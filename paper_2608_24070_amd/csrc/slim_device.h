@@ -20,20 +20,33 @@ SLIM_DEV h2_t h2_of(uint32_t x) { return __builtin_bit_cast(h2_t, x); }
 // Two fp16 copies of one fp16 bit pattern.
 SLIM_DEV h2_t splat_h2(uint32_t hbits) { return h2_of((hbits & 0xFFFFu) | (hbits << 16)); }
 
+// Constants of the nibble -> fp16 step, (x & mask) | 0x64006400. Kernels that dequantise in a
+// hot loop make them opaque register values (nibble_consts_reg): with no literal to fold, the
+// compiler forms one v_and_or_b32 per pair instead of an AND and an OR that each carry a literal.
+struct NibbleConsts {
+  uint32_t lo, hi, magic;
+};
+SLIM_DEV NibbleConsts nibble_consts() { return NibbleConsts{0x000F000Fu, 0x00F000F0u, 0x64006400u}; }
+SLIM_DEV NibbleConsts nibble_consts_reg() {
+  NibbleConsts k = nibble_consts();
+  asm volatile("" : "+s"(k.lo), "+s"(k.hi), "+v"(k.magic));
+  return k;
+}
+
 // One packed code word (16 K positions, four 2:4 groups) -> the eight kept values as the
 // compressed A operand of a sparse MFMA: dword c = (first kept, second kept) of group c.
 // Nibbles are turned into exact fp16 integers with the 1024-magic: (0x6400 | u) is 1024 + u,
 // (0x6400 | 16u) is 1024 + 16u; both become u - 8 exactly. The scale multiply is the only
 // rounding step: (u - 8) * s16 rounded to fp16.
-SLIM_DEV h8_t dequant_word(uint32_t w, h2_t s2) {
+SLIM_DEV h8_t dequant_word(uint32_t w, h2_t s2, const NibbleConsts& k = nibble_consts()) {
   const h2_t m1032 = {(_Float16)-1032.0f, (_Float16)-1032.0f};
   const h2_t r16 = {(_Float16)0.0625f, (_Float16)0.0625f};
   const h2_t m72 = {(_Float16)-72.0f, (_Float16)-72.0f};
   const uint32_t w8 = w >> 8;
-  h2_t g0 = h2_of((w & 0x000F000Fu) | 0x64006400u) + m1032;
-  h2_t g1 = h2_of((w & 0x00F000F0u) | 0x64006400u) * r16 + m72;
-  h2_t g2 = h2_of((w8 & 0x000F000Fu) | 0x64006400u) + m1032;
-  h2_t g3 = h2_of((w8 & 0x00F000F0u) | 0x64006400u) * r16 + m72;
+  h2_t g0 = h2_of((w & k.lo) | k.magic) + m1032;
+  h2_t g1 = h2_of((w & k.hi) | k.magic) * r16 + m72;
+  h2_t g2 = h2_of((w8 & k.lo) | k.magic) + m1032;
+  h2_t g3 = h2_of((w8 & k.hi) | k.magic) * r16 + m72;
   g0 = g0 * s2;
   g1 = g1 * s2;
   g2 = g2 * s2;
@@ -45,15 +58,15 @@ SLIM_DEV h8_t dequant_word(uint32_t w, h2_t s2) {
 }
 
 // Same without the scale: exact integers q = u - 8.
-SLIM_DEV h8_t dequant_word_int(uint32_t w) {
+SLIM_DEV h8_t dequant_word_int(uint32_t w, const NibbleConsts& k = nibble_consts()) {
   const h2_t m1032 = {(_Float16)-1032.0f, (_Float16)-1032.0f};
   const h2_t r16 = {(_Float16)0.0625f, (_Float16)0.0625f};
   const h2_t m72 = {(_Float16)-72.0f, (_Float16)-72.0f};
   const uint32_t w8 = w >> 8;
-  h2_t g0 = h2_of((w & 0x000F000Fu) | 0x64006400u) + m1032;
-  h2_t g1 = h2_of((w & 0x00F000F0u) | 0x64006400u) * r16 + m72;
-  h2_t g2 = h2_of((w8 & 0x000F000Fu) | 0x64006400u) + m1032;
-  h2_t g3 = h2_of((w8 & 0x00F000F0u) | 0x64006400u) * r16 + m72;
+  h2_t g0 = h2_of((w & k.lo) | k.magic) + m1032;
+  h2_t g1 = h2_of((w & k.hi) | k.magic) * r16 + m72;
+  h2_t g2 = h2_of((w8 & k.lo) | k.magic) + m1032;
+  h2_t g3 = h2_of((w8 & k.hi) | k.magic) * r16 + m72;
   h8_t a;
   a[0] = g0[0]; a[1] = g0[1]; a[2] = g1[0]; a[3] = g1[1];
   a[4] = g2[0]; a[5] = g2[1]; a[6] = g3[0]; a[7] = g3[1];

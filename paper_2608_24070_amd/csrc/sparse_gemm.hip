@@ -24,11 +24,12 @@
 //    adapter). Sparse units only store their partials; k_finish sums them in a fixed order and
 //    adds the adapter's second product, so no sparse unit waits on another.
 //  * large M: the adapter's first product runs as a dense GEMM (adapter_gemm.hip); k_tile then
-//    computes 256 x 128 output tiles on 32x32x32 sparse MFMA with a double-buffered LDS
-//    activation tile and adds the second adapter product in its epilogue.
-// Every global load is issued unconditionally from a clamped, valid address and masked when
-// used: a load under a branch makes the compiler wait for it at the join, which serialises
-// what should be one round of memory traffic.
+//    computes 512 x 96 output tiles on 32x32x32 sparse MFMA, with activations and packed words
+//    streamed into a three-stage LDS ring by direct loads, and adds the second adapter product
+//    in its epilogue.
+// Every global load is issued unconditionally from a clamped (or, through a buffer resource,
+// range-checked) address and masked when used: a load under a branch makes the compiler wait
+// for it at the join, which serialises what should be one round of memory traffic.
 #include <type_traits>
 
 #include "slim_device.h"
@@ -52,7 +53,8 @@ struct LayerArgs {
   float* out;              // [M, rows]
   // small-M path
   int split;               // reduction splits of the sparse product
-  int64_t row_tiles;       // 64-row tiles
+  int64_t row_tiles;       // 64-row tiles (small M) or 512-row tiles (large M)
+  int64_t col_tiles;       // 96-column tiles (large M)
   int ad_split;            // reduction splits of the adapter's first product
   int64_t ad_jblocks;      // 64-wide column blocks of the adapter rank
   float* part;             // sparse split partials
@@ -339,153 +341,263 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
 }
 
 // ============================================================ large-M tile kernel
-// Block = 4 waves; wave (wr, wc) owns rows [row0 + 128 wr, +128) as 4 fragments of 32 and columns
-// [m0 + 64 wc, +64) as 2 fragments of 32 (a 128 x 64 accumulator on 32x32x32 sparse MFMA).
-// Per 128-wide reduction chunk the fp16 activation tile [128 x 128] goes straight from memory to
-// LDS (16-byte direct loads) into a ring of three buffers, two chunks ahead; the packed words
-// go to registers two chunks ahead. LDS rows are 256 B with the 16-byte column
-// index XOR-swizzled by the row, so the B-fragment reads (32 rows at one column) hit distinct
-// banks. The backward also brings each wave's scale row (its 128-row group) into LDS.
-constexpr int kTR = 256, kTC = 128, kTThreads = 256, kStages = 3;
-// VMEM instructions per thread per chunk: 8 activation loads and 12 packed-word loads (codes,
-// index words, scales); the backward has no scale words but one scale-row load. Chunk c's loads
-// are issued in the body of chunk c - (kStages - 1); at least kStages - 2 whole bodies of loads
-// follow them (more in the prologue, which issues them in the same order), so they are complete
-// once at most that many are outstanding: the count the loop waits for before its barrier.
-constexpr int kTileVmemFwd = 8 + 12, kTileVmemBwd = 8 + 8 + 1;
-constexpr int kTileWaitFwd = (kStages - 2) * kTileVmemFwd, kTileWaitBwd = (kStages - 2) * kTileVmemBwd;
+// Block = 4 waves; wave w owns rows [row0 + 128 w, +128) as 4 fragments of 32 and all columns
+// [m0, m0 + 96) as 3 fragments of 32: a 128 x 96 accumulator (192 registers per lane) on 32x32x32
+// sparse MFMA. Each dequantised weight fragment feeds three MFMAs and no weight row is
+// dequantised by two waves.
+// Per 128-wide reduction chunk, the fp16 activation tile [96 x 128] and each wave's packed words
+// (codes, index words and scales of its 128 rows) go straight from memory to LDS (direct loads)
+// into a ring of three stages, two chunks ahead, so no register holds data still in flight. A
+// chunk's words are read from LDS, and its first step dequantised, during the last step of the
+// chunk before. Activation rows in LDS are 256 B with the 16-byte column index XOR-swizzled by
+// the row, so B-fragment reads (32 rows at one column) hit distinct banks. The backward also
+// brings each wave's scale row (its 128-row group) into LDS.
+constexpr int kTR = 512, kTC = 96, kTThreads = 256, kStages = 3, kBand = 4;
+// Direct loads per thread per chunk, issued in this order: packed words (4 code loads, 2 index
+// word loads, and in the forward 2 scale loads), then 6 activation loads (and in the backward one
+// scale-row load). Chunk c's loads are issued at the top of chunk c - 2.
+//  * at the top of chunk c its activations must have landed: only chunk c - 1's loads may still
+//    be outstanding;
+//  * in the last step of chunk c, chunk c + 1's words must have landed: only chunk c + 1's
+//    activation (and scale-row) loads and chunk c's loads may still be outstanding.
+// The prologue issues chunks 0 and 1 in the same order, so the same counts hold from the start.
+constexpr int kTileWordsFwd = 4 + 2 + 2, kTileWordsBwd = 4 + 2, kTileActFwd = 6, kTileActBwd = 6 + 1;
+constexpr int kTileTopFwd = kTileWordsFwd + kTileActFwd, kTileTopBwd = kTileWordsBwd + kTileActBwd;
+constexpr int kTileNextFwd = kTileActFwd + kTileTopFwd, kTileNextBwd = kTileActBwd + kTileTopBwd;
 
 // s_waitcnt immediate (gfx9 layout) waiting for at most n outstanding vector-memory operations:
 // vmcnt bits [3:0] and [15:14]; expcnt [6:4] and lgkmcnt [11:8] left at their maxima (no wait)
 constexpr unsigned vmcnt_wait(int n) { return (unsigned)(n & 15) | ((unsigned)(n >> 4) << 14) | 0x0F70u; }
-static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && kTileWaitFwd < 64, "s_waitcnt encoding");
+// the same with lgkmcnt 0: also every LDS read of this wave has returned
+constexpr unsigned vmcnt_lgkm0_wait(int n) { return vmcnt_wait(n) & ~0x0F00u; }
+static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && kTileNextFwd < 64, "s_waitcnt encoding");
+static_assert(vmcnt_lgkm0_wait(20) == 0x4074u, "s_waitcnt encoding");
 
-struct TileA {
+// The tile kernel addresses memory through buffer resources: a wave-uniform base in scalar
+// registers, a per-lane 32-bit byte offset (one vector register per address) and a uniform
+// chunk offset. A read at or past the resource's extent returns zero without touching memory.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;   // gfx9 buffer descriptor word 3: raw 32-bit data
+SLIM_DEV rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int64_t n = bytes < 0xFFFFFFFFll ? bytes : 0xFFFFFFFFll;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)(uint32_t)n, kRsrcWord3);
+}
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// One chunk's packed words of the four waves, as the direct loads lay them down (lane L of a load
+// at 16 L, or 4 L for 2-byte loads): codes [wave][fragment][lane] (16 B: the lane's four code
+// words), index words [wave][row slot] (16 B: the row's four words; row slot = 32 fragment + row
+// in fragment), scales [wave][row slot] (fp16 in the low half of a dword). Reads index these
+// arrays directly (no pointer casts, and no 8-byte reads the compiler would pair into one
+// instruction that has lost track of its address), so that the compiler can tell the stages
+// apart and does not wait for every direct load in flight.
+template <bool BWD>
+struct TileWordsLds {
+  u32x4_t cw[4][4][64];
+  u32x4_t mw[4][128];
+  uint32_t sw[BWD ? 1 : 4][BWD ? 1 : 128];
+};
+// one chunk's packed words of one lane, read from LDS
+struct TileWords {
   u32x4_t cw[4];
   u32x2_t mw[4];
   uint32_t sw[4];
 };
 
 template <bool BWD>
-SLIM_DEV void tile_load_a(const uint32_t* const* cp, const uint32_t* const* mp, const uint16_t* const* sp, int64_t c,
-                          TileA& t) {
-#pragma unroll
-  for (int fn = 0; fn < 4; ++fn) {
-    t.cw[fn] = *reinterpret_cast<const u32x4_t*>(cp[fn] + 8 * c);
-    t.mw[fn] = *reinterpret_cast<const u32x2_t*>(mp[fn] + 4 * c);
-    t.sw[fn] = BWD ? 0u : (uint32_t)sp[fn][c];
-  }
-}
-
-template <bool BWD>
 SLIM_DEV void tile_body(const LayerArgs& a) {
   // one array per stage (the stage of chunk c is c % 3, a constant in the loop unrolled by three),
   // so that reads of one stage are not ordered behind loads still landing in another
   __shared__ __attribute__((aligned(16))) _Float16 xs0[kTC][128], xs1[kTC][128], xs2[kTC][128];
+  __shared__ __attribute__((aligned(16))) TileWordsLds<BWD> ws0, ws1, ws2;
   __shared__ __attribute__((aligned(16))) _Float16 ss0[BWD ? 4 : 1][512], ss1[BWD ? 4 : 1][512], ss2[BWD ? 4 : 1][512];
   auto xs_at = [&](int stg) -> _Float16(*)[128] { return stg == 0 ? xs0 : (stg == 1 ? xs1 : xs2); };
+  auto ws_at = [&](int stg) -> TileWordsLds<BWD>& { return stg == 0 ? ws0 : (stg == 1 ? ws1 : ws2); };
   auto ss_at = [&](int stg) -> _Float16(*)[512] { return stg == 0 ? ss0 : (stg == 1 ? ss1 : ss2); };
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wr = wave & 1, wc = wave >> 1;
   const int ha = lane >> 5;
-  const int64_t row0 = (int64_t)blockIdx.x * kTR, m0 = (int64_t)blockIdx.y * kTC;
-  const int64_t wrow0 = row0 + 128 * wr;
+  // XCD-aware tile order: block b runs on XCD b % 8 (workgroups are dealt round robin), and XCD x
+  // takes positions [x Q, (x + 1) Q) of a tile order that walks bands of kBand row tiles column
+  // by column. The blocks an XCD runs together then cover a few row tiles x a few column tiles,
+  // so they share packed weights and activations in that XCD's L2.
+  const int64_t R = a.row_tiles, C = a.col_tiles, T = R * C;
+  const int64_t Q = (T + 7) / 8;
+  const int64_t pos = (int64_t)(blockIdx.x % 8) * Q + blockIdx.x / 8;
+  if (pos >= T) return;
+  const int64_t band = pos / (kBand * C), q = pos - band * kBand * C;
+  const int64_t rb = R - band * kBand < kBand ? R - band * kBand : kBand;   // rows in this band
+  const int64_t rt = band * kBand + q % rb, ct = q / rb;
+  const int64_t row0 = rt * kTR, m0 = ct * kTC;
+  const int64_t wrow0 = row0 + 128 * wave;
   const int64_t nch = a.red / 128;
 
-  const uint32_t* cp[4];
-  const uint32_t* mp[4];
-  const uint16_t* sp[4];
-#pragma unroll
-  for (int fn = 0; fn < 4; ++fn) {
-    const int64_t arow = clamp_hi(wrow0 + 32 * fn + (lane & 31), a.rows - 1);
-    cp[fn] = a.codes + arow * (a.red / 16) + 4 * ha;
-    mp[fn] = a.meta + arow * (a.red / 32) + 2 * ha;
-    sp[fn] = a.scales + arow * (a.red / 128);
-  }
+  // Addresses. Per-lane offsets are derived inside each chunk from a few base registers (made
+  // opaque per chunk) instead of being kept live across the loop. Rows past the matrix (or past
+  // M) get offsets at or beyond their resource's extent and read as zero; their results are not
+  // stored. The uniform chunk offset only ever moves a valid row within that row.
+  // packed words: resources from the wave's first row (clamped into the matrix); a lane of a
+  // words load serves row 32 f + L % 32, f = the load's first fragment + L / 32
+  const int64_t wbase = clamp_hi(wrow0, a.rows - 1), wrows = a.rows - wbase;
+  const rsrc_t rc = make_rsrc(a.codes + wbase * (a.red / 16), wrows * (a.red / 16) * 4);
+  const rsrc_t rm = make_rsrc(a.meta + wbase * (a.red / 32), wrows * (a.red / 32) * 4);
+  const rsrc_t rs = make_rsrc(a.scales + wbase * (a.red / 128), wrows * (a.red / 128) * 2);
+  const uint32_t dr0 = (uint32_t)(wrow0 - wbase) + (uint32_t)(lane & 31);   // fragment 0's row
+  const uint32_t cstr = (uint32_t)(a.red / 16) * 4u, mstr = (uint32_t)(a.red / 32) * 4u,
+                 sstr = (uint32_t)(a.red / 128) * 2u;   // bytes per row
+  const uint32_t co0 = dr0 * cstr + 16u * ha;            // codes: lane's 16 B of fragment 0
+  const uint32_t ro0 = dr0 + 32u * ha;                   // index words, scales: the lane's row
 
-  // activation chunk c -> stage c % kStages: wave w writes rows 32 w .. 32 w + 31, four per load
-  // (lane L: row + L / 16, LDS column slot L % 16 holding column (L % 16) ^ (row % 16))
+  // activation chunk c -> stage c % kStages: wave w writes rows 24 w .. 24 w + 23, four per load
+  // (lane L: row + L / 16, LDS column slot L % 16 holding column (L % 16) ^ (row % 16)).
+  // Load i covers rows 24 w + 4 i + L / 16; with S = 16 ((L % 16) ^ (L / 16)) its byte offset is
+  // (24 w + L / 16) 2 red + 8 i red + (S ^ 16 ((8 (w % 2) + 4 i) % 16)), as 2 red is a multiple
+  // of 256 and S < 256.
   const int lrow = lane >> 4, lslot = lane & 15;
-  auto dma_x = [&](int64_t c, int stg) {
-    const int64_t cc = clamp_hi(c, nch - 1);
+  const int64_t brows = a.M - m0 < kTC ? a.M - m0 : kTC;
+  const rsrc_t rx = make_rsrc(a.act16 + m0 * a.red, brows * a.red * 2);    // the block's activation rows
+  const uint32_t xo0 = (uint32_t)(24 * wave + lrow) * (uint32_t)a.red * 2u + 16u * (uint32_t)(lslot ^ lrow);
+  const uint32_t xstep = 8u * (uint32_t)a.red;
+  const rsrc_t rg = make_rsrc(a.scales + (wbase / 128) * a.red, a.red * 2);   // backward: the wave's scale row
+
+  auto dma_words = [&](int64_t c, int stg, uint32_t co, uint32_t ro) {
+    const int cc = (int)clamp_hi(c, nch - 1);
+    TileWordsLds<BWD>& W = ws_at(stg);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int row = 32 * wave + 4 * i + lrow;
-      const uint16_t* src =
-          a.act16 + clamp_hi(m0 + row, a.M - 1) * a.red + cc * 128 + 8 * (lslot ^ (row & 15));
-      __builtin_amdgcn_global_load_lds(src, &xs_at(stg)[32 * wave + 4 * i][0], 16, 0, 0);
-    }
-    if (BWD) {
-      // the wave's scale row s16[n, g] for this chunk (g = its 128-row group), four copies
-      const int64_t g = clamp_hi(wrow0, a.rows - 1) / 128;
-      const uint16_t* src = a.scales + g * a.red + cc * 128 + 8 * lslot;
-      __builtin_amdgcn_global_load_lds(src, &ss_at(stg)[wave][0], 16, 0, 0);
+    for (int fn = 0; fn < 4; ++fn)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (lds_ptr_t)&W.cw[wave][fn][0], 16, co + fn * 32u * cstr, 32 * cc, 0, 0);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rm, (lds_ptr_t)&W.mw[wave][64 * j], 16, (ro + 64u * j) * mstr, 16 * cc, 0, 0);
+    if (!BWD) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)&W.sw[wave][64 * j], 2, (ro + 64u * j) * sstr, 2 * cc, 0, 0);
     }
   };
+  auto dma_act = [&](int64_t c, int stg, uint32_t xo) {
+    const int cc = (int)clamp_hi(c, nch - 1);
+#pragma unroll
+    for (int i = 0; i < 6; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)&xs_at(stg)[24 * wave + 4 * i][0], 16,
+                                               (xo ^ (16u * ((8u * (wave & 1) + 4u * i) & 15u))) + (uint32_t)i * xstep,
+                                               256 * cc, 0, 0);
+    if (BWD) {
+      // the wave's scale row s16[n, g] for this chunk (g = its 128-row group), four copies
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, (lds_ptr_t)&ss_at(stg)[wave][0], 16, 16u * lslot, 256 * cc, 0, 0);
+    }
+  };
+  auto read_words = [&](int stg, TileWords& t) {
+    const TileWordsLds<BWD>& W = ws_at(stg);
+#pragma unroll
+    for (int fn = 0; fn < 4; ++fn) {
+      t.cw[fn] = W.cw[wave][fn][lane];
+      const u32x4_t m4 = W.mw[wave][32 * fn + (lane & 31)];
+      t.mw[fn] = ha ? u32x2_t{m4[2], m4[3]} : u32x2_t{m4[0], m4[1]};
+      t.sw[fn] = BWD ? 0u : W.sw[wave][32 * fn + (lane & 31)];
+    }
+  };
+  const NibbleConsts nk = nibble_consts_reg();
+  auto dequant = [&](const TileWords& t, int st, h8_t* av) {
+#pragma unroll
+    for (int fn = 0; fn < 4; ++fn)
+      av[fn] = BWD ? dequant_word_int(t.cw[fn][st], nk) : dequant_word(t.cw[fn][st], splat_h2(t.sw[fn]), nk);
+  };
+  // B-fragment reads: fragment fm of step st reads row 32 fm + L % 32 at 16-byte column slots
+  // (2 st + L / 32) ^ (L % 16) (low half) and that + 8 (high half); with
+  // bo = 256 (L % 32) + 16 ((L % 16) ^ (L / 32)) these are at bytes 8192 fm + (bo ^ 32 st) and
+  // 8192 fm + (bo ^ (32 st + 128)) of the stage.
+  const uint32_t bo0 = 256u * (uint32_t)(lane & 31) + 16u * (uint32_t)((lane & 15) ^ ha);
 
-  f16_t acc[4][2];
+  f16_t acc[4][3];
 #pragma unroll
   for (int fn = 0; fn < 4; ++fn)
 #pragma unroll
-    for (int fm = 0; fm < 2; ++fm)
+    for (int fm = 0; fm < 3; ++fm)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[fn][fm][v] = 0.f;
 
-  // packed words: a ring of three register sets, chunk c in set c % 3, two chunks ahead; the
-  // loop is unrolled by three so that the sets rotate without copies
-  // (issued in the order the loop issues them, so the loop entry matches its back edge)
-  TileA w[3];
-  dma_x(0, 0);
-  tile_load_a<BWD>(cp, mp, sp, 0, w[0]);
-  dma_x(1, 1);
-  tile_load_a<BWD>(cp, mp, sp, clamp_hi(1, nch - 1), w[1]);
+  // words of chunk c in set c % 3 (read during chunk c - 1); A operands double-buffered by step
+  TileWords tw[3];
+  h8_t aq[2][4];
+  dma_words(0, 0, co0, ro0);
+  dma_act(0, 0, xo0);
+  dma_words(1, 1, co0, ro0);
+  dma_act(1, 1, xo0);
+  __builtin_amdgcn_s_waitcnt(vmcnt_wait(BWD ? kTileNextBwd : kTileNextFwd));   // chunk 0's words
+  read_words(0, tw[0]);
+  dequant(tw[0], 0, aq[0]);
 
-  // one chunk: wait for its activations, refill the ring two chunks ahead, multiply
   auto chunk = [&](int64_t c, auto zc) {
     constexpr int z = decltype(zc)::value;
     const int stg = z;                      // c % 3 (c0 is a multiple of 3)
-    // chunk c's activations (and packed words) have landed once at most kStages - 2 chunks of later
-    // loads are outstanding.
+    // Nothing of the previous chunk is scheduled past this point.
+    __builtin_amdgcn_sched_barrier(0);
+    // chunk c's activations have landed once only chunk c - 1's loads are outstanding; and this
+    // wave's LDS reads of the stage refilled below have returned (lgkmcnt 0), so after the
+    // barrier no wave still reads it.
     // The barrier is issued as a bare instruction: the builtin would also make this wave wait
-    // for every direct-to-LDS load in flight, including the ones for the next two chunks.
-    __builtin_amdgcn_s_waitcnt(vmcnt_wait(BWD ? kTileWaitBwd : kTileWaitFwd));
+    // for every direct-to-LDS load in flight, including the ones for the next chunk.
+    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(BWD ? kTileTopBwd : kTileTopFwd));
     asm volatile("s_barrier" ::: "memory");
-    dma_x(c + kStages - 1, (z + 2) % 3);    // into the stage read in iteration c - 1
-    tile_load_a<BWD>(cp, mp, sp, clamp_hi(c + 2, nch - 1), w[(z + 2) % 3]);
-    // pin this chunk's packed words here: work on them cannot be scheduled into earlier chunks
-    // (which would make those wait for loads that are meant to stay in flight)
-    TileA& cur = w[z];
+    // this chunk's copies of the base offsets (opaque, so nothing derived from them is hoisted)
+    uint32_t xo = xo0, co = co0, ro = ro0, bo = bo0;
+    asm volatile("" : "+v"(xo), "+v"(co), "+v"(ro), "+v"(bo));
+    const TileWords& cur = tw[z];
+    TileWords& nxt = tw[(z + 1) % 3];
+
+    auto read_b = [&](int st, int fm, h16_t& bv) {
+      const char* xsb = reinterpret_cast<const char*>(&xs_at(stg)[0][0]);
+      h8_t lo = *reinterpret_cast<const h8_t*>(xsb + (bo ^ (32u * st)) + 8192 * fm);
+      h8_t hi = *reinterpret_cast<const h8_t*>(xsb + (bo ^ (32u * st + 128u)) + 8192 * fm);
+      if (BWD) {
+        const int c16 = 2 * st + ha;
+        lo = mul_h8(lo, *reinterpret_cast<const h8_t*>(&ss_at(stg)[wave][8 * c16]));
+        hi = mul_h8(hi, *reinterpret_cast<const h8_t*>(&ss_at(stg)[wave][8 * c16 + 64]));
+      }
+      bv = cat16(lo, hi);
+    };
+    // Software pipeline over the four steps. The MFMAs of a step run column fragment by column
+    // fragment; once the four MFMAs of fragment fm have issued, its registers are refilled with
+    // the next step's fragment fm (one B buffer), while the next step's dequantised weights go to
+    // the other A buffer. During the last step the next chunk's words are read and its first step
+    // dequantised.
+    h16_t bq[3];
 #pragma unroll
-    for (int fn = 0; fn < 4; ++fn) {
-      asm volatile("" : "+v"(cur.cw[fn]), "+v"(cur.mw[fn]), "+v"(cur.sw[fn]));
-    }
+    for (int fm = 0; fm < 3; ++fm) read_b(0, fm, bq[fm]);
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
-      h8_t av[4];
-      h16_t bv[2];
-#pragma unroll
-      for (int fn = 0; fn < 4; ++fn)
-        av[fn] = BWD ? dequant_word_int(cur.cw[fn][st]) : dequant_word(cur.cw[fn][st], splat_h2(cur.sw[fn]));
-      // B operand: columns (16-byte units) 2 st + ha and 2 st + ha + 8 of the chunk
-      const int c16 = 2 * st + ha;
-#pragma unroll
-      for (int fm = 0; fm < 2; ++fm) {
-        const int row = 64 * wc + 32 * fm + (lane & 31);
-        const _Float16* rp = &xs_at(stg)[row][0];
-        h8_t lo = *reinterpret_cast<const h8_t*>(rp + 8 * (c16 ^ (row & 15)));
-        h8_t hi = *reinterpret_cast<const h8_t*>(rp + 8 * ((c16 + 8) ^ (row & 15)));
-        if (BWD) {
-          lo = mul_h8(lo, *reinterpret_cast<const h8_t*>(&ss_at(stg)[wave][8 * c16]));
-          hi = mul_h8(hi, *reinterpret_cast<const h8_t*>(&ss_at(stg)[wave][8 * c16 + 64]));
-        }
-        bv[fm] = cat16(lo, hi);
+      // chunk c + 2's direct loads, into the stage read in chunk c - 1: words during step 0,
+      // activations during step 1, one load after each MFMA (issued in a burst at the barrier,
+      // the four waves' loads would fill the address unit's queue and stall instruction issue)
+      if (st == 0) dma_words(c + kStages - 1, (z + 2) % 3, co, ro);
+      if (st == 1) dma_act(c + kStages - 1, (z + 2) % 3, xo);
+      if (st < 3) {
+        dequant(cur, st + 1, aq[(st + 1) & 1]);
+      } else {
+        __builtin_amdgcn_s_waitcnt(vmcnt_wait(BWD ? kTileNextBwd : kTileNextFwd));   // chunk c + 1's words
+        read_words((z + 1) % 3, nxt);
+        dequant(nxt, 0, aq[0]);
       }
 #pragma unroll
-      for (int fn = 0; fn < 4; ++fn)
+      for (int fm = 0; fm < 3; ++fm) {
 #pragma unroll
-        for (int fm = 0; fm < 2; ++fm)
-          acc[fn][fm] = smfmac32(av[fn], bv[fm], acc[fn][fm], (int)cur.mw[fn][st >> 1], st & 1);
+        for (int fn = 0; fn < 4; ++fn)
+          acc[fn][fm] = smfmac32(aq[st & 1][fn], bq[fm], acc[fn][fm], (int)cur.mw[fn][st >> 1], st & 1);
+        if (st < 3) read_b(st + 1, fm, bq[fm]);
+      }
+      // interleave: each MFMA followed by a share of the VALU work and, in steps 0 and 1, by one
+      // direct load; the LDS reads of fragment fm follow its four MFMAs (the next chunk's words
+      // are read at the start of the last step)
+      const int nvm = st == 0 ? (BWD ? kTileWordsBwd : kTileWordsFwd) : st == 1 ? (BWD ? kTileActBwd : kTileActFwd) : 0;
+#pragma unroll
+      for (int i = 0; i < 12; ++i) {
+        if (st == 3 && i < 6) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);   // DS read
+        __builtin_amdgcn_sched_group_barrier(0x0008, 1, 0);                          // MFMA
+        if (i < nvm) __builtin_amdgcn_sched_group_barrier(0x0020, 1, 0);             // VMEM read
+        __builtin_amdgcn_sched_group_barrier(0x0002, 4, 0);                          // VALU
+        if (st < 3 && i % 4 == 3) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);   // DS read
+      }
     }
   };
   // full groups of three without guards (a load under a branch costs a full wait at the join),
@@ -501,43 +613,65 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   // the ring's last loads (repeats of the final chunk) must land before the block's LDS is released
   __builtin_amdgcn_s_waitcnt(0);
 
-  // adapter second product: out^T[row, m] += sum_j P[row, j] tm[m, j], on 32x32x16 fp16 MFMA;
-  // both operands are row-major along j, 64 ranks per round of loads
+  // adapter second product: out^T[row, m] += sum_j P[row, j] tm[m, j], on 32x32x16 fp16 MFMA.
+  // Both operands are row-major along j; step t covers ranks [16 t, 16 t + 16) (r is a multiple
+  // of 16, so every step is whole). The operands of step t are loaded three steps ahead into a
+  // ring of four register sets (the loop is unrolled by four; loads past the last step repeat it
+  // and are not used). Rows past the matrix or past M read clamped rows; their results are not
+  // stored.
   if (a.r > 0) {
-    for (int64_t jb = 0; jb < a.r; jb += 64) {
-      u32x4_t aq[4][4], bq[4][2];     // [kk][fn], [kk][fm]
+    const int64_t nj = a.r / 16;
+    const rsrc_t rp = make_rsrc(a.ad_p, a.rows * a.r * 2), rt = make_rsrc(a.tm, a.M * a.r * 2);
+    uint32_t po[4], to[3];
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int64_t jj = clamp_hi(jb + 16 * kk + 8 * ha, a.r - 8);
+    for (int fn = 0; fn < 4; ++fn)
+      po[fn] = ((uint32_t)clamp_hi(wrow0 + 32 * fn + (lane & 31), a.rows - 1) * (uint32_t)a.r + 8u * ha) * 2u;
+#pragma unroll
+    for (int fm = 0; fm < 3; ++fm)
+      to[fm] = ((uint32_t)clamp_hi(m0 + 32 * fm + (lane & 31), a.M - 1) * (uint32_t)a.r + 8u * ha) * 2u;
+    struct AdRegs { u32x4_t pa[4], pb[3]; };
+    AdRegs ar[4];
+    auto ad_load = [&](int64_t t, AdRegs& R) {
+      const int so = (int)(clamp_hi(t, nj - 1) * 32);
+#pragma unroll
+      for (int fn = 0; fn < 4; ++fn) R.pa[fn] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, po[fn], so, 0));
+#pragma unroll
+      for (int fm = 0; fm < 3; ++fm) R.pb[fm] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rt, to[fm], so, 0));
+    };
+    ad_load(0, ar[0]);
+    ad_load(1, ar[1]);
+    ad_load(2, ar[2]);
+    auto ad_step = [&](int64_t t, auto uc) {
+      constexpr int u = decltype(uc)::value;
+      ad_load(t + 3, ar[(u + 3) % 4]);
+      // step t's loads have landed once only the three later steps' loads are outstanding
+      __builtin_amdgcn_s_waitcnt(vmcnt_wait(3 * 7));
+      AdRegs& R = ar[u];
+#pragma unroll
+      for (int fn = 0; fn < 4; ++fn) asm volatile("" : "+v"(R.pa[fn]));
+#pragma unroll
+      for (int fm = 0; fm < 3; ++fm) asm volatile("" : "+v"(R.pb[fm]));
+      if (t < nj) {
 #pragma unroll
         for (int fn = 0; fn < 4; ++fn)
-          aq[kk][fn] =
-              *reinterpret_cast<const u32x4_t*>(a.ad_p + clamp_hi(wrow0 + 32 * fn + (lane & 31), a.rows - 1) * a.r + jj);
 #pragma unroll
-        for (int fm = 0; fm < 2; ++fm)
-          bq[kk][fm] =
-              *reinterpret_cast<const u32x4_t*>(a.tm + clamp_hi(m0 + 64 * wc + 32 * fm + (lane & 31), a.M - 1) * a.r + jj);
+          for (int fm = 0; fm < 3; ++fm)
+            acc[fn][fm] = mfma32(__builtin_bit_cast(h8_t, R.pa[fn]), __builtin_bit_cast(h8_t, R.pb[fm]), acc[fn][fm]);
       }
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const bool jok = jb + 16 * kk + 8 * ha < a.r;
-#pragma unroll
-        for (int fn = 0; fn < 4; ++fn) {
-          const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[kk][fn]) : zero_h8();
-#pragma unroll
-          for (int fm = 0; fm < 2; ++fm) {
-            const h8_t bv = (m0 + 64 * wc + 32 * fm + (lane & 31) < a.M) ? __builtin_bit_cast(h8_t, bq[kk][fm]) : zero_h8();
-            acc[fn][fm] = mfma32(av, bv, acc[fn][fm]);
-          }
-        }
-      }
+    };
+    for (int64_t t0 = 0; t0 < nj; t0 += 4) {
+      ad_step(t0, std::integral_constant<int, 0>{});
+      ad_step(t0 + 1, std::integral_constant<int, 1>{});
+      ad_step(t0 + 2, std::integral_constant<int, 2>{});
+      ad_step(t0 + 3, std::integral_constant<int, 3>{});
     }
+    __builtin_amdgcn_s_waitcnt(0);
   }
 
   // D[i][j] of a 32x32 fragment: lane j + 32 * ((i / 4) % 2), element 4 * (i / 8) + i % 4
 #pragma unroll
-  for (int fm = 0; fm < 2; ++fm) {
-    const int64_t m = m0 + 64 * wc + 32 * fm + (lane & 31);
+  for (int fm = 0; fm < 3; ++fm) {
+    const int64_t m = m0 + 32 * fm + (lane & 31);
     if (m >= a.M) continue;
 #pragma unroll
     for (int fn = 0; fn < 4; ++fn)
@@ -608,7 +742,7 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
     if (st != SLIM_OK) return st;
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
-  dim3 grid((unsigned)p.sp_row_tiles, (unsigned)p.sp_col_tiles);
+  dim3 grid((unsigned)(8 * ((p.sp_row_tiles * p.sp_col_tiles + 7) / 8)));
   SLIM_LAUNCH(timer, (k_tile<BWD>), grid, dim3(kTThreads), s, a);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }
@@ -633,6 +767,7 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.out = out;
   a.split = p.sp_split;
   a.row_tiles = p.sp_row_tiles;
+  a.col_tiles = p.sp_col_tiles;
   a.ad_split = p.ad_split;
   a.ad_jblocks = p.ad_jblocks;
   a.part = reinterpret_cast<float*>(ws + p.off_ypart);

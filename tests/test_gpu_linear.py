@@ -47,6 +47,12 @@ def test_tile_kernel_ragged(m, r):
     _fwd_case(768, 1024, r, m, name="ragged")
 
 
+@pytest.mark.parametrize("k,m", [(128, 100), (256, 97), (384, 130)])
+def test_tile_kernel_short_reduction(k, m):
+    # one to three 128-wide chunks: the tile kernel's prologue and remainder paths alone
+    _fwd_case(528, k, 16, m, name="shortk")
+
+
 def test_linear_on_oracle_pack():
     _fwd_case(1024, 1024, 64, 16, use_oracle_pack=True, name="opack")
     _fwd_case(1024, 1024, 64, 256, use_oracle_pack=True, name="opack")
