@@ -91,8 +91,17 @@ int slim_abi_version(void);
  * (SLiM preliminaries, eq. symmetric_quantization) with groups of 128 (SLiM setup).
  *
  *   W       fp32 [N, K], device.
- *   N, K    N >= 1; K >= 128 and K % 128 == 0.
- *   codes   out, uint8 [N, K/4]; meta out, uint8 [N, K/8]; scales out, uint16 [N, K/128].
+ *   N, K    N >= 16 and N % 16 == 0; K >= 128 and K % 128 == 0.
+ *   codes   out, uint8 [N/16][K/128][16][32]; meta out, uint8 [N/16][K/128][16][16];
+ *   scales  out, uint16 [N/16][K/128][16]. The packed layout keeps rows in blocks of 16 and K in
+ *           chunks of 128: row n, chunk c (positions 128c .. 128c+127) owns slot
+ *           ((n/16) * (K/128) + c) * 16 + n%16, holding 8 code words (uint32, little-endian;
+ *           word i covers positions 16i .. 16i+15 of the chunk: the kept codes, as q + 8, of
+ *           its four 2:4 groups, the first kept of group g in nibble g, the second in nibble
+ *           g+4), 8 index
+ *           half-words (uint16; nibble g = i0 | i1 << 2, the kept positions of group g) and one
+ *           fp16 scale (the chunk is one quantisation group). The blocks keep one chunk of 16
+ *           rows contiguous (512 B of codes, 256 B of indices, 32 B of scales).
  *   mask    out, optional (NULL to skip): uint8 [N, K], 1 where the weight is kept.
  * Mask rule: in each aligned group of four along K, keep the two largest |w|; on equal
  * magnitude the lower position wins (-0 and +0 are equal). Codes: q = clamp(rint(w / s16), -7, 7)
@@ -111,8 +120,10 @@ int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, uint8_t* met
  * sparsity_ratio gives the extra zeros, 9.375% for 2:4).
  *
  *   codes, meta, scales   a forward pack of an [N, K] weight (from slim_pack), device.
- *   N, K                  N >= 16 and N % 16 == 0; K % 128 == 0.
- *   codesT  out, uint8 [K, N/4]; metaT out, uint8 [K, N/8]; scalesT out, uint16 [K/128, N].
+ *   N, K                  N >= 128 and N % 128 == 0; K % 128 == 0.
+ *   codesT  out, uint8 [K/16][N/128][16][32]; metaT out, uint8 [K/16][N/128][16][16]: the packed
+ *           layout of slim_pack with rows k and reduction n (W^{R,C} transposed, pruned 2:4
+ *           along n). scalesT out, uint16 [K/128, N]: s16[n, k/128] by 128-group of k.
  *   mask_rc out, optional (NULL to skip): uint8 [N, K], 1 on the support of W^{R,C}.
  * Rule: for each column k and aligned group of four rows, keep two slots ranked by
  * (|Wc| descending, forward-kept descending, row ascending). A kept slot carries its forward

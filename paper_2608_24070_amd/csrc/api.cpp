@@ -34,8 +34,8 @@ extern "C" int slim_abi_version(void) { return SLIM_ABI_VERSION; }
 int slim_check_pack(const float* W, int64_t N, int64_t K, const void* codes, const void* meta,
                     const void* scales, const void* mask) {
   if (!W || !codes || !meta || !scales) return SLIM_EINVAL;
-  if (N < 1 || K < 128 || N >= kMaxDim || K >= kMaxDim) return SLIM_ESHAPE;
-  if (K % 128) return SLIM_ESHAPE;
+  if (N < 16 || K < 128 || N >= kMaxDim || K >= kMaxDim) return SLIM_ESHAPE;
+  if (N % 16 || K % 128) return SLIM_ESHAPE;   // whole 16-row blocks and 128-wide chunks
   if (!slim_aligned16(W) || !slim_aligned16(codes) || !slim_aligned16(meta) || !slim_aligned16(scales) ||
       (mask && !slim_aligned16(mask)))
     return SLIM_EALIGN;
@@ -45,8 +45,8 @@ int slim_check_pack(const float* W, int64_t N, int64_t K, const void* codes, con
 int slim_check_pack_bwd(const void* codes, const void* meta, const void* scales, int64_t N, int64_t K,
                         const void* codesT, const void* metaT, const void* scalesT, const void* mask_rc) {
   if (!codes || !meta || !scales || !codesT || !metaT || !scalesT) return SLIM_EINVAL;
-  if (N < 16 || K < 128 || N >= kMaxDim || K >= kMaxDim) return SLIM_ESHAPE;
-  if (N % 16 || K % 128) return SLIM_ESHAPE;
+  if (N < 128 || K < 128 || N >= kMaxDim || K >= kMaxDim) return SLIM_ESHAPE;
+  if (N % 128 || K % 128) return SLIM_ESHAPE;   // the transposed pack chunks N by 128
   if (!slim_aligned16(codes) || !slim_aligned16(meta) || !slim_aligned16(scales) || !slim_aligned16(codesT) ||
       !slim_aligned16(metaT) || !slim_aligned16(scalesT) || (mask_rc && !slim_aligned16(mask_rc)))
     return SLIM_EALIGN;

@@ -73,11 +73,12 @@ k_pack(const float4* __restrict__ W, int64_t total4, int64_t K, uint32_t* __rest
   mw |= __shfl_xor(mw, 2, 64);
   if (!valid) return;
   const int64_t row = t / (K / 4);
+  const int64_t slot = packed_slot(row, j >> 5, K / 128);   // word (j >> 2) & 7 of chunk j >> 5
   if (c == 0) {
-    codes[t >> 2] = cw;
-    meta[t >> 2] = (uint16_t)mw;
+    codes[8 * slot + ((j >> 2) & 7)] = cw;
+    meta[8 * slot + ((j >> 2) & 7)] = (uint16_t)mw;
   }
-  if ((j & 31) == 0) scales[row * (K / 128) + (j >> 5)] = s16bits;
+  if ((j & 31) == 0) scales[slot] = s16bits;
   if (mask) mask[t] = (uint32_t)keep[0] | ((uint32_t)keep[1] << 8) | ((uint32_t)keep[2] << 16) |
                       ((uint32_t)keep[3] << 24);
 }
@@ -105,8 +106,11 @@ k_pack_bwd(const uint32_t* __restrict__ codes, const uint16_t* __restrict__ meta
     const int row = tid >> 2, w = tid & 3;
     if (row < rows) {
       const int64_t n = n0 + row;
-      const uint32_t cw = codes[n * (K / 16) + (k0 >> 4) + w];
-      const uint32_t mw = meta[n * (K / 16) + (k0 >> 4) + w];
+      // k0 is a multiple of 64: the tile's four 16-column blocks are words (k0 % 128) / 16 + w
+      // of chunk k0 / 128
+      const int64_t slot = packed_slot(n, k0 >> 7, K / 128);
+      const uint32_t cw = codes[8 * slot + ((k0 & 127) >> 4) + w];
+      const uint32_t mw = meta[8 * slot + ((k0 & 127) >> 4) + w];
 #pragma unroll
       for (int p = 0; p < 16; ++p) {
         u_s[row][16 * w + p] = 8;
@@ -120,7 +124,7 @@ k_pack_bwd(const uint32_t* __restrict__ codes, const uint16_t* __restrict__ meta
         f_s[row][16 * w + 4 * c + i0] = 1;
         f_s[row][16 * w + 4 * c + i1] = 1;
       }
-      if (w == 0) sc_s[row] = h_bits_to_f(scales[n * (K / 128) + (k0 >> 7)]);
+      if (w == 0) sc_s[row] = h_bits_to_f(scales[slot]);
     }
   }
   __syncthreads();
@@ -166,9 +170,12 @@ k_pack_bwd(const uint32_t* __restrict__ codes, const uint16_t* __restrict__ meta
       sel16 |= (uint32_t)((keep[0] & fv[0]) | ((keep[1] & fv[1]) << 1) | ((keep[2] & fv[2]) << 2) |
                           ((keep[3] & fv[3]) << 3)) << (4 * c);
     }
+    // transposed pack: row k, reduction n; n0 is a multiple of 64, so the 16-row block rb is
+    // word (n0 % 128) / 16 + rb of chunk n0 / 128
     const int64_t k = k0 + col;
-    codesT[k * (N / 16) + (n0 >> 4) + rb] = cw;
-    metaT[k * (N / 16) + (n0 >> 4) + rb] = (uint16_t)mw;
+    const int64_t slotT = packed_slot(k, n0 >> 7, N / 128);
+    codesT[8 * slotT + ((n0 & 127) >> 4) + rb] = cw;
+    metaT[8 * slotT + ((n0 & 127) >> 4) + rb] = (uint16_t)mw;
   }
   if (mask_rc) {
     __syncthreads();
@@ -190,7 +197,7 @@ k_pack_bwd(const uint32_t* __restrict__ codes, const uint16_t* __restrict__ meta
     }
   }
   // scalesT: the first column tile of each 128-group copies the tile's row scales
-  if ((k0 & 127) == 0 && tid < rows) scalesT[(k0 >> 7) * N + n0 + tid] = scales[(n0 + tid) * (K / 128) + (k0 >> 7)];
+  if ((k0 & 127) == 0 && tid < rows) scalesT[(k0 >> 7) * N + n0 + tid] = scales[packed_slot(n0 + tid, k0 >> 7, K / 128)];
 }
 
 // fp16 transpose out[c][r] = in[r][c] of a row-major [R x C] matrix, through a 64 x 64 LDS tile.

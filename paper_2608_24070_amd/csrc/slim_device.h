@@ -17,6 +17,14 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 SLIM_DEV uint32_t bits_of(h2_t x) { return __builtin_bit_cast(uint32_t, x); }
 SLIM_DEV h2_t h2_of(uint32_t x) { return __builtin_bit_cast(h2_t, x); }
 
+// Packed operand layout (codes, index words, scales of a forward pack; codesT, metaT of a
+// backward pack): rows in blocks of 16, the reduction in chunks of 128. Row r, chunk c owns slot
+//   packed_slot(r, c) = ((r / 16) * nch + c) * 16 + r % 16,   nch = red / 128,
+// i.e. 8 code words (32 B) at u32 index 8 slot, 8 index half-words (16 B) at u16 index 8 slot
+// and one fp16 scale at index slot: a block of 16 rows keeps each chunk's codes (512 B), index
+// words (256 B) and scales (32 B) contiguous, so loads of one chunk for many rows coalesce.
+SLIM_DEV int64_t packed_slot(int64_t r, int64_t c, int64_t nch) { return ((r >> 4) * nch + c) * 16 + (r & 15); }
+
 // Two fp16 copies of one fp16 bit pattern.
 SLIM_DEV h2_t splat_h2(uint32_t hbits) { return h2_of((hbits & 0xFFFFu) | (hbits << 16)); }
 

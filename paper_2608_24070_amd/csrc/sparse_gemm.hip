@@ -115,9 +115,10 @@ SLIM_DEV bool split_reduce(f4_t* acc, float* part_tile, int S, int s, uint32_t* 
 }
 
 // ============================================================ small-M: sparse split units
-// Unit = 64 rows (16 per wave) x one slice of 4G quantisation groups. Lane group qa (lane / 16)
-// of the 16x16x64 sparse MFMA owns G whole groups, so its code words (32 B per group), index
-// words (16 B) and scales are contiguous: 4G loads per lane for the whole slice.
+// Unit = 64 rows (16 per wave, one 16-row block of the packed layout) x one slice of 4G
+// quantisation groups. Lane group qa (lane / 16) of the 16x16x64 sparse MFMA owns G whole
+// groups: per group one row's code words (32 B), index words (16 B) and scale, which the 16 lanes
+// of a lane group (16 rows of one block) read from one contiguous piece.
 template <bool BWD, int FM, int G>
 SLIM_DEV void decode_sparse_unit(const LayerArgs& a, int64_t u, _Float16* xs, int* last_flag) {
   constexpr int MC = 16 * FM;
@@ -143,11 +144,12 @@ SLIM_DEV void decode_sparse_unit(const LayerArgs& a, int64_t u, _Float16* xs, in
 #pragma unroll
   for (int gi = 0; gi < G; ++gi) {
     const int64_t ch = clamp_hi(cl + gi, nchunks - 1);
-    const uint32_t* cp = a.codes + lrow * (a.red / 16) + ch * 8;
+    const int64_t slot = packed_slot(lrow, ch, nchunks);
+    const uint32_t* cp = a.codes + 8 * slot;
     cw[2 * gi] = *reinterpret_cast<const u32x4_t*>(cp);
     cw[2 * gi + 1] = *reinterpret_cast<const u32x4_t*>(cp + 4);
-    mw[gi] = *reinterpret_cast<const u32x4_t*>(a.meta + lrow * (a.red / 32) + ch * 4);
-    sw[gi] = BWD ? 0u : (uint32_t)a.scales[lrow * (a.red / 128) + ch];
+    mw[gi] = *reinterpret_cast<const u32x4_t*>(a.meta + 4 * slot);
+    sw[gi] = BWD ? 0u : (uint32_t)a.scales[slot];
   }
   const int64_t sgroup = row0 / 128;
   u32x4_t xv[XV], sv[XV];
@@ -354,14 +356,14 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
 // brings each wave's scale row (its 128-row group) into LDS.
 constexpr int kTR = 512, kTC = 96, kTThreads = 256, kStages = 3, kBand = 4;
 // Direct loads per thread per chunk, issued in this order: packed words (4 code loads, 2 index
-// word loads, and in the forward 2 scale loads), then 6 activation loads (and in the backward one
+// word loads, and in the forward 1 scale load), then 6 activation loads (and in the backward one
 // scale-row load). Chunk c's loads are issued at the top of chunk c - 2.
 //  * at the top of chunk c its activations must have landed: only chunk c - 1's loads may still
 //    be outstanding;
 //  * in the last step of chunk c, chunk c + 1's words must have landed: only chunk c + 1's
 //    activation (and scale-row) loads and chunk c's loads may still be outstanding.
 // The prologue issues chunks 0 and 1 in the same order, so the same counts hold from the start.
-constexpr int kTileWordsFwd = 4 + 2 + 2, kTileWordsBwd = 4 + 2, kTileActFwd = 6, kTileActBwd = 6 + 1;
+constexpr int kTileWordsFwd = 4 + 2 + 1, kTileWordsBwd = 4 + 2, kTileActFwd = 6, kTileActBwd = 6 + 1;
 constexpr int kTileTopFwd = kTileWordsFwd + kTileActFwd, kTileTopBwd = kTileWordsBwd + kTileActBwd;
 constexpr int kTileNextFwd = kTileActFwd + kTileTopFwd, kTileNextBwd = kTileActBwd + kTileTopBwd;
 
@@ -395,7 +397,7 @@ template <bool BWD>
 struct TileWordsLds {
   u32x4_t cw[4][4][64];
   u32x4_t mw[4][128];
-  uint32_t sw[BWD ? 1 : 4][BWD ? 1 : 128];
+  uint16_t sw[BWD ? 1 : 4][BWD ? 2 : 128];
 };
 // one chunk's packed words of one lane, read from LDS
 struct TileWords {
@@ -436,17 +438,21 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   // opaque per chunk) instead of being kept live across the loop. Rows past the matrix (or past
   // M) get offsets at or beyond their resource's extent and read as zero; their results are not
   // stored. The uniform chunk offset only ever moves a valid row within that row.
-  // packed words: resources from the wave's first row (clamped into the matrix); a lane of a
-  // words load serves row 32 f + L % 32, f = the load's first fragment + L / 32
-  const int64_t wbase = clamp_hi(wrow0, a.rows - 1), wrows = a.rows - wbase;
-  const rsrc_t rc = make_rsrc(a.codes + wbase * (a.red / 16), wrows * (a.red / 16) * 4);
-  const rsrc_t rm = make_rsrc(a.meta + wbase * (a.red / 32), wrows * (a.red / 32) * 4);
-  const rsrc_t rs = make_rsrc(a.scales + wbase * (a.red / 128), wrows * (a.red / 128) * 2);
-  const uint32_t dr0 = (uint32_t)(wrow0 - wbase) + (uint32_t)(lane & 31);   // fragment 0's row
-  const uint32_t cstr = (uint32_t)(a.red / 16) * 4u, mstr = (uint32_t)(a.red / 32) * 4u,
-                 sstr = (uint32_t)(a.red / 128) * 2u;   // bytes per row
-  const uint32_t co0 = dr0 * cstr + 16u * ha;            // codes: lane's 16 B of fragment 0
-  const uint32_t ro0 = dr0 + 32u * ha;                   // index words, scales: the lane's row
+  // packed words: resources from the wave's first 16-row block (clamped into the matrix; rows is
+  // a multiple of 16). Relative to it, row d of chunk c sits in slot
+  // ((d / 16) nch + c) 16 + d % 16; the chunk adds 16 slots, and 32 rows (two blocks) add
+  // 32 nch slots, fstep bytes of codes (32 B per slot) and, per 64 rows, of index words (16 B).
+  const int64_t wblk = (wrow0 < a.rows ? wrow0 : a.rows - 16) / 16;
+  const int64_t nblk = a.rows / 16 - wblk;
+  const rsrc_t rc = make_rsrc(a.codes + wblk * nch * 128, nblk * nch * 512);
+  const rsrc_t rm = make_rsrc(a.meta + wblk * nch * 64, nblk * nch * 256);
+  const rsrc_t rs = make_rsrc(a.scales + wblk * nch * 16, nblk * nch * 32);
+  const uint32_t d0 = (uint32_t)(wrow0 - 16 * wblk), snch = 16u * (uint32_t)nch;
+  auto rel_slot = [&](uint32_t d) { return (d >> 4) * snch + (d & 15u); };
+  const uint32_t fstep = 1024u * (uint32_t)nch;
+  const uint32_t co0 = rel_slot(d0 + (uint32_t)(lane & 31)) * 32u + 16u * ha;   // codes: fragment 0
+  const uint32_t mo0 = rel_slot(d0 + (uint32_t)lane) * 16u;                     // index words: rows 0..63
+  const uint32_t so0 = rel_slot(d0 + 2u * (uint32_t)lane) * 2u;                 // scales: rows 2 L, 2 L + 1
 
   // activation chunk c -> stage c % kStages: wave w writes rows 24 w .. 24 w + 23, four per load
   // (lane L: row + L / 16, LDS column slot L % 16 holding column (L % 16) ^ (row % 16)).
@@ -458,22 +464,18 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   const rsrc_t rx = make_rsrc(a.act16 + m0 * a.red, brows * a.red * 2);    // the block's activation rows
   const uint32_t xo0 = (uint32_t)(24 * wave + lrow) * (uint32_t)a.red * 2u + 16u * (uint32_t)(lslot ^ lrow);
   const uint32_t xstep = 8u * (uint32_t)a.red;
-  const rsrc_t rg = make_rsrc(a.scales + (wbase / 128) * a.red, a.red * 2);   // backward: the wave's scale row
+  const rsrc_t rg = make_rsrc(a.scales + (16 * wblk / 128) * a.red, a.red * 2);   // backward: the wave's scale row
 
-  auto dma_words = [&](int64_t c, int stg, uint32_t co, uint32_t ro) {
+  auto dma_words = [&](int64_t c, int stg, uint32_t co, uint32_t mo, uint32_t so) {
     const int cc = (int)clamp_hi(c, nch - 1);
     TileWordsLds<BWD>& W = ws_at(stg);
 #pragma unroll
     for (int fn = 0; fn < 4; ++fn)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (lds_ptr_t)&W.cw[wave][fn][0], 16, co + fn * 32u * cstr, 32 * cc, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (lds_ptr_t)&W.cw[wave][fn][0], 16, co + fn * fstep, 512 * cc, 0, 0);
 #pragma unroll
     for (int j = 0; j < 2; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rm, (lds_ptr_t)&W.mw[wave][64 * j], 16, (ro + 64u * j) * mstr, 16 * cc, 0, 0);
-    if (!BWD) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)&W.sw[wave][64 * j], 2, (ro + 64u * j) * sstr, 2 * cc, 0, 0);
-    }
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rm, (lds_ptr_t)&W.mw[wave][64 * j], 16, mo + j * fstep, 256 * cc, 0, 0);
+    if (!BWD) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)&W.sw[wave][0], 4, so, 32 * cc, 0, 0);
   };
   auto dma_act = [&](int64_t c, int stg, uint32_t xo) {
     const int cc = (int)clamp_hi(c, nch - 1);
@@ -520,9 +522,9 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   // words of chunk c in set c % 3 (read during chunk c - 1); A operands double-buffered by step
   TileWords tw[3];
   h8_t aq[2][4];
-  dma_words(0, 0, co0, ro0);
+  dma_words(0, 0, co0, mo0, so0);
   dma_act(0, 0, xo0);
-  dma_words(1, 1, co0, ro0);
+  dma_words(1, 1, co0, mo0, so0);
   dma_act(1, 1, xo0);
   __builtin_amdgcn_s_waitcnt(vmcnt_wait(BWD ? kTileNextBwd : kTileNextFwd));   // chunk 0's words
   read_words(0, tw[0]);
@@ -541,8 +543,8 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
     __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(BWD ? kTileTopBwd : kTileTopFwd));
     asm volatile("s_barrier" ::: "memory");
     // this chunk's copies of the base offsets (opaque, so nothing derived from them is hoisted)
-    uint32_t xo = xo0, co = co0, ro = ro0, bo = bo0;
-    asm volatile("" : "+v"(xo), "+v"(co), "+v"(ro), "+v"(bo));
+    uint32_t xo = xo0, co = co0, mo = mo0, so = so0, bo = bo0;
+    asm volatile("" : "+v"(xo), "+v"(co), "+v"(mo), "+v"(so), "+v"(bo));
     const TileWords& cur = tw[z];
     TileWords& nxt = tw[(z + 1) % 3];
 
@@ -570,7 +572,7 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
       // chunk c + 2's direct loads, into the stage read in chunk c - 1: words during step 0,
       // activations during step 1, one load after each MFMA (issued in a burst at the barrier,
       // the four waves' loads would fill the address unit's queue and stall instruction issue)
-      if (st == 0) dma_words(c + kStages - 1, (z + 2) % 3, co, ro);
+      if (st == 0) dma_words(c + kStages - 1, (z + 2) % 3, co, mo, so);
       if (st == 1) dma_act(c + kStages - 1, (z + 2) % 3, xo);
       if (st < 3) {
         dequant(cur, st + 1, aq[(st + 1) & 1]);

@@ -201,10 +201,13 @@ def pack(W, with_mask: bool = False, stream=None) -> dict:
         raise TypeError("W must be fp32")
     N, K = W.shape
     dev = W.device
+    if N % 16 or K % 128:
+        raise ValueError("slim_pack needs N % 16 == 0 and K % 128 == 0")
+    # rows in blocks of 16, the reduction in chunks of 128: [N/16, K/128, 16 rows, bytes per row]
     out = {
-        "codes": torch.empty((N, K // 4), dtype=torch.uint8, device=dev),
-        "meta": torch.empty((N, K // 8), dtype=torch.uint8, device=dev),
-        "scales": torch.empty((N, K // 128), dtype=torch.int16, device=dev),
+        "codes": torch.empty((N // 16, K // 128, 16, 32), dtype=torch.uint8, device=dev),
+        "meta": torch.empty((N // 16, K // 128, 16, 16), dtype=torch.uint8, device=dev),
+        "scales": torch.empty((N // 16, K // 128, 16), dtype=torch.int16, device=dev),
         "N": N, "K": K,
     }
     mask = torch.empty((N, K), dtype=torch.uint8, device=dev) if with_mask else None
@@ -221,9 +224,12 @@ def pack_bwd(packed: dict, with_mask: bool = False, stream=None) -> dict:
     torch = _torch()
     N, K = packed["N"], packed["K"]
     dev = packed["codes"].device
+    if N % 128:
+        raise ValueError("slim_pack_bwd needs N % 128 == 0")
+    # rows (k) in blocks of 16, the reduction (n) in chunks of 128; scalesT stays [K/128, N]
     out = {
-        "codesT": torch.empty((K, N // 4), dtype=torch.uint8, device=dev),
-        "metaT": torch.empty((K, N // 8), dtype=torch.uint8, device=dev),
+        "codesT": torch.empty((K // 16, N // 128, 16, 32), dtype=torch.uint8, device=dev),
+        "metaT": torch.empty((K // 16, N // 128, 16, 16), dtype=torch.uint8, device=dev),
         "scalesT": torch.empty((K // 128, N), dtype=torch.int16, device=dev),
         "N": N, "K": K,
     }

@@ -22,13 +22,39 @@ def host(t):
     return t.detach().cpu().numpy()
 
 
+# The device pack keeps rows in blocks of 16 and the reduction in chunks of 128 (codes, meta and
+# scales of the forward pack, codesT and metaT of the backward pack): [rows/16, chunks, 16, bytes]
+# for 32 code bytes or 16 index bytes per row and chunk, [rows/16, chunks, 16] for the scales.
+# The oracle keeps each row whole, [rows, chunks * bytes]. These two permutations convert.
+BLOCKED = ("codes", "meta", "scales", "codesT", "metaT")
+
+
+def unblock(a):
+    """Device (blocked) layout -> the oracle's row-major layout."""
+    if a.ndim == 4:
+        r16, nch, r, b = a.shape
+        return np.ascontiguousarray(a.transpose(0, 2, 1, 3)).reshape(r16 * r, nch * b)
+    r16, nch, r = a.shape
+    return np.ascontiguousarray(a.transpose(0, 2, 1)).reshape(r16 * r, nch)
+
+
+def block(a, chunk_bytes):
+    """The oracle's row-major layout -> device layout; chunk_bytes per row and chunk (32 codes,
+    16 index words, 0 for scales, one element per chunk)."""
+    rows = a.shape[0]
+    if chunk_bytes == 0:
+        return np.ascontiguousarray(a.reshape(rows // 16, 16, -1).transpose(0, 2, 1))
+    return np.ascontiguousarray(a.reshape(rows // 16, 16, -1, chunk_bytes).transpose(0, 2, 1, 3))
+
+
 def host_pack(p):
-    """Device pack -> numpy arrays in the oracle's dtypes."""
+    """Device pack -> numpy arrays in the oracle's dtypes and row-major layout."""
     out = {}
     for k, v in p.items():
         if isinstance(v, torch.Tensor):
             a = host(v)
-            out[k] = a.view(np.uint16) if a.dtype == np.int16 else a
+            a = a.view(np.uint16) if a.dtype == np.int16 else a
+            out[k] = unblock(a) if k in BLOCKED else a
         else:
             out[k] = v
     return out
@@ -36,8 +62,8 @@ def host_pack(p):
 
 def oracle_pack_on_device(p, n, k):
     """Upload an oracle pack, so the layer kernels can be checked on a pack the GPU did not make."""
-    return {"codes": dev(p["codes"]), "meta": dev(p["meta"]), "scales": dev(p["scales"].view(np.int16)),
-            "N": n, "K": k}
+    return {"codes": dev(block(p["codes"], 32)), "meta": dev(block(p["meta"], 16)),
+            "scales": dev(block(p["scales"], 0).view(np.int16)), "N": n, "K": k}
 
 
 def layer_inputs(n, k, r, m, seed=0, xdtype="bf16", outliers=False, name="layer"):

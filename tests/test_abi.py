@@ -28,7 +28,7 @@ def test_version_and_status_strings():
 
 
 def test_pack_validation():
-    ok = dict(W=A, N=8, K=128, codes=A, meta=A, scales=A, mask=None, stream=None)
+    ok = dict(W=A, N=16, K=128, codes=A, meta=A, scales=A, mask=None, stream=None)
     def call(**kw):
         a = dict(ok, **kw)
         return slim.slim_pack(a["W"], a["N"], a["K"], a["codes"], a["meta"], a["scales"], a["mask"], a["stream"])
@@ -37,15 +37,18 @@ def test_pack_validation():
     assert call(K=100) == 2
     assert call(K=64) == 2
     assert call(N=0) == 2
+    assert call(N=8) == 2           # whole 16-row blocks
+    assert call(N=40) == 2
     assert call(W=MIS) == 4
     assert call(mask=MIS) == 4
 
 
 def test_pack_bwd_validation():
-    def call(N=32, K=256, codes=A, codesT=A, mask=None):
+    def call(N=128, K=256, codes=A, codesT=A, mask=None):
         return slim.slim_pack_bwd(codes, A, A, N, K, codesT, A, A, mask, None)
     assert call(codes=None) == 1
-    assert call(N=24) == 2          # N % 16
+    assert call(N=24) == 2          # N % 128: the transposed pack chunks N by 128
+    assert call(N=64) == 2
     assert call(K=200) == 2
     assert call(codesT=MIS) == 4
 
