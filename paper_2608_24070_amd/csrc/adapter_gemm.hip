@@ -2,7 +2,9 @@
 //   tm = act Q^T with act [M, red] (bf16/fp16) and Q [r, red] fp16 row-major:
 //   forward  T = X L      (Q = L^T, from slim_pack_adapter)
 //   backward U = dY R^T   (Q = R as given)
-// Result fp16 [M, r] (it only feeds the fp16 MFMA of the second product). 64 x 64 output tiles
+// Result fp16 (it only feeds the fp16 MFMA of the second product), in 32 x 16 tiles: element
+// (m, j) at ((m / 32) (r / 16) + j / 16) 512 + (m % 32) 16 + j % 16, so that one 16-rank step of
+// a 32-row operand fragment is 1 KB of contiguous memory. 64 x 64 output tiles
 // on 16x16x32 fp16 MFMA, 64-wide reduction stages double-buffered in LDS and staged through
 // registers one stage ahead. The reduction may be split across blocks; the last block of a tile
 // sums the partials in split order (deterministic) through device-scope accesses.
@@ -133,7 +135,9 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int a_bf16, int64_t M, int64_t Kd
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int64_t gm = m0 + 32 * wm + 16 * x + 4 * g + v;
-        if (gm < M && gj < r) out[gm * r + gj] = __builtin_bit_cast(uint16_t, (_Float16)acc[x][y][v]);
+        if (gm < M && gj < r)
+          out[((gm >> 5) * (r >> 4) + (gj >> 4)) * 512 + (gm & 31) * 16 + (gj & 15)] =
+              __builtin_bit_cast(uint16_t, (_Float16)acc[x][y][v]);
       }
     }
 }

@@ -118,15 +118,20 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
   if (q.n_counters > kCounterSlots) return SLIM_EUNSUPPORTED;
   // the counter region has a fixed size so that it stays at zero across calls with other sizes
   size_t off = kCounterSlots * 4;
+  // T: row-major [M, r] at small M; at large M in 32 x 16 tiles ([ceil(M/32)][r/16][32][16], see
+  // adapter_gemm.hip), which the tile kernel's epilogue reads 1 KB at a time
   q.off_t = off;
-  off = round256(off + (size_t)M * (size_t)r * 2);
+  off = round256(off + (size_t)(q.decode ? M : cdiv(M, 32) * 32) * (size_t)r * 2);
   q.off_tpart = off;
   off = round256(off + tpart_bytes);
   q.off_ypart = off;
   off = round256(off + ypart_bytes);
-  // large M: fp16 copy of bf16 activations for the tile kernel's direct-to-LDS loads
+  // large M: fp16 copy of bf16 activations for the tile kernel's direct-to-LDS loads, and the
+  // adapter's second factor P [rows, r] in 32 x 16 tiles
   q.off_x16 = off;
   if (!q.decode) off = round256(off + (size_t)M * (size_t)red * 2);
+  q.off_pb = off;
+  if (!q.decode) off = round256(off + (size_t)cdiv(rows, 32) * 32 * (size_t)r * 2);
   q.total = off;
   *p = q;
   return SLIM_OK;

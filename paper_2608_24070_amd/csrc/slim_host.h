@@ -34,7 +34,7 @@ struct SlimPlan {
   size_t lds_bytes = 0;               // dynamic LDS (unused: the kernels size their LDS statically)
   // workspace layout (byte offsets)
   size_t off_counters = 0, n_counters = 0;
-  size_t off_t = 0, off_tpart = 0, off_ypart = 0, off_x16 = 0, total = 0;
+  size_t off_t = 0, off_tpart = 0, off_ypart = 0, off_x16 = 0, off_pb = 0, total = 0;
 };
 
 // Forward (bwd == false: rows = N, red = K) or backward (bwd == true: rows = K, red = N) plan.

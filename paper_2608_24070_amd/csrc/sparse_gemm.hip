@@ -49,7 +49,8 @@ struct LayerArgs {
   int64_t r;
   const uint16_t* ad_q;    // adapter first factor, row-major [r, red]
   const uint16_t* ad_p;    // adapter second factor, row-major [rows, r]
-  uint16_t* tm;            // fp16 [M, r] adapter intermediate
+  uint16_t* ad_pb;         // large M: the same in 32 x 16 tiles (workspace)
+  uint16_t* tm;            // fp16 adapter intermediate: row-major [M, r] (small M), 32 x 16 tiles (large M)
   float* out;              // [M, rows]
   // small-M path
   int split;               // reduction splits of the sparse product
@@ -616,25 +617,25 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   __builtin_amdgcn_s_waitcnt(0);
 
   // adapter second product: out^T[row, m] += sum_j P[row, j] tm[m, j], on 32x32x16 fp16 MFMA.
-  // Both operands are row-major along j; step t covers ranks [16 t, 16 t + 16) (r is a multiple
-  // of 16, so every step is whole). The operands of step t are loaded three steps ahead into a
-  // ring of four register sets (the loop is unrolled by four; loads past the last step repeat it
-  // and are not used). Rows past the matrix or past M read clamped rows; their results are not
-  // stored.
+  // Both operands are in 32 x 16 tiles (P re-laid by k_tile_p16, tm written so by the adapter
+  // GEMM): step t (ranks [16 t, 16 t + 16), r a multiple of 16) of one 32-row fragment is 1 KB of
+  // contiguous memory, lane (L % 32, L / 32) reading row L % 32, ranks 8 (L / 32) ... + 7. The
+  // operands of step t are loaded three steps ahead into a ring of four register sets (the loop is
+  // unrolled by four; loads past the last step repeat it and are not used). Fragments past the
+  // tiled extent read zero; their results are not stored.
   if (a.r > 0) {
     const int64_t nj = a.r / 16;
-    const rsrc_t rp = make_rsrc(a.ad_p, a.rows * a.r * 2), rt = make_rsrc(a.tm, a.M * a.r * 2);
+    const rsrc_t rp = make_rsrc(a.ad_pb, (a.rows + 31) / 32 * 32 * a.r * 2), rt = make_rsrc(a.tm, (a.M + 31) / 32 * 32 * a.r * 2);
+    const uint32_t lo16 = 32u * (uint32_t)(lane & 31) + 16u * ha;   // the lane's bytes within a 1 KB tile
     uint32_t po[4], to[3];
 #pragma unroll
-    for (int fn = 0; fn < 4; ++fn)
-      po[fn] = ((uint32_t)clamp_hi(wrow0 + 32 * fn + (lane & 31), a.rows - 1) * (uint32_t)a.r + 8u * ha) * 2u;
+    for (int fn = 0; fn < 4; ++fn) po[fn] = (uint32_t)((wrow0 + 32 * fn) / 32 * nj) * 1024u + lo16;
 #pragma unroll
-    for (int fm = 0; fm < 3; ++fm)
-      to[fm] = ((uint32_t)clamp_hi(m0 + 32 * fm + (lane & 31), a.M - 1) * (uint32_t)a.r + 8u * ha) * 2u;
+    for (int fm = 0; fm < 3; ++fm) to[fm] = (uint32_t)((m0 + 32 * fm) / 32 * nj) * 1024u + lo16;
     struct AdRegs { u32x4_t pa[4], pb[3]; };
     AdRegs ar[4];
     auto ad_load = [&](int64_t t, AdRegs& R) {
-      const int so = (int)(clamp_hi(t, nj - 1) * 32);
+      const int so = (int)(clamp_hi(t, nj - 1) * 1024);
 #pragma unroll
       for (int fn = 0; fn < 4; ++fn) R.pa[fn] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, po[fn], so, 0));
 #pragma unroll
@@ -700,6 +701,18 @@ __global__ void __launch_bounds__(256) k_bf16_to_f16(const u32x4_t* __restrict__
   if (i < n8) dst[i] = __builtin_bit_cast(u32x4_t, load8_as_h(src[i], true));
 }
 
+// P [rows, r] row-major -> 32 x 16 tiles: element (row, j) at
+// ((row / 32) (r / 16) + j / 16) 512 + (row % 32) 16 + j % 16. One thread per 8 elements (16 B);
+// rows of a last partial 32-row tile are left unwritten (their results are never stored).
+__global__ void __launch_bounds__(256) k_tile_p16(const u32x4_t* __restrict__ P, int64_t rows, int64_t r,
+                                                  u32x4_t* __restrict__ Pb) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t r8 = r / 8;
+  if (i >= rows * r8) return;
+  const int64_t row = i / r8, k8 = i - row * r8;
+  Pb[((row >> 5) * (r >> 4) + (k8 >> 1)) * 64 + (row & 31) * 2 + (k8 & 1)] = P[i];
+}
+
 // ------------------------------------------------------------------------------ launch
 template <bool BWD, int FM, int G>
 void launch_decode(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
@@ -742,6 +755,11 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
   if (a.r > 0) {
     int st = slim_launch_adapter_gemm(act, act_bf16, a.M, a.red, a.ad_q, a.r, p, ws, s);
     if (st != SLIM_OK) return st;
+    SlimKernelTimer timer("adapter_p16", s);
+    const int64_t n8 = a.rows * a.r / 8;
+    SLIM_LAUNCH(timer, k_tile_p16, dim3((unsigned)((n8 + 255) / 256)), dim3(256), s,
+                reinterpret_cast<const u32x4_t*>(a.ad_p), a.rows, a.r, reinterpret_cast<u32x4_t*>(a.ad_pb));
+    if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
   dim3 grid((unsigned)(8 * ((p.sp_row_tiles * p.sp_col_tiles + 7) / 8)));
@@ -764,6 +782,7 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.r = r;
   a.ad_q = ad_q;
   a.ad_p = ad_p;
+  a.ad_pb = p.decode ? nullptr : reinterpret_cast<uint16_t*>(ws + p.off_pb);
   a.tm = reinterpret_cast<uint16_t*>(ws + p.off_t);
   a.act16 = (!p.decode && dtype == SLIM_BF16) ? reinterpret_cast<const uint16_t*>(ws + p.off_x16) : a.act;
   a.out = out;
