@@ -88,7 +88,7 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     if (q.sp_split > 1 || r > 0) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 4 * q.dec_fm * 256 * 4;
     q.lds_bytes = 0;
   } else {
-    // large M: dense adapter GEMM (64 x 64 tiles) then 512 x 96 sparse tiles
+    // large M: dense adapter GEMM (128 x 128 tiles) then 512 x 96 sparse tiles
     q.decode = false;
     q.sp_rows_tile = 512;
     q.sp_cols_tile = 96;
@@ -97,18 +97,16 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     q.sp_split = 1;
     q.sp_chunks_per_split = nchunks;
     if (r > 0) {
-      q.ad_tiles_m = (int)cdiv(M, 64);
-      q.ad_tiles_j = (int)cdiv(r, 64);
+      q.ad_tiles_m = (int)cdiv(M, 128);
+      q.ad_tiles_j = (int)cdiv(r, 128);
       const int64_t tiles = (int64_t)q.ad_tiles_m * q.ad_tiles_j;
-      const int64_t split = std::max<int64_t>(1, std::min<int64_t>(cdiv(256, tiles), red / 512));
+      // one block per CU (the GEMM's LDS ring takes 96 KB): at most 256 blocks, so one round
+      const int64_t split = std::max<int64_t>(1, std::min<int64_t>(256 / tiles, red / 512));
       const int64_t slice = cdiv(cdiv(red, split), 64) * 64;
       q.ad_split = (int)cdiv(red, slice);
       q.ad_slice = slice;
-      if (q.ad_split > 1) {
-        if (tiles > (int64_t)kCounterSlots) return SLIM_EUNSUPPORTED;
-        ad_counters = (size_t)tiles;
-        tpart_bytes = (size_t)q.ad_split * tiles * 64 * 64 * 4;
-      }
+      // split partials: fp32, one T-sized tiled array per split (summed by the next kernel)
+      if (q.ad_split > 1) tpart_bytes = (size_t)q.ad_split * (size_t)cdiv(M, 32) * 32 * (size_t)r * 4;
     }
   }
   // workspace: [counters][adapter intermediate fp16 M x r][adapter partials][sparse partials]

@@ -25,6 +25,23 @@ SLIM_DEV h2_t h2_of(uint32_t x) { return __builtin_bit_cast(h2_t, x); }
 // words (256 B) and scales (32 B) contiguous, so loads of one chunk for many rows coalesce.
 SLIM_DEV int64_t packed_slot(int64_t r, int64_t c, int64_t nch) { return ((r >> 4) * nch + c) * 16 + (r & 15); }
 
+// s_waitcnt immediate (gfx9 layout) waiting for at most n outstanding vector-memory operations:
+// vmcnt bits [3:0] and [15:14]; expcnt [6:4] and lgkmcnt [11:8] left at their maxima (no wait)
+constexpr unsigned vmcnt_wait(int n) { return (unsigned)(n & 15) | ((unsigned)(n >> 4) << 14) | 0x0F70u; }
+// the same with lgkmcnt 0: also every LDS read of this wave has returned
+constexpr unsigned vmcnt_lgkm0_wait(int n) { return vmcnt_wait(n) & ~0x0F00u; }
+
+// Buffer resources: a wave-uniform base in scalar registers, a per-lane 32-bit byte offset (one
+// vector register per address) and a uniform offset. A read at or past the resource's extent
+// returns zero without touching memory.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;   // gfx9 buffer descriptor word 3: raw 32-bit data
+SLIM_DEV rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int64_t n = bytes < 0xFFFFFFFFll ? (bytes > 0 ? bytes : 0) : 0xFFFFFFFFll;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)(uint32_t)n, kRsrcWord3);
+}
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
 // Two fp16 copies of one fp16 bit pattern.
 SLIM_DEV h2_t splat_h2(uint32_t hbits) { return h2_of((hbits & 0xFFFFu) | (hbits << 16)); }
 

@@ -5,6 +5,7 @@
 
 #include "slim_host.h"
 
-// tm = A Q^T: A [M, Kd] activations, Q [r, Kd] fp16 row-major; fp16 result [M, r] at ws + p.off_t.
-int slim_launch_adapter_gemm(const uint16_t* A, int a_bf16, int64_t M, int64_t Kd, const uint16_t* Q, int64_t r,
+// tm = A Q^T: A [M, Kd] fp16 activations, Q [r, Kd] fp16 row-major; fp16 result at ws + p.off_t in
+// 32 x 16 tiles (adapter_gemm.hip).
+int slim_launch_adapter_gemm(const uint16_t* A16, int64_t M, int64_t Kd, const uint16_t* Q, int64_t r,
                              const SlimPlan& p, char* ws, hipStream_t s);

@@ -368,24 +368,9 @@ constexpr int kTileWordsFwd = 4 + 2 + 1, kTileWordsBwd = 4 + 2, kTileActFwd = 6,
 constexpr int kTileTopFwd = kTileWordsFwd + kTileActFwd, kTileTopBwd = kTileWordsBwd + kTileActBwd;
 constexpr int kTileNextFwd = kTileActFwd + kTileTopFwd, kTileNextBwd = kTileActBwd + kTileTopBwd;
 
-// s_waitcnt immediate (gfx9 layout) waiting for at most n outstanding vector-memory operations:
-// vmcnt bits [3:0] and [15:14]; expcnt [6:4] and lgkmcnt [11:8] left at their maxima (no wait)
-constexpr unsigned vmcnt_wait(int n) { return (unsigned)(n & 15) | ((unsigned)(n >> 4) << 14) | 0x0F70u; }
-// the same with lgkmcnt 0: also every LDS read of this wave has returned
-constexpr unsigned vmcnt_lgkm0_wait(int n) { return vmcnt_wait(n) & ~0x0F00u; }
 static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && kTileNextFwd < 64, "s_waitcnt encoding");
 static_assert(vmcnt_lgkm0_wait(20) == 0x4074u, "s_waitcnt encoding");
 
-// The tile kernel addresses memory through buffer resources: a wave-uniform base in scalar
-// registers, a per-lane 32-bit byte offset (one vector register per address) and a uniform
-// chunk offset. A read at or past the resource's extent returns zero without touching memory.
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-constexpr int kRsrcWord3 = 0x00020000;   // gfx9 buffer descriptor word 3: raw 32-bit data
-SLIM_DEV rsrc_t make_rsrc(const void* base, int64_t bytes) {
-  const int64_t n = bytes < 0xFFFFFFFFll ? bytes : 0xFFFFFFFFll;
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)(uint32_t)n, kRsrcWord3);
-}
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 // One chunk's packed words of the four waves, as the direct loads lay them down (lane L of a load
 // at 16 L, or 4 L for 2-byte loads): codes [wave][fragment][lane] (16 B: the lane's four code
@@ -617,8 +602,8 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   __builtin_amdgcn_s_waitcnt(0);
 
   // adapter second product: out^T[row, m] += sum_j P[row, j] tm[m, j], on 32x32x16 fp16 MFMA.
-  // Both operands are in 32 x 16 tiles (P re-laid by k_tile_p16, tm written so by the adapter
-  // GEMM): step t (ranks [16 t, 16 t + 16), r a multiple of 16) of one 32-row fragment is 1 KB of
+  // Both operands are in 32 x 16 tiles (P re-laid and tm finished by k_adapter_finish, or tm
+  // written so by the adapter GEMM): step t (ranks [16 t, 16 t + 16), r a multiple of 16) of one 32-row fragment is 1 KB of
   // contiguous memory, lane (L % 32, L / 32) reading row L % 32, ranks 8 (L / 32) ... + 7. The
   // operands of step t are loaded three steps ahead into a ring of four register sets (the loop is
   // unrolled by four; loads past the last step repeat it and are not used). Fragments past the
@@ -701,16 +686,45 @@ __global__ void __launch_bounds__(256) k_bf16_to_f16(const u32x4_t* __restrict__
   if (i < n8) dst[i] = __builtin_bit_cast(u32x4_t, load8_as_h(src[i], true));
 }
 
-// P [rows, r] row-major -> 32 x 16 tiles: element (row, j) at
-// ((row / 32) (r / 16) + j / 16) 512 + (row % 32) 16 + j % 16. One thread per 8 elements (16 B);
-// rows of a last partial 32-row tile are left unwritten (their results are never stored).
-__global__ void __launch_bounds__(256) k_tile_p16(const u32x4_t* __restrict__ P, int64_t rows, int64_t r,
-                                                  u32x4_t* __restrict__ Pb) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+// Adapter tiles for the tile kernel's epilogue, one launch with two kinds of block:
+//  * blocks [0, np): P [rows, r] row-major -> 32 x 16 tiles, element (row, j) at
+//    ((row / 32) (r / 16) + j / 16) 512 + (row % 32) 16 + j % 16; one thread per 8 elements
+//    (16 B); rows of a last partial 32-row tile are left unwritten (their results are never
+//    stored);
+//  * blocks [np, ...): when the adapter GEMM split its reduction, tm (fp16, tiled) = the sum of
+//    its fp32 split partials in split order; one thread per 8 elements of a row m < M.
+__global__ void __launch_bounds__(256) k_adapter_finish(const u32x4_t* __restrict__ P, int64_t rows, int64_t r,
+                                                        u32x4_t* __restrict__ Pb, int64_t np,
+                                                        const float* __restrict__ part, int split, int64_t M,
+                                                        u32x4_t* __restrict__ tm) {
   const int64_t r8 = r / 8;
-  if (i >= rows * r8) return;
-  const int64_t row = i / r8, k8 = i - row * r8;
-  Pb[((row >> 5) * (r >> 4) + (k8 >> 1)) * 64 + (row & 31) * 2 + (k8 & 1)] = P[i];
+  if ((int64_t)blockIdx.x < np) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= rows * r8) return;
+    const int64_t row = i / r8, k8 = i - row * r8;
+    Pb[((row >> 5) * (r >> 4) + (k8 >> 1)) * 64 + (row & 31) * 2 + (k8 & 1)] = P[i];
+    return;
+  }
+  const int64_t i = ((int64_t)blockIdx.x - np) * 256 + threadIdx.x;   // group of 8 in tiled order
+  const int64_t total8 = (M + 31) / 32 * 32 * r8;
+  if (i >= total8) return;
+  // tiled group i: tile i / 64, row in tile (i % 64) / 2 -> m
+  const int64_t m = (i / 64) / (r >> 4) * 32 + (i % 64) / 2;
+  if (m >= M) return;
+  float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < split; ++s) {
+    const f4_t* src = reinterpret_cast<const f4_t*>(part + (int64_t)s * total8 * 8 + 8 * i);
+    const f4_t a0 = src[0], a1 = src[1];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[e] += a0[e];
+      v[4 + e] += a1[e];
+    }
+  }
+  h8_t h;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) h[e] = (_Float16)v[e];
+  tm[i] = __builtin_bit_cast(u32x4_t, h);
 }
 
 // ------------------------------------------------------------------------------ launch
@@ -753,12 +767,14 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
     if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
   }
   if (a.r > 0) {
-    int st = slim_launch_adapter_gemm(act, act_bf16, a.M, a.red, a.ad_q, a.r, p, ws, s);
+    int st = slim_launch_adapter_gemm(a.act16, a.M, a.red, a.ad_q, a.r, p, ws, s);
     if (st != SLIM_OK) return st;
-    SlimKernelTimer timer("adapter_p16", s);
-    const int64_t n8 = a.rows * a.r / 8;
-    SLIM_LAUNCH(timer, k_tile_p16, dim3((unsigned)((n8 + 255) / 256)), dim3(256), s,
-                reinterpret_cast<const u32x4_t*>(a.ad_p), a.rows, a.r, reinterpret_cast<u32x4_t*>(a.ad_pb));
+    SlimKernelTimer timer("adapter_finish", s);
+    const int64_t np = (a.rows * a.r / 8 + 255) / 256;
+    const int64_t nt = p.ad_split > 1 ? ((a.M + 31) / 32 * 32 * a.r / 8 + 255) / 256 : 0;
+    SLIM_LAUNCH(timer, k_adapter_finish, dim3((unsigned)(np + nt)), dim3(256), s,
+                reinterpret_cast<const u32x4_t*>(a.ad_p), a.rows, a.r, reinterpret_cast<u32x4_t*>(a.ad_pb), np,
+                a.tpart, p.ad_split, a.M, reinterpret_cast<u32x4_t*>(a.tm));
     if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
