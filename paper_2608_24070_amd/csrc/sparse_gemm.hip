@@ -283,7 +283,41 @@ __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
 // out[m, row] = sum_s part_s[m, row] + sum_j tm[m, j] P[row, j]. One wave per 16 output rows; the
 // split partials are summed in split order (deterministic) and the adapter's second product is
 // accumulated on top with 16x16x32 fp16 MFMA. The partials share the MFMA output layout, so each
-// lane reads its own four values per split and fragment.
+// lane reads its own four values per split and fragment. The loads of the first adapter pass and
+// of the first eight partials do not depend on each other and are all issued before any is used:
+// one memory round trip for the common case (at most eight splits, rank at most 32 kSteps).
+template <int FM>
+SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lrow, int lane, u32x4_t* aq,
+                                   u32x4_t (*bq)[FM]) {
+  constexpr int kSteps = FM == 1 ? 16 : 8;
+  const int g = lane >> 4;
+#pragma unroll
+  for (int t = 0; t < kSteps; ++t) {
+    const int64_t jj = clamp_hi(jbase + 32 * t + 8 * g, a.r - 8);
+    aq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_p + lrow * a.r + jj);
+#pragma unroll
+    for (int f = 0; f < FM; ++f)
+      bq[t][f] = *reinterpret_cast<const u32x4_t*>(a.tm + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.r + jj);
+  }
+}
+
+template <int FM>
+SLIM_DEV void finish_adapter_mfma(const LayerArgs& a, int64_t jbase, int lane, const u32x4_t* aq,
+                                  const u32x4_t (*bq)[FM], f4_t* acc) {
+  constexpr int kSteps = FM == 1 ? 16 : 8;
+  const int g = lane >> 4;
+#pragma unroll
+  for (int t = 0; t < kSteps; ++t) {
+    const bool jok = jbase + 32 * t + 8 * g < a.r;
+    const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[t]) : zero_h8();
+#pragma unroll
+    for (int f = 0; f < FM; ++f) {
+      const h8_t bv = (16 * f + (lane & 15) < a.M) ? __builtin_bit_cast(h8_t, bq[t][f]) : zero_h8();
+      acc[f] = mfma16(av, bv, acc[f]);
+    }
+  }
+}
+
 template <int FM>
 __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
   constexpr int kSteps = FM == 1 ? 16 : 8;
@@ -294,10 +328,12 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
   const int64_t rt = row0 / 64;
   const int w16 = (int)((row0 % 64) / 16);
   const int S = a.split;
+  const float* src = a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256);
+  u32x4_t aq[kSteps], bq[kSteps][FM];
+  if (a.r > 0) finish_adapter_loads<FM>(a, 0, lrow, lane, aq, bq);
   f4_t acc[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-  const float* src = a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256);
   for (int s0 = 0; s0 < S; s0 += 8) {
     f4_t pv[8][FM];
 #pragma unroll
@@ -313,25 +349,11 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
 #pragma unroll
         for (int f = 0; f < FM; ++f) acc[f] = acc[f] + pv[j][f];
   }
-  for (int64_t jbase = 0; jbase < a.r; jbase += 32 * kSteps) {
-    u32x4_t aq[kSteps], bq[kSteps][FM];
-#pragma unroll
-    for (int t = 0; t < kSteps; ++t) {
-      const int64_t jj = clamp_hi(jbase + 32 * t + 8 * g, a.r - 8);
-      aq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_p + lrow * a.r + jj);
-#pragma unroll
-      for (int f = 0; f < FM; ++f)
-        bq[t][f] = *reinterpret_cast<const u32x4_t*>(a.tm + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.r + jj);
-    }
-#pragma unroll
-    for (int t = 0; t < kSteps; ++t) {
-      const bool jok = jbase + 32 * t + 8 * g < a.r;
-      const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[t]) : zero_h8();
-#pragma unroll
-      for (int f = 0; f < FM; ++f) {
-        const h8_t bv = (16 * f + (lane & 15) < a.M) ? __builtin_bit_cast(h8_t, bq[t][f]) : zero_h8();
-        acc[f] = mfma16(av, bv, acc[f]);
-      }
+  if (a.r > 0) {
+    finish_adapter_mfma<FM>(a, 0, lane, aq, bq, acc);
+    for (int64_t jbase = 32 * kSteps; jbase < a.r; jbase += 32 * kSteps) {
+      finish_adapter_loads<FM>(a, jbase, lrow, lane, aq, bq);
+      finish_adapter_mfma<FM>(a, jbase, lane, aq, bq, acc);
     }
   }
   if (rr < a.rows) {

@@ -94,3 +94,18 @@ def test_workspace_sizes_are_modest(M, N, K, r):
     out_bytes = 4 * M * max(N, K)
     assert fwd < 64 * 2 ** 20 + out_bytes
     assert bwd < 64 * 2 ** 20 + out_bytes
+
+
+COUNTER_REGION = 4096 * 4    # the workspace's leading counter region (SLIM_COUNTER_SLOTS words)
+
+
+@pytest.mark.parametrize("M,N,K,r", [(1, 16, 128, 0), (1, 16, 128, 16), (16, 4096, 4096, 384), (33, 256, 256, 16)])
+def test_workspace_holds_counter_region_and_data(M, N, K, r):
+    # the data regions (adapter intermediate, partials) follow the counter region
+    assert slim.slim_linear_workspace(M, N, K, r) >= COUNTER_REGION + (2 * M * r if r else 0)
+    if N % 128 == 0:
+        assert slim.slim_bwd_dx_workspace(M, N, K, r) >= COUNTER_REGION + (2 * M * r if r else 0)
+
+
+def test_workspace_init_requires_counter_region():
+    assert slim.slim_workspace_init(A, COUNTER_REGION - 4, None) == 7   # SLIM_EWORKSPACE, before any GPU call

@@ -151,3 +151,26 @@ def test_bwd_is_deterministic():
     dy = dev_bits(dybits, torch.bfloat16)
     dL, dR = dev_bits(Lb, torch.float16), dev_bits(Rb, torch.float16)
     assert torch.equal(slim.bwd_dx(dy, pb, dL, dR).clone(), slim.bwd_dx(dy, pb, dL, dR).clone())
+
+
+COUNTER_BYTES = 4096 * 4   # the workspace's leading counter region
+
+
+def test_decode_counters_return_to_zero():
+    # small-M calls hand adapter partials between blocks of one launch through counters at the
+    # front of the workspace; every call must leave them at zero for the next one
+    W, X, L, R, dx, ad = layer_inputs(2048, 1024, 64, 32, name="ctr")
+    p = slim.pack(dev(W))
+    pb = slim.pack_bwd(p)
+    ws = torch.zeros(64 << 20, dtype=torch.uint8, device=dx.device)
+    dy = dx.new_empty((16, 2048)).normal_().to(dx.dtype)
+    for m in (16, 1, 7, 32, 20):
+        Y0 = slim.linear(dx[:m], p, ad).clone()
+        Y1 = slim.linear(dx[:m], p, ad, ws=ws)
+        Y2 = slim.linear(dx[:m], p, None, ws=ws)
+        D0 = slim.bwd_dx(dy[:min(m, 16)], pb, ad["L"], ad["R"]).clone()
+        D1 = slim.bwd_dx(dy[:min(m, 16)], pb, ad["L"], ad["R"], ws=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(Y0, Y1) and torch.equal(D0, D1), m
+        assert Y2.shape == (m, 2048) and dx.shape[0] == 32
+        assert int(ws[:COUNTER_BYTES].count_nonzero()) == 0, m
