@@ -10,6 +10,9 @@
 #define SLIM_COUNTER_SLOTS 4096
 // Reduction positions per adapter first-product unit of the small-M path.
 #define SLIM_DECODE_AD_SLICE 256
+// Small-M forward: most row tiles one sparse block runs, and the block count it aims for.
+#define SLIM_DECODE_MAX_UNITS 8
+#define SLIM_DECODE_BLOCKS 512
 
 // Argument checks: pure host functions, run before anything is enqueued.
 int slim_check_pack(const float* W, int64_t N, int64_t K, const void* codes, const void* meta,
@@ -30,6 +33,8 @@ struct SlimPlan {
   int sp_rows_tile = 0, sp_cols_tile = 0;  // output tile (rows of W or W^T, columns = M)
   int64_t sp_row_tiles = 0, sp_col_tiles = 0;
   int sp_split = 1;                   // reduction splits (small-M kernel only)
+  int dec_units = 1;                  // small M: row tiles per sparse block
+  int64_t sp_blocks = 0;              // small M: sparse blocks
   int64_t sp_chunks_per_split = 0;    // 128-wide chunks per split
   size_t lds_bytes = 0;               // dynamic LDS (unused: the kernels size their LDS statically)
   // workspace layout (byte offsets)

@@ -38,6 +38,8 @@
 
 namespace {
 
+constexpr int kDecodeMaxUnits = SLIM_DECODE_MAX_UNITS;
+
 struct LayerArgs {
   const uint32_t* codes;   // [rows, red/16] code words
   const uint32_t* meta;    // [rows, red/32] words = two index half-words
@@ -55,6 +57,7 @@ struct LayerArgs {
   // small-M path
   int split;               // reduction splits of the sparse product
   int64_t row_tiles;       // 64-row tiles (small M) or 512-row tiles (large M)
+  int64_t units;           // small M: row tiles per sparse block
   int64_t col_tiles;       // 96-column tiles (large M)
   int ad_split;            // reduction splits of the adapter's first product
   int64_t ad_jblocks;      // 64-wide column blocks of the adapter rank
@@ -120,39 +123,55 @@ SLIM_DEV bool split_reduce(f4_t* acc, float* part_tile, int S, int s, uint32_t* 
 // quantisation groups. Lane group qa (lane / 16) of the 16x16x64 sparse MFMA owns G whole
 // groups: per group one row's code words (32 B), index words (16 B) and scale, which the 16 lanes
 // of a lane group (16 rows of one block) read from one contiguous piece.
-template <bool BWD, int FM, int G>
-SLIM_DEV void decode_sparse_unit(const LayerArgs& a, int64_t u, _Float16* xs, int* last_flag) {
-  constexpr int MC = 16 * FM;
-  constexpr int SL = 512 * G;              // reduction positions per slice
-  constexpr int LDX = SL + 8;
-  constexpr int VPR = SL / 8;              // 16-byte activation vectors per row of the slice
-  constexpr int XV = MC * VPR / 256;       // ... per thread
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int S = a.split;
-  const int64_t rt = u / S;
-  const int s = (int)(u - rt * S);
-  const int64_t row0 = rt * 64;
-  const int64_t nchunks = a.red / 128;
-  const int64_t c0 = (int64_t)s * 4 * G;
-  const int64_t red0 = c0 * 128;
-  const bool bf16 = a.act_bf16 != 0;
-
-  const int64_t lrow = clamp_hi(row0 + 16 * wave + (lane & 15), a.rows - 1);
-  const int qa = lane >> 4;
-  const int64_t cl = c0 + (int64_t)qa * G;      // first chunk (group) of this lane group
+//
+// A block runs up to NU units of one slice, consecutive row tiles [rt0, rt1): it stages the
+// slice's activations in LDS once and loads each unit's packed words while the unit before is
+// computed. Results stay in registers until every load has been issued and are stored at the end:
+// a store between the loads would make the compiler's wait for one unit's words also wait for
+// the next unit's. The backward runs single units: its activations carry the scales of the
+// unit's 128-row group.
+template <int G>
+struct DecodeWords {
   u32x4_t cw[2 * G], mw[G];
   uint32_t sw[G];
+};
+
+template <bool BWD, int G>
+SLIM_DEV void decode_load_words(const LayerArgs& a, int64_t rt, int64_t cl, int lane, int wave, DecodeWords<G>& w) {
+  const int64_t nchunks = a.red / 128;
+  const int64_t lrow = clamp_hi(rt * 64 + 16 * wave + (lane & 15), a.rows - 1);
 #pragma unroll
   for (int gi = 0; gi < G; ++gi) {
     const int64_t ch = clamp_hi(cl + gi, nchunks - 1);
     const int64_t slot = packed_slot(lrow, ch, nchunks);
     const uint32_t* cp = a.codes + 8 * slot;
-    cw[2 * gi] = *reinterpret_cast<const u32x4_t*>(cp);
-    cw[2 * gi + 1] = *reinterpret_cast<const u32x4_t*>(cp + 4);
-    mw[gi] = *reinterpret_cast<const u32x4_t*>(a.meta + 4 * slot);
-    sw[gi] = BWD ? 0u : (uint32_t)a.scales[slot];
+    w.cw[2 * gi] = *reinterpret_cast<const u32x4_t*>(cp);
+    w.cw[2 * gi + 1] = *reinterpret_cast<const u32x4_t*>(cp + 4);
+    w.mw[gi] = *reinterpret_cast<const u32x4_t*>(a.meta + 4 * slot);
+    w.sw[gi] = BWD ? 0u : (uint32_t)a.scales[slot];
   }
-  const int64_t sgroup = row0 / 128;
+}
+
+template <bool BWD, int FM, int G, int NU>
+SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_t rt1, _Float16* xs) {
+  constexpr int MC = 16 * FM;
+  constexpr int SL = 512 * G;              // reduction positions per slice
+  constexpr int LDX = SL + 8;
+  constexpr int VPR = SL / 8;              // 16-byte activation vectors per row of the slice
+  constexpr int XV = MC * VPR / 256;       // ... per thread
+  static_assert(!BWD || NU == 1, "backward units are single: activations carry the group's scales");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int S = a.split;
+  const int64_t nchunks = a.red / 128;
+  const int64_t c0 = (int64_t)s * 4 * G;
+  const int64_t red0 = c0 * 128;
+  const bool bf16 = a.act_bf16 != 0;
+  const int qa = lane >> 4;
+  const int64_t cl = c0 + (int64_t)qa * G;      // first chunk (group) of this lane group
+
+  DecodeWords<G> wb[NU > 1 ? 2 : 1];
+  decode_load_words<BWD, G>(a, rt0, cl, lane, wave, wb[0]);
+  const int64_t sgroup = rt0 * 64 / 128;
   u32x4_t xv[XV], sv[XV];
 #pragma unroll
   for (int i = 0; i < XV; ++i) {
@@ -170,47 +189,63 @@ SLIM_DEV void decode_sparse_unit(const LayerArgs& a, int64_t u, _Float16* xs, in
   }
   __syncthreads();
 
-  f4_t acc[FM];
-#pragma unroll
-  for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
   const int qb = lane >> 4;
   const int pbase = 128 * G * (qb >> 1) + 8 * (qb & 1);
+  f4_t out[NU][FM];
 #pragma unroll
-  for (int gi = 0; gi < G; ++gi) {
-    const bool gok = cl + gi < nchunks;
-    const h2_t s2 = splat_h2(sw[gi]);
+  for (int k = 0; k < NU; ++k) {
+    if (rt0 + k >= rt1) break;
+    // the next unit's words (the last unit reloads itself: loads stay unconditional)
+    if (NU > 1) {
+      decode_load_words<BWD, G>(a, rt0 + k + 1 < rt1 ? rt0 + k + 1 : rt1 - 1, cl, lane, wave, wb[(k + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);   // keep them ahead of this unit's work
+    }
+    const DecodeWords<G>& w = wb[k & 1];
+    f4_t acc[FM];
 #pragma unroll
-    for (int t4 = 0; t4 < 8; ++t4) {
-      const uint32_t word = cw[2 * gi + (t4 >> 2)][t4 & 3];
-      h8_t av = BWD ? dequant_word_int(word) : dequant_word(word, s2);
-      av = gok ? av : zero_h8();
-      const int idx = (int)mw[gi][t4 >> 1];
-      const int p0 = pbase + 16 * (8 * gi + t4);
+    for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int f = 0; f < FM; ++f) {
-        const _Float16* xr = xs + (16 * f + (lane & 15)) * LDX + p0;
-        acc[f] = smfmac16(av, cat16(*reinterpret_cast<const h8_t*>(xr), *reinterpret_cast<const h8_t*>(xr + 256 * G)),
-                          acc[f], idx, t4 & 1);
+    for (int gi = 0; gi < G; ++gi) {
+      const bool gok = cl + gi < nchunks;
+      const h2_t s2 = splat_h2(w.sw[gi]);
+#pragma unroll
+      for (int t4 = 0; t4 < 8; ++t4) {
+        const uint32_t word = w.cw[2 * gi + (t4 >> 2)][t4 & 3];
+        h8_t av = BWD ? dequant_word_int(word) : dequant_word(word, s2);
+        av = gok ? av : zero_h8();
+        const int idx = (int)w.mw[gi][t4 >> 1];
+        const int p0 = pbase + 16 * (8 * gi + t4);
+#pragma unroll
+        for (int f = 0; f < FM; ++f) {
+          const _Float16* xr = xs + (16 * f + (lane & 15)) * LDX + p0;
+          acc[f] = smfmac16(av, cat16(*reinterpret_cast<const h8_t*>(xr), *reinterpret_cast<const h8_t*>(xr + 256 * G)),
+                            acc[f], idx, t4 & 1);
+        }
       }
     }
+#pragma unroll
+    for (int f = 0; f < FM; ++f) out[k][f] = acc[f];
   }
 
-  (void)last_flag;
-  if (a.finish) {
-    // k_finish sums the split partials (and adds the adapter); the kernel boundary orders them
-    float* dst = a.part + ((rt * S + s) * 4 + wave) * (int64_t)(FM * 256);
 #pragma unroll
-    for (int f = 0; f < FM; ++f) *reinterpret_cast<f4_t*>(dst + f * 256 + 4 * lane) = acc[f];
-    return;
-  }
-
-  // out^T fragment: lane (col + 16 * (row / 4)), element row % 4 -> 4 consecutive rows
-  const int64_t rr = row0 + 16 * wave + 4 * (lane >> 4);
-  if (rr < a.rows) {
+  for (int k = 0; k < NU; ++k) {
+    if (rt0 + k >= rt1) break;
+    const int64_t rt = rt0 + k;
+    if (a.finish) {
+      // k_finish sums the split partials (and adds the adapter); the kernel boundary orders them
+      float* dst = a.part + ((rt * S + s) * 4 + wave) * (int64_t)(FM * 256);
 #pragma unroll
-    for (int f = 0; f < FM; ++f) {
-      const int64_t m = 16 * f + (lane & 15);
-      if (m < a.M) *reinterpret_cast<f4_t*>(a.out + m * a.rows + rr) = acc[f];
+      for (int f = 0; f < FM; ++f) *reinterpret_cast<f4_t*>(dst + f * 256 + 4 * lane) = out[k][f];
+      continue;
+    }
+    // out^T fragment: lane (col + 16 * (row / 4)), element row % 4 -> 4 consecutive rows
+    const int64_t rr = rt * 64 + 16 * wave + 4 * (lane >> 4);
+    if (rr < a.rows) {
+#pragma unroll
+      for (int f = 0; f < FM; ++f) {
+        const int64_t m = 16 * f + (lane & 15);
+        if (m < a.M) *reinterpret_cast<f4_t*>(a.out + m * a.rows + rr) = out[k][f];
+      }
     }
   }
 }
@@ -268,15 +303,22 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, int* last_flag)
 }
 
 // Blocks [0, jblocks * ad_split) are adapter units (dispatched first: their reduction is the
-// longer path); the rest are sparse units.
-template <bool BWD, int FM, int G>
+// longer path); the rest are sparse blocks, block i of them taking slice i % split and row tiles
+// [(i / split) NU', + NU') with NU' = a.units (at most NU).
+template <bool BWD, int FM, int G, int NU>
 __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
   __shared__ __attribute__((aligned(16))) _Float16 xs[16 * FM * (512 * G + 8)];
   __shared__ int last_flag;
   const int64_t nA = a.r > 0 ? a.ad_jblocks * a.ad_split : 0;
   const int64_t b = blockIdx.x;
-  if (b < nA) decode_adapter_unit<FM>(a, b, &last_flag);
-  else decode_sparse_unit<BWD, FM, G>(a, b - nA, xs, &last_flag);
+  if (b < nA) {
+    decode_adapter_unit<FM>(a, b, &last_flag);
+    return;
+  }
+  const int64_t i = b - nA, S = a.split;
+  const int64_t rt0 = (i / S) * a.units;
+  const int64_t rt1 = rt0 + a.units < a.row_tiles ? rt0 + a.units : a.row_tiles;
+  decode_sparse_range<BWD, FM, G, NU>(a, (int)(i % S), rt0, rt1, xs);
 }
 
 // ============================================================ small-M: finish
@@ -750,11 +792,17 @@ __global__ void __launch_bounds__(256) k_adapter_finish(const u32x4_t* __restric
 }
 
 // ------------------------------------------------------------------------------ launch
-template <bool BWD, int FM, int G>
+template <bool BWD, int FM, int G, int NU>
 void launch_decode(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
   SlimKernelTimer timer(BWD ? "decode_bwd" : "decode_fwd", s);
-  dim3 grid((unsigned)(p.sp_row_tiles * p.sp_split + (a.r > 0 ? p.ad_jblocks * p.ad_split : 0)));
-  SLIM_LAUNCH(timer, (k_decode<BWD, FM, G>), grid, dim3(256), s, a);
+  dim3 grid((unsigned)(p.sp_blocks + (a.r > 0 ? p.ad_jblocks * p.ad_split : 0)));
+  SLIM_LAUNCH(timer, (k_decode<BWD, FM, G, NU>), grid, dim3(256), s, a);
+}
+
+template <bool BWD, int FM, int G>
+void launch_decode_units(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
+  if (!BWD && p.dec_units > 1) launch_decode<BWD, FM, G, BWD ? 1 : kDecodeMaxUnits>(a, p, s);
+  else launch_decode<BWD, FM, G, 1>(a, p, s);
 }
 
 template <int FM>
@@ -767,10 +815,10 @@ template <bool BWD>
 int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int act_bf16, char* ws, hipStream_t s) {
   if (p.decode) {
     if (p.dec_fm == 1) {
-      if (p.dec_g == 1) launch_decode<BWD, 1, 1>(a, p, s);
-      else launch_decode<BWD, 1, 2>(a, p, s);
+      if (p.dec_g == 1) launch_decode_units<BWD, 1, 1>(a, p, s);
+      else launch_decode_units<BWD, 1, 2>(a, p, s);
     } else {
-      launch_decode<BWD, 2, 1>(a, p, s);
+      launch_decode_units<BWD, 2, 1>(a, p, s);
     }
     if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
     if (a.finish) {
@@ -826,6 +874,7 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.out = out;
   a.split = p.sp_split;
   a.row_tiles = p.sp_row_tiles;
+  a.units = p.dec_units;
   a.col_tiles = p.sp_col_tiles;
   a.ad_split = p.ad_split;
   a.ad_jblocks = p.ad_jblocks;

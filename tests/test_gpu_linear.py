@@ -53,6 +53,16 @@ def test_tile_kernel_short_reduction(k, m):
     _fwd_case(528, k, 16, m, name="shortk")
 
 
+@pytest.mark.parametrize("m", [1, 16, 27])
+def test_decode_blocks_run_several_row_tiles(m):
+    # 313 row tiles: forward sparse blocks take 3 (m <= 16) or 5 (m > 16) row tiles each, the last
+    # block fewer; the sampled rows include the last tiles
+    n = 20032
+    rows = np.unique(np.concatenate([synth.stream(5, "rows").choice(n, size=384, replace=False),
+                                     np.arange(n - 200, n)]))
+    _fwd_case(n, 4096, 64, m, rows=rows, name="units")
+
+
 def test_linear_on_oracle_pack():
     _fwd_case(1024, 1024, 64, 16, use_oracle_pack=True, name="opack")
     _fwd_case(1024, 1024, 64, 256, use_oracle_pack=True, name="opack")
@@ -157,8 +167,8 @@ COUNTER_BYTES = 4096 * 4   # the workspace's leading counter region
 
 
 def test_decode_counters_return_to_zero():
-    # small-M calls hand adapter partials between blocks of one launch through counters at the
-    # front of the workspace; every call must leave them at zero for the next one
+    # the front of the workspace is a counter region that every call must leave at zero; calls on
+    # one workspace give the results of calls on fresh ones
     W, X, L, R, dx, ad = layer_inputs(2048, 1024, 64, 32, name="ctr")
     p = slim.pack(dev(W))
     pb = slim.pack_bwd(p)
