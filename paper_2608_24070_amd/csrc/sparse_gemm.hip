@@ -232,10 +232,12 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
     if (rt0 + k >= rt1) break;
     const int64_t rt = rt0 + k;
     if (a.finish) {
-      // k_finish sums the split partials (and adds the adapter); the kernel boundary orders them
+      // k_finish sums the split partials (and adds the adapter); the kernel boundary orders them.
+      // Lanes of columns past M hold nothing and store nothing.
       float* dst = a.part + ((rt * S + s) * 4 + wave) * (int64_t)(FM * 256);
 #pragma unroll
-      for (int f = 0; f < FM; ++f) *reinterpret_cast<f4_t*>(dst + f * 256 + 4 * lane) = out[k][f];
+      for (int f = 0; f < FM; ++f)
+        if (16 * f + (lane & 15) < a.M) *reinterpret_cast<f4_t*>(dst + f * 256 + 4 * lane) = out[k][f];
       continue;
     }
     // out^T fragment: lane (col + 16 * (row / 4)), element row % 4 -> 4 consecutive rows
@@ -325,9 +327,10 @@ __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
 // out[m, row] = sum_s part_s[m, row] + sum_j tm[m, j] P[row, j]. One wave per 16 output rows; the
 // split partials are summed in split order (deterministic) and the adapter's second product is
 // accumulated on top with 16x16x32 fp16 MFMA. The partials share the MFMA output layout, so each
-// lane reads its own four values per split and fragment. The loads of the first adapter pass and
-// of the first eight partials do not depend on each other and are all issued before any is used:
-// one memory round trip for the common case (at most eight splits, rank at most 32 kSteps).
+// lane reads its own four values per split and fragment (lanes of columns past M read nothing).
+// The loads of the first adapter pass and of the first eight partials do not depend on each other
+// and are all issued before any is used: one memory round trip for the common case (at most
+// eight splits, rank at most 32 kSteps).
 template <int FM>
 SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lrow, int lane, u32x4_t* aq,
                                    u32x4_t (*bq)[FM]) {
@@ -370,7 +373,7 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
   const int64_t rt = row0 / 64;
   const int w16 = (int)((row0 % 64) / 16);
   const int S = a.split;
-  const float* src = a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256);
+  const rsrc_t pr = make_rsrc(a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256), ((int64_t)(S - 1) * 4 + 1) * FM * 256 * 4);
   u32x4_t aq[kSteps], bq[kSteps][FM];
   if (a.r > 0) finish_adapter_loads<FM>(a, 0, lrow, lane, aq, bq);
   f4_t acc[FM];
@@ -382,8 +385,11 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
     for (int j = 0; j < 8; ++j) {
       const int ss = s0 + j < S ? s0 + j : S - 1;
 #pragma unroll
-      for (int f = 0; f < FM; ++f)
-        pv[j][f] = *reinterpret_cast<const f4_t*>(src + (int64_t)ss * 4 * FM * 256 + f * 256 + 4 * lane);
+      for (int f = 0; f < FM; ++f) {
+        // a lane whose column is past M points past the resource: no memory access, zero returned
+        const uint32_t off = 16 * f + (lane & 15) < a.M ? (uint32_t)(((ss * 4 * FM + f) * 256 + 4 * lane) * 4) : 0x80000000u;
+        pv[j][f] = __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(pr, off, 0, 0));
+      }
     }
 #pragma unroll
     for (int j = 0; j < 8; ++j)
