@@ -93,12 +93,16 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     if (q.sp_split > 1 || r > 0) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 4 * q.dec_fm * 256 * 4;
     q.lds_bytes = 0;
   } else {
-    // large M: dense adapter GEMM (128 x 128 tiles) then 512 x 96 sparse tiles
+    // large M: dense adapter GEMM (128 x 128 tiles) then 512 x 96 or 512 x 128 sparse tiles
     q.decode = false;
     q.sp_rows_tile = 512;
-    q.sp_cols_tile = 96;
     q.sp_row_tiles = cdiv(rows, 512);
-    q.sp_col_tiles = cdiv(M, 96);
+    // 512 x 128 tiles spend less dequantisation per MFMA (a tile takes about 1.12x the time of a
+    // 512 x 96 one for 4/3 the work); 512 x 96 tiles are more and can fill the last round of
+    // blocks (one per CU) better. Take the one with fewer rounds, weighted.
+    const int64_t r96 = cdiv(q.sp_row_tiles * cdiv(M, 96), 256), r128 = cdiv(q.sp_row_tiles * cdiv(M, 128), 256);
+    q.sp_cols_tile = 112 * r128 <= 100 * r96 ? 128 : 96;
+    q.sp_col_tiles = cdiv(M, q.sp_cols_tile);
     q.sp_split = 1;
     q.sp_chunks_per_split = nchunks;
     if (r > 0) {

@@ -24,9 +24,9 @@
 //    adapter). Sparse units only store their partials; k_finish sums them in a fixed order and
 //    adds the adapter's second product, so no sparse unit waits on another.
 //  * large M: the adapter's first product runs as a dense GEMM (adapter_gemm.hip); k_tile then
-//    computes 512 x 96 output tiles on 32x32x32 sparse MFMA, with activations and packed words
-//    streamed into a three-stage LDS ring by direct loads, and adds the second adapter product
-//    in its epilogue.
+//    computes 512 x 96 or 512 x 128 output tiles on 32x32x32 sparse MFMA, with activations and
+//    packed words streamed into LDS rings by direct loads, and adds the second adapter product in
+//    its epilogue.
 // Every global load is issued unconditionally from a clamped (or, through a buffer resource,
 // range-checked) address and masked when used: a load under a branch makes the compiler wait
 // for it at the join, which serialises what should be one round of memory traffic.
@@ -58,7 +58,7 @@ struct LayerArgs {
   int split;               // reduction splits of the sparse product
   int64_t row_tiles;       // 64-row tiles (small M) or 512-row tiles (large M)
   int64_t units;           // small M: row tiles per sparse block
-  int64_t col_tiles;       // 96-column tiles (large M)
+  int64_t col_tiles;       // 96- or 128-column tiles (large M)
   int ad_split;            // reduction splits of the adapter's first product
   int64_t ad_jblocks;      // 64-wide column blocks of the adapter rank
   float* part;             // sparse split partials
@@ -415,30 +415,54 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
 
 // ============================================================ large-M tile kernel
 // Block = 4 waves; wave w owns rows [row0 + 128 w, +128) as 4 fragments of 32 and all columns
-// [m0, m0 + 96) as 3 fragments of 32: a 128 x 96 accumulator (192 registers per lane) on 32x32x32
-// sparse MFMA. Each dequantised weight fragment feeds three MFMAs and no weight row is
-// dequantised by two waves.
-// Per 128-wide reduction chunk, the fp16 activation tile [96 x 128] and each wave's packed words
-// (codes, index words and scales of its 128 rows) go straight from memory to LDS (direct loads)
-// into a ring of three stages, two chunks ahead, so no register holds data still in flight. A
+// [m0, m0 + TC) as TC / 32 fragments of 32 (TC = 96 or 128): a 128 x TC accumulator (TC * 2
+// registers per lane, in the accumulation registers) on 32x32x32 sparse MFMA. Each dequantised
+// weight fragment feeds TC / 32 MFMAs and no weight row is dequantised by two waves; the wider
+// tile spends less dequantisation per MFMA, the narrower one gives more tiles to even out the
+// last round of blocks (the plan picks per shape).
+// Per 128-wide reduction chunk, each wave's packed words (codes, index words and scales of its
+// 128 rows) and the fp16 activation tile [TC x 128] go straight from memory to LDS (direct
+// loads), so no register holds data still in flight: the words into a ring of three stages, two
+// chunks ahead; the activations into a ring of three stages, two chunks ahead, at TC = 96, or of
+// two stages, one chunk ahead, at TC = 128 (three would not fit in LDS next to the words). A
 // chunk's words are read from LDS, and its first step dequantised, during the last step of the
 // chunk before. Activation rows in LDS are 256 B with the 16-byte column index XOR-swizzled by
 // the row, so B-fragment reads (32 rows at one column) hit distinct banks. The backward also
-// brings each wave's scale row (its 128-row group) into LDS.
-constexpr int kTR = 512, kTC = 96, kTThreads = 256, kStages = 3, kBand = 4;
-// Direct loads per thread per chunk, issued in this order: packed words (4 code loads, 2 index
-// word loads, and in the forward 1 scale load), then 6 activation loads (and in the backward one
-// scale-row load). Chunk c's loads are issued at the top of chunk c - 2.
-//  * at the top of chunk c its activations must have landed: only chunk c - 1's loads may still
-//    be outstanding;
+// brings each wave's scale row (its 128-row group) into LDS with the activations.
+constexpr int kTR = 512, kTThreads = 256, kBand = 4;
+template <int TC> struct TileShape {
+  static constexpr int kFm = TC / 32;                  // column fragments per wave
+  static constexpr int kActRows = TC / 4;              // activation rows each wave brings in
+  static constexpr int kActLoads = TC / 16;            // ... four rows per direct load
+  static constexpr int kStagesX = TC == 128 ? 2 : 3;   // activation stages
+  static constexpr int kAhead = kStagesX - 1;          // chunks of activations in flight ahead
+};
+// Direct loads per thread per chunk: activation loads (TC / 16, and in the backward one scale-row
+// load) and packed words (4 code loads, 2 index word loads, and in the forward 1 scale load).
+// kAhead 2: chunk c issues chunk c + 2's words in its first step and chunk c + 2's activations in
+// its second.
+//  * at the top of chunk c its words and activations must have landed: only chunk c + 1's loads
+//    may still be outstanding;
 //  * in the last step of chunk c, chunk c + 1's words must have landed: only chunk c + 1's
-//    activation (and scale-row) loads and chunk c's loads may still be outstanding.
-// The prologue issues chunks 0 and 1 in the same order, so the same counts hold from the start.
-constexpr int kTileWordsFwd = 4 + 2 + 1, kTileWordsBwd = 4 + 2, kTileActFwd = 6, kTileActBwd = 6 + 1;
-constexpr int kTileTopFwd = kTileWordsFwd + kTileActFwd, kTileTopBwd = kTileWordsBwd + kTileActBwd;
-constexpr int kTileNextFwd = kTileActFwd + kTileTopFwd, kTileNextBwd = kTileActBwd + kTileTopBwd;
+//    activations and chunk c + 2's loads may still be outstanding.
+// kAhead 1: chunk c issues chunk c + 1's activations in its first step and chunk c + 2's words in
+// its second.
+//  * at the top of chunk c its activations and words must have landed: only chunk c + 1's words
+//    (issued after chunk c's activations) may still be outstanding;
+//  * in the last step of chunk c, chunk c + 1's words must have landed: only chunk c + 1's
+//    activations and chunk c + 2's words may still be outstanding.
+// The prologue issues the loads of the chunks before in the same order, so the same counts hold
+// from the start.
+constexpr int kTileWordsFwd = 4 + 2 + 1, kTileWordsBwd = 4 + 2;
+template <bool BWD, int TC> struct TileCounts {
+  static constexpr bool kActFirst = TileShape<TC>::kAhead == 1;
+  static constexpr int kWords = BWD ? kTileWordsBwd : kTileWordsFwd;
+  static constexpr int kAct = TileShape<TC>::kActLoads + (BWD ? 1 : 0);
+  static constexpr int kTop = kActFirst ? kWords : kAct + kWords;
+  static constexpr int kNext = kActFirst ? kAct + kWords : kAct + kWords + kAct;
+};
 
-static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && kTileNextFwd < 64, "s_waitcnt encoding");
+static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && TileCounts<true, 128>::kNext < 64, "s_waitcnt encoding");
 static_assert(vmcnt_lgkm0_wait(20) == 0x4074u, "s_waitcnt encoding");
 
 
@@ -462,13 +486,18 @@ struct TileWords {
   uint32_t sw[4];
 };
 
-template <bool BWD>
+template <bool BWD, int TC>
 SLIM_DEV void tile_body(const LayerArgs& a) {
-  // one array per stage (the stage of chunk c is c % 3, a constant in the loop unrolled by three),
-  // so that reads of one stage are not ordered behind loads still landing in another
-  __shared__ __attribute__((aligned(16))) _Float16 xs0[kTC][128], xs1[kTC][128], xs2[kTC][128];
+  using Sh = TileShape<TC>;
+  using Ct = TileCounts<BWD, TC>;
+  constexpr int kTC = TC, kFm = Sh::kFm, kStagesX = Sh::kStagesX;
+  // one array per stage (the stages of chunk c are c % 3 for the words and c % kStagesX for the
+  // activations, constants in the loop unrolled by six), so that reads of one stage are not
+  // ordered behind loads still landing in another
+  __shared__ __attribute__((aligned(16))) _Float16 xs0[kTC][128], xs1[kTC][128], xs2[kStagesX == 3 ? kTC : 1][128];
   __shared__ __attribute__((aligned(16))) TileWordsLds<BWD> ws0, ws1, ws2;
-  __shared__ __attribute__((aligned(16))) _Float16 ss0[BWD ? 4 : 1][512], ss1[BWD ? 4 : 1][512], ss2[BWD ? 4 : 1][512];
+  __shared__ __attribute__((aligned(16))) _Float16 ss0[BWD ? 4 : 1][512], ss1[BWD ? 4 : 1][512],
+      ss2[BWD && kStagesX == 3 ? 4 : 1][512];
   auto xs_at = [&](int stg) -> _Float16(*)[128] { return stg == 0 ? xs0 : (stg == 1 ? xs1 : xs2); };
   auto ws_at = [&](int stg) -> TileWordsLds<BWD>& { return stg == 0 ? ws0 : (stg == 1 ? ws1 : ws2); };
   auto ss_at = [&](int stg) -> _Float16(*)[512] { return stg == 0 ? ss0 : (stg == 1 ? ss1 : ss2); };
@@ -510,15 +539,15 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   const uint32_t mo0 = rel_slot(d0 + (uint32_t)lane) * 16u;                     // index words: rows 0..63
   const uint32_t so0 = rel_slot(d0 + 2u * (uint32_t)lane) * 2u;                 // scales: rows 2 L, 2 L + 1
 
-  // activation chunk c -> stage c % kStages: wave w writes rows 24 w .. 24 w + 23, four per load
-  // (lane L: row + L / 16, LDS column slot L % 16 holding column (L % 16) ^ (row % 16)).
-  // Load i covers rows 24 w + 4 i + L / 16; with S = 16 ((L % 16) ^ (L / 16)) its byte offset is
-  // (24 w + L / 16) 2 red + 8 i red + (S ^ 16 ((8 (w % 2) + 4 i) % 16)), as 2 red is a multiple
-  // of 256 and S < 256.
+  // activation chunk c -> stage c % kStagesX: wave w writes rows R w .. R w + R - 1 (R = TC / 4),
+  // four per load (lane L: row + L / 16, LDS column slot L % 16 holding column
+  // (L % 16) ^ (row % 16)). Load i covers rows R w + 4 i + L / 16; with S = 16 ((L % 16) ^ (L / 16))
+  // its byte offset is (R w + L / 16) 2 red + 8 i red + (S ^ 16 ((R w + 4 i) % 16)), as 2 red is a
+  // multiple of 256 and S < 256.
   const int lrow = lane >> 4, lslot = lane & 15;
   const int64_t brows = a.M - m0 < kTC ? a.M - m0 : kTC;
   const rsrc_t rx = make_rsrc(a.act16 + m0 * a.red, brows * a.red * 2);    // the block's activation rows
-  const uint32_t xo0 = (uint32_t)(24 * wave + lrow) * (uint32_t)a.red * 2u + 16u * (uint32_t)(lslot ^ lrow);
+  const uint32_t xo0 = (uint32_t)(Sh::kActRows * wave + lrow) * (uint32_t)a.red * 2u + 16u * (uint32_t)(lslot ^ lrow);
   const uint32_t xstep = 8u * (uint32_t)a.red;
   const rsrc_t rg = make_rsrc(a.scales + (16 * wblk / 128) * a.red, a.red * 2);   // backward: the wave's scale row
 
@@ -536,9 +565,9 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   auto dma_act = [&](int64_t c, int stg, uint32_t xo) {
     const int cc = (int)clamp_hi(c, nch - 1);
 #pragma unroll
-    for (int i = 0; i < 6; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)&xs_at(stg)[24 * wave + 4 * i][0], 16,
-                                               (xo ^ (16u * ((8u * (wave & 1) + 4u * i) & 15u))) + (uint32_t)i * xstep,
+    for (int i = 0; i < Sh::kActLoads; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)&xs_at(stg)[Sh::kActRows * wave + 4 * i][0], 16,
+                                               (xo ^ (16u * ((uint32_t)(Sh::kActRows * wave + 4 * i) & 15u))) + (uint32_t)i * xstep,
                                                256 * cc, 0, 0);
     if (BWD) {
       // the wave's scale row s16[n, g] for this chunk (g = its 128-row group), four copies
@@ -567,11 +596,11 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   // 8192 fm + (bo ^ (32 st + 128)) of the stage.
   const uint32_t bo0 = 256u * (uint32_t)(lane & 31) + 16u * (uint32_t)((lane & 15) ^ ha);
 
-  f16_t acc[4][3];
+  f16_t acc[4][kFm];
 #pragma unroll
   for (int fn = 0; fn < 4; ++fn)
 #pragma unroll
-    for (int fm = 0; fm < 3; ++fm)
+    for (int fm = 0; fm < kFm; ++fm)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[fn][fm][v] = 0.f;
 
@@ -581,14 +610,14 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   dma_words(0, 0, co0, mo0, so0);
   dma_act(0, 0, xo0);
   dma_words(1, 1, co0, mo0, so0);
-  dma_act(1, 1, xo0);
-  __builtin_amdgcn_s_waitcnt(vmcnt_wait(BWD ? kTileNextBwd : kTileNextFwd));   // chunk 0's words
+  if (!Ct::kActFirst) dma_act(1, 1, xo0);
+  __builtin_amdgcn_s_waitcnt(vmcnt_wait(Ct::kNext));   // chunk 0's words
   read_words(0, tw[0]);
   dequant(tw[0], 0, aq[0]);
 
-  auto chunk = [&](int64_t c, auto zc) {
-    constexpr int z = decltype(zc)::value;
-    const int stg = z;                      // c % 3 (c0 is a multiple of 3)
+  auto chunk = [&](int64_t c, auto zc, auto xc) {
+    constexpr int z = decltype(zc)::value;    // c % 3: word stage and register set
+    constexpr int stg = decltype(xc)::value;  // c % kStagesX: activation stage
     // Nothing of the previous chunk is scheduled past this point.
     __builtin_amdgcn_sched_barrier(0);
     // chunk c's activations have landed once only chunk c - 1's loads are outstanding; and this
@@ -596,7 +625,7 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
     // barrier no wave still reads it.
     // The barrier is issued as a bare instruction: the builtin would also make this wave wait
     // for every direct-to-LDS load in flight, including the ones for the next chunk.
-    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(BWD ? kTileTopBwd : kTileTopFwd));
+    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(Ct::kTop));
     asm volatile("s_barrier" ::: "memory");
     // this chunk's copies of the base offsets (opaque, so nothing derived from them is hoisted)
     uint32_t xo = xo0, co = co0, mo = mo0, so = so0, bo = bo0;
@@ -620,25 +649,25 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
     // the next step's fragment fm (one B buffer), while the next step's dequantised weights go to
     // the other A buffer. During the last step the next chunk's words are read and its first step
     // dequantised.
-    h16_t bq[3];
+    h16_t bq[kFm];
 #pragma unroll
-    for (int fm = 0; fm < 3; ++fm) read_b(0, fm, bq[fm]);
+    for (int fm = 0; fm < kFm; ++fm) read_b(0, fm, bq[fm]);
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
-      // chunk c + 2's direct loads, into the stage read in chunk c - 1: words during step 0,
-      // activations during step 1, one load after each MFMA (issued in a burst at the barrier,
-      // the four waves' loads would fill the address unit's queue and stall instruction issue)
-      if (st == 0) dma_words(c + kStages - 1, (z + 2) % 3, co, mo, so);
-      if (st == 1) dma_act(c + kStages - 1, (z + 2) % 3, xo);
+      // direct loads into the stages read in chunk c - 1 (chunk c + kAhead's activations, chunk
+      // c + 2's words) during steps 0 and 1, one load after each MFMA (issued in a burst at the
+      // barrier, the four waves' loads would fill the address unit's queue and stall issue)
+      if (st == (Ct::kActFirst ? 0 : 1)) dma_act(c + Sh::kAhead, (stg + Sh::kAhead) % kStagesX, xo);
+      if (st == (Ct::kActFirst ? 1 : 0)) dma_words(c + 2, (z + 2) % 3, co, mo, so);
       if (st < 3) {
         dequant(cur, st + 1, aq[(st + 1) & 1]);
       } else {
-        __builtin_amdgcn_s_waitcnt(vmcnt_wait(BWD ? kTileNextBwd : kTileNextFwd));   // chunk c + 1's words
+        __builtin_amdgcn_s_waitcnt(vmcnt_wait(Ct::kNext));   // chunk c + 1's words
         read_words((z + 1) % 3, nxt);
         dequant(nxt, 0, aq[0]);
       }
 #pragma unroll
-      for (int fm = 0; fm < 3; ++fm) {
+      for (int fm = 0; fm < kFm; ++fm) {
 #pragma unroll
         for (int fn = 0; fn < 4; ++fn)
           acc[fn][fm] = smfmac32(aq[st & 1][fn], bq[fm], acc[fn][fm], (int)cur.mw[fn][st >> 1], st & 1);
@@ -647,9 +676,9 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
       // interleave: each MFMA followed by a share of the VALU work and, in steps 0 and 1, by one
       // direct load; the LDS reads of fragment fm follow its four MFMAs (the next chunk's words
       // are read at the start of the last step)
-      const int nvm = st == 0 ? (BWD ? kTileWordsBwd : kTileWordsFwd) : st == 1 ? (BWD ? kTileActBwd : kTileActFwd) : 0;
+      const int nvm = st == 0 ? (Ct::kActFirst ? Ct::kAct : Ct::kWords) : st == 1 ? (Ct::kActFirst ? Ct::kWords : Ct::kAct) : 0;
 #pragma unroll
-      for (int i = 0; i < 12; ++i) {
+      for (int i = 0; i < 4 * kFm; ++i) {
         if (st == 3 && i < 6) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);   // DS read
         __builtin_amdgcn_sched_group_barrier(0x0008, 1, 0);                          // MFMA
         if (i < nvm) __builtin_amdgcn_sched_group_barrier(0x0020, 1, 0);             // VMEM read
@@ -658,16 +687,31 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
       }
     }
   };
-  // full groups of three without guards (a load under a branch costs a full wait at the join),
-  // then at most two chunks
+  // full groups of six without guards (a load under a branch costs a full wait at the join),
+  // then at most five chunks
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using X0 = std::integral_constant<int, 0>;
+  using X1 = std::integral_constant<int, 1>;
+  using X2 = std::integral_constant<int, kStagesX == 3 ? 2 : 0>;
+  using X3 = std::integral_constant<int, kStagesX == 3 ? 0 : 1>;
+  using X4 = std::integral_constant<int, kStagesX == 3 ? 1 : 0>;
+  using X5 = std::integral_constant<int, kStagesX == 3 ? 2 : 1>;
   int64_t c0 = 0;
-  for (; c0 + 3 <= nch; c0 += 3) {
-    chunk(c0, std::integral_constant<int, 0>{});
-    chunk(c0 + 1, std::integral_constant<int, 1>{});
-    chunk(c0 + 2, std::integral_constant<int, 2>{});
+  for (; c0 + 6 <= nch; c0 += 6) {
+    chunk(c0, I0{}, X0{});
+    chunk(c0 + 1, I1{}, X1{});
+    chunk(c0 + 2, I2{}, X2{});
+    chunk(c0 + 3, I0{}, X3{});
+    chunk(c0 + 4, I1{}, X4{});
+    chunk(c0 + 5, I2{}, X5{});
   }
-  if (c0 < nch) chunk(c0, std::integral_constant<int, 0>{});
-  if (c0 + 1 < nch) chunk(c0 + 1, std::integral_constant<int, 1>{});
+  if (c0 < nch) chunk(c0, I0{}, X0{});
+  if (c0 + 1 < nch) chunk(c0 + 1, I1{}, X1{});
+  if (c0 + 2 < nch) chunk(c0 + 2, I2{}, X2{});
+  if (c0 + 3 < nch) chunk(c0 + 3, I0{}, X3{});
+  if (c0 + 4 < nch) chunk(c0 + 4, I1{}, X4{});
   // the ring's last loads (repeats of the final chunk) must land before the block's LDS is released
   __builtin_amdgcn_s_waitcnt(0);
 
@@ -682,19 +726,19 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
     const int64_t nj = a.r / 16;
     const rsrc_t rp = make_rsrc(a.ad_pb, (a.rows + 31) / 32 * 32 * a.r * 2), rt = make_rsrc(a.tm, (a.M + 31) / 32 * 32 * a.r * 2);
     const uint32_t lo16 = 32u * (uint32_t)(lane & 31) + 16u * ha;   // the lane's bytes within a 1 KB tile
-    uint32_t po[4], to[3];
+    uint32_t po[4], to[kFm];
 #pragma unroll
     for (int fn = 0; fn < 4; ++fn) po[fn] = (uint32_t)((wrow0 + 32 * fn) / 32 * nj) * 1024u + lo16;
 #pragma unroll
-    for (int fm = 0; fm < 3; ++fm) to[fm] = (uint32_t)((m0 + 32 * fm) / 32 * nj) * 1024u + lo16;
-    struct AdRegs { u32x4_t pa[4], pb[3]; };
+    for (int fm = 0; fm < kFm; ++fm) to[fm] = (uint32_t)((m0 + 32 * fm) / 32 * nj) * 1024u + lo16;
+    struct AdRegs { u32x4_t pa[4], pb[kFm]; };
     AdRegs ar[4];
     auto ad_load = [&](int64_t t, AdRegs& R) {
       const int so = (int)(clamp_hi(t, nj - 1) * 1024);
 #pragma unroll
       for (int fn = 0; fn < 4; ++fn) R.pa[fn] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, po[fn], so, 0));
 #pragma unroll
-      for (int fm = 0; fm < 3; ++fm) R.pb[fm] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rt, to[fm], so, 0));
+      for (int fm = 0; fm < kFm; ++fm) R.pb[fm] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rt, to[fm], so, 0));
     };
     ad_load(0, ar[0]);
     ad_load(1, ar[1]);
@@ -703,17 +747,17 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
       constexpr int u = decltype(uc)::value;
       ad_load(t + 3, ar[(u + 3) % 4]);
       // step t's loads have landed once only the three later steps' loads are outstanding
-      __builtin_amdgcn_s_waitcnt(vmcnt_wait(3 * 7));
+      __builtin_amdgcn_s_waitcnt(vmcnt_wait(3 * (4 + kFm)));
       AdRegs& R = ar[u];
 #pragma unroll
       for (int fn = 0; fn < 4; ++fn) asm volatile("" : "+v"(R.pa[fn]));
 #pragma unroll
-      for (int fm = 0; fm < 3; ++fm) asm volatile("" : "+v"(R.pb[fm]));
+      for (int fm = 0; fm < kFm; ++fm) asm volatile("" : "+v"(R.pb[fm]));
       if (t < nj) {
 #pragma unroll
         for (int fn = 0; fn < 4; ++fn)
 #pragma unroll
-          for (int fm = 0; fm < 3; ++fm)
+          for (int fm = 0; fm < kFm; ++fm)
             acc[fn][fm] = mfma32(__builtin_bit_cast(h8_t, R.pa[fn]), __builtin_bit_cast(h8_t, R.pb[fm]), acc[fn][fm]);
       }
     };
@@ -728,7 +772,7 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
 
   // D[i][j] of a 32x32 fragment: lane j + 32 * ((i / 4) % 2), element 4 * (i / 8) + i % 4
 #pragma unroll
-  for (int fm = 0; fm < 3; ++fm) {
+  for (int fm = 0; fm < kFm; ++fm) {
     const int64_t m = m0 + 32 * fm + (lane & 31);
     if (m >= a.M) continue;
 #pragma unroll
@@ -744,9 +788,9 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   }
 }
 
-template <bool BWD>
+template <bool BWD, int TC>
 __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
-  tile_body<BWD>(a);
+  tile_body<BWD, TC>(a);
 }
 
 // bf16 -> fp16 (round to nearest even), 8 values per thread
@@ -855,7 +899,8 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
   dim3 grid((unsigned)(8 * ((p.sp_row_tiles * p.sp_col_tiles + 7) / 8)));
-  SLIM_LAUNCH(timer, (k_tile<BWD>), grid, dim3(kTThreads), s, a);
+  if (p.sp_cols_tile == 128) SLIM_LAUNCH(timer, (k_tile<BWD, 128>), grid, dim3(kTThreads), s, a);
+  else SLIM_LAUNCH(timer, (k_tile<BWD, 96>), grid, dim3(kTThreads), s, a);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }
 

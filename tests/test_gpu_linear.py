@@ -63,6 +63,14 @@ def test_decode_blocks_run_several_row_tiles(m):
     _fwd_case(n, 4096, 64, m, rows=rows, name="units")
 
 
+def test_tile_kernel_wide_tiles_ragged_m():
+    # 22 row tiles x 1400 columns: the plan takes 512 x 128 tiles (11 column tiles, the last 120
+    # wide); the sampled columns include the last ones
+    rows = np.sort(synth.stream(6, "rows").choice(11008, size=256, replace=False))
+    ms = np.unique(np.concatenate([synth.stream(6, "ms").choice(1400, size=40, replace=False), np.arange(1380, 1400)]))
+    _fwd_case(11008, 2048, 48, 1400, rows=rows, ms=ms, name="wide")
+
+
 def test_linear_on_oracle_pack():
     _fwd_case(1024, 1024, 64, 16, use_oracle_pack=True, name="opack")
     _fwd_case(1024, 1024, 64, 256, use_oracle_pack=True, name="opack")
@@ -150,6 +158,12 @@ def test_bwd_decode_shape():
 def test_bwd_mlp70b_sampled(m, seed):
     ms = None if m <= 16 else np.sort(synth.stream(seed, "bms").choice(m, size=24, replace=False))
     _bwd_case(28672, 8192, 512, m, seed=seed, ks=(0, 31, 63), ms=ms, name="mlp70b")
+
+
+def test_bwd_wide_tiles_ragged_m():
+    # backward rows = K = 11008 (22 row tiles), 1400 columns: 512 x 128 tiles with a ragged last one
+    ms = np.unique(np.concatenate([synth.stream(7, "ms").choice(1400, size=24, replace=False), np.arange(1390, 1400)]))
+    _bwd_case(2048, 11008, 48, 1400, seed=3, ks=(0, 85), ms=ms, name="bwide")
 
 
 def test_bwd_is_deterministic():
