@@ -141,7 +141,10 @@ int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const uint16_t* sca
  *
  *   L    fp16 [K, r], device.     R    fp16 [r, N], device.
  *   K, N >= 1; r >= 16, r % 16 == 0.
- *   Lt   out, fp16 [r, K] = L^T.  Rt   out, fp16 [N, r] = R^T.
+ *   Lt   out, fp16 [r, K] = L^T, row-major.
+ *   Rt   out, fp16 R^T in 32 x 16 tiles: ceil(N/32) * 32 * r elements, element (n, j) of R^T at
+ *        ((n / 32) * (r / 16) + j / 16) * 512 + (n % 32) * 16 + j % 16; rows n >= N of the last
+ *        tile are zero. One tile is 1 KiB of contiguous memory, the unit the kernels load.
  * Asynchronous on `stream`; a pure data movement (bit-exact).
  */
 int slim_pack_adapter(const uint16_t* L, const uint16_t* R, int64_t K, int64_t N, int64_t r, uint16_t* Lt,

@@ -133,12 +133,13 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
   off = round256(off + tpart_bytes);
   q.off_ypart = off;
   off = round256(off + ypart_bytes);
-  // large M: fp16 copy of bf16 activations for the tile kernel's direct-to-LDS loads, and the
-  // adapter's second factor P [rows, r] in 32 x 16 tiles
+  // large M: fp16 copy of bf16 activations for the tile kernel's direct-to-LDS loads, and (backward:
+  // the forward's factor comes tiled from slim_pack_adapter) the adapter's second factor P
+  // [rows, r] re-laid in 32 x 16 tiles
   q.off_x16 = off;
   if (!q.decode) off = round256(off + (size_t)M * (size_t)red * 2);
   q.off_pb = off;
-  if (!q.decode) off = round256(off + (size_t)cdiv(rows, 32) * 32 * (size_t)r * 2);
+  if (!q.decode && bwd) off = round256(off + (size_t)cdiv(rows, 32) * 32 * (size_t)r * 2);
   q.total = off;
   *p = q;
   return SLIM_OK;

@@ -219,6 +219,20 @@ k_transpose16(const uint16_t* __restrict__ in, int64_t R, int64_t C, uint16_t* _
   }
 }
 
+// R [r, N] row-major -> R^T in 32 x 16 tiles: element (n, j) at ((n / 32) (r / 16) + j / 16) 512 +
+// (n % 32) 16 + j % 16, rows n >= N of the last tile zero. One thread per output element, in
+// output order (a one-time pack: the strided reads do not matter).
+__global__ void __launch_bounds__(256) k_tile_rt(const uint16_t* __restrict__ R, int64_t r, int64_t N,
+                                                 uint16_t* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (N + 31) / 32 * 32 * r;
+  if (i >= total) return;
+  const int64_t tile = i >> 9, within = i & 511;
+  const int64_t tn = tile / (r >> 4), tj = tile - tn * (r >> 4);
+  const int64_t n = 32 * tn + (within >> 4), j = 16 * tj + (within & 15);
+  out[i] = n < N ? R[j * N + n] : (uint16_t)0;
+}
+
 }  // namespace
 
 extern "C" int slim_pack_adapter(const uint16_t* L, const uint16_t* R, int64_t K, int64_t N, int64_t r, uint16_t* Lt,
@@ -235,8 +249,8 @@ extern "C" int slim_pack_adapter(const uint16_t* L, const uint16_t* R, int64_t K
   }
   {
     SlimKernelTimer timer("pack_adapter", s);
-    SLIM_LAUNCH(timer, k_transpose16, dim3((unsigned)((N + 63) / 64), (unsigned)((r + 63) / 64)), dim3(256), s, R, r, N,
-                Rt);
+    const int64_t total = (N + 31) / 32 * 32 * r;
+    SLIM_LAUNCH(timer, k_tile_rt, dim3((unsigned)((total + 255) / 256)), dim3(256), s, R, r, N, Rt);
   }
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }

@@ -50,8 +50,10 @@ struct LayerArgs {
   int64_t M, rows, red;
   int64_t r;
   const uint16_t* ad_q;    // adapter first factor, row-major [r, red]
-  const uint16_t* ad_p;    // adapter second factor, row-major [rows, r]
-  uint16_t* ad_pb;         // large M: the same in 32 x 16 tiles (workspace)
+  const uint16_t* ad_p;    // adapter second factor [rows, r]: 32 x 16 tiles (forward, from
+                           // slim_pack_adapter) or row-major (backward, L as given)
+  int p_tiled;             // ad_p is in 32 x 16 tiles
+  const uint16_t* ad_pb;   // large M: the factor in 32 x 16 tiles (ad_p, or a re-laid copy)
   uint16_t* tm;            // fp16 adapter intermediate: row-major [M, r] (small M), 32 x 16 tiles (large M)
   float* out;              // [M, rows]
   // small-M path
@@ -339,7 +341,10 @@ SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lr
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
     const int64_t jj = clamp_hi(jbase + 32 * t + 8 * g, a.r - 8);
-    aq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_p + lrow * a.r + jj);
+    // tiled: 8 consecutive ranks of a row stay within one 32 x 16 tile (jj % 16 is 0 or 8)
+    const int64_t po = a.p_tiled ? ((lrow >> 5) * (a.r >> 4) + (jj >> 4)) * 512 + (lrow & 31) * 16 + (jj & 15)
+                                 : lrow * a.r + jj;
+    aq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_p + po);
 #pragma unroll
     for (int f = 0; f < FM; ++f)
       bq[t][f] = *reinterpret_cast<const u32x4_t*>(a.tm + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.r + jj);
@@ -889,13 +894,18 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
   if (a.r > 0) {
     int st = slim_launch_adapter_gemm(a.act16, a.M, a.red, a.ad_q, a.r, p, ws, s);
     if (st != SLIM_OK) return st;
-    SlimKernelTimer timer("adapter_finish", s);
-    const int64_t np = (a.rows * a.r / 8 + 255) / 256;
+    // the factor needs re-laying only when given row-major (backward); tm needs summing only
+    // when the GEMM split its reduction
+    const int64_t np = a.p_tiled ? 0 : (a.rows * a.r / 8 + 255) / 256;
     const int64_t nt = p.ad_split > 1 ? ((a.M + 31) / 32 * 32 * a.r / 8 + 255) / 256 : 0;
-    SLIM_LAUNCH(timer, k_adapter_finish, dim3((unsigned)(np + nt)), dim3(256), s,
-                reinterpret_cast<const u32x4_t*>(a.ad_p), a.rows, a.r, reinterpret_cast<u32x4_t*>(a.ad_pb), np,
-                a.tpart, p.ad_split, a.M, reinterpret_cast<u32x4_t*>(a.tm));
-    if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
+    if (np + nt > 0) {
+      SlimKernelTimer timer("adapter_finish", s);
+      SLIM_LAUNCH(timer, k_adapter_finish, dim3((unsigned)(np + nt)), dim3(256), s,
+                  reinterpret_cast<const u32x4_t*>(a.ad_p), a.rows, a.r,
+                  reinterpret_cast<u32x4_t*>(const_cast<uint16_t*>(a.ad_pb)), np, a.tpart, p.ad_split, a.M,
+                  reinterpret_cast<u32x4_t*>(a.tm));
+      if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
+    }
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
   dim3 grid((unsigned)(8 * ((p.sp_row_tiles * p.sp_col_tiles + 7) / 8)));
@@ -906,7 +916,7 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
 
 LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int64_t M, int64_t rows, int64_t red,
                     const uint8_t* codes, const uint8_t* meta, const uint16_t* scales, const uint16_t* ad_q,
-                    const uint16_t* ad_p, int64_t r, float* out) {
+                    const uint16_t* ad_p, bool p_tiled, int64_t r, float* out) {
   LayerArgs a;
   a.codes = reinterpret_cast<const uint32_t*>(codes);
   a.meta = reinterpret_cast<const uint32_t*>(meta);
@@ -919,7 +929,8 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.r = r;
   a.ad_q = ad_q;
   a.ad_p = ad_p;
-  a.ad_pb = p.decode ? nullptr : reinterpret_cast<uint16_t*>(ws + p.off_pb);
+  a.p_tiled = p_tiled;
+  a.ad_pb = p.decode ? nullptr : (p_tiled ? ad_p : reinterpret_cast<const uint16_t*>(ws + p.off_pb));
   a.tm = reinterpret_cast<uint16_t*>(ws + p.off_t);
   a.act16 = (!p.decode && dtype == SLIM_BF16) ? reinterpret_cast<const uint16_t*>(ws + p.off_x16) : a.act;
   a.out = out;
@@ -951,7 +962,7 @@ extern "C" int slim_linear(const void* X, int xdtype, int64_t M, int64_t N, int6
   int st = slim_check_linear(false, X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, ws, ws_bytes, &p);
   if (st != SLIM_OK) return st;
   char* w = reinterpret_cast<char*>(ws);
-  const LayerArgs a = make_args(p, w, X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y);
+  const LayerArgs a = make_args(p, w, X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, true, r, Y);
   return launch_layer<false>(a, p, reinterpret_cast<const uint16_t*>(X), xdtype == SLIM_BF16, w, (hipStream_t)stream);
 }
 
@@ -963,6 +974,6 @@ extern "C" int slim_linear_bwd_dx(const void* dY, int dydtype, int64_t M, int64_
   int st = slim_check_linear(true, dY, dydtype, M, N, K, codesT, metaT, scalesT, L, R, r, dX, ws, ws_bytes, &p);
   if (st != SLIM_OK) return st;
   char* w = reinterpret_cast<char*>(ws);
-  const LayerArgs a = make_args(p, w, dY, dydtype, M, K, N, codesT, metaT, scalesT, R, L, r, dX);
+  const LayerArgs a = make_args(p, w, dY, dydtype, M, K, N, codesT, metaT, scalesT, R, L, false, r, dX);
   return launch_layer<true>(a, p, reinterpret_cast<const uint16_t*>(dY), dydtype == SLIM_BF16, w, (hipStream_t)stream);
 }

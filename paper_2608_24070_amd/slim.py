@@ -244,13 +244,15 @@ def pack_bwd(packed: dict, with_mask: bool = False, stream=None) -> dict:
 
 def pack_adapter(L, R, stream=None) -> dict:
     """slim_pack_adapter of fp16 L [K, r] and R [r, N]: returns {"Lt", "Rt", "L", "R"} (the forward
-    takes Lt, Rt; the backward takes L, R)."""
+    takes Lt, Rt; the backward takes L, R). Lt is L^T [r, K]; Rt is R^T in 32 x 16 tiles,
+    [ceil(N/32), r/16, 32, 16]."""
     torch = _torch()
     _on_gpu(L, R)
     K, r = L.shape
     N = R.shape[1]
     out = {"Lt": torch.empty((r, K), dtype=torch.float16, device=L.device),
-           "Rt": torch.empty((N, r), dtype=torch.float16, device=L.device), "L": L, "R": R}
+           "Rt": torch.empty(((N + 31) // 32, r // 16, 32, 16), dtype=torch.float16, device=L.device),
+           "L": L, "R": R}
     _check(slim_pack_adapter(_ptr(L), _ptr(R), K, N, r, _ptr(out["Lt"]), _ptr(out["Rt"]), _stream(stream)),
            "slim_pack_adapter")
     return out

@@ -117,7 +117,12 @@ def test_pack_adapter_is_exact_transpose(k, n, r):
     Lb, Rb, _, _ = synth.adapter(k, n, r, seed=5, name="tp/")
     ad = slim.pack_adapter(dev_bits(Lb, torch.float16), dev_bits(Rb, torch.float16))
     assert np.array_equal(host(ad["Lt"]).view(np.uint16), Lb.T)
-    assert np.array_equal(host(ad["Rt"]).view(np.uint16), Rb.T)
+    # Rt: R^T in 32 x 16 tiles [ceil(n/32), r/16, 32, 16], rows past n zero
+    rt = host(ad["Rt"]).view(np.uint16)
+    assert rt.shape == ((n + 31) // 32, r // 16, 32, 16)
+    rowmajor = rt.transpose(0, 2, 1, 3).reshape((n + 31) // 32 * 32, r)
+    assert np.array_equal(rowmajor[:n], Rb.T)
+    assert not rowmajor[n:].any()
 
 
 # ------------------------------------------------------------------------------ backward
