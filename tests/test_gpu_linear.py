@@ -37,6 +37,14 @@ def test_decode_shape(m):
     _fwd_case(4096, 4096, 384, m, name="decode")
 
 
+@pytest.mark.parametrize("n,k,m,r", [(16, 128, 1, 0), (16, 128, 5, 16), (80, 384, 32, 16), (80, 384, 7, 0),
+                                     (16, 256, 40, 16), (80, 640, 100, 32)])
+def test_smallest_shapes(n, k, m, r):
+    # one 16-row block, a ragged 64-row tile (80 rows), one to five 128-wide chunks (K = 640 leaves a
+    # lane group of the small-M kernel without a chunk), on both paths
+    _fwd_case(n, k, r, m, name="edge")
+
+
 @pytest.mark.parametrize("m", [17, 32, 33, 64])
 def test_small_m_multi_fragment(m):
     _fwd_case(1024, 2048, 64, m, name="smallm")
@@ -153,6 +161,11 @@ def _bwd_case(n, k, r, m, seed=0, ks=None, ms=None, name="bwd", dydtype="bf16"):
 @pytest.mark.parametrize("m,r", [(16, 32), (1, 0), (5, 32), (64, 32), (200, 32), (256, 0)])
 def test_bwd_small(m, r):
     _bwd_case(512, 512, r, m, name="bwd_small")
+
+
+@pytest.mark.parametrize("n,k,m,r", [(128, 128, 1, 0), (128, 128, 9, 16), (256, 384, 33, 16), (384, 640, 70, 32)])
+def test_bwd_smallest_shapes(n, k, m, r):
+    _bwd_case(n, k, r, m, name="bwd_edge")
 
 
 def test_bwd_decode_shape():
