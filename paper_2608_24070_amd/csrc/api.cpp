@@ -76,15 +76,19 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     q.dec_g = (q.dec_fm == 1 && q.sp_row_tiles * cdiv(nchunks, 8) >= 256) ? 2 : 1;
     q.sp_chunks_per_split = 4 * q.dec_g;
     q.sp_split = (int)cdiv(nchunks, q.sp_chunks_per_split);
-    // forward sparse blocks run several row tiles of one slice when there are more units than
-    // the target block count (the backward's activations depend on the row group: single units)
+    // sparse blocks run several row tiles of one slice when there are more units than the target
+    // block count (the backward's staged activations carry one 128-row group's scales: at most
+    // the two row tiles of a group, starting at an even tile)
     const int64_t units = q.sp_row_tiles * q.sp_split;
-    q.dec_units = bwd ? 1 : (int)std::min<int64_t>(SLIM_DECODE_MAX_UNITS, cdiv(units, SLIM_DECODE_BLOCKS));
+    q.dec_units = (int)std::min<int64_t>(bwd ? 2 : SLIM_DECODE_MAX_UNITS, cdiv(units, SLIM_DECODE_BLOCKS));
     q.sp_blocks = cdiv(q.sp_row_tiles, q.dec_units) * q.sp_split;
     if (r > 0) {
       q.ad_jblocks = cdiv(r, 64);
-      q.ad_slice = kDecodeAdSlice;
-      q.ad_split = (int)cdiv(red, kDecodeAdSlice);
+      // at most about 32 splits: a unit takes several 256-position slices of a long reduction
+      const int64_t slices = cdiv(red, kDecodeAdSlice);
+      q.ad_sub = (int)cdiv(slices, 32);
+      q.ad_slice = kDecodeAdSlice * q.ad_sub;
+      q.ad_split = (int)cdiv(slices, q.ad_sub);
       if (q.ad_split > 1) {
         ad_counters = (size_t)q.ad_jblocks;
         tpart_bytes = (size_t)q.ad_jblocks * q.ad_split * 4 * q.dec_fm * 256 * 4;

@@ -25,6 +25,7 @@ struct SlimPlan {
   // dense adapter GEMM (T = X L forward, U = dY R^T backward)
   int ad_tiles_m = 0, ad_tiles_j = 0, ad_split = 1;
   int64_t ad_slice = 0;               // reduction length per split
+  int ad_sub = 1;                     // small M: SLIM_DECODE_AD_SLICE slices per adapter unit
   int64_t ad_jblocks = 0;             // small-M path: 64-wide blocks of the adapter rank
   // sparse contraction
   bool decode = false;                // small-M kernel (16-column MFMA tiles, split reduction)

@@ -62,6 +62,7 @@ struct LayerArgs {
   int64_t units;           // small M: row tiles per sparse block
   int64_t col_tiles;       // 96- or 128-column tiles (large M)
   int ad_split;            // reduction splits of the adapter's first product
+  int ad_sub;              // small M: slices of SLIM_DECODE_AD_SLICE positions per adapter unit
   int64_t ad_jblocks;      // 64-wide column blocks of the adapter rank
   float* part;             // sparse split partials
   float* tpart;            // adapter split partials
@@ -102,16 +103,17 @@ SLIM_DEV bool split_reduce(f4_t* acc, float* part_tile, int S, int s, uint32_t* 
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
   const float* src = part_tile + (int64_t)wave * kPer;
-  for (int s0 = 0; s0 < S; s0 += 8) {
-    float pv[8][FM * 4];
+  constexpr int kR = 16 / FM;   // partials per load round
+  for (int s0 = 0; s0 < S; s0 += kR) {
+    float pv[kR][FM * 4];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 0; j < kR; ++j) {
       const int ss = s0 + j < S ? s0 + j : S - 1;
 #pragma unroll
       for (int e = 0; e < FM * 4; ++e) pv[j][e] = ld_dev(src + (int64_t)ss * 4 * kPer + e * 64 + lane);
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < kR; ++j)
       if (s0 + j < S)
 #pragma unroll
         for (int e = 0; e < FM * 4; ++e) acc[e >> 2][e & 3] += pv[j][e];
@@ -130,8 +132,8 @@ SLIM_DEV bool split_reduce(f4_t* acc, float* part_tile, int S, int s, uint32_t* 
 // slice's activations in LDS once and loads each unit's packed words while the unit before is
 // computed. Results stay in registers until every load has been issued and are stored at the end:
 // a store between the loads would make the compiler's wait for one unit's words also wait for
-// the next unit's. The backward runs single units: its activations carry the scales of the
-// unit's 128-row group.
+// the next unit's. In the backward the staged activations carry the scales of a 128-row group,
+// so a block runs at most the two row tiles of one group (rt0 even).
 template <int G>
 struct DecodeWords {
   u32x4_t cw[2 * G], mw[G];
@@ -161,7 +163,7 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
   constexpr int LDX = SL + 8;
   constexpr int VPR = SL / 8;              // 16-byte activation vectors per row of the slice
   constexpr int XV = MC * VPR / 256;       // ... per thread
-  static_assert(!BWD || NU == 1, "backward units are single: activations carry the group's scales");
+  static_assert(!BWD || NU <= 2, "backward blocks stay within one 128-row group: activations carry its scales");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int S = a.split;
   const int64_t nchunks = a.red / 128;
@@ -255,8 +257,10 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
 }
 
 // ============================================================ small-M: adapter first-product units
-// tm[m, j] = sum_red act[m, red] Q[j, red]. Unit = 64 adapter columns (16 per wave) x one slice
-// of 256 reduction positions; both operands are read straight from global memory.
+// tm[m, j] = sum_red act[m, red] Q[j, red]. Unit = 64 adapter columns (16 per wave) x ad_sub
+// slices of 256 reduction positions (more than one when the reduction is long, so that the
+// last unit to finish sums at most about 32 partials); both operands are read straight from
+// global memory.
 constexpr int kAdSlice = SLIM_DECODE_AD_SLICE;
 
 template <int FM>
@@ -266,32 +270,36 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, int* last_flag)
   const int SA = a.ad_split;
   const int64_t jb = v / SA;
   const int sa = (int)(v - jb * SA);
-  const int64_t r0 = (int64_t)sa * kAdSlice;
+  const int64_t r0 = (int64_t)sa * a.ad_sub * kAdSlice;
   const bool bf16 = a.act_bf16 != 0;
   const int g = lane >> 4;
   const int64_t jcol = jb * 64 + 16 * wave + (lane & 15);
   const int64_t jl = clamp_hi(jcol, a.r - 1);
 
-  u32x4_t aq[kSteps][FM], bq[kSteps];
-#pragma unroll
-  for (int t = 0; t < kSteps; ++t) {
-    const int64_t rk = clamp_hi(r0 + 32 * t + 8 * g, a.red - 8);
-#pragma unroll
-    for (int f = 0; f < FM; ++f)
-      aq[t][f] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.red + rk);
-    bq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_q + jl * a.red + rk);
-  }
   f4_t acc[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+  // a.ad_sub consecutive slices of kAdSlice positions (one load round each)
+  for (int sub = 0; sub < a.ad_sub; ++sub) {
+    const int64_t rs = r0 + (int64_t)sub * kAdSlice;
+    u32x4_t aq[kSteps][FM], bq[kSteps];
 #pragma unroll
-  for (int t = 0; t < kSteps; ++t) {
-    const bool kok = r0 + 32 * t + 8 * g < a.red;
-    const h8_t bv = (kok && jcol < a.r) ? __builtin_bit_cast(h8_t, bq[t]) : zero_h8();
+    for (int t = 0; t < kSteps; ++t) {
+      const int64_t rk = clamp_hi(rs + 32 * t + 8 * g, a.red - 8);
 #pragma unroll
-    for (int f = 0; f < FM; ++f) {
-      const h8_t av = (16 * f + (lane & 15) < a.M) ? load8_as_h(aq[t][f], bf16) : zero_h8();
-      acc[f] = mfma16(av, bv, acc[f]);
+      for (int f = 0; f < FM; ++f)
+        aq[t][f] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.red + rk);
+      bq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_q + jl * a.red + rk);
+    }
+#pragma unroll
+    for (int t = 0; t < kSteps; ++t) {
+      const bool kok = rs + 32 * t + 8 * g < a.red;
+      const h8_t bv = (kok && jcol < a.r) ? __builtin_bit_cast(h8_t, bq[t]) : zero_h8();
+#pragma unroll
+      for (int f = 0; f < FM; ++f) {
+        const h8_t av = (16 * f + (lane & 15) < a.M) ? load8_as_h(aq[t][f], bf16) : zero_h8();
+        acc[f] = mfma16(av, bv, acc[f]);
+      }
     }
   }
   if (SA > 1 && !split_reduce<FM>(acc, a.tpart + jb * (int64_t)SA * 4 * FM * 256, SA, sa, &a.tcounters[jb], last_flag))
@@ -856,7 +864,7 @@ void launch_decode(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
 
 template <bool BWD, int FM, int G>
 void launch_decode_units(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
-  if (!BWD && p.dec_units > 1) launch_decode<BWD, FM, G, BWD ? 1 : kDecodeMaxUnits>(a, p, s);
+  if (p.dec_units > 1) launch_decode<BWD, FM, G, BWD ? 2 : kDecodeMaxUnits>(a, p, s);
   else launch_decode<BWD, FM, G, 1>(a, p, s);
 }
 
@@ -939,6 +947,7 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.units = p.dec_units;
   a.col_tiles = p.sp_col_tiles;
   a.ad_split = p.ad_split;
+  a.ad_sub = p.ad_sub;
   a.ad_jblocks = p.ad_jblocks;
   a.part = reinterpret_cast<float*>(ws + p.off_ypart);
   a.tpart = reinterpret_cast<float*>(ws + p.off_tpart);

@@ -45,6 +45,12 @@ def test_smallest_shapes(n, k, m, r):
     _fwd_case(n, k, r, m, name="edge")
 
 
+@pytest.mark.parametrize("m", [1, 20])
+def test_decode_long_reduction(m):
+    # K = 13824: 54 adapter slices of 256, so each adapter unit takes two (27 splits)
+    _fwd_case(512, 13824, 32, m, name="longk")
+
+
 @pytest.mark.parametrize("m", [17, 32, 33, 64])
 def test_small_m_multi_fragment(m):
     _fwd_case(1024, 2048, 64, m, name="smallm")
