@@ -84,9 +84,10 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     q.sp_blocks = cdiv(q.sp_row_tiles, q.dec_units) * q.sp_split;
     if (r > 0) {
       q.ad_jblocks = cdiv(r, 64);
-      // at most about 32 splits: a unit takes several 256-position slices of a long reduction
+      // at most about SLIM_DECODE_AD_SPLITS splits: a unit takes several 256-position slices of a
+      // long reduction
       const int64_t slices = cdiv(red, kDecodeAdSlice);
-      q.ad_sub = (int)cdiv(slices, 32);
+      q.ad_sub = (int)cdiv(slices, SLIM_DECODE_AD_SPLITS);
       q.ad_slice = kDecodeAdSlice * q.ad_sub;
       q.ad_split = (int)cdiv(slices, q.ad_sub);
       if (q.ad_split > 1) {

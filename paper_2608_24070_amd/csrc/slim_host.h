@@ -8,8 +8,10 @@
 
 // Completion counters live in a fixed-size region at the start of the workspace.
 #define SLIM_COUNTER_SLOTS 4096
-// Reduction positions per adapter first-product unit of the small-M path.
+// Reduction positions per load round of an adapter first-product unit of the small-M path, and
+// the most reduction splits of that product (longer reductions give a unit several rounds).
 #define SLIM_DECODE_AD_SLICE 256
+#define SLIM_DECODE_AD_SPLITS 32
 // Small-M forward: most row tiles one sparse block runs, and the block count it aims for.
 #define SLIM_DECODE_MAX_UNITS 8
 #define SLIM_DECODE_BLOCKS 512
