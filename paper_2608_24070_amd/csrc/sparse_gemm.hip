@@ -891,8 +891,9 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
     }
     return SLIM_OK;
   }
-  if (act_bf16) {
-    // the tile kernel streams fp16 activations straight into LDS: convert them once
+  if (act_bf16 && a.r == 0) {
+    // the tile kernel streams fp16 activations straight into LDS: convert them once (with an
+    // adapter, its first product's GEMM reads the bf16 activations and writes the copy)
     SlimKernelTimer timer("to_f16", s);
     const int64_t n8 = a.M * a.red / 8;
     SLIM_LAUNCH(timer, k_bf16_to_f16, dim3((unsigned)((n8 + 255) / 256)), dim3(256), s,
@@ -900,7 +901,8 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
     if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
   }
   if (a.r > 0) {
-    int st = slim_launch_adapter_gemm(a.act16, a.M, a.red, a.ad_q, a.r, p, ws, s);
+    int st = slim_launch_adapter_gemm(act_bf16 ? act : a.act16, act_bf16, a.M, a.red, a.ad_q, a.r, p, ws,
+                                      const_cast<uint16_t*>(a.act16), s);
     if (st != SLIM_OK) return st;
     // the factor needs re-laying only when given row-major (backward); tm needs summing only
     // when the GEMM split its reduction
