@@ -134,8 +134,8 @@ def main():
         copy_probe(args.copy_probe)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported in this build "
-              "(the layer shards along N across GPUs by design, but no multi-GPU path is built).",
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the layer would shard along N across GPUs; no multi-GPU path is implemented).",
               file=sys.stderr)
         sys.exit(2)
 

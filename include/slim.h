@@ -73,7 +73,7 @@ typedef enum {
   SLIM_ERANGE = 6,        /* a group scale max|w|/7 overflows fp16 */
   SLIM_EWORKSPACE = 7,    /* workspace missing or smaller than the query returned */
   SLIM_EDEVICE = 8,       /* a HIP runtime call or a kernel launch failed */
-  SLIM_EUNSUPPORTED = 9   /* valid but not supported by this build (e.g. no gfx950 device) */
+  SLIM_EUNSUPPORTED = 9   /* valid but not supported by this library (e.g. no gfx950 device) */
 } slim_status;
 
 typedef enum { SLIM_F16 = 0, SLIM_BF16 = 1 } slim_dtype;

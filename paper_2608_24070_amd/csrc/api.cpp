@@ -24,7 +24,7 @@ extern "C" const char* slim_status_string(int status) {
     case SLIM_ERANGE: return "SLIM_ERANGE: group scale overflows fp16";
     case SLIM_EWORKSPACE: return "SLIM_EWORKSPACE: workspace missing or too small";
     case SLIM_EDEVICE: return "SLIM_EDEVICE: HIP runtime or launch failure";
-    case SLIM_EUNSUPPORTED: return "SLIM_EUNSUPPORTED: not supported by this build";
+    case SLIM_EUNSUPPORTED: return "SLIM_EUNSUPPORTED: valid but not supported by this library";
     default: return "unknown slim status";
   }
 }
