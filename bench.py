@@ -106,7 +106,7 @@ def layer_bytes(M, N, K, r):
     return N * K * PACK_BYTES_PER_WEIGHT + 2 * r * (K + N) + 2 * M * K + 4 * M * N
 
 
-def kernel_bytes(kernel, M, N, K, r, bwd):
+def kernel_bytes(kernel, M, N, K, r, bwd, act_bf16=True):
     """Algorithmic HBM bytes of one launch of a library kernel on one layer: the operands it must
     read and the results it must produce, once each (split partials and re-reads not counted).
     Forward: rows = N, reduction = K; backward: rows = K, reduction = N."""
@@ -118,8 +118,8 @@ def kernel_bytes(kernel, M, N, K, r, bwd):
         return 2 * r * rows + 2 * M * r + 4 * M * rows
     if kernel.startswith("tile"):        # packed weight + activations + second factor + T -> Y
         return weight + 2 * M * red + 2 * r * rows + 2 * M * r + 4 * M * rows
-    if kernel.startswith("adapter_gemm"):
-        return 2 * M * red + 2 * r * red + 2 * M * r
+    if kernel.startswith("adapter_gemm"):  # activations + first factor -> T (+ the fp16 copy of bf16 X)
+        return 2 * M * red + 2 * r * red + 2 * M * r + (2 * M * red if act_bf16 else 0)
     return 0
 
 
