@@ -83,16 +83,16 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     q.dec_units = (int)std::min<int64_t>(bwd ? 2 : SLIM_DECODE_MAX_UNITS, cdiv(units, SLIM_DECODE_BLOCKS));
     q.sp_blocks = cdiv(q.sp_row_tiles, q.dec_units) * q.sp_split;
     if (r > 0) {
-      q.ad_jblocks = cdiv(r, 64);
-      // at most about SLIM_DECODE_AD_SPLITS splits: a unit takes several 256-position slices of a
-      // long reduction
-      const int64_t slices = cdiv(red, kDecodeAdSlice);
+      // adapter units: 16 ranks x 4 waves x ad_sub slices of SLIM_DECODE_AD_SLICE positions, at
+      // most about SLIM_DECODE_AD_SPLITS splits (a wave takes several slices of a long reduction)
+      q.ad_jblocks = cdiv(r, 16);
+      const int64_t slices = cdiv(red, 4 * kDecodeAdSlice);
       q.ad_sub = (int)cdiv(slices, SLIM_DECODE_AD_SPLITS);
-      q.ad_slice = kDecodeAdSlice * q.ad_sub;
+      q.ad_slice = 4 * kDecodeAdSlice * q.ad_sub;
       q.ad_split = (int)cdiv(slices, q.ad_sub);
       if (q.ad_split > 1) {
         ad_counters = (size_t)q.ad_jblocks;
-        tpart_bytes = (size_t)q.ad_jblocks * q.ad_split * 4 * q.dec_fm * 256 * 4;
+        tpart_bytes = (size_t)q.ad_jblocks * q.ad_split * q.dec_fm * 256 * 4;
       }
     }
     if (q.sp_split > 1 || r > 0) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 4 * q.dec_fm * 256 * 4;

@@ -158,14 +158,18 @@ SLIM_DEV f16_t smfmac32(h8_t a, h16_t b, f16_t c, int idx, int abid) {
 }
 
 // ----------------------------------------------------------------------------------------------
-// Cross-block hand-off of partial tiles. The partials are stored and loaded with device-scope
-// relaxed atomic accesses (sc1), which are coherent across the XCDs' separate L2s by themselves,
-// so no L2-wide write-back or invalidate (what a device-scope fence costs) is needed. Before a
-// block bumps the tile counter, s_waitcnt(0) makes sure its partial stores have completed.
+// Cross-block hand-off of partial tiles. The partials are stored and loaded 16 bytes per lane with
+// the sc1 cache policy, the one the compiler gives device-scope relaxed atomic loads and stores
+// (coherent across the XCDs' separate L2s by themselves), so no L2-wide write-back or invalidate
+// (what a device-scope fence costs) is needed. Before a block bumps the tile counter,
+// s_waitcnt(0) makes sure its partial stores have completed.
 // ----------------------------------------------------------------------------------------------
-SLIM_DEV void st_dev(float* p, float v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-SLIM_DEV float ld_dev(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+constexpr int kCpolSc1 = 16;   // buffer instruction cache-policy operand: sc1
+SLIM_DEV void st_dev4(rsrc_t r, uint32_t off, f4_t v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, off, 0, kCpolSc1);
+}
+SLIM_DEV f4_t ld_dev4(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolSc1));
 }
 SLIM_DEV void drain_stores() { __builtin_amdgcn_s_waitcnt(0); }
 SLIM_DEV uint32_t counter_arrive(uint32_t* c) {

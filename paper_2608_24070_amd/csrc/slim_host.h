@@ -8,10 +8,11 @@
 
 // Completion counters live in a fixed-size region at the start of the workspace.
 #define SLIM_COUNTER_SLOTS 4096
-// Reduction positions per load round of an adapter first-product unit of the small-M path, and
-// the most reduction splits of that product (longer reductions give a unit several rounds).
+// Reduction positions per load round of a wave of an adapter first-product unit of the small-M
+// path, and the most reduction splits of that product (longer reductions give a wave several
+// rounds).
 #define SLIM_DECODE_AD_SLICE 256
-#define SLIM_DECODE_AD_SPLITS 32
+#define SLIM_DECODE_AD_SPLITS 8
 // Small-M forward: most row tiles one sparse block runs, and the block count it aims for.
 #define SLIM_DECODE_MAX_UNITS 8
 #define SLIM_DECODE_BLOCKS 512
@@ -27,8 +28,8 @@ struct SlimPlan {
   // dense adapter GEMM (T = X L forward, U = dY R^T backward)
   int ad_tiles_m = 0, ad_tiles_j = 0, ad_split = 1;
   int64_t ad_slice = 0;               // reduction length per split
-  int ad_sub = 1;                     // small M: SLIM_DECODE_AD_SLICE slices per adapter unit
-  int64_t ad_jblocks = 0;             // small-M path: 64-wide blocks of the adapter rank
+  int ad_sub = 1;                      // small M: SLIM_DECODE_AD_SLICE slices per adapter wave
+  int64_t ad_jblocks = 0;             // small-M path: 16-wide blocks of the adapter rank
   // sparse contraction
   bool decode = false;                // small-M kernel (16-column MFMA tiles, split reduction)
   int dec_fm = 1;                     // 16-column fragments per wave in the small-M kernel

@@ -62,8 +62,8 @@ struct LayerArgs {
   int64_t units;           // small M: row tiles per sparse block
   int64_t col_tiles;       // 96- or 128-column tiles (large M)
   int ad_split;            // reduction splits of the adapter's first product
-  int ad_sub;              // small M: slices of SLIM_DECODE_AD_SLICE positions per adapter unit
-  int64_t ad_jblocks;      // 64-wide column blocks of the adapter rank
+  int ad_sub;              // small M: slices of SLIM_DECODE_AD_SLICE positions per adapter wave
+  int64_t ad_jblocks;      // 16-wide column blocks of the adapter rank (small M)
   float* part;             // sparse split partials
   float* tpart;            // adapter split partials
   uint32_t* tcounters;     // per adapter column block
@@ -84,41 +84,39 @@ SLIM_DEV h8_t act8_scaled(u32x4_t v, u32x4_t sv, bool bf16) {
   return h;
 }
 
-// Reduce split partials of one tile: every block stores its FM x 4 accumulator values per lane
-// (device scope), the last one to arrive sums all S partials in split order.
+// Reduce the split partials of one adapter column block, run by wave 0 of each unit (the unit's
+// sum is in its registers): every unit stores its FM x 4 accumulator values per lane (device
+// scope, one 16-byte store per fragment), the last one to arrive sums all S partials in split
+// order. A partial is [FM][64 lanes][4] fp32.
 template <int FM>
-SLIM_DEV bool split_reduce(f4_t* acc, float* part_tile, int S, int s, uint32_t* counter, int* last_flag) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  constexpr int kPer = FM * 256;                    // floats per wave per split
-  float* dst = part_tile + ((int64_t)s * 4 + wave) * kPer;
+SLIM_DEV bool split_reduce_wave(f4_t* acc, float* part, int S, int s, uint32_t* counter) {
+  const int lane = threadIdx.x & 63;
+  const rsrc_t pr = make_rsrc(part, (int64_t)S * FM * 1024);
+  auto off = [&](int ss, int f) { return (uint32_t)(((ss * FM + f) * 256 + 4 * lane) * 4); };
 #pragma unroll
-  for (int f = 0; f < FM; ++f)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) st_dev(dst + (f * 4 + v) * 64 + lane, acc[f][v]);
+  for (int f = 0; f < FM; ++f) st_dev4(pr, off(s, f), acc[f]);
   drain_stores();
-  __syncthreads();
-  if (tid == 0) *last_flag = counter_arrive(counter) == (uint32_t)(S - 1);
-  __syncthreads();
-  if (!*last_flag) return false;
+  uint32_t prev = 0;
+  if (lane == 0) prev = counter_arrive(counter);
+  if (__shfl(prev, 0) != (uint32_t)(S - 1)) return false;
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-  const float* src = part_tile + (int64_t)wave * kPer;
   constexpr int kR = 16 / FM;   // partials per load round
   for (int s0 = 0; s0 < S; s0 += kR) {
-    float pv[kR][FM * 4];
+    f4_t pv[kR][FM];
 #pragma unroll
     for (int j = 0; j < kR; ++j) {
       const int ss = s0 + j < S ? s0 + j : S - 1;
 #pragma unroll
-      for (int e = 0; e < FM * 4; ++e) pv[j][e] = ld_dev(src + (int64_t)ss * 4 * kPer + e * 64 + lane);
+      for (int f = 0; f < FM; ++f) pv[j][f] = ld_dev4(pr, off(ss, f));
     }
 #pragma unroll
     for (int j = 0; j < kR; ++j)
       if (s0 + j < S)
 #pragma unroll
-        for (int e = 0; e < FM * 4; ++e) acc[e >> 2][e & 3] += pv[j][e];
+        for (int f = 0; f < FM; ++f) acc[f] = acc[f] + pv[j][f];
   }
-  if (tid == 0) counter_reset(counter);
+  if (lane == 0) counter_reset(counter);
   return true;
 }
 
@@ -257,23 +255,25 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
 }
 
 // ============================================================ small-M: adapter first-product units
-// tm[m, j] = sum_red act[m, red] Q[j, red]. Unit = 64 adapter columns (16 per wave) x ad_sub
-// slices of 256 reduction positions (more than one when the reduction is long, so that the
-// last unit to finish sums at most about 32 partials); both operands are read straight from
-// global memory.
+// tm[m, j] = sum_red act[m, red] Q[j, red]. Unit = 16 adapter columns x 4 parts of ad_sub slices
+// of 256 reduction positions: wave w takes part w (more than one slice when the reduction is long,
+// so that there are at most about 8 splits), reading both operands straight from global memory.
+// The four parts are added in LDS in part order, and the last unit of a column block to finish
+// sums the units' partials in split order. The partial a unit hands over is one 16 x 16
+// fragment per 16 activation rows (1 KB), which keeps the last unit's loads few.
 constexpr int kAdSlice = SLIM_DECODE_AD_SLICE;
 
 template <int FM>
-SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, int* last_flag) {
+SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) {
   constexpr int kSteps = kAdSlice / 32;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int SA = a.ad_split;
-  const int64_t jb = v / SA;
+  const int64_t jb = v / SA;                    // 16-column block
   const int sa = (int)(v - jb * SA);
-  const int64_t r0 = (int64_t)sa * a.ad_sub * kAdSlice;
+  const int64_t r0 = ((int64_t)sa * 4 + wave) * a.ad_sub * kAdSlice;
   const bool bf16 = a.act_bf16 != 0;
   const int g = lane >> 4;
-  const int64_t jcol = jb * 64 + 16 * wave + (lane & 15);
+  const int64_t jcol = jb * 16 + (lane & 15);
   const int64_t jl = clamp_hi(jcol, a.r - 1);
 
   f4_t acc[FM];
@@ -302,8 +302,17 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, int* last_flag)
       }
     }
   }
-  if (SA > 1 && !split_reduce<FM>(acc, a.tpart + jb * (int64_t)SA * 4 * FM * 256, SA, sa, &a.tcounters[jb], last_flag))
-    return;
+  // the unit's sum: waves 1..3 hand theirs to wave 0 through LDS
+  if (wave > 0)
+#pragma unroll
+    for (int f = 0; f < FM; ++f) red_lds[((wave - 1) * FM + f) * 64 + lane] = acc[f];
+  __syncthreads();
+  if (wave > 0) return;
+#pragma unroll
+  for (int w = 0; w < 3; ++w)
+#pragma unroll
+    for (int f = 0; f < FM; ++f) acc[f] = acc[f] + red_lds[(w * FM + f) * 64 + lane];
+  if (SA > 1 && !split_reduce_wave<FM>(acc, a.tpart + jb * (int64_t)SA * FM * 256, SA, sa, &a.tcounters[jb])) return;
   // D[m][j] fragment: lane (j + 16 * (m / 4)), element m % 4
 #pragma unroll
   for (int f = 0; f < FM; ++f)
@@ -320,11 +329,11 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, int* last_flag)
 template <bool BWD, int FM, int G, int NU>
 __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
   __shared__ __attribute__((aligned(16))) _Float16 xs[16 * FM * (512 * G + 8)];
-  __shared__ int last_flag;
+  static_assert(sizeof(xs) >= 3 * FM * 64 * sizeof(f4_t), "adapter units sum their waves in xs");
   const int64_t nA = a.r > 0 ? a.ad_jblocks * a.ad_split : 0;
   const int64_t b = blockIdx.x;
   if (b < nA) {
-    decode_adapter_unit<FM>(a, b, &last_flag);
+    decode_adapter_unit<FM>(a, b, reinterpret_cast<f4_t*>(xs));
     return;
   }
   const int64_t i = b - nA, S = a.split;
