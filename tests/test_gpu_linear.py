@@ -47,8 +47,16 @@ def test_smallest_shapes(n, k, m, r):
 
 @pytest.mark.parametrize("m", [1, 20])
 def test_decode_long_reduction(m):
-    # K = 13824: 54 adapter slices of 256, so each adapter unit takes two (27 splits)
+    # K = 13824: 14 adapter units' worth of 1024 positions, so each wave of a unit takes two 256-position
+    # slices (7 splits); the last unit's fourth wave lies wholly past K
     _fwd_case(512, 13824, 32, m, name="longk")
+
+
+@pytest.mark.parametrize("k,r,m", [(4096, 16, 16), (4096, 48, 1), (3200, 80, 16), (1152, 112, 3), (384, 16, 32)])
+def test_decode_adapter_ranks(k, r, m):
+    # adapter units are 16 ranks wide: one to seven column blocks, one to four splits, ragged last
+    # splits (K = 3200 and 1152 end inside a unit) and a single split (K = 384)
+    _fwd_case(320, k, r, m, name="adranks")
 
 
 @pytest.mark.parametrize("m", [17, 32, 33, 64])
@@ -176,6 +184,13 @@ def test_bwd_smallest_shapes(n, k, m, r):
 
 def test_bwd_decode_shape():
     _bwd_case(4096, 4096, 384, 16, name="bwd_decode")
+
+
+@pytest.mark.parametrize("n,r,m", [(9216, 48, 16), (3328, 16, 1)])
+def test_bwd_decode_adapter_ranks(n, r, m):
+    # backward reduction over N: 9216 positions give 9 units' worth, so each wave takes two slices
+    # (5 splits, the last ragged); N = 3328 ends inside the fourth unit
+    _bwd_case(n, 256, r, m, name="bwd_adranks")
 
 
 @pytest.mark.parametrize("m,seed", [(1, 0), (16, 1), (512, 2), (8192, 0)])
