@@ -9,8 +9,10 @@
 // 128 x 128 output tiles; wave (wm, wr) of the block's four owns rows 64 wm .. + 63 and ranks
 // 64 wr .. + 63 as 2 x 2 fragments of 32x32x16 fp16 MFMA. Both operands are contiguous along the
 // reduction, so both stream the same way: per 64-wide reduction chunk, 128 rows x 128 B of each go
-// straight from memory to LDS (direct loads, 16 B per lane) into a ring of three stages, two
-// chunks ahead; LDS rows are 128 B with the 16-byte column index XOR-swizzled by the row, so that
+// straight from memory to LDS (direct loads, 16 B per lane) into a ring of two stages, one chunk
+// ahead (64 KB, so that two blocks share a CU and one's MFMAs overlap the other's loads, barriers
+// and conversions: a block runs one wave per SIMD and its issue work, not memory, sets its pace);
+// LDS rows are 128 B with the 16-byte column index XOR-swizzled by the row, so that
 // fragment reads (32 rows at one column) hit distinct banks. Rows past M or r read as zero (the
 // loads go through buffer resources whose extent ends with the matrix).
 // The reduction may be split across blocks: each split then stores its fp32 partial in the same
@@ -37,10 +39,10 @@ __global__ void __launch_bounds__(256)
 k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint16_t* __restrict__ Q, int64_t r,
                int64_t slice, int split, uint16_t* __restrict__ out, float* __restrict__ part,
                uint16_t* __restrict__ a16) {
-  __shared__ __attribute__((aligned(16))) _Float16 as0[kT][kBK], as1[kT][kBK], as2[kT][kBK];
-  __shared__ __attribute__((aligned(16))) _Float16 bs0[kT][kBK], bs1[kT][kBK], bs2[kT][kBK];
-  auto as_at = [&](int stg) -> _Float16(*)[kBK] { return stg == 0 ? as0 : (stg == 1 ? as1 : as2); };
-  auto bs_at = [&](int stg) -> _Float16(*)[kBK] { return stg == 0 ? bs0 : (stg == 1 ? bs1 : bs2); };
+  __shared__ __attribute__((aligned(16))) _Float16 as0[kT][kBK], as1[kT][kBK];
+  __shared__ __attribute__((aligned(16))) _Float16 bs0[kT][kBK], bs1[kT][kBK];
+  auto as_at = [&](int stg) -> _Float16(*)[kBK] { return stg == 0 ? as0 : as1; };
+  auto bs_at = [&](int stg) -> _Float16(*)[kBK] { return stg == 0 ? bs0 : bs1; };
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wr = wave >> 1, ha = lane >> 5;
@@ -103,11 +105,11 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint
   // MFMAs run
   auto chunk = [&](int t, auto zc) {
     constexpr int z = decltype(zc)::value;
-    // chunk t has landed once only chunk t + 1's loads are outstanding; with this wave's LDS
-    // reads returned, after the barrier no wave reads the stage refilled below
-    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(kLoads));
+    // chunk t has landed once nothing is outstanding (the previous chunk's copy stores included);
+    // with this wave's LDS reads returned, after the barrier no wave reads the stage refilled below
+    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(0));
     asm volatile("s_barrier" ::: "memory");
-    dma(t + 2, (z + 2) % 3);
+    dma(t + 1, (z + 1) % 2);
     h8_t af[2][2], bf[2][2];
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
@@ -128,21 +130,16 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint
 #pragma unroll
         for (int y = 0; y < 2; ++y) acc[x][y] = mfma32(af[st & 1][x], bf[st & 1][y], acc[x][y]);
     }
-    // the stage stays untouched until the next chunk's barrier; the stores count as vector
-    // memory operations, so the wait at the next chunk's top (only the loads issued after that
-    // chunk's: the next chunk's) still covers that chunk's loads
+    // the stage stays untouched until the next chunk's barrier
     if (ABF16) copy_chunk(t, as_at(z));
   };
   dma(0, 0);
-  dma(1, 1);
   int t0 = 0;
-  for (; t0 + 3 <= nst; t0 += 3) {
+  for (; t0 + 2 <= nst; t0 += 2) {
     chunk(t0, std::integral_constant<int, 0>{});
     chunk(t0 + 1, std::integral_constant<int, 1>{});
-    chunk(t0 + 2, std::integral_constant<int, 2>{});
   }
   if (t0 < nst) chunk(t0, std::integral_constant<int, 0>{});
-  if (t0 + 1 < nst) chunk(t0 + 1, std::integral_constant<int, 1>{});
   // the ring's last loads (repeats of the final chunk) must land before the block's LDS is released
   __builtin_amdgcn_s_waitcnt(0);
 

@@ -114,8 +114,8 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
       q.ad_tiles_m = (int)cdiv(M, 128);
       q.ad_tiles_j = (int)cdiv(r, 128);
       const int64_t tiles = (int64_t)q.ad_tiles_m * q.ad_tiles_j;
-      // one block per CU (the GEMM's LDS ring takes 96 KB): at most 256 blocks, so one round
-      const int64_t split = std::max<int64_t>(1, std::min<int64_t>(256 / tiles, red / 512));
+      // two blocks per CU (the GEMM's LDS ring takes 64 KB): at most 512 blocks, so one round
+      const int64_t split = std::max<int64_t>(1, std::min<int64_t>(512 / tiles, red / 512));
       const int64_t slice = cdiv(cdiv(red, split), 64) * 64;
       q.ad_split = (int)cdiv(red, slice);
       q.ad_slice = slice;
