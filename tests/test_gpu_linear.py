@@ -85,6 +85,24 @@ def test_decode_blocks_run_several_row_tiles(m):
     _fwd_case(n, 4096, 64, m, rows=rows, name="units")
 
 
+@pytest.mark.parametrize("m", [1, 16, 27])
+def test_decode_long_blocks_repeat(m):
+    # K = 8192: 5 (m <= 16) or 8 (m > 16) row tiles per forward sparse block with 8 or 16 splits; a
+    # second call on the same workspace gives the same bits and leaves the counters at zero
+    n, k = 20032, 8192
+    rows = np.unique(np.concatenate([synth.stream(6, "rows").choice(n, size=320, replace=False),
+                                     np.arange(n - 160, n)]))
+    _fwd_case(n, k, 64, m, rows=rows, name="shared")
+    W, X, L, R, dx, ad = layer_inputs(n, k, 64, m, name="shared")
+    p = slim.pack(dev(W))
+    ws = torch.zeros(slim.slim_linear_workspace(m, n, k, 64), dtype=torch.uint8, device=dx.device)
+    y0 = slim.linear(dx, p, ad, ws=ws).clone()
+    y1 = slim.linear(dx, p, ad, ws=ws).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1)
+    assert int(ws[:COUNTER_BYTES].count_nonzero()) == 0
+
+
 def test_tile_kernel_wide_tiles_ragged_m():
     # 22 row tiles x 1400 columns: the plan takes 512 x 128 tiles (11 column tiles, the last 120
     # wide); the sampled columns include the last ones
