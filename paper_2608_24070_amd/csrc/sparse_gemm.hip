@@ -343,17 +343,17 @@ __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
 }
 
 // ============================================================ small-M: finish
-// out[m, row] = sum_s part_s[m, row] + sum_j tm[m, j] P[row, j]. One wave per 16 output rows; the
-// split partials are summed in split order (deterministic) and the adapter's second product is
-// accumulated on top with 16x16x32 fp16 MFMA. The partials share the MFMA output layout, so each
+// out[m, row] = sum_s part_s[m, row] + sum_j tm[m, j] P[row, j]. One or two waves (NW) per 16 output
+// rows; the split partials are summed in split order (deterministic) and the adapter's second
+// product is accumulated on top with 16x16x32 fp16 MFMA; with two waves each takes alternate
+// passes of the rank, and wave 0 adds wave 1's sum last. The partials share the MFMA output layout, so each
 // lane reads its own four values per split and fragment (lanes of columns past M read nothing).
 // The loads of the first adapter pass and of the first eight partials do not depend on each other
 // and are all issued before any is used: one memory round trip for the common case (at most
-// eight splits, rank at most 32 kSteps).
-template <int FM>
+// eight splits, a rank within the waves' first passes).
+template <int FM, int kSteps>
 SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lrow, int lane, u32x4_t* aq,
                                    u32x4_t (*bq)[FM]) {
-  constexpr int kSteps = FM == 1 ? 16 : 8;
   const int g = lane >> 4;
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
@@ -368,10 +368,9 @@ SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lr
   }
 }
 
-template <int FM>
+template <int FM, int kSteps>
 SLIM_DEV void finish_adapter_mfma(const LayerArgs& a, int64_t jbase, int lane, const u32x4_t* aq,
                                   const u32x4_t (*bq)[FM], f4_t* acc) {
-  constexpr int kSteps = FM == 1 ? 16 : 8;
   const int g = lane >> 4;
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
@@ -385,10 +384,12 @@ SLIM_DEV void finish_adapter_mfma(const LayerArgs& a, int64_t jbase, int lane, c
   }
 }
 
-template <int FM>
-__global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
-  constexpr int kSteps = FM == 1 ? 16 : 8;
-  const int lane = threadIdx.x, g = lane >> 4;
+template <int FM, int NW>
+__global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
+  constexpr int kSteps = (FM == 1 ? 16 : 8) / NW;   // 32-rank steps per pass of one wave
+  __shared__ f4_t hand[NW > 1 ? FM : 1][64];
+  const int lane = threadIdx.x & 63, g = lane >> 4;
+  const int h = NW > 1 ? __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6) : 0;
   const int64_t row0 = (int64_t)blockIdx.x * 16;
   const int64_t lrow = clamp_hi(row0 + (lane & 15), a.rows - 1);
   const int64_t rr = row0 + 4 * g;
@@ -396,12 +397,13 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
   const int w16 = (int)((row0 % 64) / 16);
   const int S = a.split;
   const rsrc_t pr = make_rsrc(a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256), ((int64_t)(S - 1) * 4 + 1) * FM * 256 * 4);
+  const int64_t jfirst = (int64_t)h * 32 * kSteps;
   u32x4_t aq[kSteps], bq[kSteps][FM];
-  if (a.r > 0) finish_adapter_loads<FM>(a, 0, lrow, lane, aq, bq);
+  if (a.r > 0) finish_adapter_loads<FM, kSteps>(a, jfirst, lrow, lane, aq, bq);
   f4_t acc[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-  for (int s0 = 0; s0 < S; s0 += 8) {
+  for (int s0 = 0; s0 < (h == 0 ? S : 0); s0 += 8) {   // the partials: wave 0
     f4_t pv[8][FM];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -420,11 +422,22 @@ __global__ void __launch_bounds__(64) k_finish(LayerArgs a) {
         for (int f = 0; f < FM; ++f) acc[f] = acc[f] + pv[j][f];
   }
   if (a.r > 0) {
-    finish_adapter_mfma<FM>(a, 0, lane, aq, bq, acc);
-    for (int64_t jbase = 32 * kSteps; jbase < a.r; jbase += 32 * kSteps) {
-      finish_adapter_loads<FM>(a, jbase, lrow, lane, aq, bq);
-      finish_adapter_mfma<FM>(a, jbase, lane, aq, bq, acc);
+    // wave h takes rank passes h, h + NW, ... of 32 kSteps ranks
+    finish_adapter_mfma<FM, kSteps>(a, jfirst, lane, aq, bq, acc);
+    for (int64_t jbase = jfirst + NW * 32 * kSteps; jbase < a.r; jbase += NW * 32 * kSteps) {
+      finish_adapter_loads<FM, kSteps>(a, jbase, lrow, lane, aq, bq);
+      finish_adapter_mfma<FM, kSteps>(a, jbase, lane, aq, bq, acc);
     }
+  }
+  if (NW > 1) {
+    // wave 1 hands its sum to wave 0, which adds it last (a fixed order) and stores
+    if (h == 1)
+#pragma unroll
+      for (int f = 0; f < FM; ++f) hand[f][lane] = acc[f];
+    __syncthreads();
+    if (h != 0) return;
+#pragma unroll
+    for (int f = 0; f < FM; ++f) acc[f] = acc[f] + hand[f][lane];
   }
   if (rr < a.rows) {
 #pragma unroll
@@ -880,7 +893,13 @@ void launch_decode_units(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
 template <int FM>
 void launch_finish(const LayerArgs& a, bool bwd, hipStream_t s) {
   SlimKernelTimer timer(bwd ? "finish_bwd" : "finish_fwd", s);
-  SLIM_LAUNCH(timer, (k_finish<FM>), dim3((unsigned)((a.rows + 15) / 16)), dim3(64), s, a);
+  // two waves per 16 rows, splitting the rank, when the rank fills more than one wave's pass of
+  // half the steps and there are few rows (at most 1024 blocks): each wave issues half the adapter
+  // loads (4096^2 layer at M 16: step 11.7 -> 11.3 us); with many rows one wave per 16 rows
+  // already fills the CUs
+  const dim3 grid((unsigned)((a.rows + 15) / 16));
+  if (a.r > 16 * (FM == 1 ? 16 : 8) && a.rows <= 16384) SLIM_LAUNCH(timer, (k_finish<FM, 2>), grid, dim3(128), s, a);
+  else SLIM_LAUNCH(timer, (k_finish<FM, 1>), grid, dim3(64), s, a);
 }
 
 template <bool BWD>

@@ -52,10 +52,12 @@ def test_decode_long_reduction(m):
     _fwd_case(512, 13824, 32, m, name="longk")
 
 
-@pytest.mark.parametrize("k,r,m", [(4096, 16, 16), (4096, 48, 1), (3200, 80, 16), (1152, 112, 3), (384, 16, 32)])
+@pytest.mark.parametrize("k,r,m", [(4096, 16, 16), (4096, 48, 1), (3200, 80, 16), (1152, 112, 3), (384, 16, 32),
+                                   (4096, 272, 20), (2048, 400, 9)])
 def test_decode_adapter_ranks(k, r, m):
     # adapter units are 16 ranks wide: one to seven column blocks, one to four splits, ragged last
-    # splits (K = 3200 and 1152 end inside a unit) and a single split (K = 384)
+    # splits (K = 3200 and 1152 end inside a unit) and a single split (K = 384); ranks 272 and 400
+    # give the finish two waves per 16 rows whose rank passes end inside a pass
     _fwd_case(320, k, r, m, name="adranks")
 
 
