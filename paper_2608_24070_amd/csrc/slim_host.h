@@ -11,7 +11,7 @@
 // Reduction positions per load round of a wave of an adapter first-product unit of the small-M
 // path, and the most reduction splits of that product (longer reductions give a wave several
 // rounds).
-#define SLIM_DECODE_AD_SLICE 256
+#define SLIM_DECODE_AD_SLICE 128
 #define SLIM_DECODE_AD_SPLITS 8
 // Small-M forward: most row tiles one sparse block runs, and the block count it aims for.
 #define SLIM_DECODE_MAX_UNITS 8

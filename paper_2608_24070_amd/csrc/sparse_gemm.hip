@@ -256,8 +256,9 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
 
 // ============================================================ small-M: adapter first-product units
 // tm[m, j] = sum_red act[m, red] Q[j, red]. Unit = 16 adapter columns x 4 parts of ad_sub slices
-// of 256 reduction positions: wave w takes part w (more than one slice when the reduction is long,
-// so that there are at most about 8 splits), reading both operands straight from global memory.
+// of SLIM_DECODE_AD_SLICE (128) reduction positions: wave w takes part w (more than one slice when
+// the reduction is long, so that there are at most about 8 splits), reading both operands straight
+// from global memory.
 // The four parts are added in LDS in part order, and the last unit of a column block to finish
 // sums the units' partials in split order. The partial a unit hands over is one 16 x 16
 // fragment per 16 activation rows (1 KB), which keeps the last unit's loads few.

@@ -47,7 +47,7 @@ def test_smallest_shapes(n, k, m, r):
 
 @pytest.mark.parametrize("m", [1, 20])
 def test_decode_long_reduction(m):
-    # K = 13824: 14 adapter units' worth of 1024 positions, so each wave of a unit takes two 256-position
+    # K = 13824: 27 adapter units' worth of 512 positions, so each wave of a unit takes four 128-position
     # slices (7 splits); the last unit's fourth wave lies wholly past K
     _fwd_case(512, 13824, 32, m, name="longk")
 
@@ -55,7 +55,7 @@ def test_decode_long_reduction(m):
 @pytest.mark.parametrize("k,r,m", [(4096, 16, 16), (4096, 48, 1), (3200, 80, 16), (1152, 112, 3), (384, 16, 32),
                                    (4096, 272, 20), (2048, 400, 9)])
 def test_decode_adapter_ranks(k, r, m):
-    # adapter units are 16 ranks wide: one to seven column blocks, one to four splits, ragged last
+    # adapter units are 16 ranks wide: one to seven column blocks, one to eight splits, ragged last
     # splits (K = 3200 and 1152 end inside a unit) and a single split (K = 384); ranks 272 and 400
     # give the finish two waves per 16 rows whose rank passes end inside a pass
     _fwd_case(320, k, r, m, name="adranks")
@@ -208,8 +208,8 @@ def test_bwd_decode_shape():
 
 @pytest.mark.parametrize("n,r,m", [(9216, 48, 16), (3328, 16, 1)])
 def test_bwd_decode_adapter_ranks(n, r, m):
-    # backward reduction over N: 9216 positions give 9 units' worth, so each wave takes two slices
-    # (5 splits, the last ragged); N = 3328 ends inside the fourth unit
+    # backward reduction over N: 9216 positions give 18 units' worth of 512, so each wave takes three
+    # 128-position slices (6 splits); N = 3328 ends inside the seventh unit
     _bwd_case(n, 256, r, m, name="bwd_adranks")
 
 
