@@ -11,7 +11,8 @@ from tests.gpu_common import dev, dev_bits, layer_inputs
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("n,k,r,m", [(4096, 4096, 384, 16), (1024, 2048, 64, 48), (1024, 1024, 64, 256)])
+@pytest.mark.parametrize("n,k,r,m", [(4096, 4096, 384, 16), (1024, 2048, 64, 48), (1024, 1024, 64, 256),
+                                     (20032, 8192, 64, 16)])
 def test_forward_graph_replays(n, k, r, m):
     print(f"graph fwd n={n} k={k} r={r} m={m}", flush=True)
     W, X, L, R, dx, ad = layer_inputs(n, k, r, m, name="graph")
@@ -33,8 +34,9 @@ def test_forward_graph_replays(n, k, r, m):
         assert torch.equal(out, eager), f"replay {rep} differs"
 
 
-def test_bwd_graph_replays():
-    n, k, r, m = 4096, 4096, 384, 16
+@pytest.mark.parametrize("n,k,r,m", [(4096, 4096, 384, 16), (1024, 1024, 64, 256)])
+def test_bwd_graph_replays(n, k, r, m):
+    print(f"graph bwd n={n} k={k} r={r} m={m}", flush=True)
     W = synth.weights(n, k, seed=3, name="gbwd/W")
     yb, _ = synth.activations(m, n, seed=3, name="gbwd/dY")
     Lb, Rb, _, _ = synth.adapter(k, n, r, seed=3, name="gbwd/")
