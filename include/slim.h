@@ -181,6 +181,8 @@ int slim_workspace_init(void* ws, size_t ws_bytes, void* stream);
  *   ws      device workspace of at least slim_linear_workspace(M, N, K, r) bytes, zeroed once
  *           with slim_workspace_init before its first use. Two calls that overlap in time must
  *           not share a workspace.
+ * Sizes past the kernels' 32-bit offsets return SLIM_EUNSUPPORTED: for M > 32, K above 2^23, or
+ * ceil(M/32)*32*r or ceil(N/32)*32*r of 2^30 or more.
  * Operand precision: bf16 activations are converted to fp16 (exact for |x| in
  * [2^-14, 65504]); dequantised weights are (u-8)*s16 rounded to fp16; the adapter intermediate
  * X*L is accumulated in fp32 and rounded to fp16 for the second product. Deterministic:
@@ -201,6 +203,8 @@ int slim_linear(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, cons
  *   L, R    fp16 [K, r] and [r, N]; both NULL when r == 0. r % 16 == 0.
  *   dX      out, fp32 [M, K].
  *   ws      workspace of at least slim_bwd_dx_workspace(M, N, K, r) bytes, zeroed once.
+ * Sizes past the kernels' 32-bit offsets return SLIM_EUNSUPPORTED: for M > 32, N above 2^23, or
+ * ceil(M/32)*32*r or ceil(K/32)*32*r of 2^30 or more.
  * Operand precision: the weight codes enter the matrix cores as exact small integers and the
  * fp16 scale is folded into dY per (row n, 128-group of k), rounded to fp16.
  */

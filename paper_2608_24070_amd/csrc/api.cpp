@@ -6,6 +6,8 @@
 
 namespace {
 constexpr int64_t kMaxDim = int64_t(1) << 31;
+constexpr int64_t kMaxLargeRed = int64_t(1) << 23;     // large M: longest reduction
+constexpr int64_t kMaxTiledElems = int64_t(1) << 30;   // large M: M r and rows r (fp16, 32-bit byte offsets)
 constexpr size_t kCounterSlots = SLIM_COUNTER_SLOTS;
 constexpr int64_t kDecodeAdSlice = SLIM_DECODE_AD_SLICE;
 
@@ -98,7 +100,11 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     if (q.sp_split > 1 || r > 0) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 4 * q.dec_fm * 256 * 4;
     q.lds_bytes = 0;
   } else {
-    // large M: dense adapter GEMM (128 x 128 tiles) then 512 x 96 or 512 x 128 sparse tiles
+    // large M: dense adapter GEMM (128 x 128 tiles) then 512 x 96 or 512 x 128 sparse tiles. Their
+    // per-lane buffer offsets are 32-bit: an activation offset spans up to 128 rows of the
+    // reduction, and T and the adapter's second factor are addressed from their start.
+    if (red > kMaxLargeRed || cdiv(M, 32) * 32 * r >= kMaxTiledElems || cdiv(rows, 32) * 32 * r >= kMaxTiledElems)
+      return SLIM_EUNSUPPORTED;
     q.decode = false;
     q.sp_rows_tile = 512;
     q.sp_row_tiles = cdiv(rows, 512);

@@ -86,6 +86,24 @@ def test_bwd_workspace_and_shape_rules():
     assert call(N=1040) == 2
 
 
+def test_sizes_past_32bit_offsets_are_refused():
+    # large M: the reduction at most 2^23 and M r, rows r below 2^30 (32-bit buffer offsets);
+    # small M has no such limit
+    big = (1 << 23) + 128
+    assert slim.slim_linear_workspace(16, 16, big, 0) > 0
+    assert slim.slim_linear_workspace(64, 16, 1 << 23, 0) > 0
+    with pytest.raises(slim.SlimError):
+        slim.slim_linear_workspace(64, 16, big, 0)
+    with pytest.raises(slim.SlimError):
+        slim.slim_bwd_dx_workspace(64, big, 128, 0)                # backward reduction is N
+    assert slim.slim_linear_workspace(1 << 21, 16, 128, 256) > 0
+    with pytest.raises(slim.SlimError):
+        slim.slim_linear_workspace(1 << 21, 16, 128, 512)          # M r = 2^30
+    with pytest.raises(slim.SlimError):
+        slim.slim_linear_workspace(64, 1 << 21, 128, 512)          # N r = 2^30
+    assert slim.slim_linear(A, 1, 64, 16, big, A, A, A, None, None, 0, A, A, 1 << 30, None) == 9
+
+
 @pytest.mark.parametrize("M,N,K,r", [(1, 4096, 4096, 384), (16, 4096, 4096, 384), (2048, 11008, 4096, 384),
                                      (8192, 28672, 8192, 512), (4096, 5120, 13824, 512)])
 def test_workspace_sizes_are_modest(M, N, K, r):
