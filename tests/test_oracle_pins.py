@@ -58,6 +58,52 @@ def test_scale_uses_fp32_division_then_fp16():
     assert np.array_equal(s, want)
 
 
+def _exact_rne_f16_of_a_over_7(a):
+    """RNE of the exact quotient a/7 to binary16, by exact comparisons against the table of every
+    finite binary16 value: 7 t and 2 a are exact in float64 (t has 11 significant bits, a 24),
+    and so is 7 (t_lo + t_hi), so no step here rounds."""
+    table = B._f16_table()
+    a = np.asarray(a, dtype=np.float64)
+    lo = np.searchsorted(table, a / 7.0, side="right") - 1
+    lo = np.clip(lo, 0, len(table) - 2)
+    lo = np.where(7.0 * table[lo] > a, lo - 1, lo)              # t_lo <= a/7 exactly
+    lo = np.where(7.0 * table[lo + 1] <= a, lo + 1, lo)         # a/7 < t_hi exactly
+    two_a, mid7 = 2.0 * a, 7.0 * (table[lo] + table[lo + 1])
+    pick_hi = (two_a > mid7) | ((two_a == mid7) & (lo % 2 == 1))   # ties to the even bit pattern
+    return np.where(pick_hi, table[lo + 1], table[lo])
+
+
+def test_scale_is_exact_rne_of_a_over_7_at_every_fp16_midpoint():
+    # Double rounding (a/7 -> fp32 -> fp16) can differ from one rounding of the exact quotient only
+    # where the fp32 quotient lands on a binary16 midpoint m. For float32 a that needs
+    # |a - 7m| <= 3.5 ulp32(m), while 7m is a float32 whose neighbours are 4 or 8 ulp32(m) away:
+    # only a = 7m itself qualifies (an exact tie). This checks every positive midpoint (normal and
+    # subnormal binary16) with a = 7m and its two float32 neighbours on each side, against the exact
+    # rational rounding. It fails a reciprocal multiply a * fp32(1/7) (17384 of these cases differ)
+    # and truncation; computing a/7 in float64 and rounding once to fp16 gives the same scales
+    # everywhere, which is why the reading's fp32 division is pinned as exact RNE of a/7.
+    table = B._f16_table()
+    mids = (table[:-1] + table[1:]) / 2.0
+    a0 = (7.0 * mids).astype(np.float32)
+    assert np.array_equal(a0.astype(np.float64), 7.0 * mids)
+    up1, dn1 = np.nextafter(a0, np.float32(np.inf)), np.nextafter(a0, np.float32(0))
+    a = np.concatenate([a0, up1, dn1, np.nextafter(up1, np.float32(np.inf)), np.nextafter(dn1, np.float32(0))])
+    a = a[(a > 0) & (a.astype(np.float64) / 7.0 < 65504.0)]
+    want = _exact_rne_f16_of_a_over_7(a)
+    got = np.empty(len(a))
+    for c0 in range(0, len(a), 16384):
+        blk = a[c0:c0 + 16384]
+        W = np.zeros((len(blk), 128), dtype=np.float32)
+        W[:, 77] = blk
+        W[:, 3] = -blk * np.float32(0.5)
+        got[c0:c0 + len(blk)] = O.group_scales(W)[:, 0].astype(np.float64)
+    assert np.array_equal(got, want)
+    ties = a0[a0.astype(np.float64) / 7.0 < 65504.0]
+    assert len(ties) > 30000                                   # exact ties of both parities are in the set
+    spot = synth.stream(2, "spot").choice(len(a), size=64, replace=False)
+    assert [B.f16_nearest(B.to_f32(float(a[i]) / 7.0)) for i in spot] == list(want[spot])
+
+
 # ----------------------------------------------------------- mask (P1, P2, P10)
 
 @pytest.mark.parametrize("seed", [0, 1])
@@ -376,3 +422,20 @@ def test_tolerance_gate():
     Z = Y.copy()
     Z[0, 0] += 0.02
     assert not O.within_tolerance(Z, Y)[0]
+
+
+def test_tolerance_gate_max_abs_leg_alone():
+    # One element off by 1.5e-2 of max|Y_ref| in a large array: the relative Frobenius error stays
+    # far below 2e-3, so only the max-abs leg (max|Y - Y_ref| <= 1e-2 max|Y_ref|) can reject it.
+    Yref = synth.stream(3, "gate").standard_normal((256, 1024))
+    inf = np.max(np.abs(Yref))
+    Y = Yref.copy()
+    Y[17, 333] += 1.5e-2 * inf
+    ok, rf, ma = O.within_tolerance(Y, Yref)
+    assert rf < 2e-4 and abs(ma - 1.5e-2) < 1e-12
+    assert not ok
+    # just inside both legs: accepted
+    Y[17, 333] = Yref[17, 333] + 0.9e-2 * inf
+    assert O.within_tolerance(Y, Yref)[0]
+    # and the Frobenius leg alone still rejects a uniform 3e-3 relative error
+    assert not O.within_tolerance(Yref * (1 + 3e-3), Yref)[0]
