@@ -19,8 +19,9 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  * Shapes: W is [N x K] (N output features, K input features), X is [M x K], Y is [M x N],
- * L is [K x r], R is [r x N], dY is [M x N], dX is [M x K]. Everything is dense row-major
- * with no padding between rows.
+ * L is [K x r], R is [r x N], dY is [M x N], dX is [M x K]. Activations, outputs and the
+ * adapter factors as given are dense row-major with no padding between rows; the packed
+ * weights and the forward's adapter factors use the layouts below.
  *
  * Pointers: every array argument is a DEVICE pointer unless the comment says "host". The
  * caller allocates and owns every buffer, including workspace. The library never frees
@@ -38,18 +39,41 @@
  *
  * Packed format (all multi-byte words little-endian)
  * --------------------------------------------------
- *   codes  uint8 [N, K/4]: read as uint32 words [N, K/16]. Word b of row n covers K positions
- *          16b..16b+15, which form four groups of four (c = 0..3). Bits 4c..4c+3 hold the code
- *          u = q + 8 of group c's lower kept position; bits 16+4c..16+4c+3 hold that of its
- *          higher kept position. q is in [-7, 7], so u is in [1, 15].
- *   meta   uint8 [N, K/8]: read as uint16 half-words [N, K/16]. Half-word b holds, for group c of
- *          the same 16 positions, the kept offsets i0 < i1 (0..3) as i0 in bits 4c..4c+1 and
- *          i1 in bits 4c+2..4c+3.
- *   scales uint16 [N, K/128]: fp16 bit patterns, s16 = fp16_RNE(fp32(max|w| of the group) / 7).
- *   The value of kept weight (n, k) is (u - 8) * s16[n, k/128]; every other weight is zero.
+ * Words. Per row and 16 consecutive reduction positions (four aligned 2:4 groups, g = 0..3):
+ *   one code word (uint32): nibble g = u of group g's lower kept position, nibble g + 4 = u of
+ *     its higher kept position, where u = q + 8 and q in [-7, 7] is the signed code;
+ *   one index half-word (uint16): nibble g = i0 | i1 << 2, the kept offsets i0 < i1 (0..3).
+ * Per row and 128 consecutive reduction positions (one quantisation group): one fp16 scale
+ *   s16 = fp16_RNE(fp32(max |w| of the group) / 7).
+ * The value of kept weight (n, k) is (u - 8) * s16[n, k / 128]; every other weight is zero.
  *
- * Backward pack: the same code/meta format along N instead of K, one row per input feature:
- *   codesT uint8 [K, N/4], metaT uint8 [K, N/8], scalesT uint16 [K/128, N] (scales transposed).
+ * Layout. Rows are kept in blocks of 16 and the reduction in chunks of 128 (nch = reduction
+ * length / 128). Row n, chunk c owns slot ((n / 16) * nch + c) * 16 + n % 16, which holds its 8
+ * code words at bytes 32 slot .. 32 slot + 31 of `codes`, its 8 index half-words at bytes
+ * 16 slot .. 16 slot + 15 of `meta` and its scale at element `slot` of `scales`:
+ *   codes  uint8 [rows/16][nch][16][32], meta uint8 [rows/16][nch][16][16], scales fp16 [rows/16][nch][16].
+ * One chunk of a 16-row block is thus contiguous (512 B of codes, 256 B of index words, 32 B of
+ * scales). The forward pack has rows n and reduction k; the backward pack (codesT, metaT) has
+ * rows k and reduction n, and its scales are scalesT fp16 [K/128][N] = s16[n, k/128].
+ * 3.125 bits per dense weight (0.390625 bytes).
+ *
+ * Precision
+ * ---------
+ * Products accumulate in fp32 and Y / dX are fp32. Operands reach the matrix cores in fp16:
+ *   - dequantised forward weights (u - 8) * s16, rounded to fp16 once;
+ *   - activations (X, dY): each row of activations is multiplied by a power of two 2^e chosen
+ *     so that its largest magnitude lies in [16, 32), rounded to fp16, and the fp32 results are
+ *     multiplied by 2^-e (both exact), so bf16 inputs of any magnitude keep fp16's relative
+ *     precision. At M <= 32 the exponent is chosen per slice of the reduction that one block
+ *     or wave stages (at most 1024 positions); at M > 32 per whole row;
+ *   - backward: the scale s16[n, k/128] multiplies the (row-scaled) gradient, and the product is
+ *     rounded to fp16 once; the codes enter as exact small integers;
+ *   - adapter: the first product (X L, or dY R^T) accumulates in fp32. At M <= 32 it stays fp32
+ *     and is row-scaled into fp16 for the second product per pass of at most 512 ranks; at
+ *     M > 32 it is formed from the row-scaled activations and stored in fp16, so its entries
+ *     must stay below 65504 after that scaling: |T[m, j]| < 2^11 max_k |X[m, k]| (true when
+ *     sum_k |L[k, j]| < 2^11).
+ * Deterministic: identical inputs give identical bits.
  */
 #ifndef SLIM_H
 #define SLIM_H
@@ -61,7 +85,7 @@
 extern "C" {
 #endif
 
-#define SLIM_ABI_VERSION 1
+#define SLIM_ABI_VERSION 2
 
 typedef enum {
   SLIM_OK = 0,
@@ -70,13 +94,14 @@ typedef enum {
   SLIM_EDTYPE = 3,        /* unsupported dtype code */
   SLIM_EALIGN = 4,        /* a device array is not 16-byte aligned */
   SLIM_ENONFINITE = 5,    /* W holds a NaN or an infinity */
-  SLIM_ERANGE = 6,        /* a group scale max|w|/7 overflows fp16 */
-  SLIM_EWORKSPACE = 7,    /* workspace missing or smaller than the query returned */
-  SLIM_EDEVICE = 8,       /* a HIP runtime call or a kernel launch failed */
-  SLIM_EUNSUPPORTED = 9   /* valid but not supported by this library (e.g. no gfx950 device) */
+  SLIM_EWORKSPACE = 6,    /* workspace missing or smaller than the query returned */
+  SLIM_EDEVICE = 7,       /* a HIP runtime call or a kernel launch failed */
+  SLIM_EUNSUPPORTED = 8,  /* valid but not supported by this library (e.g. no gfx950 device) */
+  SLIM_ERANGE = 9         /* a group scale the packed format or the backward cannot represent */
 } slim_status;
 
-typedef enum { SLIM_F16 = 0, SLIM_BF16 = 1 } slim_dtype;
+/* Element types. Activations (X, dY) are SLIM_F16 or SLIM_BF16; Y and dX are always SLIM_F32. */
+typedef enum { SLIM_F16 = 0, SLIM_BF16 = 1, SLIM_F32 = 2 } slim_dtype;
 
 /* Human-readable name of a status code (static string, never NULL). */
 const char* slim_status_string(int status);
@@ -127,7 +152,11 @@ int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, uint8_t* met
  *   mask_rc out, optional (NULL to skip): uint8 [N, K], 1 on the support of W^{R,C}.
  * Rule: for each column k and aligned group of four rows, keep two slots ranked by
  * (|Wc| descending, forward-kept descending, row ascending). A kept slot carries its forward
- * code (8, i.e. zero, if the forward mask had dropped it). Asynchronous on `stream`.
+ * code (8, i.e. zero, if the forward mask had dropped it).
+ * Returns SLIM_ERANGE if a forward scale is 2048 or more (a group max |w| of about 14336): the
+ * M > 32 backward forms dY * s16 in fp16 from row-scaled gradients below 32, which would overflow.
+ * The outputs are then unspecified. This call synchronises `stream` (it reads back a status word)
+ * and allocates 4 bytes of device memory for that word for the duration of the call.
  */
 int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const uint16_t* scales, int64_t N,
                   int64_t K, uint8_t* codesT, uint8_t* metaT, uint16_t* scalesT, uint8_t* mask_rc,
@@ -136,8 +165,11 @@ int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const uint16_t* sca
 /*
  * slim_pack_adapter - one-time layout of the adapter factors for slim_linear.
  * Thesis: the rank-r adapter W ~ W^C + L R (SLiM "SLiM-LoRA low-rank adapters"); like the weight
- * pack, this runs once per layer. The forward consumes both factors along their rank
- * dimension, so it takes them transposed; the backward (slim_linear_bwd_dx) takes L and R as given.
+ * pack (set up once, multiply many times), this runs once per layer. The forward reads L along
+ * K for each rank (X L) and R along the rank for each output row (T R), so it takes L^T
+ * row-major and R^T in tiles of 32 rows x 16 ranks; re-laying them inside every slim_linear call
+ * would add a launch and 4 r (K + N) bytes of traffic per call. The backward
+ * (slim_linear_bwd_dx) reads L and R as given.
  *
  *   L    fp16 [K, r], device.     R    fp16 [r, N], device.
  *   K, N >= 1; r >= 16, r % 16 == 0.
@@ -175,7 +207,8 @@ int slim_workspace_init(void* ws, size_t ws_bytes, void* stream);
  *   X       [M, K] in `xdtype` (SLIM_BF16 or SLIM_F16), device.
  *   M, N, K M >= 1, N >= 16, N % 16 == 0, K % 128 == 0.
  *   codes, meta, scales   forward pack of W (slim_pack).
- *   Lt, Rt  the adapter from slim_pack_adapter: fp16 [r, K] = L^T and [N, r] = R^T; both NULL when
+ *   Lt, Rt  the adapter laid out by slim_pack_adapter: Lt fp16 [r, K] = L^T row-major, Rt fp16 R^T
+ *           in 32 x 16 tiles (a plain row-major R^T gives wrong results); both NULL when
  *           r == 0. r % 16 == 0.
  *   Y       out, fp32 [M, N]. Must not alias any input.
  *   ws      device workspace of at least slim_linear_workspace(M, N, K, r) bytes, zeroed once
@@ -183,10 +216,8 @@ int slim_workspace_init(void* ws, size_t ws_bytes, void* stream);
  *           not share a workspace.
  * Sizes past the kernels' 32-bit offsets return SLIM_EUNSUPPORTED: for M > 32, K above 2^23, or
  * ceil(M/32)*32*r or ceil(N/32)*32*r of 2^30 or more.
- * Operand precision: bf16 activations are converted to fp16 (exact for |x| in
- * [2^-14, 65504]); dequantised weights are (u-8)*s16 rounded to fp16; the adapter intermediate
- * X*L is accumulated in fp32 and rounded to fp16 for the second product. Deterministic:
- * identical inputs give identical bits.
+ * Operand precision: see "Precision" above (row-scaled fp16 activations, fp16 dequantised
+ * weights, fp32 accumulation). Deterministic: identical inputs give identical bits.
  */
 int slim_linear(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const uint8_t* codes,
                 const uint8_t* meta, const uint16_t* scales, const uint16_t* Lt, const uint16_t* Rt,
@@ -205,8 +236,9 @@ int slim_linear(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, cons
  *   ws      workspace of at least slim_bwd_dx_workspace(M, N, K, r) bytes, zeroed once.
  * Sizes past the kernels' 32-bit offsets return SLIM_EUNSUPPORTED: for M > 32, N above 2^23, or
  * ceil(M/32)*32*r or ceil(K/32)*32*r of 2^30 or more.
- * Operand precision: the weight codes enter the matrix cores as exact small integers and the
- * fp16 scale is folded into dY per (row n, 128-group of k), rounded to fp16.
+ * Operand precision: the weight codes enter the matrix cores as exact small integers; the fp16
+ * scale s16[n, k/128] multiplies the row-scaled gradient and the product is rounded to fp16 once
+ * (see "Precision" above). Deterministic.
  */
 int slim_linear_bwd_dx(const void* dY, int dydtype, int64_t M, int64_t N, int64_t K,
                        const uint8_t* codesT, const uint8_t* metaT, const uint16_t* scalesT,
@@ -219,7 +251,10 @@ int slim_linear_bwd_dx(const void* dY, int dydtype, int64_t M, int64_t N, int64_
  * before and after itself on the caller's stream. slim_timing_read waits for the recorded
  * events and writes one line per kernel name, "name launches total_ms\n", into buf (host);
  * it returns 0, or the buffer size needed when buf is NULL or too small. slim_timing_reset
- * clears the totals. Thread-safe; timing adds two event records per launch while enabled.
+ * clears the totals. These three calls are the library's only process-wide mutable state (a
+ * mutex-guarded switch, event pool and totals); with timing off, which is the default, the layer
+ * calls read nothing of it but the switch. Thread-safe; timing adds two event records per launch
+ * while enabled, and never records inside a stream capture.
  */
 int slim_timing_enable(int on);
 int slim_timing_reset(void);

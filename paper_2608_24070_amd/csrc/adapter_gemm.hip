@@ -18,9 +18,8 @@
 // The reduction may be split across blocks: each split then stores its fp32 partial in the same
 // tiled order with plain stores, and k_adapter_finish (sparse_gemm.hip) sums the splits in order
 // (deterministic) after the kernel boundary has made them visible.
-// bf16 activations are streamed as they are and converted when a fragment is read; the blocks
-// also write the fp16 copy the sparse tile kernel streams: chunk c of a row tile by the block of
-// column tile c % (column tiles), so each element is converted and written once.
+// The activations are the fp16 copy k_rowprep writes, each row scaled by a power of two, so the
+// result is T (or U) with the same row scaling; the tile kernel unscales its fp32 output.
 #include <type_traits>
 
 #include "slim_device.h"
@@ -34,11 +33,9 @@ constexpr int kBK = 64;     // reduction per chunk
 // direct loads per thread per chunk: 4 for the activation rows, 4 for the Q rows
 constexpr int kLoads = 8;
 
-template <bool ABF16>
 __global__ void __launch_bounds__(256)
 k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint16_t* __restrict__ Q, int64_t r,
-               int64_t slice, int split, uint16_t* __restrict__ out, float* __restrict__ part,
-               uint16_t* __restrict__ a16) {
+               int64_t slice, int split, uint16_t* __restrict__ out, float* __restrict__ part) {
   __shared__ __attribute__((aligned(16))) _Float16 as0[kT][kBK], as1[kT][kBK];
   __shared__ __attribute__((aligned(16))) _Float16 bs0[kT][kBK], bs1[kT][kBK];
   auto as_at = [&](int stg) -> _Float16(*)[kBK] { return stg == 0 ? as0 : as1; };
@@ -84,23 +81,6 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint
   auto frag = [&](const _Float16 (*tile)[kBK], int row, int t) {
     return *reinterpret_cast<const h8_t*>(&tile[row][8 * ((2 * t + ha) ^ (row & 7))]);
   };
-  auto frag_a = [&](const _Float16 (*tile)[kBK], int row, int t) {
-    if (!ABF16) return frag(tile, row, t);
-    return load8_as_h(*reinterpret_cast<const u32x4_t*>(&tile[row][8 * ((2 * t + ha) ^ (row & 7))]), true);
-  };
-  // bf16: chunk t's fp16 copy, from the stage it sits in (16-byte group c of row `row` is at LDS
-  // slot c ^ (row % 8)); rows past M are not written
-  auto copy_chunk = [&](int t, const _Float16 (*tile)[kBK]) {
-    const int64_t gt = kbeg / kBK + t;
-    if (gt % (int64_t)gridDim.y != (int64_t)blockIdx.y) return;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int v = tid + 256 * i, row = v >> 3, c = v & 7;
-      const u32x4_t x = *reinterpret_cast<const u32x4_t*>(&tile[row][8 * (c ^ (row & 7))]);
-      if (m0 + row < M)
-        *reinterpret_cast<h8_t*>(a16 + (m0 + row) * Kd + gt * kBK + 8 * c) = load8_as_h(x, true);
-    }
-  };
   // steps of a chunk: 16-wide reductions; the fragments of step st + 1 are read while step st's
   // MFMAs run
   auto chunk = [&](int t, auto zc) {
@@ -113,7 +93,7 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint
     h8_t af[2][2], bf[2][2];
 #pragma unroll
     for (int f = 0; f < 2; ++f) {
-      af[0][f] = frag_a(as_at(z), 64 * wm + 32 * f + (lane & 31), 0);
+      af[0][f] = frag(as_at(z), 64 * wm + 32 * f + (lane & 31), 0);
       bf[0][f] = frag(bs_at(z), 64 * wr + 32 * f + (lane & 31), 0);
     }
 #pragma unroll
@@ -121,7 +101,7 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint
       if (st + 1 < kBK / 16) {
 #pragma unroll
         for (int f = 0; f < 2; ++f) {
-          af[(st + 1) & 1][f] = frag_a(as_at(z), 64 * wm + 32 * f + (lane & 31), st + 1);
+          af[(st + 1) & 1][f] = frag(as_at(z), 64 * wm + 32 * f + (lane & 31), st + 1);
           bf[(st + 1) & 1][f] = frag(bs_at(z), 64 * wr + 32 * f + (lane & 31), st + 1);
         }
       }
@@ -130,8 +110,6 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint
 #pragma unroll
         for (int y = 0; y < 2; ++y) acc[x][y] = mfma32(af[st & 1][x], bf[st & 1][y], acc[x][y]);
     }
-    // the stage stays untouched until the next chunk's barrier
-    if (ABF16) copy_chunk(t, as_at(z));
   };
   dma(0, 0);
   int t0 = 0;
@@ -165,15 +143,12 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint
 
 }  // namespace
 
-int slim_launch_adapter_gemm(const uint16_t* A, int a_bf16, int64_t M, int64_t Kd, const uint16_t* Q, int64_t r,
-                             const SlimPlan& p, char* ws, uint16_t* a16, hipStream_t s) {
+int slim_launch_adapter_gemm(const uint16_t* A, int64_t M, int64_t Kd, const uint16_t* Q, int64_t r, const SlimPlan& p,
+                             char* ws, hipStream_t s) {
   dim3 grid((unsigned)p.ad_tiles_m, (unsigned)p.ad_tiles_j, (unsigned)p.ad_split);
   uint16_t* out = reinterpret_cast<uint16_t*>(ws + p.off_t);
   float* part = reinterpret_cast<float*>(ws + p.off_tpart);
   SlimKernelTimer timer("adapter_gemm", s);
-  if (a_bf16)
-    SLIM_LAUNCH(timer, k_adapter_gemm<true>, grid, dim3(256), s, A, M, Kd, Q, r, p.ad_slice, p.ad_split, out, part, a16);
-  else
-    SLIM_LAUNCH(timer, k_adapter_gemm<false>, grid, dim3(256), s, A, M, Kd, Q, r, p.ad_slice, p.ad_split, out, part, a16);
+  SLIM_LAUNCH(timer, k_adapter_gemm, grid, dim3(256), s, A, M, Kd, Q, r, p.ad_slice, p.ad_split, out, part);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }

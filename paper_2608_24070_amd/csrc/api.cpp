@@ -136,19 +136,22 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
   if (q.n_counters > kCounterSlots) return SLIM_EUNSUPPORTED;
   // the counter region has a fixed size so that it stays at zero across calls with other sizes
   size_t off = kCounterSlots * 4;
-  // T: row-major [M, r] at small M; at large M in 32 x 16 tiles ([ceil(M/32)][r/16][32][16], see
-  // adapter_gemm.hip), which the tile kernel's epilogue reads 1 KB at a time
+  // T: fp32 row-major [M, r] at small M; at large M fp16 in 32 x 16 tiles ([ceil(M/32)][r/16][32][16],
+  // see adapter_gemm.hip), which the tile kernel's epilogue reads 1 KB at a time
   q.off_t = off;
-  off = round256(off + (size_t)(q.decode ? M : cdiv(M, 32) * 32) * (size_t)r * 2);
+  off = round256(off + (q.decode ? (size_t)M * (size_t)r * 4 : (size_t)cdiv(M, 32) * 32 * (size_t)r * 2));
   q.off_tpart = off;
   off = round256(off + tpart_bytes);
   q.off_ypart = off;
   off = round256(off + ypart_bytes);
-  // large M: fp16 copy of bf16 activations for the tile kernel's direct-to-LDS loads, and (backward:
+  // large M: the row-scaled fp16 copy of the activations for the tile kernel's direct-to-LDS loads, and (backward:
   // the forward's factor comes tiled from slim_pack_adapter) the adapter's second factor P
   // [rows, r] re-laid in 32 x 16 tiles
   q.off_x16 = off;
   if (!q.decode) off = round256(off + (size_t)M * (size_t)red * 2);
+  // large M: 2^-e per activation row (the rows of the fp16 copy are scaled by 2^e)
+  q.off_rowinv = off;
+  if (!q.decode) off = round256(off + (size_t)M * 4);
   q.off_pb = off;
   if (!q.decode && bwd) off = round256(off + (size_t)cdiv(rows, 32) * 32 * (size_t)r * 2);
   q.total = off;
@@ -170,6 +173,7 @@ int slim_check_linear(bool bwd, const void* X, int xdtype, int64_t M, int64_t N,
     return SLIM_EALIGN;
   if (!ws || ws_bytes < plan->total) return SLIM_EWORKSPACE;
   if (!slim_aligned16(ws)) return SLIM_EALIGN;
+  plan->scaled = !plan->decode && (bwd || xdtype == SLIM_BF16 || r > 0);
   return SLIM_OK;
 }
 

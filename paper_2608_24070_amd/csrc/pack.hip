@@ -88,11 +88,16 @@ k_pack(const float4* __restrict__ W, int64_t total4, int64_t K, uint32_t* __rest
 // column k and one 16-row block, prunes each aligned 4-row group to its top two
 // (|Wc| desc, forward-kept desc, row asc) and emits one codesT word and one metaT half-word.
 constexpr int kBT = 64;
+// Largest forward scale the backward accepts: its large-M path multiplies gradients scaled below
+// 2^(kActExp + 1) = 32 by s16 in fp16, which stays below 65504 for s16 < 2048.
+constexpr float kBwdScaleLimit = 2048.0f;
+static_assert(kActExp == 4, "kBwdScaleLimit assumes row-scaled activations below 32");
 
 __global__ void __launch_bounds__(256)
 k_pack_bwd(const uint32_t* __restrict__ codes, const uint16_t* __restrict__ meta,
            const uint16_t* __restrict__ scales, int64_t N, int64_t K, uint32_t* __restrict__ codesT,
-           uint16_t* __restrict__ metaT, uint16_t* __restrict__ scalesT, uint8_t* __restrict__ mask_rc) {
+           uint16_t* __restrict__ metaT, uint16_t* __restrict__ scalesT, uint8_t* __restrict__ mask_rc,
+           int* __restrict__ status) {
   __shared__ uint8_t u_s[kBT][kBT + 4];     // forward code per (row, col), 8 where pruned
   __shared__ uint8_t f_s[kBT][kBT + 4];     // forward-kept bit, later the W^{R,C} support bit
   __shared__ float sc_s[kBT];               // scale of each row for this column tile
@@ -124,7 +129,11 @@ k_pack_bwd(const uint32_t* __restrict__ codes, const uint16_t* __restrict__ meta
         f_s[row][16 * w + 4 * c + i0] = 1;
         f_s[row][16 * w + 4 * c + i1] = 1;
       }
-      if (w == 0) sc_s[row] = h_bits_to_f(scales[slot]);
+      if (w == 0) {
+        sc_s[row] = h_bits_to_f(scales[slot]);
+        // the backward's fp16 product of a row-scaled gradient (below 32) and s16 must stay finite
+        if (!(sc_s[row] < kBwdScaleLimit)) atomicOr(status, 2);
+      }
     }
   }
   __syncthreads();
@@ -289,10 +298,25 @@ extern "C" int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const ui
                              void* stream) {
   int st = slim_check_pack_bwd(codes, meta, scales, N, K, codesT, metaT, scalesT, mask_rc);
   if (st != SLIM_OK) return st;
-  dim3 grid((unsigned)(K / kBT), (unsigned)((N + kBT - 1) / kBT));
-  SlimKernelTimer timer("pack_bwd", (hipStream_t)stream);
-  SLIM_LAUNCH(timer, k_pack_bwd, grid, dim3(256), (hipStream_t)stream, reinterpret_cast<const uint32_t*>(codes),
-              reinterpret_cast<const uint16_t*>(meta), scales, N, K, reinterpret_cast<uint32_t*>(codesT),
-              reinterpret_cast<uint16_t*>(metaT), scalesT, mask_rc);
-  return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
+  hipStream_t s = (hipStream_t)stream;
+  int* d_status = nullptr;
+  if (hipMalloc(&d_status, sizeof(int)) != hipSuccess) return SLIM_EDEVICE;
+  int h_status = 0;
+  int rc = SLIM_OK;
+  do {
+    if (hipMemsetAsync(d_status, 0, sizeof(int), s) != hipSuccess) { rc = SLIM_EDEVICE; break; }
+    {
+      dim3 grid((unsigned)(K / kBT), (unsigned)((N + kBT - 1) / kBT));
+      SlimKernelTimer timer("pack_bwd", s);
+      SLIM_LAUNCH(timer, k_pack_bwd, grid, dim3(256), s, reinterpret_cast<const uint32_t*>(codes),
+                  reinterpret_cast<const uint16_t*>(meta), scales, N, K, reinterpret_cast<uint32_t*>(codesT),
+                  reinterpret_cast<uint16_t*>(metaT), scalesT, mask_rc, d_status);
+    }
+    if (hipGetLastError() != hipSuccess) { rc = SLIM_EDEVICE; break; }
+    if (hipMemcpyAsync(&h_status, d_status, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess) { rc = SLIM_EDEVICE; break; }
+    if (h_status & 2) rc = SLIM_ERANGE;
+  } while (0);
+  (void)hipFree(d_status);
+  return rc;
 }

@@ -98,6 +98,70 @@ SLIM_DEV h8_t dequant_word_int(uint32_t w, const NibbleConsts& k = nibble_consts
   return a;
 }
 
+// ----------------------------------------------------------------------------------------------
+// Per-row power-of-two scaling of activations. fp16 covers 2^-24 .. 65504, while bf16 activations
+// and gradients (dY of order 1e-3 .. 1e-6, and dY times a weight scale of order 1e-2) can lie far
+// outside it. Before a row of activations is rounded to fp16 it is multiplied by 2^e, with e chosen
+// so that the row's largest magnitude lies in [2^kActExp, 2^(kActExp+1)); the fp32 results are
+// multiplied by 2^-e. Both multiplications are exact (powers of two, normal fp32 range), so the
+// only rounding is the one to fp16, now at full relative precision for every value within 2^-18
+// of the row's largest. kActExp = 4 leaves 2^11 of headroom below fp16's maximum for fp16
+// intermediates formed from the scaled rows (the adapter's X L, and the backward's dY s16 with
+// scales below 2048).
+// ----------------------------------------------------------------------------------------------
+constexpr int kActExp = 4;
+
+// 2^e as fp32, for e in [-126, 127] (built from the exponent field, so no rounding).
+SLIM_DEV float exp2i(int e) { return __builtin_bit_cast(float, (uint32_t)(e + 127) << 23); }
+
+// Scaling exponent for a row whose largest magnitude has fp32 bit pattern `maxbits` (sign
+// cleared): kActExp - floor(log2(max)), clamped to [-126, 126] so that 2^e and 2^-e are normal.
+// A zero row (and a non-finite maximum) gets 0.
+SLIM_DEV int act_exponent(uint32_t maxbits) {
+  const int E = (int)(maxbits >> 23);   // biased exponent; 0 for zero and fp32 subnormals
+  if (maxbits == 0u || E == 255) return 0;
+  const int e = kActExp - (E == 0 ? -127 : E - 127);
+  return e < -126 ? -126 : (e > 126 ? 126 : e);
+}
+
+SLIM_DEV uint32_t abs_bits(float x) { return __builtin_bit_cast(uint32_t, x) & 0x7FFFFFFFu; }
+
+// Largest value over the 64 lanes of a wave (all lanes get it).
+SLIM_DEV uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off, 64));
+  return v;
+}
+
+// Eight fp32 values times s (a power of two), rounded to fp16.
+SLIM_DEV h8_t scale8_to_h(const float* v, float s) {
+  h8_t h;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) h[e] = (_Float16)(v[e] * s);
+  return h;
+}
+
+// Eight 16-bit activations (bf16 or fp16 bits in a uint4) as fp32 (exact).
+SLIM_DEV void act8_to_f(u32x4_t v, bool is_bf16, float* f) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (is_bf16) {
+      f[2 * i] = __builtin_bit_cast(float, v[i] << 16);
+      f[2 * i + 1] = __builtin_bit_cast(float, v[i] & 0xFFFF0000u);
+    } else {
+      f[2 * i] = (float)__builtin_bit_cast(_Float16, (uint16_t)(v[i] & 0xFFFFu));
+      f[2 * i + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(v[i] >> 16));
+    }
+  }
+}
+
+SLIM_DEV uint32_t max_abs_bits8(const float* f) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) m = max(m, abs_bits(f[e]));
+  return m;
+}
+
 // bf16 bits -> fp16 (through fp32; exact for |x| in [2^-14, 65504]).
 SLIM_DEV _Float16 bf16_to_h(uint32_t b) { return (_Float16)__builtin_bit_cast(float, b << 16); }
 

@@ -41,9 +41,12 @@ struct SlimPlan {
   int64_t sp_blocks = 0;              // small M: sparse blocks
   int64_t sp_chunks_per_split = 0;    // 128-wide chunks per split
   size_t lds_bytes = 0;               // dynamic LDS (unused: the kernels size their LDS statically)
+  // large M: activations scaled per row into an fp16 copy (set by slim_check_linear: every
+  // backward, bf16 activations, or an adapter; fp16 activations without one stream as given)
+  bool scaled = false;
   // workspace layout (byte offsets)
   size_t off_counters = 0, n_counters = 0;
-  size_t off_t = 0, off_tpart = 0, off_ypart = 0, off_x16 = 0, off_pb = 0, total = 0;
+  size_t off_t = 0, off_tpart = 0, off_ypart = 0, off_x16 = 0, off_rowinv = 0, off_pb = 0, total = 0;
 };
 
 // Forward (bwd == false: rows = N, red = K) or backward (bwd == true: rows = K, red = N) plan.

@@ -54,7 +54,9 @@ struct LayerArgs {
                            // slim_pack_adapter) or row-major (backward, L as given)
   int p_tiled;             // ad_p is in 32 x 16 tiles
   const uint16_t* ad_pb;   // large M: the factor in 32 x 16 tiles (ad_p, or a re-laid copy)
-  uint16_t* tm;            // fp16 adapter intermediate: row-major [M, r] (small M), 32 x 16 tiles (large M)
+  uint16_t* tm;            // large M: fp16 adapter intermediate (scaled rows) in 32 x 16 tiles
+  float* tm32;             // small M: fp32 adapter intermediate, row-major [M, r]
+  const float* rowinv;     // large M: 2^-e per activation row (the rows were scaled by 2^e), or null
   float* out;              // [M, rows]
   // small-M path
   int split;               // reduction splits of the sparse product
@@ -72,17 +74,6 @@ struct LayerArgs {
 
 SLIM_DEV u32x4_t zero_u4() { return u32x4_t{0u, 0u, 0u, 0u}; }
 SLIM_DEV int64_t clamp_hi(int64_t x, int64_t hi) { return x < hi ? x : hi; }
-
-// bits of eight fp16 scales times eight activations (backward fold), rounded once to fp16.
-SLIM_DEV h8_t act8_scaled(u32x4_t v, u32x4_t sv, bool bf16) {
-  h8_t h;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    h[2 * i] = (_Float16)(act_to_f(v[i] & 0xFFFFu, bf16) * h_bits_to_f(sv[i] & 0xFFFFu));
-    h[2 * i + 1] = (_Float16)(act_to_f(v[i] >> 16, bf16) * h_bits_to_f(sv[i] >> 16));
-  }
-  return h;
-}
 
 // Reduce the split partials of one adapter column block, run by wave 0 of each unit (the unit's
 // sum is in its registers): every unit stores its FM x 4 accumulator values per lane (device
@@ -182,14 +173,48 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
     xv[i] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(m, a.M - 1) * a.red + pos);
     if (BWD) sv[i] = *reinterpret_cast<const u32x4_t*>(a.scales + sgroup * a.red + pos);
   }
+  // The staged B operand in fp32: the activations, in the backward times the fp16 scales of the
+  // block's 128-row group (the product is formed exactly in fp32 and rounded once, below).
+  // Vector i of thread tid belongs to row m = q / VPR (q = tid + 256 i), which is
+  // wave / G + (4 / G) i: all 64 lanes of a wave share the row of each i, and G waves hold one row.
+  float xf[XV][8];
+  uint32_t mx[XV];
 #pragma unroll
   for (int i = 0; i < XV; ++i) {
     const int q = tid + 256 * i, m = q / VPR, vc = q % VPR;
     const bool ok = m < a.M && red0 + 8 * vc < a.red;
-    const h8_t h = BWD ? act8_scaled(xv[i], sv[i], bf16) : load8_as_h(xv[i], bf16);
-    *reinterpret_cast<h8_t*>(&xs[m * LDX + 8 * vc]) = ok ? h : zero_h8();
+    act8_to_f(xv[i], bf16, xf[i]);
+    if (BWD) {
+      float sf[8];
+      act8_to_f(sv[i], false, sf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xf[i][e] *= sf[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) xf[i][e] = ok ? xf[i][e] : 0.f;
+    mx[i] = wave_max_u32(max_abs_bits8(xf[i]));
+  }
+  // per-row scaling over this slice (see act_exponent): the G waves of a row combine their maxima
+  __shared__ uint32_t rpart[4][XV];
+  __shared__ float runscale[MC];
+  if (lane == 0)
+#pragma unroll
+    for (int i = 0; i < XV; ++i) rpart[wave][i] = mx[i];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < XV; ++i) {
+    const int q = tid + 256 * i, m = q / VPR, vc = q % VPR;
+    uint32_t rm = 0;
+#pragma unroll
+    for (int g2 = 0; g2 < G; ++g2) rm = max(rm, rpart[(wave / G) * G + g2][i]);
+    const int e = act_exponent(rm);
+    if (lane == 0 && wave % G == 0) runscale[m] = exp2i(-e);
+    *reinterpret_cast<h8_t*>(&xs[m * LDX + 8 * vc]) = scale8_to_h(xf[i], exp2i(e));
   }
   __syncthreads();
+  float unscale[FM];
+#pragma unroll
+  for (int f = 0; f < FM; ++f) unscale[f] = runscale[16 * f + (lane & 15)];
 
   const int qb = lane >> 4;
   const int pbase = 128 * G * (qb >> 1) + 8 * (qb & 1);
@@ -226,7 +251,7 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
       }
     }
 #pragma unroll
-    for (int f = 0; f < FM; ++f) out[k][f] = acc[f];
+    for (int f = 0; f < FM; ++f) out[k][f] = acc[f] * unscale[f];   // lane (m + 16 (row / 4)): column m = lane % 16
   }
 
 #pragma unroll
@@ -292,15 +317,35 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
         aq[t][f] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.red + rk);
       bq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_q + jl * a.red + rk);
     }
+    // this round's activations of row m = 16 f + lane % 16, scaled per row (see act_exponent): the
+    // four lane groups of a row exchange their maxima; the round's product is unscaled in fp32
 #pragma unroll
-    for (int t = 0; t < kSteps; ++t) {
-      const bool kok = rs + 32 * t + 8 * g < a.red;
-      const h8_t bv = (kok && jcol < a.r) ? __builtin_bit_cast(h8_t, bq[t]) : zero_h8();
+    for (int f = 0; f < FM; ++f) {
+      const bool mok = 16 * f + (lane & 15) < a.M;
+      float xf[kSteps][8];
+      uint32_t mx = 0;
 #pragma unroll
-      for (int f = 0; f < FM; ++f) {
-        const h8_t av = (16 * f + (lane & 15) < a.M) ? load8_as_h(aq[t][f], bf16) : zero_h8();
-        acc[f] = mfma16(av, bv, acc[f]);
+      for (int t = 0; t < kSteps; ++t) {
+        const bool ok = mok && rs + 32 * t + 8 * g < a.red;
+        act8_to_f(aq[t][f], bf16, xf[t]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xf[t][e] = ok ? xf[t][e] : 0.f;
+        mx = max(mx, max_abs_bits8(xf[t]));
       }
+      mx = max(mx, (uint32_t)__shfl_xor((int)mx, 16, 64));
+      mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32, 64));
+      const int e = act_exponent(mx);
+      const float sc = exp2i(e), inv = exp2i(-e);
+      f4_t racc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < kSteps; ++t) {
+        const bool kok = rs + 32 * t + 8 * g < a.red;
+        const h8_t bv = (kok && jcol < a.r) ? __builtin_bit_cast(h8_t, bq[t]) : zero_h8();
+        racc = mfma16(scale8_to_h(xf[t], sc), bv, racc);
+      }
+      // D[m][j]: lane (j + 16 (m / 4)), element m % 4; row 16 f + 4 g + v's factor sits in lane 4 g + v
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[f][v] += racc[v] * __shfl(inv, 4 * g + v, 64);
     }
   }
   // the unit's sum: waves 1..3 hand theirs to wave 0 through LDS
@@ -320,7 +365,7 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
 #pragma unroll
     for (int vv = 0; vv < 4; ++vv) {
       const int64_t m = 16 * f + 4 * g + vv;
-      if (m < a.M && jcol < a.r) a.tm[m * a.r + jcol] = __builtin_bit_cast(uint16_t, (_Float16)acc[f][vv]);
+      if (m < a.M && jcol < a.r) a.tm32[m * a.r + jcol] = acc[f][vv];
     }
 }
 
@@ -354,7 +399,7 @@ __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
 // eight splits, a rank within the waves' first passes).
 template <int FM, int kSteps>
 SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lrow, int lane, u32x4_t* aq,
-                                   u32x4_t (*bq)[FM]) {
+                                   u32x4_t (*bq)[FM][2]) {
   const int g = lane >> 4;
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
@@ -364,24 +409,55 @@ SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lr
                                  : lrow * a.r + jj;
     aq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_p + po);
 #pragma unroll
-    for (int f = 0; f < FM; ++f)
-      bq[t][f] = *reinterpret_cast<const u32x4_t*>(a.tm + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.r + jj);
+    for (int f = 0; f < FM; ++f) {
+      const float* tp = a.tm32 + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.r + jj;
+      bq[t][f][0] = *reinterpret_cast<const u32x4_t*>(tp);
+      bq[t][f][1] = *reinterpret_cast<const u32x4_t*>(tp + 4);
+    }
   }
 }
 
+// One rank pass of the second product: T (fp32) of row m = 16 f + lane % 16 is scaled per row over
+// the pass (see act_exponent; the four lane groups of a row exchange their maxima), rounded to
+// fp16, multiplied on the MFMA and unscaled in fp32. D[row][m] sits in lane m + 16 (row / 4), so
+// each lane unscales with its own row's factor.
 template <int FM, int kSteps>
 SLIM_DEV void finish_adapter_mfma(const LayerArgs& a, int64_t jbase, int lane, const u32x4_t* aq,
-                                  const u32x4_t (*bq)[FM], f4_t* acc) {
+                                  const u32x4_t (*bq)[FM][2], f4_t* acc) {
   const int g = lane >> 4;
 #pragma unroll
-  for (int t = 0; t < kSteps; ++t) {
-    const bool jok = jbase + 32 * t + 8 * g < a.r;
-    const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[t]) : zero_h8();
+  for (int f = 0; f < FM; ++f) {
+    const bool mok = 16 * f + (lane & 15) < a.M;
+    uint32_t mx = 0;
 #pragma unroll
-    for (int f = 0; f < FM; ++f) {
-      const h8_t bv = (16 * f + (lane & 15) < a.M) ? __builtin_bit_cast(h8_t, bq[t][f]) : zero_h8();
-      acc[f] = mfma16(av, bv, acc[f]);
+    for (int t = 0; t < kSteps; ++t) {
+      const bool ok = mok && jbase + 32 * t + 8 * g < a.r;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mx = max(mx, ok ? (bq[t][f][h][e] & 0x7FFFFFFFu) : 0u);
     }
+    mx = max(mx, (uint32_t)__shfl_xor((int)mx, 16, 64));
+    mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32, 64));
+    const int e = act_exponent(mx);
+    const float sc = exp2i(e), inv = exp2i(-e);
+    f4_t pacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < kSteps; ++t) {
+      const bool jok = jbase + 32 * t + 8 * g < a.r;
+      const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[t]) : zero_h8();
+      // whole-vector casts: hipcc (ROCm 7.2) compiles __builtin_bit_cast(float, v[e]) of a vector
+      // element lvalue as a read of element 0 for every e
+      const f4_t lo = __builtin_bit_cast(f4_t, bq[t][f][0]) * sc, hi = __builtin_bit_cast(f4_t, bq[t][f][1]) * sc;
+      h8_t bv;
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        bv[e2] = (_Float16)lo[e2];
+        bv[4 + e2] = (_Float16)hi[e2];
+      }
+      pacc = mfma16(av, (mok && jok) ? bv : zero_h8(), pacc);
+    }
+    acc[f] = acc[f] + pacc * inv;
   }
 }
 
@@ -399,7 +475,7 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
   const int S = a.split;
   const rsrc_t pr = make_rsrc(a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256), ((int64_t)(S - 1) * 4 + 1) * FM * 256 * 4);
   const int64_t jfirst = (int64_t)h * 32 * kSteps;
-  u32x4_t aq[kSteps], bq[kSteps][FM];
+  u32x4_t aq[kSteps], bq[kSteps][FM][2];
   if (a.r > 0) finish_adapter_loads<FM, kSteps>(a, jfirst, lrow, lane, aq, bq);
   f4_t acc[FM];
 #pragma unroll
@@ -806,11 +882,13 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
     __builtin_amdgcn_s_waitcnt(0);
   }
 
-  // D[i][j] of a 32x32 fragment: lane j + 32 * ((i / 4) % 2), element 4 * (i / 8) + i % 4
+  // D[i][j] of a 32x32 fragment: lane j + 32 * ((i / 4) % 2), element 4 * (i / 8) + i % 4; column
+  // m's activation row was scaled by 2^e (k_rowprep), so its results are multiplied by 2^-e
 #pragma unroll
   for (int fm = 0; fm < kFm; ++fm) {
     const int64_t m = m0 + 32 * fm + (lane & 31);
     if (m >= a.M) continue;
+    const float inv = a.rowinv ? a.rowinv[m] : 1.0f;
 #pragma unroll
     for (int fn = 0; fn < 4; ++fn)
 #pragma unroll
@@ -818,7 +896,7 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
         const int64_t rr = wrow0 + 32 * fn + 8 * q + 4 * ha;
         if (rr < a.rows) {
           const f4_t o = {acc[fn][fm][4 * q], acc[fn][fm][4 * q + 1], acc[fn][fm][4 * q + 2], acc[fn][fm][4 * q + 3]};
-          *reinterpret_cast<f4_t*>(a.out + m * a.rows + rr) = o;
+          *reinterpret_cast<f4_t*>(a.out + m * a.rows + rr) = o * inv;
         }
       }
   }
@@ -829,11 +907,61 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
   tile_body<BWD, TC>(a);
 }
 
-// bf16 -> fp16 (round to nearest even), 8 values per thread
-__global__ void __launch_bounds__(256) k_bf16_to_f16(const u32x4_t* __restrict__ src, u32x4_t* __restrict__ dst,
-                                                     int64_t n8) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n8) dst[i] = __builtin_bit_cast(u32x4_t, load8_as_h(src[i], true));
+// Large-M activation preparation, one block per row m of act [M, red] (bf16 or fp16): the row's
+// largest magnitude gives its scaling exponent e (act_exponent); the row times 2^e, rounded to
+// fp16, goes to act16 (the copy the adapter GEMM and the tile kernel stream) and 2^-e to
+// rowinv[m]. Rows of up to 256 x NR vectors of 8 (NR > 0) stay in registers between the two
+// passes; longer rows (NR == 0) are read twice (the second read mostly from L2).
+constexpr int kRowRegs = 16;
+template <bool BF16, int NR>
+__global__ void __launch_bounds__(256) k_rowprep(const u32x4_t* __restrict__ act, int64_t nv, u32x4_t* __restrict__ act16,
+                                                 float* __restrict__ rowinv) {
+  constexpr int kR = NR > 0 ? NR : 1;
+  __shared__ uint32_t wmax[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t row = blockIdx.x;
+  const u32x4_t* src = act + row * nv;
+  u32x4_t* dst = act16 + row * nv;
+  constexpr bool regs = NR > 0;
+  u32x4_t v[kR];
+  uint32_t mx = 0;
+  if (regs) {
+#pragma unroll
+    for (int i = 0; i < kR; ++i) v[i] = src[clamp_hi(tid + 256 * i, nv - 1)];
+#pragma unroll
+    for (int i = 0; i < kR; ++i) {
+      float f[8];
+      act8_to_f(v[i], BF16, f);
+      if (tid + 256 * i < nv) mx = max(mx, max_abs_bits8(f));
+    }
+  } else {
+    for (int64_t i = tid; i < nv; i += 256) {
+      float f[8];
+      act8_to_f(src[i], BF16, f);
+      mx = max(mx, max_abs_bits8(f));
+    }
+  }
+  mx = wave_max_u32(mx);
+  if (lane == 0) wmax[wave] = mx;
+  __syncthreads();
+  mx = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
+  const int e = act_exponent(mx);
+  const float sc = exp2i(e);
+  if (tid == 0) rowinv[row] = exp2i(-e);
+  if (regs) {
+#pragma unroll
+    for (int i = 0; i < kR; ++i) {
+      float f[8];
+      act8_to_f(v[i], BF16, f);
+      if (tid + 256 * i < nv) dst[tid + 256 * i] = __builtin_bit_cast(u32x4_t, scale8_to_h(f, sc));
+    }
+  } else {
+    for (int64_t i = tid; i < nv; i += 256) {
+      float f[8];
+      act8_to_f(src[i], BF16, f);
+      dst[i] = __builtin_bit_cast(u32x4_t, scale8_to_h(f, sc));
+    }
+  }
 }
 
 // Adapter tiles for the tile kernel's epilogue, one launch with two kinds of block:
@@ -920,18 +1048,34 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
     }
     return SLIM_OK;
   }
-  if (act_bf16 && a.r == 0) {
-    // the tile kernel streams fp16 activations straight into LDS: convert them once (with an
-    // adapter, its first product's GEMM reads the bf16 activations and writes the copy)
-    SlimKernelTimer timer("to_f16", s);
-    const int64_t n8 = a.M * a.red / 8;
-    SLIM_LAUNCH(timer, k_bf16_to_f16, dim3((unsigned)((n8 + 255) / 256)), dim3(256), s,
-                reinterpret_cast<const u32x4_t*>(act), reinterpret_cast<u32x4_t*>(const_cast<uint16_t*>(a.act16)), n8);
+  if (a.rowinv) {
+    // scale each activation row into the fp16 copy the adapter GEMM and the tile kernel stream
+    SlimKernelTimer timer("rowprep", s);
+    const int64_t nv = a.red / 8;
+    const dim3 grid((unsigned)a.M);
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(const_cast<uint16_t*>(a.act16));
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(act);
+    float* rinv = const_cast<float*>(a.rowinv);
+    const int nr = nv <= 512 ? 2 : nv <= 1024 ? 4 : nv <= 2048 ? 8 : nv <= 256 * kRowRegs ? 16 : 0;
+#define SLIM_ROWPREP(B, NR) SLIM_LAUNCH(timer, (k_rowprep<B, NR>), grid, dim3(256), s, src, nv, dst, rinv)
+    if (act_bf16) {
+      if (nr == 2) SLIM_ROWPREP(true, 2);
+      else if (nr == 4) SLIM_ROWPREP(true, 4);
+      else if (nr == 8) SLIM_ROWPREP(true, 8);
+      else if (nr == 16) SLIM_ROWPREP(true, 16);
+      else SLIM_ROWPREP(true, 0);
+    } else {
+      if (nr == 2) SLIM_ROWPREP(false, 2);
+      else if (nr == 4) SLIM_ROWPREP(false, 4);
+      else if (nr == 8) SLIM_ROWPREP(false, 8);
+      else if (nr == 16) SLIM_ROWPREP(false, 16);
+      else SLIM_ROWPREP(false, 0);
+    }
+#undef SLIM_ROWPREP
     if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
   }
   if (a.r > 0) {
-    int st = slim_launch_adapter_gemm(act_bf16 ? act : a.act16, act_bf16, a.M, a.red, a.ad_q, a.r, p, ws,
-                                      const_cast<uint16_t*>(a.act16), s);
+    int st = slim_launch_adapter_gemm(a.act16, a.M, a.red, a.ad_q, a.r, p, ws, s);
     if (st != SLIM_OK) return st;
     // the factor needs re-laying only when given row-major (backward); tm needs summing only
     // when the GEMM split its reduction
@@ -971,7 +1115,11 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.p_tiled = p_tiled;
   a.ad_pb = p.decode ? nullptr : (p_tiled ? ad_p : reinterpret_cast<const uint16_t*>(ws + p.off_pb));
   a.tm = reinterpret_cast<uint16_t*>(ws + p.off_t);
-  a.act16 = (!p.decode && dtype == SLIM_BF16) ? reinterpret_cast<const uint16_t*>(ws + p.off_x16) : a.act;
+  a.tm32 = reinterpret_cast<float*>(ws + p.off_t);
+  // large M: the activations are scaled per row into an fp16 copy (p.scaled), except fp16
+  // activations of a forward without an adapter, which the tile kernel streams as they are
+  a.act16 = p.scaled ? reinterpret_cast<const uint16_t*>(ws + p.off_x16) : a.act;
+  a.rowinv = p.scaled ? reinterpret_cast<const float*>(ws + p.off_rowinv) : nullptr;
   a.out = out;
   a.split = p.sp_split;
   a.row_tiles = p.sp_row_tiles;

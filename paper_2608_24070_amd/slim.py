@@ -18,8 +18,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libslim.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "slim.h")
 
-SLIM_OK = 0
-SLIM_F16, SLIM_BF16 = 0, 1
+# slim_status and slim_dtype of include/slim.h (a CPU test checks them against the header)
+(SLIM_OK, SLIM_EINVAL, SLIM_ESHAPE, SLIM_EDTYPE, SLIM_EALIGN, SLIM_ENONFINITE, SLIM_EWORKSPACE, SLIM_EDEVICE,
+ SLIM_EUNSUPPORTED, SLIM_ERANGE) = range(10)
+SLIM_F16, SLIM_BF16, SLIM_F32 = 0, 1, 2
 
 _c_i64 = ctypes.c_int64
 _c_p = ctypes.c_void_p

@@ -47,12 +47,17 @@ def weights(n: int, k: int, seed: int = 0, name: str = "W", std: float = 0.02) -
 
 
 def activations(m: int, k: int, seed: int = 0, name: str = "X", dtype: str = "bf16",
-                outliers: bool = False) -> tuple[np.ndarray, np.ndarray]:
-    """Returns (bits uint16 [m, k], values float64 [m, k]) for dtype 'bf16' or 'fp16'."""
+                outliers: bool = False, scale: float = 1.0) -> tuple[np.ndarray, np.ndarray]:
+    """Returns (bits uint16 [m, k], values float64 [m, k]) for dtype 'bf16' or 'fp16'.
+
+    ``scale`` multiplies the N(0, 1) draws (in float32) before the cast: gradient-sized inputs
+    (1e-3 .. 1e-7) or activations beyond the fp16 range (1e6 in bf16)."""
     x = stream(seed, name).standard_normal((m, k), dtype=np.float32)
     if outliers:
         ch = stream(seed, name + "/outlier_channels").choice(k, size=int(0.01 * k), replace=False)
         x[:, ch] *= np.float32(20.0)
+    if scale != 1.0:
+        x *= np.float32(scale)
     if dtype == "bf16":
         bits = bf16_bits(x)
         return bits, bf16_to_f64(bits)

@@ -66,9 +66,9 @@ def oracle_pack_on_device(p, n, k):
             "scales": dev(block(p["scales"], 0).view(np.int16)), "N": n, "K": k}
 
 
-def layer_inputs(n, k, r, m, seed=0, xdtype="bf16", outliers=False, name="layer"):
+def layer_inputs(n, k, r, m, seed=0, xdtype="bf16", outliers=False, name="layer", xscale=1.0):
     W = synth.weights(n, k, seed=seed, name=name + "/W")
-    xbits, X = synth.activations(m, k, seed=seed, name=name + "/X", dtype=xdtype, outliers=outliers)
+    xbits, X = synth.activations(m, k, seed=seed, name=name + "/X", dtype=xdtype, outliers=outliers, scale=xscale)
     Lb, Rb, L, R = synth.adapter(k, n, max(r, 16), seed=seed, name=name + "/")
     if r == 0:
         Lb = Rb = L = R = None

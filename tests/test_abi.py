@@ -1,6 +1,7 @@
 """libslim loads, exports every entry point of include/slim.h, and rejects bad arguments on the
 host before touching a GPU (no compute call here needs a device)."""
 import ctypes
+import re
 
 import pytest
 
@@ -21,7 +22,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert slim.slim_abi_version() == 1
+    assert slim.slim_abi_version() == 2
     for code in range(10):
         assert slim.status_string(code).startswith("SLIM_")
     assert "unknown" in slim.status_string(99)
@@ -73,8 +74,8 @@ def test_linear_validation_and_workspace():
     assert call(r=24) == 2
     assert call(M=0) == 2
     assert call(X=MIS) == 4
-    assert call(wsb=need - 1) == 7
-    assert call(ws=None) == 7
+    assert call(wsb=need - 1) == slim.SLIM_EWORKSPACE
+    assert call(ws=None) == slim.SLIM_EWORKSPACE
 
 
 def test_bwd_workspace_and_shape_rules():
@@ -101,7 +102,7 @@ def test_sizes_past_32bit_offsets_are_refused():
         slim.slim_linear_workspace(1 << 21, 16, 128, 512)          # M r = 2^30
     with pytest.raises(slim.SlimError):
         slim.slim_linear_workspace(64, 1 << 21, 128, 512)          # N r = 2^30
-    assert slim.slim_linear(A, 1, 64, 16, big, A, A, A, None, None, 0, A, A, 1 << 30, None) == 9
+    assert slim.slim_linear(A, 1, 64, 16, big, A, A, A, None, None, 0, A, A, 1 << 30, None) == slim.SLIM_EUNSUPPORTED
 
 
 @pytest.mark.parametrize("M,N,K,r", [(1, 4096, 4096, 384), (16, 4096, 4096, 384), (2048, 11008, 4096, 384),
@@ -126,4 +127,13 @@ def test_workspace_holds_counter_region_and_data(M, N, K, r):
 
 
 def test_workspace_init_requires_counter_region():
-    assert slim.slim_workspace_init(A, COUNTER_REGION - 4, None) == 7   # SLIM_EWORKSPACE, before any GPU call
+    assert slim.slim_workspace_init(A, COUNTER_REGION - 4, None) == slim.SLIM_EWORKSPACE   # before any GPU call
+
+
+def test_binding_constants_match_header_enums():
+    text = open(slim.HEADER).read()
+    enums = dict((k, int(v)) for k, v in re.findall(r"\b(SLIM_[A-Z0-9]+)\s*=\s*(\d+)", text))
+    assert len(enums) == 13
+    for name, value in enums.items():
+        assert getattr(slim, name) == value, name
+    assert int(re.search(r"#define SLIM_ABI_VERSION (\d+)", text).group(1)) == slim.slim_abi_version()

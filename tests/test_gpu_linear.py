@@ -12,9 +12,10 @@ pytestmark = pytest.mark.gpu
 
 
 def _fwd_case(n, k, r, m, xdtype="bf16", outliers=False, seed=0, rows=None, ms=None, name="layer",
-              use_oracle_pack=False):
-    print(f"fwd n={n} k={k} r={r} m={m} {xdtype} outliers={outliers} seed={seed}", flush=True)
-    W, X, L, R, dx, ad = layer_inputs(n, k, r, m, seed=seed, xdtype=xdtype, outliers=outliers, name=name)
+              use_oracle_pack=False, xscale=1.0):
+    print(f"fwd n={n} k={k} r={r} m={m} {xdtype} outliers={outliers} seed={seed} xscale={xscale}", flush=True)
+    W, X, L, R, dx, ad = layer_inputs(n, k, r, m, seed=seed, xdtype=xdtype, outliers=outliers, name=name,
+                                      xscale=xscale)
     if use_oracle_pack:
         p = oracle_pack_on_device(O.pack(W), n, k)
     else:
@@ -169,10 +170,10 @@ def test_pack_adapter_is_exact_transpose(k, n, r):
 
 # ------------------------------------------------------------------------------ backward
 
-def _bwd_case(n, k, r, m, seed=0, ks=None, ms=None, name="bwd", dydtype="bf16"):
-    print(f"bwd n={n} k={k} r={r} m={m} seed={seed}", flush=True)
+def _bwd_case(n, k, r, m, seed=0, ks=None, ms=None, name="bwd", dydtype="bf16", dyscale=1.0):
+    print(f"bwd n={n} k={k} r={r} m={m} seed={seed} {dydtype} dyscale={dyscale}", flush=True)
     W = synth.weights(n, k, seed=seed, name=name + "/W")
-    dybits, dY = synth.activations(m, n, seed=seed, name=name + "/dY", dtype=dydtype)
+    dybits, dY = synth.activations(m, n, seed=seed, name=name + "/dY", dtype=dydtype, scale=dyscale)
     Lb, Rb, L, R = synth.adapter(k, n, max(r, 16), seed=seed, name=name + "/")
     if r == 0:
         L = R = dL = dR = None
@@ -257,3 +258,56 @@ def test_decode_counters_return_to_zero():
         assert torch.equal(Y0, Y1) and torch.equal(D0, D1), m
         assert Y2.shape == (m, 2048) and dx.shape[0] == 32
         assert int(ws[:COUNTER_BYTES].count_nonzero()) == 0, m
+
+
+# ------------------------------------------------------------ magnitudes outside fp16's range
+# The kernels scale each activation row by a power of two before rounding it to fp16, so
+# gradient-sized dY (products dY * s16 far below fp16's normal range) and bf16 activations beyond
+# fp16's maximum stay within the gate.
+
+@pytest.mark.parametrize("m,dydtype,dyscale", [(16, "bf16", 1e-3), (16, "bf16", 1e-5), (1, "bf16", 1e-7),
+                                               (27, "fp16", 1e-4), (200, "bf16", 1e-3), (200, "bf16", 1e-5),
+                                               (96, "fp16", 1e-5), (64, "bf16", 1e-7)])
+def test_bwd_gradient_magnitudes(m, dydtype, dyscale):
+    _bwd_case(1024, 512, 32, m, name="gradmag", dydtype=dydtype, dyscale=dyscale)
+
+
+@pytest.mark.parametrize("m,r", [(16, 0), (200, 0)])
+def test_bwd_gradient_magnitudes_no_adapter(m, r):
+    _bwd_case(1024, 512, r, m, name="gradmag0", dyscale=1e-5)
+
+
+def test_bwd_gradient_magnitudes_mlp70b_sampled():
+    # the 70B shape at gradient size on both paths, sampled K groups
+    _bwd_case(28672, 8192, 512, 16, seed=1, ks=(0, 40), name="mlp70b", dyscale=1e-5)
+    ms = np.sort(synth.stream(1, "gms").choice(512, size=16, replace=False))
+    _bwd_case(28672, 8192, 512, 512, seed=1, ks=(7, 63), ms=ms, name="mlp70b", dyscale=1e-5)
+
+
+@pytest.mark.parametrize("m,r,xscale", [(16, 32, 1e6), (16, 32, 1e-6), (1, 0, 1e6), (20, 48, 3e4),
+                                        (200, 32, 1e6), (200, 32, 1e-6), (100, 0, 1e6), (96, 0, 1e-6)])
+def test_forward_activations_beyond_fp16_range(m, r, xscale):
+    _fwd_case(1024, 2048, r, m, name="xmag", xscale=xscale)
+
+
+@pytest.mark.parametrize("m", [16, 200])
+def test_forward_fp16_small_activations(m):
+    # fp16 activations of 1e-5 (near fp16's subnormal range) with an adapter: the adapter's
+    # intermediate X L is scaled with the rows
+    _fwd_case(1024, 2048, 64, m, xdtype="fp16", name="xmag16", xscale=1e-5)
+
+
+# ------------------------------------------------------------ every configuration's shapes
+
+@pytest.mark.parametrize("n,k", [(5120, 5120), (13824, 5120)])
+def test_block13b_q_and_gate_sampled(n, k):
+    rows = np.sort(synth.stream(8, "rows").choice(n, size=512, replace=False))
+    ms = np.sort(synth.stream(8, "ms").choice(4096, size=48, replace=False))
+    _fwd_case(n, k, 512, 4096, rows=rows, ms=ms, name=f"b13_{n}x{k}")
+
+
+@pytest.mark.parametrize("m,seed", [(16, 1), (16, 2), (8192, 1), (8192, 2)])
+def test_mlp70b_fwd_seeds_sampled(m, seed):
+    rows = np.sort(synth.stream(10 + seed, "rows").choice(28672, size=384, replace=False))
+    ms = None if m <= 16 else np.sort(synth.stream(10 + seed, "ms").choice(m, size=24, replace=False))
+    _fwd_case(28672, 8192, 512, m, seed=seed, rows=rows, ms=ms, name="mlp70b")

@@ -47,7 +47,7 @@ def test_pack_zero_and_tiny_groups():
     _check_pack(W)
 
 
-@pytest.mark.parametrize("n,k", [(11008, 4096), (28672, 8192)])
+@pytest.mark.parametrize("n,k", [(11008, 4096), (28672, 8192), (5120, 5120), (13824, 5120), (5120, 13824)])
 def test_pack_full_size_sampled_rows(n, k):
     print(f"pack full n={n} k={k}", flush=True)
     W = synth.weights(n, k, seed=0)
@@ -69,15 +69,15 @@ def test_pack_rejects_nonfinite_and_overflow():
     W[2, 17] = np.nan
     with pytest.raises(slim.SlimError) as e:
         slim.pack(dev(W))
-    assert e.value.status == 5
+    assert e.value.status == slim.SLIM_ENONFINITE
     W[2, 17] = np.inf
     with pytest.raises(slim.SlimError) as e:
         slim.pack(dev(W))
-    assert e.value.status == 5
+    assert e.value.status == slim.SLIM_ENONFINITE
     W[2, 17] = 7.0 * 65520.0
     with pytest.raises(slim.SlimError) as e:
         slim.pack(dev(W))
-    assert e.value.status == 6
+    assert e.value.status == slim.SLIM_ERANGE
 
 
 @pytest.mark.parametrize("n,k,tied", [(512, 512, False), (128, 384, True), (4096, 4096, False)])
@@ -111,3 +111,17 @@ def test_double_pruning_statistic_on_device():
     b = slim.pack_bwd(p, with_mask=True)
     extra = (p["mask"].sum().item() - b["mask_rc"].sum().item()) / (n * k)
     assert abs(extra - O.lemma_extra_sparsity(2, 4)) < 1e-3
+
+
+def test_pack_bwd_rejects_scales_the_backward_cannot_hold():
+    # the large-M backward multiplies gradients row-scaled below 32 by s16 in fp16: a forward scale
+    # of 2048 or more (group max |w| >= 14336) is refused; 2047 is accepted
+    n, k = 128, 256
+    W = synth.weights(n, k, seed=9)
+    W[5, 130] = np.float32(7.0 * 2047.0)
+    b = slim.pack_bwd(slim.pack(dev(W)))
+    assert host(b["scalesT"]).view(np.float16)[1, 5] == np.float16(2047.0)
+    W[5, 130] = np.float32(7.0 * 2048.0)
+    with pytest.raises(slim.SlimError) as e:
+        slim.pack_bwd(slim.pack(dev(W)))
+    assert e.value.status == slim.SLIM_ERANGE
