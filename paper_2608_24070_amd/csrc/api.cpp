@@ -94,7 +94,8 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
       q.ad_split = (int)cdiv(slices, q.ad_sub);
       if (q.ad_split > 1) {
         ad_counters = (size_t)q.ad_jblocks;
-        tpart_bytes = (size_t)q.ad_jblocks * q.ad_split * q.dec_fm * 256 * 4;
+        // per split and 16-row fragment: 256 fp32 partials and 16 row maxima
+        tpart_bytes = (size_t)q.ad_jblocks * q.ad_split * q.dec_fm * 272 * 4;
       }
     }
     if (q.sp_split > 1 || r > 0) ypart_bytes = (size_t)q.sp_row_tiles * q.sp_split * 4 * q.dec_fm * 256 * 4;
@@ -136,10 +137,11 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
   if (q.n_counters > kCounterSlots) return SLIM_EUNSUPPORTED;
   // the counter region has a fixed size so that it stays at zero across calls with other sizes
   size_t off = kCounterSlots * 4;
-  // T: fp32 row-major [M, r] at small M; at large M fp16 in 32 x 16 tiles ([ceil(M/32)][r/16][32][16],
-  // see adapter_gemm.hip), which the tile kernel's epilogue reads 1 KB at a time
+  // T (fp16, from row-scaled activations): row-major [M, r] at small M; at large M in 32 x 16 tiles
+  // ([ceil(M/32)][r/16][32][16], see adapter_gemm.hip), which the tile kernel's epilogue reads 1 KB
+  // at a time
   q.off_t = off;
-  off = round256(off + (q.decode ? (size_t)M * (size_t)r * 4 : (size_t)cdiv(M, 32) * 32 * (size_t)r * 2));
+  off = round256(off + (size_t)(q.decode ? M : cdiv(M, 32) * 32) * (size_t)r * 2);
   q.off_tpart = off;
   off = round256(off + tpart_bytes);
   q.off_ypart = off;
@@ -149,9 +151,10 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
   // [rows, r] re-laid in 32 x 16 tiles
   q.off_x16 = off;
   if (!q.decode) off = round256(off + (size_t)M * (size_t)red * 2);
-  // large M: 2^-e per activation row (the rows of the fp16 copy are scaled by 2^e)
+  // 2^-e per activation row: large M, the rows of the fp16 copy are scaled by 2^e; small M, the
+  // rows of T are
   q.off_rowinv = off;
-  if (!q.decode) off = round256(off + (size_t)M * 4);
+  off = round256(off + (size_t)M * 4);
   q.off_pb = off;
   if (!q.decode && bwd) off = round256(off + (size_t)cdiv(rows, 32) * 32 * (size_t)r * 2);
   q.total = off;

@@ -126,11 +126,24 @@ SLIM_DEV int act_exponent(uint32_t maxbits) {
 
 SLIM_DEV uint32_t abs_bits(float x) { return __builtin_bit_cast(uint32_t, x) & 0x7FFFFFFFu; }
 
-// Largest value over the 64 lanes of a wave (all lanes get it).
+// Largest value over the 64 lanes of a wave, returned wave-uniform: rotations within each row of
+// 16 lanes (DPP row_ror 1, 2, 4, 8) leave every lane with its row's maximum, and the four rows'
+// maxima are read into scalar registers.
 SLIM_DEV uint32_t wave_max_u32(uint32_t v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, off, 64));
-  return v;
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x121, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x122, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xF, 0xF, false));
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false));
+  const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v, 0), b = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+  const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v, 32), d = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+  return max(max(a, b), max(c, d));
+}
+
+// Largest value over the four lanes L % 16 + {0, 16, 32, 48} (lanes that share a column of an
+// MFMA operand), returned to each of them.
+SLIM_DEV uint32_t col4_max_u32(uint32_t v) {
+  v = max(v, (uint32_t)__shfl_xor((int)v, 16, 64));
+  return max(v, (uint32_t)__shfl_xor((int)v, 32, 64));
 }
 
 // Eight fp32 values times s (a power of two), rounded to fp16.
@@ -235,6 +248,8 @@ SLIM_DEV void st_dev4(rsrc_t r, uint32_t off, f4_t v) {
 SLIM_DEV f4_t ld_dev4(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(f4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolSc1));
 }
+SLIM_DEV void st_dev1(rsrc_t r, uint32_t off, uint32_t v) { __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, kCpolSc1); }
+SLIM_DEV uint32_t ld_dev1(rsrc_t r, uint32_t off) { return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kCpolSc1); }
 SLIM_DEV void drain_stores() { __builtin_amdgcn_s_waitcnt(0); }
 SLIM_DEV uint32_t counter_arrive(uint32_t* c) {
   return __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

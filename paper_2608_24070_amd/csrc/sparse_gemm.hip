@@ -54,8 +54,9 @@ struct LayerArgs {
                            // slim_pack_adapter) or row-major (backward, L as given)
   int p_tiled;             // ad_p is in 32 x 16 tiles
   const uint16_t* ad_pb;   // large M: the factor in 32 x 16 tiles (ad_p, or a re-laid copy)
-  uint16_t* tm;            // large M: fp16 adapter intermediate (scaled rows) in 32 x 16 tiles
-  float* tm32;             // small M: fp32 adapter intermediate, row-major [M, r]
+  uint16_t* tm;            // fp16 adapter intermediate of the row-scaled activations: row-major
+                           // [M, r] (small M), 32 x 16 tiles (large M)
+  float* trinv;            // small M: 2^-e per row of tm (written by the adapter units)
   const float* rowinv;     // large M: 2^-e per activation row (the rows were scaled by 2^e), or null
   float* out;              // [M, rows]
   // small-M path
@@ -77,15 +78,20 @@ SLIM_DEV int64_t clamp_hi(int64_t x, int64_t hi) { return x < hi ? x : hi; }
 
 // Reduce the split partials of one adapter column block, run by wave 0 of each unit (the unit's
 // sum is in its registers): every unit stores its FM x 4 accumulator values per lane (device
-// scope, one 16-byte store per fragment), the last one to arrive sums all S partials in split
-// order. A partial is [FM][64 lanes][4] fp32.
+// scope, one 16-byte store per fragment) and its per-row maxima of |activation| (16 words per
+// fragment), and the last one to arrive sums all S partials in split order and takes the maxima's
+// maximum. A partial is [FM][64 lanes][4] fp32; the maxima follow all S partials, [S][FM][16].
 template <int FM>
-SLIM_DEV bool split_reduce_wave(f4_t* acc, float* part, int S, int s, uint32_t* counter) {
+SLIM_DEV bool split_reduce_wave(f4_t* acc, uint32_t* amx, float* part, int S, int s, uint32_t* counter) {
   const int lane = threadIdx.x & 63;
-  const rsrc_t pr = make_rsrc(part, (int64_t)S * FM * 1024);
+  const rsrc_t pr = make_rsrc(part, (int64_t)S * FM * 1088);
   auto off = [&](int ss, int f) { return (uint32_t)(((ss * FM + f) * 256 + 4 * lane) * 4); };
+  auto moff = [&](int ss, int f) { return (uint32_t)(S * FM * 1024 + ((ss * FM + f) * 16 + (lane & 15)) * 4); };
 #pragma unroll
-  for (int f = 0; f < FM; ++f) st_dev4(pr, off(s, f), acc[f]);
+  for (int f = 0; f < FM; ++f) {
+    st_dev4(pr, off(s, f), acc[f]);
+    if (lane < 16) st_dev1(pr, moff(s, f), amx[f]);
+  }
   drain_stores();
   uint32_t prev = 0;
   if (lane == 0) prev = counter_arrive(counter);
@@ -95,17 +101,24 @@ SLIM_DEV bool split_reduce_wave(f4_t* acc, float* part, int S, int s, uint32_t* 
   constexpr int kR = 16 / FM;   // partials per load round
   for (int s0 = 0; s0 < S; s0 += kR) {
     f4_t pv[kR][FM];
+    uint32_t pm[kR][FM];
 #pragma unroll
     for (int j = 0; j < kR; ++j) {
       const int ss = s0 + j < S ? s0 + j : S - 1;
 #pragma unroll
-      for (int f = 0; f < FM; ++f) pv[j][f] = ld_dev4(pr, off(ss, f));
+      for (int f = 0; f < FM; ++f) {
+        pv[j][f] = ld_dev4(pr, off(ss, f));
+        pm[j][f] = ld_dev1(pr, moff(ss, f));
+      }
     }
 #pragma unroll
     for (int j = 0; j < kR; ++j)
       if (s0 + j < S)
 #pragma unroll
-        for (int f = 0; f < FM; ++f) acc[f] = acc[f] + pv[j][f];
+        for (int f = 0; f < FM; ++f) {
+          acc[f] = acc[f] + pv[j][f];
+          amx[f] = max(amx[f], pm[j][f]);
+        }
   }
   if (lane == 0) counter_reset(counter);
   return true;
@@ -165,51 +178,50 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
   DecodeWords<G> wb[NU > 1 ? 2 : 1];
   decode_load_words<BWD, G>(a, rt0, cl, lane, wave, wb[0]);
   const int64_t sgroup = rt0 * 64 / 128;
-  u32x4_t xv[XV], sv[XV];
+  // Activations of the slice: wave w stages rows m = w + 4 i (i < MC / 4), each row as G runs of 64
+  // lanes x 8 positions (position 8 (lane + 64 j)), so a wave holds whole rows: each row's scaling
+  // exponent is a reduction within one wave, with no exchange between waves.
+  constexpr int RW = MC / 4;                 // rows per wave
+  u32x4_t xv[RW][G], sv[G];
 #pragma unroll
-  for (int i = 0; i < XV; ++i) {
-    const int q = tid + 256 * i, m = q / VPR, vc = q % VPR;
-    const int64_t pos = clamp_hi(red0 + 8 * vc, a.red - 8);
-    xv[i] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(m, a.M - 1) * a.red + pos);
-    if (BWD) sv[i] = *reinterpret_cast<const u32x4_t*>(a.scales + sgroup * a.red + pos);
-  }
-  // The staged B operand in fp32: the activations, in the backward times the fp16 scales of the
-  // block's 128-row group (the product is formed exactly in fp32 and rounded once, below).
-  // Vector i of thread tid belongs to row m = q / VPR (q = tid + 256 i), which is
-  // wave / G + (4 / G) i: all 64 lanes of a wave share the row of each i, and G waves hold one row.
-  float xf[XV][8];
-  uint32_t mx[XV];
+  for (int i = 0; i < RW; ++i)
 #pragma unroll
-  for (int i = 0; i < XV; ++i) {
-    const int q = tid + 256 * i, m = q / VPR, vc = q % VPR;
-    const bool ok = m < a.M && red0 + 8 * vc < a.red;
-    act8_to_f(xv[i], bf16, xf[i]);
-    if (BWD) {
-      float sf[8];
-      act8_to_f(sv[i], false, sf);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) xf[i][e] *= sf[e];
+    for (int j = 0; j < G; ++j) {
+      const int64_t pos = clamp_hi(red0 + 8 * (lane + 64 * j), a.red - 8);
+      xv[i][j] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(wave + 4 * i, a.M - 1) * a.red + pos);
     }
+  if (BWD)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) xf[i][e] = ok ? xf[i][e] : 0.f;
-    mx[i] = wave_max_u32(max_abs_bits8(xf[i]));
-  }
-  // per-row scaling over this slice (see act_exponent): the G waves of a row combine their maxima
-  __shared__ uint32_t rpart[4][XV];
+    for (int j = 0; j < G; ++j)
+      sv[j] = *reinterpret_cast<const u32x4_t*>(a.scales + sgroup * a.red + clamp_hi(red0 + 8 * (lane + 64 * j), a.red - 8));
+  // The staged B operand in fp32: the activations, in the backward times the fp16 scales of the
+  // block's 128-row group (the product is formed exactly in fp32 and rounded once, below), scaled
+  // per row (see act_exponent).
   __shared__ float runscale[MC];
-  if (lane == 0)
 #pragma unroll
-    for (int i = 0; i < XV; ++i) rpart[wave][i] = mx[i];
-  __syncthreads();
+  for (int i = 0; i < RW; ++i) {
+    const int m = wave + 4 * i;
+    float xf[G][8];
+    uint32_t mx = 0;
 #pragma unroll
-  for (int i = 0; i < XV; ++i) {
-    const int q = tid + 256 * i, m = q / VPR, vc = q % VPR;
-    uint32_t rm = 0;
+    for (int j = 0; j < G; ++j) {
+      const bool ok = m < a.M && red0 + 8 * (lane + 64 * j) < a.red;
+      act8_to_f(xv[i][j], bf16, xf[j]);
+      if (BWD) {
+        float sf[8];
+        act8_to_f(sv[j], false, sf);
 #pragma unroll
-    for (int g2 = 0; g2 < G; ++g2) rm = max(rm, rpart[(wave / G) * G + g2][i]);
-    const int e = act_exponent(rm);
-    if (lane == 0 && wave % G == 0) runscale[m] = exp2i(-e);
-    *reinterpret_cast<h8_t*>(&xs[m * LDX + 8 * vc]) = scale8_to_h(xf[i], exp2i(e));
+        for (int e = 0; e < 8; ++e) xf[j][e] *= sf[e];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xf[j][e] = ok ? xf[j][e] : 0.f;
+      mx = max(mx, max_abs_bits8(xf[j]));
+    }
+    const int e = act_exponent(wave_max_u32(mx));
+    const float sc = exp2i(e);
+    if (lane == 0) runscale[m] = exp2i(-e);
+#pragma unroll
+    for (int j = 0; j < G; ++j) *reinterpret_cast<h8_t*>(&xs[m * LDX + 8 * (lane + 64 * j)]) = scale8_to_h(xf[j], sc);
   }
   __syncthreads();
   float unscale[FM];
@@ -303,8 +315,12 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
   const int64_t jl = clamp_hi(jcol, a.r - 1);
 
   f4_t acc[FM];
+  uint32_t amx[FM];   // largest |activation| of row 16 f + lane % 16 seen by this wave
 #pragma unroll
-  for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+  for (int f = 0; f < FM; ++f) {
+    acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+    amx[f] = 0u;
+  }
   // a.ad_sub consecutive slices of kAdSlice positions (one load round each)
   for (int sub = 0; sub < a.ad_sub; ++sub) {
     const int64_t rs = r0 + (int64_t)sub * kAdSlice;
@@ -332,41 +348,57 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
         for (int e = 0; e < 8; ++e) xf[t][e] = ok ? xf[t][e] : 0.f;
         mx = max(mx, max_abs_bits8(xf[t]));
       }
-      mx = max(mx, (uint32_t)__shfl_xor((int)mx, 16, 64));
-      mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32, 64));
+      mx = col4_max_u32(mx);
+      amx[f] = max(amx[f], mx);
       const int e = act_exponent(mx);
       const float sc = exp2i(e), inv = exp2i(-e);
+      // D[j][m] = sum_k Q[j][k] X[m][k] (A = the factor's rows, B = the scaled activations): lane
+      // (m + 16 (j / 4)) holds column m, so each lane unscales with its own row's factor
       f4_t racc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < kSteps; ++t) {
         const bool kok = rs + 32 * t + 8 * g < a.red;
-        const h8_t bv = (kok && jcol < a.r) ? __builtin_bit_cast(h8_t, bq[t]) : zero_h8();
-        racc = mfma16(scale8_to_h(xf[t], sc), bv, racc);
+        const h8_t qv = (kok && jcol < a.r) ? __builtin_bit_cast(h8_t, bq[t]) : zero_h8();
+        racc = mfma16(qv, scale8_to_h(xf[t], sc), racc);
       }
-      // D[m][j]: lane (j + 16 (m / 4)), element m % 4; row 16 f + 4 g + v's factor sits in lane 4 g + v
-#pragma unroll
-      for (int v = 0; v < 4; ++v) acc[f][v] += racc[v] * __shfl(inv, 4 * g + v, 64);
+      acc[f] = acc[f] + racc * inv;
     }
   }
-  // the unit's sum: waves 1..3 hand theirs to wave 0 through LDS
+  // the unit's sum: waves 1..3 hand theirs (and their maxima) to wave 0 through LDS
+  __shared__ uint32_t mx_lds[3][FM][64];
   if (wave > 0)
 #pragma unroll
-    for (int f = 0; f < FM; ++f) red_lds[((wave - 1) * FM + f) * 64 + lane] = acc[f];
+    for (int f = 0; f < FM; ++f) {
+      red_lds[((wave - 1) * FM + f) * 64 + lane] = acc[f];
+      mx_lds[wave - 1][f][lane] = amx[f];
+    }
   __syncthreads();
   if (wave > 0) return;
 #pragma unroll
   for (int w = 0; w < 3; ++w)
 #pragma unroll
-    for (int f = 0; f < FM; ++f) acc[f] = acc[f] + red_lds[(w * FM + f) * 64 + lane];
-  if (SA > 1 && !split_reduce_wave<FM>(acc, a.tpart + jb * (int64_t)SA * FM * 256, SA, sa, &a.tcounters[jb])) return;
-  // D[m][j] fragment: lane (j + 16 * (m / 4)), element m % 4
-#pragma unroll
-  for (int f = 0; f < FM; ++f)
-#pragma unroll
-    for (int vv = 0; vv < 4; ++vv) {
-      const int64_t m = 16 * f + 4 * g + vv;
-      if (m < a.M && jcol < a.r) a.tm32[m * a.r + jcol] = acc[f][vv];
+    for (int f = 0; f < FM; ++f) {
+      acc[f] = acc[f] + red_lds[(w * FM + f) * 64 + lane];
+      amx[f] = max(amx[f], mx_lds[w][f][lane]);
     }
+  if (SA > 1 &&
+      !split_reduce_wave<FM>(acc, amx, a.tpart + jb * (int64_t)SA * FM * 272, SA, sa, &a.tcounters[jb]))
+    return;
+  // amx is now the largest |activation| of the row over the whole reduction, the same in every
+  // column block (each block's units cover the whole reduction with the same slices): T is stored
+  // in fp16 scaled by that row's exponent, and column block 0 records 2^-e for the finish.
+  // D[j][m] fragment: lane (m + 16 (j / 4)) holds ranks 16 jb + 4 g .. + 3 of row m = 16 f + lane % 16
+  // (r % 16 == 0, so the four ranks are all in range or all past r)
+#pragma unroll
+  for (int f = 0; f < FM; ++f) {
+    const int64_t m = 16 * f + (lane & 15);
+    const int e = act_exponent(amx[f]);
+    const f4_t ts = acc[f] * exp2i(e);
+    h2_t lo2 = {(_Float16)ts[0], (_Float16)ts[1]}, hi2 = {(_Float16)ts[2], (_Float16)ts[3]};
+    if (m < a.M && jb * 16 < a.r)
+      *reinterpret_cast<u32x2_t*>(a.tm + m * a.r + jb * 16 + 4 * g) = u32x2_t{bits_of(lo2), bits_of(hi2)};
+    if (m < a.M && jb == 0 && g == 0) a.trinv[m] = exp2i(-e);
+  }
 }
 
 // Blocks [0, jblocks * ad_split) are adapter units (dispatched first: their reduction is the
@@ -399,7 +431,7 @@ __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
 // eight splits, a rank within the waves' first passes).
 template <int FM, int kSteps>
 SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lrow, int lane, u32x4_t* aq,
-                                   u32x4_t (*bq)[FM][2]) {
+                                   u32x4_t (*bq)[FM]) {
   const int g = lane >> 4;
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
@@ -409,55 +441,26 @@ SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lr
                                  : lrow * a.r + jj;
     aq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_p + po);
 #pragma unroll
-    for (int f = 0; f < FM; ++f) {
-      const float* tp = a.tm32 + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.r + jj;
-      bq[t][f][0] = *reinterpret_cast<const u32x4_t*>(tp);
-      bq[t][f][1] = *reinterpret_cast<const u32x4_t*>(tp + 4);
-    }
+    for (int f = 0; f < FM; ++f)
+      bq[t][f] = *reinterpret_cast<const u32x4_t*>(a.tm + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.r + jj);
   }
 }
 
-// One rank pass of the second product: T (fp32) of row m = 16 f + lane % 16 is scaled per row over
-// the pass (see act_exponent; the four lane groups of a row exchange their maxima), rounded to
-// fp16, multiplied on the MFMA and unscaled in fp32. D[row][m] sits in lane m + 16 (row / 4), so
-// each lane unscales with its own row's factor.
+// One rank pass of the second product on the row-scaled fp16 T (D[row][m] = sum_j P[row][j] T[m][j]);
+// the caller unscales the sum of all passes.
 template <int FM, int kSteps>
 SLIM_DEV void finish_adapter_mfma(const LayerArgs& a, int64_t jbase, int lane, const u32x4_t* aq,
-                                  const u32x4_t (*bq)[FM][2], f4_t* acc) {
+                                  const u32x4_t (*bq)[FM], f4_t* adacc) {
   const int g = lane >> 4;
 #pragma unroll
-  for (int f = 0; f < FM; ++f) {
-    const bool mok = 16 * f + (lane & 15) < a.M;
-    uint32_t mx = 0;
+  for (int t = 0; t < kSteps; ++t) {
+    const bool jok = jbase + 32 * t + 8 * g < a.r;
+    const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[t]) : zero_h8();
 #pragma unroll
-    for (int t = 0; t < kSteps; ++t) {
-      const bool ok = mok && jbase + 32 * t + 8 * g < a.r;
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) mx = max(mx, ok ? (bq[t][f][h][e] & 0x7FFFFFFFu) : 0u);
+    for (int f = 0; f < FM; ++f) {
+      const h8_t bv = (16 * f + (lane & 15) < a.M) ? __builtin_bit_cast(h8_t, bq[t][f]) : zero_h8();
+      adacc[f] = mfma16(av, bv, adacc[f]);
     }
-    mx = max(mx, (uint32_t)__shfl_xor((int)mx, 16, 64));
-    mx = max(mx, (uint32_t)__shfl_xor((int)mx, 32, 64));
-    const int e = act_exponent(mx);
-    const float sc = exp2i(e), inv = exp2i(-e);
-    f4_t pacc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int t = 0; t < kSteps; ++t) {
-      const bool jok = jbase + 32 * t + 8 * g < a.r;
-      const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[t]) : zero_h8();
-      // whole-vector casts: hipcc (ROCm 7.2) compiles __builtin_bit_cast(float, v[e]) of a vector
-      // element lvalue as a read of element 0 for every e
-      const f4_t lo = __builtin_bit_cast(f4_t, bq[t][f][0]) * sc, hi = __builtin_bit_cast(f4_t, bq[t][f][1]) * sc;
-      h8_t bv;
-#pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        bv[e2] = (_Float16)lo[e2];
-        bv[4 + e2] = (_Float16)hi[e2];
-      }
-      pacc = mfma16(av, (mok && jok) ? bv : zero_h8(), pacc);
-    }
-    acc[f] = acc[f] + pacc * inv;
   }
 }
 
@@ -475,8 +478,13 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
   const int S = a.split;
   const rsrc_t pr = make_rsrc(a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256), ((int64_t)(S - 1) * 4 + 1) * FM * 256 * 4);
   const int64_t jfirst = (int64_t)h * 32 * kSteps;
-  u32x4_t aq[kSteps], bq[kSteps][FM][2];
-  if (a.r > 0) finish_adapter_loads<FM, kSteps>(a, jfirst, lrow, lane, aq, bq);
+  u32x4_t aq[kSteps], bq[kSteps][FM];
+  float trinv[FM];
+  if (a.r > 0) {
+    finish_adapter_loads<FM, kSteps>(a, jfirst, lrow, lane, aq, bq);
+#pragma unroll
+    for (int f = 0; f < FM; ++f) trinv[f] = a.trinv[clamp_hi(16 * f + (lane & 15), a.M - 1)];
+  }
   f4_t acc[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
@@ -499,12 +507,18 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
         for (int f = 0; f < FM; ++f) acc[f] = acc[f] + pv[j][f];
   }
   if (a.r > 0) {
-    // wave h takes rank passes h, h + NW, ... of 32 kSteps ranks
-    finish_adapter_mfma<FM, kSteps>(a, jfirst, lane, aq, bq, acc);
+    // wave h takes rank passes h, h + NW, ... of 32 kSteps ranks; D[row][m] sits in lane
+    // m + 16 (row / 4), so each lane unscales with its own row's factor
+    f4_t adacc[FM];
+#pragma unroll
+    for (int f = 0; f < FM; ++f) adacc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+    finish_adapter_mfma<FM, kSteps>(a, jfirst, lane, aq, bq, adacc);
     for (int64_t jbase = jfirst + NW * 32 * kSteps; jbase < a.r; jbase += NW * 32 * kSteps) {
       finish_adapter_loads<FM, kSteps>(a, jbase, lrow, lane, aq, bq);
-      finish_adapter_mfma<FM, kSteps>(a, jbase, lane, aq, bq, acc);
+      finish_adapter_mfma<FM, kSteps>(a, jbase, lane, aq, bq, adacc);
     }
+#pragma unroll
+    for (int f = 0; f < FM; ++f) acc[f] = acc[f] + adacc[f] * trinv[f];
   }
   if (NW > 1) {
     // wave 1 hands its sum to wave 0, which adds it last (a fixed order) and stores
@@ -1115,7 +1129,7 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.p_tiled = p_tiled;
   a.ad_pb = p.decode ? nullptr : (p_tiled ? ad_p : reinterpret_cast<const uint16_t*>(ws + p.off_pb));
   a.tm = reinterpret_cast<uint16_t*>(ws + p.off_t);
-  a.tm32 = reinterpret_cast<float*>(ws + p.off_t);
+  a.trinv = reinterpret_cast<float*>(ws + p.off_rowinv);
   // large M: the activations are scaled per row into an fp16 copy (p.scaled), except fp16
   // activations of a forward without an adapter, which the tile kernel streams as they are
   a.act16 = p.scaled ? reinterpret_cast<const uint16_t*>(ws + p.off_x16) : a.act;

@@ -9,8 +9,9 @@ whose own error is of order 1e-7) and shows two things at gradient-sized inputs:
   into fp16's subnormal range;
 * the kernels' per-row power-of-two scaling (largest magnitude brought into [16, 32) before any
   fp16 rounding, undone exactly in fp32) keeps the error at the level of |dY| ~ 1 for every
-  magnitude, on both the small-M form (exponents per reduction slice, fp32 adapter intermediate)
-  and the large-M form (exponents per row, fp16 adapter intermediate).
+  magnitude, on both the small-M form (exponents per reduction slice for the sparse product, the
+  adapter intermediate accumulated in fp32 and stored in fp16 with its row's exponent) and the
+  large-M form (exponents per row throughout).
 
 The model is test infrastructure: it neither calls nor imitates any code of the library, only
 the rounding sequence the library's header documents.
@@ -68,8 +69,8 @@ def model_bwd_unscaled(dY, Q, s, L, R):
 
 
 def model_bwd_small_m(dY, Q, s, L, R, slice_len=512):
-    """M <= 32: exponents per (row, reduction slice) on dY * s16 formed in fp32; U in fp32, scaled
-    per rank pass into fp16 for the second product."""
+    """M <= 32: exponents per (row, reduction slice) on dY * s16 formed in fp32; U accumulated in
+    fp32 and stored in fp16 scaled by the exponent of the row's largest |dY|."""
     n, k = Q.shape
     dX = np.zeros((dY.shape[0], k))
     for g in range(k // 128):
@@ -79,8 +80,8 @@ def model_bwd_small_m(dY, Q, s, L, R, slice_len=512):
             e = row_exp(Ps)
             B = f16(Ps * 2.0 ** e) * 2.0 ** -e
             dX[:, 128 * g:128 * g + 128] += B @ Q[a:a + slice_len, 128 * g:128 * g + 128]
-    U = dY @ R.T                                               # fp32 intermediate
-    e = row_exp(U)
+    U = dY @ R.T                                               # fp32 accumulation
+    e = row_exp(dY)
     return dX + (f16(U * 2.0 ** e) @ L.T) * 2.0 ** -e
 
 
@@ -118,7 +119,8 @@ def model_fwd_large_m(X, p, L, R, n, k):
 
 
 def model_fwd_small_m(X, p, L, R, n, k, slice_len=512):
-    """M <= 32 forward: exponents per (row, slice) of X; T = X L in fp32, scaled per rank pass."""
+    """M <= 32 forward: exponents per (row, slice) of X; T = X L accumulated in fp32 from rounds of
+    128 positions, stored in fp16 scaled by the exponent of the row's largest |X|."""
     Wc = f16(O.unpack(p["codes"], p["meta"], p["scales"], n, k))
     Y = np.zeros((X.shape[0], n))
     for a in range(0, k, slice_len):
@@ -130,7 +132,7 @@ def model_fwd_small_m(X, p, L, R, n, k, slice_len=512):
         Xa = X[:, a:a + 128]
         e = row_exp(Xa)
         T += (f16(Xa * 2.0 ** e) @ L[a:a + 128]) * 2.0 ** -e
-    e = row_exp(T)
+    e = row_exp(X)
     return Y + (f16(T * 2.0 ** e) @ R) * 2.0 ** -e
 
 
