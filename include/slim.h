@@ -246,6 +246,26 @@ int slim_linear_bwd_dx(const void* dY, int dydtype, int64_t M, int64_t N, int64_
                        size_t ws_bytes, void* stream);
 
 /*
+ * slim_linear_noalloc - slim_linear without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation). Same arguments, results and precision as slim_linear, minus ws / ws_bytes.
+ *
+ * The workspace is a fixed array of SLIM_NOALLOC_SCRATCH_BYTES (64 MiB) of device memory that the
+ * library holds per device from the first call on that device until the process ends; its first
+ * call on a device also enqueues a small kernel that clears the array's counter region. The call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine) and records no timing
+ * events. Sizes whose slim_linear_workspace exceeds SLIM_NOALLOC_SCRATCH_BYTES return
+ * SLIM_EWORKSPACE before touching any device; that covers every M <= 32 layer of the shapes here
+ * and the 11008 x 4096 layer at M = 2048, but not, for example, a 5120 x 5120 layer at M = 4096.
+ * All calls on one device share its array, so two calls that overlap in time on one device
+ * (different streams or threads) race and give undefined results; serialise them.
+ */
+#define SLIM_NOALLOC_SCRATCH_BYTES (64u << 20)
+int slim_linear_noalloc(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const uint8_t* codes,
+                        const uint8_t* meta, const uint16_t* scales, const uint16_t* Lt, const uint16_t* Rt,
+                        int64_t r, float* Y, void* stream);
+
+/*
  * Per-kernel timing for benchmarks (host-side bookkeeping; not part of the layer's math).
  * slim_timing_enable(1) makes every later kernel launch of this library record a hipEvent
  * before and after itself on the caller's stream. slim_timing_read waits for the recorded

@@ -21,6 +21,13 @@ class SlimKernelTimer {
   void* b_ = nullptr;
 };
 
+// While one of these lives on a thread, the library's launches on that thread record no events.
+struct SlimTimingOff {
+  SlimTimingOff();
+  ~SlimTimingOff();
+  bool prev;
+};
+
 // untimed launches (timing off, or a stream under graph capture) take the plain launch path
 #define SLIM_LAUNCH(timer, kernel, grid, block, stream, ...)                                               \
   do {                                                                                                    \

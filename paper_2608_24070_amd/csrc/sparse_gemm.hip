@@ -30,6 +30,7 @@
 // Every global load is issued unconditionally from a clamped (or, through a buffer resource,
 // range-checked) address and masked when used: a load under a branch makes the compiler wait
 // for it at the join, which serialises what should be one round of memory traffic.
+#include <mutex>
 #include <type_traits>
 
 #include "slim_device.h"
@@ -1178,4 +1179,62 @@ extern "C" int slim_linear_bwd_dx(const void* dY, int dydtype, int64_t M, int64_
   char* w = reinterpret_cast<char*>(ws);
   const LayerArgs a = make_args(p, w, dY, dydtype, M, K, N, codesT, metaT, scalesT, R, L, false, r, dX);
   return launch_layer<true>(a, p, reinterpret_cast<const uint16_t*>(dY), dydtype == SLIM_BF16, w, (hipStream_t)stream);
+}
+
+// ------------------------------------------------------------------- no-allocation entry point
+// slim_linear_noalloc runs slim_linear's kernels on this file-scope array instead of a caller
+// workspace. Each device the library runs on holds its own copy until the process ends. Host code
+// never passes the array's name to a kernel (on the host it is only a stand-in for the symbol):
+// the device address comes from hipGetSymbolAddress, once per device, with that device current.
+static __device__ __align__(256) uint8_t scratch[SLIM_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+__global__ void __launch_bounds__(256) k_zero_u32(uint32_t* __restrict__ p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
+// The current device's scratch address. At its first use on a device the counter region (which
+// every call leaves at zero) is cleared by a fill kernel on `s`, ahead of the call's kernels.
+int scratch_for_current_device(hipStream_t s, char** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return SLIM_EDEVICE;
+  if (dev < 0 || dev >= kMaxDevices) return SLIM_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return SLIM_EDEVICE;
+    hipLaunchKernelGGL(k_zero_u32, dim3(SLIM_COUNTER_SLOTS / 256), dim3(256), 0, s, reinterpret_cast<uint32_t*>(ptr),
+                       (int64_t)SLIM_COUNTER_SLOTS);
+    if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
+    g_scratch_ptr[dev] = reinterpret_cast<char*>(ptr);
+  }
+  *out = g_scratch_ptr[dev];
+  return SLIM_OK;
+}
+static_assert(SLIM_COUNTER_SLOTS % 256 == 0, "counter region cleared by whole blocks");
+}  // namespace
+
+extern "C" int slim_linear_noalloc(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const uint8_t* codes,
+                                   const uint8_t* meta, const uint16_t* scales, const uint16_t* Lt,
+                                   const uint16_t* Rt, int64_t r, float* Y, void* stream) {
+  // the size checks come first, so a call the scratch cannot hold touches no device
+  SlimPlan p;
+  int st = slim_make_plan(false, M, N, K, r, &p);
+  if (st != SLIM_OK) return st;
+  if (p.total > (size_t)SLIM_NOALLOC_SCRATCH_BYTES) return SLIM_EWORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  char* w = nullptr;
+  st = scratch_for_current_device(s, &w);
+  if (st != SLIM_OK) return st;
+  st = slim_check_linear(false, X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, w,
+                         (size_t)SLIM_NOALLOC_SCRATCH_BYTES, &p);
+  if (st != SLIM_OK) return st;
+  SlimTimingOff no_events;   // timing would create hip events on first use
+  const LayerArgs a = make_args(p, w, X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, true, r, Y);
+  return launch_layer<false>(a, p, reinterpret_cast<const uint16_t*>(X), xdtype == SLIM_BF16, w, s);
 }

@@ -22,6 +22,7 @@ bool g_on = false;
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_pool;
 std::map<std::string, std::pair<long long, double>> g_total;
+thread_local bool t_off = false;
 
 hipEvent_t take_event() {
   if (!g_pool.empty()) {
@@ -49,7 +50,11 @@ void drain_locked() {
 }
 }  // namespace
 
+SlimTimingOff::SlimTimingOff() : prev(t_off) { t_off = true; }
+SlimTimingOff::~SlimTimingOff() { t_off = prev; }
+
 SlimKernelTimer::SlimKernelTimer(const char* name, hipStream_t s) : name_(name) {
+  if (t_off) return;
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on) return;
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;

@@ -38,6 +38,8 @@ _SIGS = {
                                    _c_p, _c_p, ctypes.c_size_t, _c_p]),
     "slim_linear_bwd_dx": (ctypes.c_int, [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p,
                                           _c_i64, _c_p, _c_p, ctypes.c_size_t, _c_p]),
+    "slim_linear_noalloc": (ctypes.c_int, [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p,
+                                           _c_i64, _c_p, _c_p]),
     "slim_timing_enable": (ctypes.c_int, [ctypes.c_int]),
     "slim_timing_reset": (ctypes.c_int, []),
     "slim_timing_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_size_t]),
@@ -122,6 +124,13 @@ def slim_workspace_init(ws, nbytes, stream) -> int:
 
 def slim_linear(X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, ws, ws_bytes, stream) -> int:
     return lib().slim_linear(X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, ws, ws_bytes, stream)
+
+
+def slim_linear_noalloc(X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, stream) -> int:
+    return lib().slim_linear_noalloc(X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, stream)
+
+
+SLIM_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 def slim_linear_bwd_dx(dY, dydtype, M, N, K, codesT, metaT, scalesT, L, R, r, dX, ws, ws_bytes, stream) -> int:
@@ -297,4 +306,22 @@ def bwd_dx(dY, packed_bwd: dict, L=None, R=None, out=None, ws=None, stream=None)
                             _ptr(packed_bwd["metaT"]), _ptr(packed_bwd["scalesT"]), _ptr(L), _ptr(R), r,
                             _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "slim_linear_bwd_dx")
+    return out
+
+
+def linear_noalloc(X, packed: dict, adapter: dict | None = None, out=None, stream=None):
+    """Y = X Wc^T + (X L) R through slim_linear_noalloc (the library's own per-device scratch; no
+    workspace). Only `out` is allocated here when not given."""
+    torch = _torch()
+    Lt = None if adapter is None else adapter["Lt"]
+    Rt = None if adapter is None else adapter["Rt"]
+    _on_gpu(X, Lt, Rt, out)
+    M, K = X.shape
+    N = packed["N"]
+    r = 0 if Lt is None else Lt.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=X.device)
+    st = slim_linear_noalloc(_ptr(X), _dtype_code(X), M, N, K, _ptr(packed["codes"]), _ptr(packed["meta"]),
+                             _ptr(packed["scales"]), _ptr(Lt), _ptr(Rt), r, _ptr(out), _stream(stream))
+    _check(st, "slim_linear_noalloc")
     return out

@@ -137,3 +137,12 @@ def test_binding_constants_match_header_enums():
     for name, value in enums.items():
         assert getattr(slim, name) == value, name
     assert int(re.search(r"#define SLIM_ABI_VERSION (\d+)", text).group(1)) == slim.slim_abi_version()
+
+
+def test_noalloc_refuses_sizes_past_its_scratch_before_touching_a_device():
+    # a 5120 x 5120 layer at M = 4096 needs 76 MiB of workspace, more than the 64 MiB scratch
+    assert slim.slim_linear_workspace(4096, 5120, 5120, 512) > slim.SLIM_NOALLOC_SCRATCH_BYTES
+    assert slim.slim_linear_noalloc(A, 1, 4096, 5120, 5120, A, A, A, A, A, 512, A, None) == slim.SLIM_EWORKSPACE
+    # argument errors are reported the same way as by slim_linear
+    assert slim.slim_linear_noalloc(A, 1, 16, 100, 512, A, A, A, None, None, 0, A, None) == slim.SLIM_ESHAPE
+    assert "noalloc" in " ".join(slim.header_symbols())
