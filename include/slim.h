@@ -269,7 +269,7 @@ int slim_linear_noalloc(const void* X, int xdtype, int64_t M, int64_t N, int64_t
  * Per-kernel timing for benchmarks (host-side bookkeeping; not part of the layer's math).
  * slim_timing_enable(1) makes every later kernel launch of this library record a hipEvent
  * before and after itself on the caller's stream. slim_timing_read waits for the recorded
- * events and writes one line per kernel name, "name launches total_ms\n", into buf (host);
+ * events and writes one line per kernel name, "name launches total_ms median_ms\n", into buf (host);
  * it returns 0, or the buffer size needed when buf is NULL or too small. slim_timing_reset
  * clears the totals. These three calls are the library's only process-wide mutable state (a
  * mutex-guarded switch, event pool and totals); with timing off, which is the default, the layer

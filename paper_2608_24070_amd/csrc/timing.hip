@@ -4,6 +4,7 @@
 // summed milliseconds per kernel name. Off by default; costs nothing when off.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdio>
 #include <map>
 #include <mutex>
@@ -21,7 +22,12 @@ std::mutex g_mu;
 bool g_on = false;
 std::vector<Pending> g_pending;
 std::vector<hipEvent_t> g_pool;
-std::map<std::string, std::pair<long long, double>> g_total;
+struct Totals {
+  long long launches = 0;
+  double total_ms = 0.0;
+  std::vector<float> each_ms;
+};
+std::map<std::string, Totals> g_total;
 thread_local bool t_off = false;
 
 hipEvent_t take_event() {
@@ -40,8 +46,9 @@ void drain_locked() {
     float ms = 0.f;
     if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
       auto& t = g_total[p.name];
-      t.first += 1;
-      t.second += ms;
+      t.launches += 1;
+      t.total_ms += ms;
+      t.each_ms.push_back(ms);
     }
     g_pool.push_back(p.a);
     g_pool.push_back(p.b);
@@ -94,8 +101,14 @@ extern "C" int slim_timing_read(char* buf, size_t buf_len) {
   drain_locked();
   std::string out;
   for (auto& kv : g_total) {
+    std::vector<float> v = kv.second.each_ms;
+    double med = 0.0;
+    if (!v.empty()) {
+      std::sort(v.begin(), v.end());
+      med = v.size() % 2 ? v[v.size() / 2] : 0.5 * ((double)v[v.size() / 2 - 1] + v[v.size() / 2]);
+    }
     char line[256];
-    std::snprintf(line, sizeof line, "%s %lld %.6f\n", kv.first.c_str(), kv.second.first, kv.second.second);
+    std::snprintf(line, sizeof line, "%s %lld %.6f %.6f\n", kv.first.c_str(), kv.second.launches, kv.second.total_ms, med);
     out += line;
   }
   if (!buf || buf_len == 0) return (int)out.size() + 1;

@@ -146,14 +146,14 @@ def slim_timing_reset() -> int:
 
 
 def slim_timing_read() -> dict:
-    """{kernel name: (launches, total_ms)} since the last reset (waits for recorded events)."""
+    """{kernel name: (launches, total_ms, median_ms)} since the last reset (waits for recorded events)."""
     need = lib().slim_timing_read(None, 0)
     buf = ctypes.create_string_buffer(max(need, 1) + 256)
     lib().slim_timing_read(buf, len(buf))
     out = {}
     for line in buf.value.decode().splitlines():
-        name, n, ms = line.split()
-        out[name] = (int(n), float(ms))
+        name, n, ms, med = line.split()
+        out[name] = (int(n), float(ms), float(med))
     return out
 
 
