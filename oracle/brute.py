@@ -157,3 +157,18 @@ def bwd_dx(dY, W, L, R):
             for j in range(k):
                 dX[m][j] += sum(U[m][t] * L[j][t] for t in range(r))
     return dX
+
+
+def adapter_dequant(A, group=128):
+    """Quantize-dequantize of an adapter factor given as rows (lists), groups of `group` consecutive
+    elements of a row: scale by exhaustive fp16 search of fp32(max |a|) / 7, codes by ``rtn_code``."""
+    out = []
+    for row in A:
+        q = [0.0] * len(row)
+        for g0 in range(0, len(row), group):
+            a = max(abs(v) for v in row[g0:g0 + group])
+            s = f16_nearest(to_f32(to_f32(a) / 7.0))
+            for j in range(g0, min(g0 + group, len(row))):
+                q[j] = rtn_code(row[j], s) * s
+        out.append(q)
+    return out

@@ -24,6 +24,10 @@ What it computes, and where the thesis defines it
   (dY R^T) L^T because it is a parallel dense path.
 * ``lemma_extra_sparsity``: the closed form of Lemma sparsity_ratio
   (eq. sparsity_ratio).
+* ``pack_adapter_q`` / ``linear_qa``: the quantized adapters of SLiM-LoRA^Q (SLiM,
+  "Low-rank adapter quantization"): AbsMax 4-bit group quantization with groups of
+  128 elements, here along each factor's input dimension (K for L, r for R), with the
+  weights' scale and rounding rules; the layer then uses the dequantized factors.
 
 Readings where the thesis is silent, garbled or inconsistent
 --------------------------------------------------------------
@@ -293,6 +297,95 @@ def lemma_extra_sparsity(N: int, M: int) -> float:
     from math import comb
     s = N / M
     return sum(comb(M, j) * s ** j * (1 - s) ** (M - j) * (j - N) / M for j in range(N + 1, M + 1))
+
+
+# ------------------------------------------------- quantized adapters (SLiM-LoRA^Q)
+
+ADAPTER_GROUP = 128   # adapter elements sharing one scale, along each factor's input dimension
+
+
+def adapter_group_scales(A) -> np.ndarray:
+    """AbsMax scales of an adapter factor laid out [rows, length] with groups of 128 consecutive
+    elements along `length` (the factor's input dimension; the last group of a row holds
+    length % 128 elements when 128 does not divide it): s16 = fp16_RNE(fp32(max|a|) / 7), the
+    weights' rule (SLiM "Low-rank adapter quantization": AbsMax group quantization, group 128).
+    Returns float16 [rows, ceil(length / 128)]."""
+    A = np.asarray(A, dtype=np.float64)
+    if not np.all(np.isfinite(A)):
+        raise OracleError("non-finite adapter element")
+    rows, n = A.shape
+    ng = -(-n // ADAPTER_GROUP)
+    s = np.zeros((rows, ng), dtype=np.float16)
+    for g in range(ng):
+        a = np.abs(A[:, ADAPTER_GROUP * g:ADAPTER_GROUP * (g + 1)]).max(axis=1).astype(np.float32)
+        s[:, g] = fp16_rne(a / np.float32(QMAX))
+    return s
+
+
+def adapter_quantize(A, s16) -> np.ndarray:
+    """Codes q = clamp(rint(a / s16), -7, 7) of every element (0 where s16 == 0); int8 [rows, length]."""
+    A = np.asarray(A, dtype=np.float64)
+    rows, n = A.shape
+    S = np.repeat(s16.astype(np.float64), ADAPTER_GROUP, axis=1)[:, :n]
+    with np.errstate(divide="ignore", invalid="ignore"):
+        t = np.where(S > 0, A / np.where(S > 0, S, 1.0), 0.0)
+    return np.clip(np.rint(t), -QMAX, QMAX).astype(np.int8)
+
+
+def _encode_dense(q: np.ndarray) -> np.ndarray:
+    """Dense 4-bit codes u = q + 8 of [rows, length] (length % 8 == 0) as bytes [rows, length / 2]:
+    each little-endian 32-bit word holds 8 consecutive elements, element 2c in nibble c and
+    element 2c + 1 in nibble c + 4 (c = 0..3)."""
+    rows, n = q.shape
+    u = (q.astype(np.int16) + CODE_OFFSET).astype(np.uint32).reshape(rows, n // 8, 4, 2)
+    c = np.arange(4, dtype=np.uint32)
+    word = ((u[..., 0] << (4 * c)) | (u[..., 1] << (4 * c + 16))).sum(axis=2, dtype=np.uint32)
+    return np.ascontiguousarray(word.astype("<u4").view(np.uint8).reshape(rows, n // 2))
+
+
+def _decode_dense(codes: np.ndarray, rows: int, n: int) -> np.ndarray:
+    """Inverse of ``_encode_dense``: signed codes int8 [rows, length]."""
+    word = np.ascontiguousarray(codes).view("<u4").reshape(rows, n // 8).astype(np.uint32)
+    c = np.arange(4, dtype=np.uint32)
+    lo = (word[..., None] >> (4 * c)) & 0xF
+    hi = (word[..., None] >> (4 * c + 16)) & 0xF
+    u = np.stack([lo, hi], axis=-1).reshape(rows, n)
+    return (u.astype(np.int16) - CODE_OFFSET).astype(np.int8)
+
+
+def pack_adapter_q(L, R) -> dict:
+    """4-bit AbsMax group-128 pack of the adapter factors for the forward (inference) layer.
+
+    L [K, r] is quantized as L^T [r, K] (groups along K, the input of X L) and R [r, N] as R^T [N, r]
+    (groups along r, the input of T R). Returns Lq uint8 [r, K/2], Ls uint16 [r, ceil(K/128)],
+    Rq uint8 [N, r/2], Rs uint16 [N, ceil(r/128)] (fp16 bit patterns)."""
+    Lt = np.asarray(L, dtype=np.float64).T
+    Rt = np.asarray(R, dtype=np.float64).T
+    if Lt.shape[0] % 8 or Lt.shape[1] % 8:
+        raise OracleError("adapter sizes must be multiples of 8")
+    Ls, Rs = adapter_group_scales(Lt), adapter_group_scales(Rt)
+    return {"Lq": _encode_dense(adapter_quantize(Lt, Ls)), "Ls": Ls.view(np.uint16).copy(),
+            "Rq": _encode_dense(adapter_quantize(Rt, Rs)), "Rs": Rs.view(np.uint16).copy()}
+
+
+def unpack_adapter_q(pq: dict, K: int, N: int, r: int):
+    """Dequantized factors (float64, exact q s16): L [K, r] and R [r, N]."""
+    def deq(codes, scales, rows, n):
+        q = _decode_dense(codes, rows, n).astype(np.float64)
+        S = np.repeat(np.asarray(scales, dtype=np.uint16).view(np.float16).astype(np.float64), ADAPTER_GROUP, axis=1)
+        return q * S[:, :n]
+    return deq(pq["Lq"], pq["Ls"], r, K).T, deq(pq["Rq"], pq["Rs"], N, r).T
+
+
+def adapter_q_bytes(K: int, N: int, r: int) -> int:
+    """Bytes of a quantized adapter: half a byte per element plus one fp16 scale per group."""
+    return r * K // 2 + 2 * r * (-(-K // ADAPTER_GROUP)) + N * r // 2 + 2 * N * (-(-r // ADAPTER_GROUP))
+
+
+def linear_qa(X, packed: dict, pq: dict, n: int, k: int, r: int) -> np.ndarray:
+    """Y = X Wc^T + (X L^Q) R^Q in float64, with the dequantized adapter factors of ``pack_adapter_q``."""
+    Lq, Rq = unpack_adapter_q(pq, k, n, r)
+    return linear(X, packed, Lq, Rq, n, k)
 
 
 # ------------------------------------------------------------------ tolerances

@@ -232,6 +232,7 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
   const int qb = lane >> 4;
   const int pbase = 128 * G * (qb >> 1) + 8 * (qb & 1);
   f4_t out[NU][FM];
+  h16_t bfr[8 * G][FM];   // B fragments of step 8 gi + t4: positions pbase + 16 step (+ 256 G)
 #pragma unroll
   for (int k = 0; k < NU; ++k) {
     if (rt0 + k >= rt1) break;
@@ -241,9 +242,22 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
       __builtin_amdgcn_sched_barrier(0);   // keep them ahead of this unit's work
     }
     const DecodeWords<G>& w = wb[k & 1];
-    f4_t acc[FM];
+    // Every B fragment of the slice is read from LDS before the first MFMA (the first unit only:
+    // later units of the block reuse them), so the reads overlap each other instead of each
+    // MFMA waiting for its own; two accumulators halve the MFMA dependency chain.
+    if (k == 0) {
 #pragma unroll
-    for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+      for (int st = 0; st < 8 * G; ++st)
+#pragma unroll
+        for (int f = 0; f < FM; ++f) {
+          const _Float16* xr = xs + (16 * f + (lane & 15)) * LDX + pbase + 16 * st;
+          bfr[st][f] = cat16(*reinterpret_cast<const h8_t*>(xr), *reinterpret_cast<const h8_t*>(xr + 256 * G));
+        }
+      __builtin_amdgcn_sched_barrier(0);   // the scheduler would otherwise sink the reads to their uses
+    }
+    f4_t acc[2][FM];
+#pragma unroll
+    for (int f = 0; f < FM; ++f) acc[0][f] = acc[1][f] = f4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int gi = 0; gi < G; ++gi) {
       const bool gok = cl + gi < nchunks;
@@ -254,17 +268,13 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
         h8_t av = BWD ? dequant_word_int(word) : dequant_word(word, s2);
         av = gok ? av : zero_h8();
         const int idx = (int)w.mw[gi][t4 >> 1];
-        const int p0 = pbase + 16 * (8 * gi + t4);
 #pragma unroll
-        for (int f = 0; f < FM; ++f) {
-          const _Float16* xr = xs + (16 * f + (lane & 15)) * LDX + p0;
-          acc[f] = smfmac16(av, cat16(*reinterpret_cast<const h8_t*>(xr), *reinterpret_cast<const h8_t*>(xr + 256 * G)),
-                            acc[f], idx, t4 & 1);
-        }
+        for (int f = 0; f < FM; ++f)
+          acc[t4 & 1][f] = smfmac16(av, bfr[8 * gi + t4][f], acc[t4 & 1][f], idx, t4 & 1);
       }
     }
 #pragma unroll
-    for (int f = 0; f < FM; ++f) out[k][f] = acc[f] * unscale[f];   // lane (m + 16 (row / 4)): column m = lane % 16
+    for (int f = 0; f < FM; ++f) out[k][f] = (acc[0][f] + acc[1][f]) * unscale[f];   // lane (m + 16 (row / 4)): column m = lane % 16
   }
 
 #pragma unroll

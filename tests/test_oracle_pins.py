@@ -439,3 +439,87 @@ def test_tolerance_gate_max_abs_leg_alone():
     assert O.within_tolerance(Y, Yref)[0]
     # and the Frobenius leg alone still rejects a uniform 3e-3 relative error
     assert not O.within_tolerance(Yref * (1 + 3e-3), Yref)[0]
+
+
+# ------------------------------------------------------ quantized adapters (SLiM-LoRA^Q)
+
+def test_adapter_quant_matches_bruteforce():
+    # K = 256 (two groups of L^T rows), r = 48 (one partial group of R^T rows), ties from repeated levels
+    K, N, r = 256, 32, 48
+    Lb, Rb, L, R = synth.adapter(K, N, r, seed=11, name="aqb/")
+    L = L.copy()
+    L[5, 3] = L[9, 3] = 0.0                       # zeros and a tie between equal magnitudes
+    L[7, 3] = -np.abs(L[:, 3]).max()
+    # a group of rank 9 whose maximum is 10 * 2^-24: s16 = fp16(10/7 2^-24) = 2^-24 (subnormal, rounded
+    # down), so a / s16 = 10 and the clamp to 7 decides the code
+    L[:128, 9] = 0.0
+    L[0, 9], L[1, 9] = 10 * 2.0 ** -24, -3 * 2.0 ** -24
+    pqt = O.pack_adapter_q(L, R)
+    assert pqt["Ls"][9, 0] == 0x0001
+    Ld, Rd = O.unpack_adapter_q(pqt, K, N, r)
+    assert Ld[0, 9] == 7 * 2.0 ** -24 and Ld[1, 9] == -3 * 2.0 ** -24
+    assert np.array_equal(Ld.T, np.array(B.adapter_dequant(L.T.tolist())))
+    assert np.array_equal(Rd.T, np.array(B.adapter_dequant(R.T.tolist())))
+
+
+def test_adapter_quant_roundtrip_bound_and_full_scale_code():
+    K, N, r = 512, 256, 80
+    _, _, L, R = synth.adapter(K, N, r, seed=12, name="aqr/")
+    for A in (L.T, R.T):                          # factors as quantized: rows along the input dimension
+        s = O.adapter_group_scales(A).astype(np.float64)
+        assert np.all(s >= 2.0 ** -14)
+        q = O.adapter_quantize(A, s.astype(np.float16)).astype(np.float64)
+        S = np.repeat(s, O.ADAPTER_GROUP, axis=1)[:, :A.shape[1]]
+        assert np.all(np.abs(A - q * S) <= S / 2)
+        for g in range(s.shape[1]):
+            blk = slice(128 * g, 128 * g + 128)
+            i = np.argmax(np.abs(A[:, blk]), axis=1)
+            assert np.all(np.abs(q[:, blk][np.arange(A.shape[0]), i]) == 7)
+
+
+def test_adapter_worked_example_bytes():
+    # Hand derivation, one row of L^T (rank j = 0, K = 128, r = 8): elements 0..3 are 3.5, -1.0, 0.25,
+    # 0.75, the rest 0. Group absmax 3.5: s16 = fp16(fp32(3.5) / 7) = 0.5 (bits 0x3800). Codes
+    # q = rint(v / 0.5): 7, -2, rint(0.5) = 0 (tie to even), rint(1.5) = 2 (tie to even); u = q + 8:
+    # 15, 6, 8, 10, then 8s. Word 0 holds elements 0..7 with element 2c in nibble c and 2c + 1 in
+    # nibble c + 4: nibbles (7..0) = 8 8 A 6 | 8 8 8 F -> 0x88A6888F, bytes 8F 88 A6 88; every other
+    # word is 0x88888888.
+    L = np.zeros((128, 8))
+    L[0, 0], L[1, 0], L[2, 0], L[3, 0] = 3.5, -1.0, 0.25, 0.75
+    R = np.zeros((8, 16))
+    pq = O.pack_adapter_q(L, R)
+    assert list(pq["Lq"][0, :4]) == [0x8F, 0x88, 0xA6, 0x88]
+    assert np.all(pq["Lq"][0, 4:] == 0x88) and np.all(pq["Lq"][1:] == 0x88)
+    assert pq["Ls"][0, 0] == 0x3800 and np.all(pq["Ls"][1:] == 0)
+    assert np.all(pq["Rq"] == 0x88) and np.all(pq["Rs"] == 0)
+    Ld, _ = O.unpack_adapter_q(pq, 128, 16, 8)
+    assert list(Ld[:4, 0]) == [3.5, -1.0, 0.0, 1.0]
+
+
+def test_adapter_exact_values_make_linear_qa_equal_linear():
+    # factors whose groups hold values q 2^e with a group maximum of 7 2^e dequantize to themselves
+    rng = synth.stream(13, "aqx")
+    K, N, r, m = 256, 64, 32, 3
+    e = rng.integers(-9, -4, size=(r, K // 128))
+    Lt = rng.integers(-7, 8, size=(r, K)).astype(np.float64) * np.repeat(2.0 ** e, 128, axis=1)
+    Lt[:, ::128] = 7 * 2.0 ** e
+    Rt = rng.integers(-7, 8, size=(N, r)).astype(np.float64) * 2.0 ** -6
+    Rt[:, 0] = 7 * 2.0 ** -6
+    L, R = Lt.T, Rt.T
+    pq = O.pack_adapter_q(L, R)
+    Ld, Rd = O.unpack_adapter_q(pq, K, N, r)
+    assert np.array_equal(Ld, L) and np.array_equal(Rd, R)
+    W = synth.weights(N, K, seed=13)
+    _, X = synth.activations(m, K, seed=13)
+    p = O.pack(W)
+    assert np.array_equal(O.linear_qa(X, p, pq, N, K, r), O.linear(X, p, L, R, N, K))
+
+
+def test_adapter_q_bytes():
+    # 4 bits per element plus an fp16 scale per 128: 4.125 bits, 16 / 4.125 = 3.88x fewer bytes than fp16
+    K = N = 4096
+    r = 384
+    assert O.adapter_q_bytes(K, N, r) * 8 == (r * K + N * r) * 4.125
+    assert abs(2 * r * (K + N) / O.adapter_q_bytes(K, N, r) - 16 / 4.125) < 1e-12
+    pq = O.pack_adapter_q(np.zeros((256, 48)), np.zeros((48, 32)))
+    assert sum(v.nbytes for v in pq.values()) == O.adapter_q_bytes(256, 32, 48)
