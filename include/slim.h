@@ -183,6 +183,29 @@ int slim_pack_adapter(const uint16_t* L, const uint16_t* R, int64_t K, int64_t N
                       uint16_t* Rt, void* stream);
 
 /*
+ * slim_pack_adapter_q - one-time 4-bit pack of the adapter factors for slim_linear_qa.
+ * Thesis: SLiM "Low-rank adapter quantization" (SLiM-LoRA^Q): AbsMax group quantization of the
+ * adapters with groups of 128 elements, which cuts their bytes about 4x. The groups run along each
+ * factor's input dimension: L^T [r, K] by rows j along K (the reduction of X L) and R^T [N, r] by
+ * rows n along r (the reduction of T R); a row's last group holds r % 128 elements when 128 does
+ * not divide r. Scale and codes follow the weights' rules: s16 = fp16_RNE(fp32(max |a|) / 7),
+ * q = clamp(rint(a / s16), -7, 7) (double-precision division, ties to even; 0 when s16 == 0).
+ *
+ *   L    fp16 [K, r], device.     R    fp16 [r, N], device.
+ *   K % 128 == 0, N >= 1, r >= 32 and r % 32 == 0.
+ *   Lq   out, uint8 [r, K/2]: row j holds the codes u = q + 8 of L[:, j], 8 consecutive elements
+ *        per little-endian 32-bit word, element 2c in nibble c and element 2c + 1 in nibble c + 4.
+ *   Ls   out, fp16 bits [r, ceil(K/128)].
+ *   Rq   out, uint8 [N, r/2]: row n holds the codes of R[:, n], same word format.
+ *   Rs   out, fp16 bits [N, ceil(r/128)].
+ * Bytes: r (K + N) / 2 codes plus 2 (r ceil(K/128) + N ceil(r/128)) scales (4.125 bits per element
+ * when 128 divides both). Returns SLIM_ENONFINITE if L or R holds a NaN/Inf. Synchronises `stream`
+ * (status read back) and allocates 4 bytes of device memory for the duration of the call.
+ */
+int slim_pack_adapter_q(const uint16_t* L, const uint16_t* R, int64_t K, int64_t N, int64_t r, uint8_t* Lq,
+                        uint16_t* Ls, uint8_t* Rq, uint16_t* Rs, void* stream);
+
+/*
  * slim_linear_workspace - bytes of device workspace slim_linear needs for these sizes
  * (written to *bytes, host pointer). Depends only on the sizes. Pure host function.
  */
@@ -222,6 +245,24 @@ int slim_workspace_init(void* ws, size_t ws_bytes, void* stream);
 int slim_linear(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const uint8_t* codes,
                 const uint8_t* meta, const uint16_t* scales, const uint16_t* Lt, const uint16_t* Rt,
                 int64_t r, float* Y, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * slim_linear_qa - Y = X * Wc^T + (X * L^Q) * R^Q with the 4-bit adapters of slim_pack_adapter_q
+ * (L^Q, R^Q their dequantized values (u - 8) * s16). Thesis: SLiM-LoRA^Q, the quantized adapters of
+ * SLiM's deployed layer ("Low-rank adapter quantization"; quantized-adapter rows of the SLiM
+ * results and speedup tables).
+ *
+ *   Arguments as slim_linear, with Lq, Ls, Rq, Rs in place of Lt, Rt; r >= 32, r % 32 == 0.
+ *   ws      at least slim_linear_qa_workspace(M, N, K, r) bytes, zeroed once with slim_workspace_init.
+ * At M <= 32 the kernels dequantize the factors in registers as they stream them; at M > 32 the
+ * first launch expands them to fp16 in the workspace. The dequantized factor values are
+ * (u - 8) * s16 rounded to fp16 (as for the weights); otherwise precision as slim_linear.
+ */
+int slim_linear_qa_workspace(int64_t M, int64_t N, int64_t K, int64_t r, size_t* bytes);
+int slim_linear_qa(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const uint8_t* codes,
+                   const uint8_t* meta, const uint16_t* scales, const uint8_t* Lq, const uint16_t* Ls,
+                   const uint8_t* Rq, const uint16_t* Rs, int64_t r, float* Y, void* ws, size_t ws_bytes,
+                   void* stream);
 
 /*
  * slim_linear_bwd_dx - dX = dY * W^{R,C} + (dY * R^T) * L^T, fp32 accumulation, fp32 output.

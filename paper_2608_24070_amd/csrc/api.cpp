@@ -195,3 +195,42 @@ extern "C" int slim_bwd_dx_workspace(int64_t M, int64_t N, int64_t K, int64_t r,
   if (st == SLIM_OK) *bytes = p.total;
   return st;
 }
+
+int slim_make_plan_qa(int64_t M, int64_t N, int64_t K, int64_t r, SlimPlan* p) {
+  if (r < 32 || r % 32) return SLIM_ESHAPE;   // 4-bit factor rows are whole 16-byte runs
+  int st = slim_make_plan(false, M, N, K, r, p);
+  if (st != SLIM_OK) return st;
+  if (!p->decode) {
+    size_t off = p->total;
+    p->off_q16 = off;
+    off = round256(off + (size_t)r * (size_t)K * 2);
+    p->off_p16 = off;
+    off = round256(off + (size_t)cdiv(N, 32) * 32 * (size_t)r * 2);
+    p->total = off;
+  }
+  return SLIM_OK;
+}
+
+int slim_check_linear_qa(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const void* codes,
+                         const void* meta, const void* scales, const void* Lq, const void* Ls, const void* Rq,
+                         const void* Rs, int64_t r, const void* Y, const void* ws, size_t ws_bytes, SlimPlan* plan) {
+  if (!X || !codes || !meta || !scales || !Y || !Lq || !Ls || !Rq || !Rs) return SLIM_EINVAL;
+  if (xdtype != SLIM_F16 && xdtype != SLIM_BF16) return SLIM_EDTYPE;
+  int st = slim_make_plan_qa(M, N, K, r, plan);
+  if (st != SLIM_OK) return st;
+  if (!slim_aligned16(X) || !slim_aligned16(codes) || !slim_aligned16(meta) || !slim_aligned16(scales) ||
+      !slim_aligned16(Y) || !slim_aligned16(Lq) || !slim_aligned16(Ls) || !slim_aligned16(Rq) || !slim_aligned16(Rs))
+    return SLIM_EALIGN;
+  if (!ws || ws_bytes < plan->total) return SLIM_EWORKSPACE;
+  if (!slim_aligned16(ws)) return SLIM_EALIGN;
+  plan->scaled = !plan->decode;
+  return SLIM_OK;
+}
+
+extern "C" int slim_linear_qa_workspace(int64_t M, int64_t N, int64_t K, int64_t r, size_t* bytes) {
+  if (!bytes) return SLIM_EINVAL;
+  SlimPlan p;
+  int st = slim_make_plan_qa(M, N, K, r, &p);
+  if (st == SLIM_OK) *bytes = p.total;
+  return st;
+}

@@ -242,7 +242,87 @@ __global__ void __launch_bounds__(256) k_tile_rt(const uint16_t* __restrict__ R,
   out[i] = n < N ? R[j * N + n] : (uint16_t)0;
 }
 
+// 4-bit AbsMax pack of one adapter factor laid out as [rows, len] (row-major view of a transposed
+// source: element (row, col) is src[col * ld + row]), groups of 128 along len (the last group of a
+// row may be shorter). Sixteen consecutive threads share one (row, group): thread i of them codes
+// the 8 elements at col = 128 g + 8 i into one 32-bit word (element 2c in nibble c, 2c + 1 in
+// nibble c + 4), the group's absmax comes from a 16-lane shuffle, and thread 0 writes the scale.
+__global__ void __launch_bounds__(256)
+k_pack_adapter_q(const uint16_t* __restrict__ src, int64_t ld, int64_t rows, int64_t len, uint32_t* __restrict__ codes,
+                 uint16_t* __restrict__ scales, int* __restrict__ status) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t ng = (len + 127) / 128;
+  const int64_t pair = t / 16;
+  const int i = (int)(t % 16);
+  const int64_t row = pair / ng, g = pair % ng;
+  const int64_t col0 = 128 * g + 8 * i;
+  const bool valid = row < rows && col0 < len;
+  float v[8];
+  float amax = 0.f;
+  int bad = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    v[e] = valid ? h_bits_to_f(src[(col0 + e) * ld + row]) : 0.f;
+    if (!__builtin_isfinite(v[e])) bad = 1;
+    amax = fmaxf(amax, fabsf(v[e]));
+  }
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 16));
+  if (valid && bad) atomicOr(status, 1);
+  // s16 = fp16_RNE(fp32 absmax / 7), IEEE division; codes against the stored s16 in double precision
+  const _Float16 s16 = (_Float16)__fdiv_rn(amax, 7.0f);
+  const double sd = (double)(float)s16;
+  uint32_t word = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    double q = sd > 0.0 ? rint((double)v[e] / sd) : 0.0;
+    q = q < -7.0 ? -7.0 : (q > 7.0 ? 7.0 : q);
+    const uint32_t u = (uint32_t)((int)q + 8);
+    word |= u << (4 * (e >> 1) + 16 * (e & 1));
+  }
+  if (!valid) return;
+  codes[row * (len / 8) + col0 / 8] = word;
+  if (i == 0) scales[row * ng + g] = __builtin_bit_cast(uint16_t, s16);
+}
+
 }  // namespace
+
+extern "C" int slim_pack_adapter_q(const uint16_t* L, const uint16_t* R, int64_t K, int64_t N, int64_t r, uint8_t* Lq,
+                                   uint16_t* Ls, uint8_t* Rq, uint16_t* Rs, void* stream) {
+  if (!L || !R || !Lq || !Ls || !Rq || !Rs) return SLIM_EINVAL;
+  if (K < 128 || N < 1 || r < 32 || r % 32 || K % 128 || K >= (int64_t(1) << 31) || N >= (int64_t(1) << 31) ||
+      r >= 65536)
+    return SLIM_ESHAPE;
+  if (!slim_aligned16(L) || !slim_aligned16(R) || !slim_aligned16(Lq) || !slim_aligned16(Ls) || !slim_aligned16(Rq) ||
+      !slim_aligned16(Rs))
+    return SLIM_EALIGN;
+  hipStream_t s = (hipStream_t)stream;
+  int* d_status = nullptr;
+  if (hipMalloc(&d_status, sizeof(int)) != hipSuccess) return SLIM_EDEVICE;
+  int h_status = 0;
+  int rc = SLIM_OK;
+  do {
+    if (hipMemsetAsync(d_status, 0, sizeof(int), s) != hipSuccess) { rc = SLIM_EDEVICE; break; }
+    // L^T [r, K]: element (j, k) = L[k * r + j]; R^T [N, r]: element (n, j) = R[j * N + n]
+    const int64_t tl = r * ((K + 127) / 128) * 16, tr = N * ((r + 127) / 128) * 16;
+    {
+      SlimKernelTimer timer("pack_adapter_q", s);
+      SLIM_LAUNCH(timer, k_pack_adapter_q, dim3((unsigned)((tl + 255) / 256)), dim3(256), s, L, r, r, K,
+                  reinterpret_cast<uint32_t*>(Lq), Ls, d_status);
+    }
+    {
+      SlimKernelTimer timer("pack_adapter_q", s);
+      SLIM_LAUNCH(timer, k_pack_adapter_q, dim3((unsigned)((tr + 255) / 256)), dim3(256), s, R, N, N, r,
+                  reinterpret_cast<uint32_t*>(Rq), Rs, d_status);
+    }
+    if (hipGetLastError() != hipSuccess) { rc = SLIM_EDEVICE; break; }
+    if (hipMemcpyAsync(&h_status, d_status, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess) { rc = SLIM_EDEVICE; break; }
+    if (h_status & 1) rc = SLIM_ENONFINITE;
+  } while (0);
+  (void)hipFree(d_status);
+  return rc;
+}
 
 extern "C" int slim_pack_adapter(const uint16_t* L, const uint16_t* R, int64_t K, int64_t N, int64_t r, uint16_t* Lt,
                                  uint16_t* Rt, void* stream) {

@@ -47,7 +47,16 @@ struct SlimPlan {
   // workspace layout (byte offsets)
   size_t off_counters = 0, n_counters = 0;
   size_t off_t = 0, off_tpart = 0, off_ypart = 0, off_x16 = 0, off_rowinv = 0, off_pb = 0, total = 0;
+  // 4-bit adapters at large M: their fp16 expansions (Q = L^T row-major, P = R^T in 32 x 16 tiles)
+  size_t off_q16 = 0, off_p16 = 0;
 };
+
+// Forward plan with 4-bit adapters (slim_linear_qa): slim_make_plan plus, at large M, room for the
+// adapters' fp16 expansions.
+int slim_make_plan_qa(int64_t M, int64_t N, int64_t K, int64_t r, SlimPlan* plan);
+int slim_check_linear_qa(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const void* codes,
+                         const void* meta, const void* scales, const void* Lq, const void* Ls, const void* Rq,
+                         const void* Rs, int64_t r, const void* Y, const void* ws, size_t ws_bytes, SlimPlan* plan);
 
 // Forward (bwd == false: rows = N, red = K) or backward (bwd == true: rows = K, red = N) plan.
 int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPlan* plan);

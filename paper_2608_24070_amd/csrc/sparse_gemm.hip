@@ -54,6 +54,12 @@ struct LayerArgs {
   const uint16_t* ad_p;    // adapter second factor [rows, r]: 32 x 16 tiles (forward, from
                            // slim_pack_adapter) or row-major (backward, L as given)
   int p_tiled;             // ad_p is in 32 x 16 tiles
+  // 4-bit adapters (slim_linear_qa): codes of Q = L^T [r, red/8 words] and P = R^T [rows, r/8 words]
+  // with fp16 group-128 scales along the reduction of each product; null for fp16 adapters
+  const uint32_t* q4;
+  const uint16_t* q4s;     // [r, ceil(red/128)]
+  const uint32_t* p4;
+  const uint16_t* p4s;     // [rows, ceil(r/128)]
   const uint16_t* ad_pb;   // large M: the factor in 32 x 16 tiles (ad_p, or a re-laid copy)
   uint16_t* tm;            // fp16 adapter intermediate of the row-scaled activations: row-major
                            // [M, r] (small M), 32 x 16 tiles (large M)
@@ -332,17 +338,30 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
     acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
     amx[f] = 0u;
   }
-  // a.ad_sub consecutive slices of kAdSlice positions (one load round each)
+  // a.ad_sub consecutive slices of kAdSlice positions (one load round each). In a round at rs, lane
+  // group g takes the 32 positions rs + 32 g .. + 31, step t the eight at rs + 32 g + 8 t (for
+  // both operands, so every position enters once): a lane's 4-bit factor codes for the round are
+  // one 16-byte load, and the round lies in one 128-group (one scale).
+  const int64_t red8 = a.red / 8, ngk = (a.red + 127) / 128;
+  const rsrc_t rq4 = make_rsrc(a.q4, a.r * a.red / 2);
   for (int sub = 0; sub < a.ad_sub; ++sub) {
     const int64_t rs = r0 + (int64_t)sub * kAdSlice;
-    u32x4_t aq[kSteps][FM], bq[kSteps];
+    const int64_t run = rs + 32 * g;
+    u32x4_t aq[kSteps][FM], bq[kSteps], qw = zero_u4();
+    uint32_t qs = 0;
 #pragma unroll
     for (int t = 0; t < kSteps; ++t) {
-      const int64_t rk = clamp_hi(rs + 32 * t + 8 * g, a.red - 8);
+      const int64_t rk = clamp_hi(run + 8 * t, a.red - 8);
 #pragma unroll
       for (int f = 0; f < FM; ++f)
         aq[t][f] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.red + rk);
-      bq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_q + jl * a.red + rk);
+      if (!a.q4) bq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_q + jl * a.red + rk);
+    }
+    if (a.q4) {
+      // out-of-range offsets (a run past the reduction) read zero through the resource
+      qw = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                           rq4, (uint32_t)((jl * red8 + run / 8) * 4), 0, 0));
+      qs = a.q4s[jl * ngk + clamp_hi(rs / 128, ngk - 1)];
     }
     // this round's activations of row m = 16 f + lane % 16, scaled per row (see act_exponent): the
     // four lane groups of a row exchange their maxima; the round's product is unscaled in fp32
@@ -353,7 +372,7 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
       uint32_t mx = 0;
 #pragma unroll
       for (int t = 0; t < kSteps; ++t) {
-        const bool ok = mok && rs + 32 * t + 8 * g < a.red;
+        const bool ok = mok && run + 8 * t < a.red;
         act8_to_f(aq[t][f], bf16, xf[t]);
 #pragma unroll
         for (int e = 0; e < 8; ++e) xf[t][e] = ok ? xf[t][e] : 0.f;
@@ -368,9 +387,9 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
       f4_t racc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < kSteps; ++t) {
-        const bool kok = rs + 32 * t + 8 * g < a.red;
-        const h8_t qv = (kok && jcol < a.r) ? __builtin_bit_cast(h8_t, bq[t]) : zero_h8();
-        racc = mfma16(qv, scale8_to_h(xf[t], sc), racc);
+        const bool kok = run + 8 * t < a.red && jcol < a.r;
+        const h8_t qv = a.q4 ? dequant_word(qw[t], splat_h2(qs)) : __builtin_bit_cast(h8_t, bq[t]);
+        racc = mfma16(kok ? qv : zero_h8(), scale8_to_h(xf[t], sc), racc);
       }
       acc[f] = acc[f] + racc * inv;
     }
@@ -440,17 +459,37 @@ __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
 // The loads of the first adapter pass and of the first eight partials do not depend on each other
 // and are all issued before any is used: one memory round trip for the common case (at most
 // eight splits, a rank within the waves' first passes).
+// Rank assignment of one pass at jbase: lane group g takes the run of 8 kSteps ranks starting at
+// jbase + 8 kSteps g, step t its eight ranks at jbase + 8 kSteps g + 8 t (for both operands). A
+// run lies within one 128-rank group (jbase is a multiple of 32 NW kSteps), so a 4-bit P needs one
+// scale per lane and pass, and its codes are kSteps / 4 loads of 16 bytes.
+template <int kSteps>
+SLIM_DEV int64_t finish_rank(int64_t jbase, int g, int t) { return jbase + 8 * kSteps * g + 8 * t; }
+
 template <int FM, int kSteps>
 SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lrow, int lane, u32x4_t* aq,
-                                   u32x4_t (*bq)[FM]) {
+                                   u32x4_t (*bq)[FM], uint32_t& ps) {
   const int g = lane >> 4;
+  if (a.p4) {
+    // 4-bit P: the run's codes (kSteps words of 8 ranks); past r or the buffer they read zero
+    const rsrc_t rp = make_rsrc(a.p4, a.rows * a.r / 2);
+    const int64_t run = finish_rank<kSteps>(jbase, g, 0);
+#pragma unroll
+    for (int i = 0; i < kSteps / 4; ++i)
+      aq[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                              rp, (uint32_t)((lrow * (a.r / 8) + run / 8 + 4 * i) * 4), 0, 0));
+    const int64_t ngr = (a.r + 127) / 128;
+    ps = a.p4s[lrow * ngr + clamp_hi(run / 128, ngr - 1)];
+  }
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
-    const int64_t jj = clamp_hi(jbase + 32 * t + 8 * g, a.r - 8);
-    // tiled: 8 consecutive ranks of a row stay within one 32 x 16 tile (jj % 16 is 0 or 8)
-    const int64_t po = a.p_tiled ? ((lrow >> 5) * (a.r >> 4) + (jj >> 4)) * 512 + (lrow & 31) * 16 + (jj & 15)
-                                 : lrow * a.r + jj;
-    aq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_p + po);
+    const int64_t jj = clamp_hi(finish_rank<kSteps>(jbase, g, t), a.r - 8);
+    if (!a.p4) {
+      // tiled: 8 consecutive ranks of a row stay within one 32 x 16 tile (jj % 16 is 0 or 8)
+      const int64_t po = a.p_tiled ? ((lrow >> 5) * (a.r >> 4) + (jj >> 4)) * 512 + (lrow & 31) * 16 + (jj & 15)
+                                   : lrow * a.r + jj;
+      aq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_p + po);
+    }
 #pragma unroll
     for (int f = 0; f < FM; ++f)
       bq[t][f] = *reinterpret_cast<const u32x4_t*>(a.tm + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.r + jj);
@@ -461,12 +500,13 @@ SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lr
 // the caller unscales the sum of all passes.
 template <int FM, int kSteps>
 SLIM_DEV void finish_adapter_mfma(const LayerArgs& a, int64_t jbase, int lane, const u32x4_t* aq,
-                                  const u32x4_t (*bq)[FM], f4_t* adacc) {
+                                  const u32x4_t (*bq)[FM], uint32_t ps, f4_t* adacc) {
   const int g = lane >> 4;
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
-    const bool jok = jbase + 32 * t + 8 * g < a.r;
-    const h8_t av = jok ? __builtin_bit_cast(h8_t, aq[t]) : zero_h8();
+    const bool jok = finish_rank<kSteps>(jbase, g, t) < a.r;
+    const h8_t pv = a.p4 ? dequant_word(aq[t / 4][t % 4], splat_h2(ps)) : __builtin_bit_cast(h8_t, aq[t]);
+    const h8_t av = jok ? pv : zero_h8();
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
       const h8_t bv = (16 * f + (lane & 15) < a.M) ? __builtin_bit_cast(h8_t, bq[t][f]) : zero_h8();
@@ -490,9 +530,10 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
   const rsrc_t pr = make_rsrc(a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256), ((int64_t)(S - 1) * 4 + 1) * FM * 256 * 4);
   const int64_t jfirst = (int64_t)h * 32 * kSteps;
   u32x4_t aq[kSteps], bq[kSteps][FM];
+  uint32_t ps = 0;
   float trinv[FM];
   if (a.r > 0) {
-    finish_adapter_loads<FM, kSteps>(a, jfirst, lrow, lane, aq, bq);
+    finish_adapter_loads<FM, kSteps>(a, jfirst, lrow, lane, aq, bq, ps);
 #pragma unroll
     for (int f = 0; f < FM; ++f) trinv[f] = a.trinv[clamp_hi(16 * f + (lane & 15), a.M - 1)];
   }
@@ -523,10 +564,10 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
     f4_t adacc[FM];
 #pragma unroll
     for (int f = 0; f < FM; ++f) adacc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-    finish_adapter_mfma<FM, kSteps>(a, jfirst, lane, aq, bq, adacc);
+    finish_adapter_mfma<FM, kSteps>(a, jfirst, lane, aq, bq, ps, adacc);
     for (int64_t jbase = jfirst + NW * 32 * kSteps; jbase < a.r; jbase += NW * 32 * kSteps) {
-      finish_adapter_loads<FM, kSteps>(a, jbase, lrow, lane, aq, bq);
-      finish_adapter_mfma<FM, kSteps>(a, jbase, lane, aq, bq, adacc);
+      finish_adapter_loads<FM, kSteps>(a, jbase, lrow, lane, aq, bq, ps);
+      finish_adapter_mfma<FM, kSteps>(a, jbase, lane, aq, bq, ps, adacc);
     }
 #pragma unroll
     for (int f = 0; f < FM; ++f) acc[f] = acc[f] + adacc[f] * trinv[f];
@@ -938,9 +979,40 @@ __global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
 // rowinv[m]. Rows of up to 256 x NR vectors of 8 (NR > 0) stay in registers between the two
 // passes; longer rows (NR == 0) are read twice (the second read mostly from L2).
 constexpr int kRowRegs = 16;
+// With 4-bit adapters the same launch also expands them into the fp16 layouts the adapter GEMM and
+// the tile epilogue read (blocks past the M row blocks, one thread per word of 8 codes):
+// Q = L^T [r, red] row-major, P = R^T [rows, r] in 32 x 16 tiles.
+struct AdapterExpand {
+  const uint32_t* q4;
+  const uint16_t* q4s;
+  uint16_t* q16;
+  const uint32_t* p4;
+  const uint16_t* p4s;
+  uint16_t* p16;
+  int64_t r, red, rows, M;
+};
+
+SLIM_DEV void expand_adapter_block(const AdapterExpand& d, int64_t b) {
+  const int64_t i = b * 256 + threadIdx.x;     // word index: Q words first, then P words
+  const int64_t nq = d.r * d.red / 8, np = d.rows * d.r / 8;
+  if (i < nq) {
+    const int64_t row = i / (d.red / 8), col = (i % (d.red / 8)) * 8;
+    const h8_t v = dequant_word(d.q4[i], splat_h2(d.q4s[row * ((d.red + 127) / 128) + col / 128]));
+    *reinterpret_cast<h8_t*>(d.q16 + row * d.red + col) = v;
+  } else if (i < nq + np) {
+    const int64_t w = i - nq, row = w / (d.r / 8), col = (w % (d.r / 8)) * 8;
+    const h8_t v = dequant_word(d.p4[w], splat_h2(d.p4s[row * ((d.r + 127) / 128) + col / 128]));
+    *reinterpret_cast<h8_t*>(d.p16 + ((row >> 5) * (d.r >> 4) + (col >> 4)) * 512 + (row & 31) * 16 + (col & 15)) = v;
+  }
+}
+
 template <bool BF16, int NR>
 __global__ void __launch_bounds__(256) k_rowprep(const u32x4_t* __restrict__ act, int64_t nv, u32x4_t* __restrict__ act16,
-                                                 float* __restrict__ rowinv) {
+                                                 float* __restrict__ rowinv, AdapterExpand ex) {
+  if ((int64_t)blockIdx.x >= ex.M) {
+    expand_adapter_block(ex, (int64_t)blockIdx.x - ex.M);
+    return;
+  }
   constexpr int kR = NR > 0 ? NR : 1;
   __shared__ uint32_t wmax[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1077,12 +1149,15 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
     // scale each activation row into the fp16 copy the adapter GEMM and the tile kernel stream
     SlimKernelTimer timer("rowprep", s);
     const int64_t nv = a.red / 8;
-    const dim3 grid((unsigned)a.M);
+    AdapterExpand ex{a.q4, a.q4s, const_cast<uint16_t*>(a.ad_q), a.p4, a.p4s, const_cast<uint16_t*>(a.ad_pb),
+                     a.r, a.red, a.rows, a.M};
+    const int64_t nexp = a.q4 ? (a.r * a.red / 8 + a.rows * a.r / 8 + 255) / 256 : 0;
+    const dim3 grid((unsigned)(a.M + nexp));
     u32x4_t* dst = reinterpret_cast<u32x4_t*>(const_cast<uint16_t*>(a.act16));
     const u32x4_t* src = reinterpret_cast<const u32x4_t*>(act);
     float* rinv = const_cast<float*>(a.rowinv);
     const int nr = nv <= 512 ? 2 : nv <= 1024 ? 4 : nv <= 2048 ? 8 : nv <= 256 * kRowRegs ? 16 : 0;
-#define SLIM_ROWPREP(B, NR) SLIM_LAUNCH(timer, (k_rowprep<B, NR>), grid, dim3(256), s, src, nv, dst, rinv)
+#define SLIM_ROWPREP(B, NR) SLIM_LAUNCH(timer, (k_rowprep<B, NR>), grid, dim3(256), s, src, nv, dst, rinv, ex)
     if (act_bf16) {
       if (nr == 2) SLIM_ROWPREP(true, 2);
       else if (nr == 4) SLIM_ROWPREP(true, 4);
@@ -1157,6 +1232,10 @@ LayerArgs make_args(const SlimPlan& p, char* ws, const void* act, int dtype, int
   a.tpart = reinterpret_cast<float*>(ws + p.off_tpart);
   a.tcounters = reinterpret_cast<uint32_t*>(ws + p.off_counters);
   a.finish = p.decode && (p.sp_split > 1 || r > 0);
+  a.q4 = nullptr;
+  a.q4s = nullptr;
+  a.p4 = nullptr;
+  a.p4s = nullptr;
   return a;
 }
 
@@ -1176,6 +1255,26 @@ extern "C" int slim_linear(const void* X, int xdtype, int64_t M, int64_t N, int6
   if (st != SLIM_OK) return st;
   char* w = reinterpret_cast<char*>(ws);
   const LayerArgs a = make_args(p, w, X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, true, r, Y);
+  return launch_layer<false>(a, p, reinterpret_cast<const uint16_t*>(X), xdtype == SLIM_BF16, w, (hipStream_t)stream);
+}
+
+extern "C" int slim_linear_qa(const void* X, int xdtype, int64_t M, int64_t N, int64_t K, const uint8_t* codes,
+                              const uint8_t* meta, const uint16_t* scales, const uint8_t* Lq, const uint16_t* Ls,
+                              const uint8_t* Rq, const uint16_t* Rs, int64_t r, float* Y, void* ws, size_t ws_bytes,
+                              void* stream) {
+  SlimPlan p;
+  int st = slim_check_linear_qa(X, xdtype, M, N, K, codes, meta, scales, Lq, Ls, Rq, Rs, r, Y, ws, ws_bytes, &p);
+  if (st != SLIM_OK) return st;
+  char* w = reinterpret_cast<char*>(ws);
+  // the fp16 factor pointers are the large-M expansions in the workspace (unused at small M, where the
+  // kernels dequantize the 4-bit factors in registers)
+  const uint16_t* q16 = reinterpret_cast<const uint16_t*>(w + p.off_q16);
+  const uint16_t* p16 = reinterpret_cast<const uint16_t*>(w + p.off_p16);
+  LayerArgs a = make_args(p, w, X, xdtype, M, N, K, codes, meta, scales, q16, p16, true, r, Y);
+  a.q4 = reinterpret_cast<const uint32_t*>(Lq);
+  a.q4s = Ls;
+  a.p4 = reinterpret_cast<const uint32_t*>(Rq);
+  a.p4s = Rs;
   return launch_layer<false>(a, p, reinterpret_cast<const uint16_t*>(X), xdtype == SLIM_BF16, w, (hipStream_t)stream);
 }
 

@@ -38,6 +38,10 @@ _SIGS = {
                                    _c_p, _c_p, ctypes.c_size_t, _c_p]),
     "slim_linear_bwd_dx": (ctypes.c_int, [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p,
                                           _c_i64, _c_p, _c_p, ctypes.c_size_t, _c_p]),
+    "slim_pack_adapter_q": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "slim_linear_qa_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "slim_linear_qa": (ctypes.c_int, [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
+                                      _c_p, _c_i64, _c_p, _c_p, ctypes.c_size_t, _c_p]),
     "slim_linear_noalloc": (ctypes.c_int, [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p,
                                            _c_i64, _c_p, _c_p]),
     "slim_timing_enable": (ctypes.c_int, [ctypes.c_int]),
@@ -124,6 +128,20 @@ def slim_workspace_init(ws, nbytes, stream) -> int:
 
 def slim_linear(X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, ws, ws_bytes, stream) -> int:
     return lib().slim_linear(X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, ws, ws_bytes, stream)
+
+
+def slim_pack_adapter_q(L, R, K, N, r, Lq, Ls, Rq, Rs, stream) -> int:
+    return lib().slim_pack_adapter_q(L, R, K, N, r, Lq, Ls, Rq, Rs, stream)
+
+
+def slim_linear_qa_workspace(M, N, K, r) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().slim_linear_qa_workspace(M, N, K, r, ctypes.byref(out)), "slim_linear_qa_workspace")
+    return out.value
+
+
+def slim_linear_qa(X, xdtype, M, N, K, codes, meta, scales, Lq, Ls, Rq, Rs, r, Y, ws, ws_bytes, stream) -> int:
+    return lib().slim_linear_qa(X, xdtype, M, N, K, codes, meta, scales, Lq, Ls, Rq, Rs, r, Y, ws, ws_bytes, stream)
 
 
 def slim_linear_noalloc(X, xdtype, M, N, K, codes, meta, scales, Lt, Rt, r, Y, stream) -> int:
@@ -324,4 +342,39 @@ def linear_noalloc(X, packed: dict, adapter: dict | None = None, out=None, strea
     st = slim_linear_noalloc(_ptr(X), _dtype_code(X), M, N, K, _ptr(packed["codes"]), _ptr(packed["meta"]),
                              _ptr(packed["scales"]), _ptr(Lt), _ptr(Rt), r, _ptr(out), _stream(stream))
     _check(st, "slim_linear_noalloc")
+    return out
+
+
+def pack_adapter_q(L, R, stream=None) -> dict:
+    """slim_pack_adapter_q of fp16 L [K, r] and R [r, N]: {"Lq", "Ls", "Rq", "Rs", "K", "N", "r"}."""
+    torch = _torch()
+    _on_gpu(L, R)
+    K, r = L.shape
+    N = R.shape[1]
+    dev = L.device
+    out = {"Lq": torch.empty((r, K // 2), dtype=torch.uint8, device=dev),
+           "Ls": torch.empty((r, (K + 127) // 128), dtype=torch.int16, device=dev),
+           "Rq": torch.empty((N, r // 2), dtype=torch.uint8, device=dev),
+           "Rs": torch.empty((N, (r + 127) // 128), dtype=torch.int16, device=dev),
+           "K": K, "N": N, "r": r}
+    _check(slim_pack_adapter_q(_ptr(L), _ptr(R), K, N, r, _ptr(out["Lq"]), _ptr(out["Ls"]), _ptr(out["Rq"]),
+                               _ptr(out["Rs"]), _stream(stream)), "slim_pack_adapter_q")
+    return out
+
+
+def linear_qa(X, packed: dict, qadapter: dict, out=None, ws=None, stream=None):
+    """Y = X Wc^T + (X L^Q) R^Q through slim_linear_qa (qadapter from pack_adapter_q). Y fp32 [M, N]."""
+    torch = _torch()
+    _on_gpu(X, out)
+    M, K = X.shape
+    N, r = packed["N"], qadapter["r"]
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=X.device)
+    need = slim_linear_qa_workspace(M, N, K, r)
+    if ws is None:
+        ws = workspace(need, X.device, stream)
+    st = slim_linear_qa(_ptr(X), _dtype_code(X), M, N, K, _ptr(packed["codes"]), _ptr(packed["meta"]),
+                        _ptr(packed["scales"]), _ptr(qadapter["Lq"]), _ptr(qadapter["Ls"]), _ptr(qadapter["Rq"]),
+                        _ptr(qadapter["Rs"]), r, _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "slim_linear_qa")
     return out
