@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true",
                     help="decode workload only: skip the second (prefill, M = 2048) measurement")
+    ap.add_argument("--qadapter", action="store_true",
+                    help="forward with 4-bit group-128 adapters (slim_pack_adapter_q / slim_linear_qa)")
     ap.add_argument("--dispatches", type=int, default=200,
                     help="steps of the per-kernel pass (median per kernel; at least --steps)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU budget of the oracle baseline (about 10-30 s)")
@@ -107,21 +109,23 @@ def copy_probe(mb):
                       "read_plus_write_GBps": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}))
 
 
-def layer_bytes(M, N, K, r):
-    """Algorithmic bytes of one forward layer call: packed weight + fp16 adapter + bf16 X + fp32 Y."""
-    return N * K * PACK_BYTES_PER_WEIGHT + 2 * r * (K + N) + 2 * M * K + 4 * M * N
+def layer_bytes(M, N, K, r, qadapter=False):
+    """Algorithmic bytes of one forward layer call: packed weight + adapter + bf16 X + fp32 Y."""
+    return N * K * PACK_BYTES_PER_WEIGHT + adapter_bytes(K, N, r, qadapter) + 2 * M * K + 4 * M * N
 
 
-def kernel_bytes(kernel, M, N, K, r, bwd, has_finish=True):
+def kernel_bytes(kernel, M, N, K, r, bwd, has_finish=True, qadapter=False):
     """Algorithmic HBM bytes of one launch of a library kernel on one layer: the operands it must
     read and the results it must produce, once each (split partials and re-reads not counted).
     Forward: rows = N, reduction = K; backward: rows = K, reduction = N."""
     rows, red = (K, N) if bwd else (N, K)
     weight = N * K * PACK_BYTES_PER_WEIGHT
+    first = (r * red // 2 + 2 * r * ((red + 127) // 128)) if qadapter else 2 * r * red
+    second = (rows * r // 2 + 2 * rows * ((r + 127) // 128)) if qadapter else 2 * r * rows
     if kernel.startswith("decode"):      # packed weight + adapter first factor + activations -> T (fp16)
-        return weight + 2 * r * red + 2 * M * red + 2 * M * r + (0 if has_finish else 4 * M * rows)
+        return weight + first + 2 * M * red + 2 * M * r + (0 if has_finish else 4 * M * rows)
     if kernel.startswith("finish"):      # adapter second factor + T -> Y
-        return 2 * r * rows + 2 * M * r + 4 * M * rows
+        return second + 2 * M * r + 4 * M * rows
     if kernel.startswith("tile"):        # packed weight + fp16 activations + second factor + T -> Y
         return weight + 2 * M * red + 2 * r * rows + 2 * M * r + 4 * M * rows
     if kernel.startswith("adapter_gemm"):  # fp16 activations + first factor -> T
@@ -152,7 +156,14 @@ def workload_layers(wk, m):
     return configs.TINY.layers, m or 16
 
 
-def measure(wk, m, steps, warmup, dispatches, cyc_per_ms):
+def adapter_bytes(K, N, r, qadapter):
+    """Bytes of the adapter factors: fp16, or 4-bit codes plus an fp16 scale per 128 elements."""
+    if not qadapter:
+        return 2 * r * (K + N)
+    return r * K // 2 + 2 * r * ((K + 127) // 128) + N * r // 2 + 2 * N * ((r + 127) // 128)
+
+
+def measure(wk, m, steps, warmup, dispatches, cyc_per_ms, qadapter=False):
     """Set up one workload (synthetic inputs resident in HBM, packed once, > 3x the MALL of distinct
     weight copies) and time it: K timed steps back to back, then `dispatches` steps with per-kernel
     events. Every pass takes the next copy from one running counter, so a copy is read again only
@@ -182,7 +193,10 @@ def measure(wk, m, steps, warmup, dispatches, cyc_per_ms):
         pack_ms += (time.perf_counter() - tp) * 1e3
         del W
         ad = slim.pack_adapter(dev_bits(Lb, torch.float16), dev_bits(Rb, torch.float16))
-        per_layer.append({"layer": ly, "pack": p, "L": ad["L"], "R": ad["R"], "Lt": ad["Lt"], "Rt": ad["Rt"]})
+        pl = {"layer": ly, "pack": p, "L": ad["L"], "R": ad["R"], "Lt": ad["Lt"], "Rt": ad["Rt"]}
+        if qadapter:
+            pl["qa"] = slim.pack_adapter_q(ad["L"], ad["R"])
+        per_layer.append(pl)
     # activations: q/k/v/gate/up of the block share X; o and down get their own
     acts = {}
     for ly in layers:
@@ -205,14 +219,18 @@ def measure(wk, m, steps, warmup, dispatches, cyc_per_ms):
     for c in range(n_copies):
         cp = []
         for pl in per_layer:
-            ad = {"L": pl["L"], "R": pl["R"]} if bwd else {"Lt": pl["Lt"], "Rt": pl["Rt"]}
+            if qadapter:
+                ad = {k: v for k, v in pl["qa"].items()}
+            else:
+                ad = {"L": pl["L"], "R": pl["R"]} if bwd else {"Lt": pl["Lt"], "Rt": pl["Rt"]}
             if c == 0:
                 cp.append({"pack": pl["pack"], "ad": ad})
             else:
                 cp.append({"pack": {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in pl["pack"].items()},
-                           "ad": {k: v.clone() for k, v in ad.items()}})
+                           "ad": {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in ad.items()}})
         copies.append(cp)
-    ws_need = max((slim.slim_bwd_dx_workspace if bwd else slim.slim_linear_workspace)(
+    wsq = slim.slim_bwd_dx_workspace if bwd else (slim.slim_linear_qa_workspace if qadapter else slim.slim_linear_workspace)
+    ws_need = max(wsq(
         M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
     ws = torch.zeros(ws_need + 256, dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
@@ -226,6 +244,8 @@ def measure(wk, m, steps, warmup, dispatches, cyc_per_ms):
         for pl, c in zip(per_layer, cp):
             if bwd:
                 slim.bwd_dx(pl["x"], c["pack"], c["ad"]["L"], c["ad"]["R"], out=pl["out"], ws=ws)
+            elif qadapter:
+                slim.linear_qa(pl["x"], c["pack"], c["ad"], out=pl["out"], ws=ws)
             else:
                 slim.linear(pl["x"], c["pack"], c["ad"], out=pl["out"], ws=ws)
 
@@ -273,14 +293,14 @@ def measure(wk, m, steps, warmup, dispatches, cyc_per_ms):
     launches_per_step = kt[dominant][0] / dispatches
     med_s = kt[dominant][2] * 1e-3
 
-    tot_bytes = sum(layer_bytes(M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
+    tot_bytes = sum(layer_bytes(M, pl["layer"].n, pl["layer"].k, pl["layer"].r, qadapter) for pl in per_layer)
     tot_flops = sum(layer_flops(M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
     has_finish = any(k.startswith("finish") for k in kt)
     wkey = f"{wk}_m{M}"
     if M <= 32:
         unit = "GB/s"
         value = tot_bytes / (ms_per_step * 1e-3) / 1e9
-        dk_bytes = sum(kernel_bytes(dominant, M, pl["layer"].n, pl["layer"].k, pl["layer"].r, bwd, has_finish)
+        dk_bytes = sum(kernel_bytes(dominant, M, pl["layer"].n, pl["layer"].k, pl["layer"].r, bwd, has_finish, qadapter)
                        for pl in per_layer) / launches_per_step
         achieved = dk_bytes / med_s / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -307,7 +327,8 @@ def measure(wk, m, steps, warmup, dispatches, cyc_per_ms):
         "value": round(value, 2), "unit": unit, "ms_per_step": round(ms_per_step, 6),
         "config": {
             "workload": f"{wk}: M={M}, {shape}, bf16 {'dY' if bwd else 'X'}, "
-                        f"{'dX' if bwd else 'Y'} fp32, 2:4 + int4 group-128 weights",
+                        f"{'dX' if bwd else 'Y'} fp32, 2:4 + int4 group-128 weights"
+                        + (", int4 group-128 adapters" if qadapter else ", fp16 adapters"),
             "M": M, "layers": len(layers), "N": ly0.n, "K": ly0.k, "r": ly0.r,
             "bytes_per_step": int(tot_bytes), "dense_equiv_flops_per_step": int(tot_flops),
             "weight_copies_rotated": n_copies, "pack_ms_one_time": round(pack_ms, 2),
@@ -337,11 +358,15 @@ def main():
     torch.cuda.set_device(0)
     cyc_per_ms = sleep_calibration(torch)
     dispatches = max(args.dispatches, args.steps)
-    res, layers, M, bwd = measure(args.workload, args.m, args.steps, args.warmup, dispatches, cyc_per_ms)
+    if args.qadapter and args.workload == "mlp70b_bwd":
+        print("--qadapter applies to the forward only", file=sys.stderr)
+        sys.exit(2)
+    res, layers, M, bwd = measure(args.workload, args.m, args.steps, args.warmup, dispatches, cyc_per_ms,
+                                  args.qadapter)
     second = None
     if args.workload == "decode" and not args.no_prefill:
         # the M >= 2048 half of the metric: the prefill layer (11008 x 4096, rank 384) at M = 2048
-        s_res, _, _, _ = measure("prefill", None, args.steps, args.warmup, dispatches, cyc_per_ms)
+        s_res, _, _, _ = measure("prefill", None, args.steps, args.warmup, dispatches, cyc_per_ms, args.qadapter)
         second = {"metric": "dense-equiv TFLOP/s (M≥2048)", **s_res}
 
     cpu = None

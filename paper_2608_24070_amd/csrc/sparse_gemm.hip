@@ -238,7 +238,6 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
   const int qb = lane >> 4;
   const int pbase = 128 * G * (qb >> 1) + 8 * (qb & 1);
   f4_t out[NU][FM];
-  h16_t bfr[8 * G][FM];   // B fragments of step 8 gi + t4: positions pbase + 16 step (+ 256 G)
 #pragma unroll
   for (int k = 0; k < NU; ++k) {
     if (rt0 + k >= rt1) break;
@@ -248,22 +247,9 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
       __builtin_amdgcn_sched_barrier(0);   // keep them ahead of this unit's work
     }
     const DecodeWords<G>& w = wb[k & 1];
-    // Every B fragment of the slice is read from LDS before the first MFMA (the first unit only:
-    // later units of the block reuse them), so the reads overlap each other instead of each
-    // MFMA waiting for its own; two accumulators halve the MFMA dependency chain.
-    if (k == 0) {
+    f4_t acc[FM];
 #pragma unroll
-      for (int st = 0; st < 8 * G; ++st)
-#pragma unroll
-        for (int f = 0; f < FM; ++f) {
-          const _Float16* xr = xs + (16 * f + (lane & 15)) * LDX + pbase + 16 * st;
-          bfr[st][f] = cat16(*reinterpret_cast<const h8_t*>(xr), *reinterpret_cast<const h8_t*>(xr + 256 * G));
-        }
-      __builtin_amdgcn_sched_barrier(0);   // the scheduler would otherwise sink the reads to their uses
-    }
-    f4_t acc[2][FM];
-#pragma unroll
-    for (int f = 0; f < FM; ++f) acc[0][f] = acc[1][f] = f4_t{0.f, 0.f, 0.f, 0.f};
+    for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int gi = 0; gi < G; ++gi) {
       const bool gok = cl + gi < nchunks;
@@ -274,13 +260,17 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
         h8_t av = BWD ? dequant_word_int(word) : dequant_word(word, s2);
         av = gok ? av : zero_h8();
         const int idx = (int)w.mw[gi][t4 >> 1];
+        const int p0 = pbase + 16 * (8 * gi + t4);
 #pragma unroll
-        for (int f = 0; f < FM; ++f)
-          acc[t4 & 1][f] = smfmac16(av, bfr[8 * gi + t4][f], acc[t4 & 1][f], idx, t4 & 1);
+        for (int f = 0; f < FM; ++f) {
+          const _Float16* xr = xs + (16 * f + (lane & 15)) * LDX + p0;
+          acc[f] = smfmac16(av, cat16(*reinterpret_cast<const h8_t*>(xr), *reinterpret_cast<const h8_t*>(xr + 256 * G)),
+                            acc[f], idx, t4 & 1);
+        }
       }
     }
 #pragma unroll
-    for (int f = 0; f < FM; ++f) out[k][f] = (acc[0][f] + acc[1][f]) * unscale[f];   // lane (m + 16 (row / 4)): column m = lane % 16
+    for (int f = 0; f < FM; ++f) out[k][f] = acc[f] * unscale[f];   // lane (m + 16 (row / 4)): column m = lane % 16
   }
 
 #pragma unroll
@@ -318,7 +308,7 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
 // fragment per 16 activation rows (1 KB), which keeps the last unit's loads few.
 constexpr int kAdSlice = SLIM_DECODE_AD_SLICE;
 
-template <int FM>
+template <int FM, bool QA>
 SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) {
   constexpr int kSteps = kAdSlice / 32;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -338,31 +328,26 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
     acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
     amx[f] = 0u;
   }
-  // a.ad_sub consecutive slices of kAdSlice positions (one load round each). In a round at rs, lane
-  // group g takes the 32 positions rs + 32 g .. + 31, step t the eight at rs + 32 g + 8 t (for
-  // both operands, so every position enters once): a lane's 4-bit factor codes for the round are
-  // one 16-byte load, and the round lies in one 128-group (one scale).
+  // a.ad_sub consecutive slices of kAdSlice positions (one load round each); in a round at rs, step t
+  // of lane group g covers positions rs + 32 t + 8 g .. + 7, so a step's loads of 16 rows read 64
+  // contiguous bytes per row. A 4-bit factor row gives one 32-bit word of 8 codes per step; the
+  // round lies in one 128-group (one scale).
   const int64_t red8 = a.red / 8, ngk = (a.red + 127) / 128;
   const rsrc_t rq4 = make_rsrc(a.q4, a.r * a.red / 2);
   for (int sub = 0; sub < a.ad_sub; ++sub) {
     const int64_t rs = r0 + (int64_t)sub * kAdSlice;
-    const int64_t run = rs + 32 * g;
-    u32x4_t aq[kSteps][FM], bq[kSteps], qw = zero_u4();
-    uint32_t qs = 0;
+    u32x4_t aq[kSteps][FM], bq[kSteps];
+    uint32_t qw[kSteps], qs = 0;
 #pragma unroll
     for (int t = 0; t < kSteps; ++t) {
-      const int64_t rk = clamp_hi(run + 8 * t, a.red - 8);
+      const int64_t rk = clamp_hi(rs + 32 * t + 8 * g, a.red - 8);
 #pragma unroll
       for (int f = 0; f < FM; ++f)
         aq[t][f] = *reinterpret_cast<const u32x4_t*>(a.act + clamp_hi(16 * f + (lane & 15), a.M - 1) * a.red + rk);
-      if (!a.q4) bq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_q + jl * a.red + rk);
+      if (QA) qw[t] = __builtin_amdgcn_raw_buffer_load_b32(rq4, (uint32_t)((jl * red8 + rk / 8) * 4), 0, 0);
+      else bq[t] = *reinterpret_cast<const u32x4_t*>(a.ad_q + jl * a.red + rk);
     }
-    if (a.q4) {
-      // out-of-range offsets (a run past the reduction) read zero through the resource
-      qw = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                           rq4, (uint32_t)((jl * red8 + run / 8) * 4), 0, 0));
-      qs = a.q4s[jl * ngk + clamp_hi(rs / 128, ngk - 1)];
-    }
+    if (QA) qs = a.q4s[jl * ngk + clamp_hi(rs / 128, ngk - 1)];
     // this round's activations of row m = 16 f + lane % 16, scaled per row (see act_exponent): the
     // four lane groups of a row exchange their maxima; the round's product is unscaled in fp32
 #pragma unroll
@@ -372,7 +357,7 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
       uint32_t mx = 0;
 #pragma unroll
       for (int t = 0; t < kSteps; ++t) {
-        const bool ok = mok && run + 8 * t < a.red;
+        const bool ok = mok && rs + 32 * t + 8 * g < a.red;
         act8_to_f(aq[t][f], bf16, xf[t]);
 #pragma unroll
         for (int e = 0; e < 8; ++e) xf[t][e] = ok ? xf[t][e] : 0.f;
@@ -387,8 +372,8 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
       f4_t racc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < kSteps; ++t) {
-        const bool kok = run + 8 * t < a.red && jcol < a.r;
-        const h8_t qv = a.q4 ? dequant_word(qw[t], splat_h2(qs)) : __builtin_bit_cast(h8_t, bq[t]);
+        const bool kok = rs + 32 * t + 8 * g < a.red && jcol < a.r;
+        const h8_t qv = QA ? dequant_word(qw[t], splat_h2(qs)) : __builtin_bit_cast(h8_t, bq[t]);
         racc = mfma16(kok ? qv : zero_h8(), scale8_to_h(xf[t], sc), racc);
       }
       acc[f] = acc[f] + racc * inv;
@@ -434,14 +419,14 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
 // Blocks [0, jblocks * ad_split) are adapter units (dispatched first: their reduction is the
 // longer path); the rest are sparse blocks, block i of them taking slice i % split and row tiles
 // [(i / split) NU', + NU') with NU' = a.units (at most NU).
-template <bool BWD, int FM, int G, int NU>
+template <bool BWD, int FM, int G, int NU, bool QA>
 __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
   __shared__ __attribute__((aligned(16))) _Float16 xs[16 * FM * (512 * G + 8)];
   static_assert(sizeof(xs) >= 3 * FM * 64 * sizeof(f4_t), "adapter units sum their waves in xs");
   const int64_t nA = a.r > 0 ? a.ad_jblocks * a.ad_split : 0;
   const int64_t b = blockIdx.x;
   if (b < nA) {
-    decode_adapter_unit<FM>(a, b, reinterpret_cast<f4_t*>(xs));
+    decode_adapter_unit<FM, QA>(a, b, reinterpret_cast<f4_t*>(xs));
     return;
   }
   const int64_t i = b - nA, S = a.split;
@@ -459,32 +444,22 @@ __global__ void __launch_bounds__(256) k_decode(LayerArgs a) {
 // The loads of the first adapter pass and of the first eight partials do not depend on each other
 // and are all issued before any is used: one memory round trip for the common case (at most
 // eight splits, a rank within the waves' first passes).
-// Rank assignment of one pass at jbase: lane group g takes the run of 8 kSteps ranks starting at
-// jbase + 8 kSteps g, step t its eight ranks at jbase + 8 kSteps g + 8 t (for both operands). A
-// run lies within one 128-rank group (jbase is a multiple of 32 NW kSteps), so a 4-bit P needs one
-// scale per lane and pass, and its codes are kSteps / 4 loads of 16 bytes.
-template <int kSteps>
-SLIM_DEV int64_t finish_rank(int64_t jbase, int g, int t) { return jbase + 8 * kSteps * g + 8 * t; }
-
-template <int FM, int kSteps>
+// Step t of a pass at jbase: lane group g takes ranks jbase + 32 t + 8 g .. + 7 (for both operands).
+// A 4-bit P row gives one 32-bit word of 8 codes per step; the scale changes every 4 steps (one
+// 128-rank group; jbase is a multiple of 128).
+template <int FM, int kSteps, bool QA>
 SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lrow, int lane, u32x4_t* aq,
-                                   u32x4_t (*bq)[FM], uint32_t& ps) {
+                                   u32x4_t (*bq)[FM], uint32_t* ps) {
   const int g = lane >> 4;
-  if (a.p4) {
-    // 4-bit P: the run's codes (kSteps words of 8 ranks); past r or the buffer they read zero
-    const rsrc_t rp = make_rsrc(a.p4, a.rows * a.r / 2);
-    const int64_t run = finish_rank<kSteps>(jbase, g, 0);
-#pragma unroll
-    for (int i = 0; i < kSteps / 4; ++i)
-      aq[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                              rp, (uint32_t)((lrow * (a.r / 8) + run / 8 + 4 * i) * 4), 0, 0));
-    const int64_t ngr = (a.r + 127) / 128;
-    ps = a.p4s[lrow * ngr + clamp_hi(run / 128, ngr - 1)];
-  }
+  const rsrc_t rp = make_rsrc(a.p4, a.rows * a.r / 2);
+  const int64_t ngr = (a.r + 127) / 128;
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
-    const int64_t jj = clamp_hi(finish_rank<kSteps>(jbase, g, t), a.r - 8);
-    if (!a.p4) {
+    const int64_t jj = clamp_hi(jbase + 32 * t + 8 * g, a.r - 8);
+    if (QA) {
+      aq[t][0] = __builtin_amdgcn_raw_buffer_load_b32(rp, (uint32_t)((lrow * (a.r / 8) + jj / 8) * 4), 0, 0);
+      if (t % 4 == 0) ps[t / 4] = a.p4s[lrow * ngr + clamp_hi((jbase + 32 * t) / 128, ngr - 1)];
+    } else {
       // tiled: 8 consecutive ranks of a row stay within one 32 x 16 tile (jj % 16 is 0 or 8)
       const int64_t po = a.p_tiled ? ((lrow >> 5) * (a.r >> 4) + (jj >> 4)) * 512 + (lrow & 31) * 16 + (jj & 15)
                                    : lrow * a.r + jj;
@@ -498,14 +473,14 @@ SLIM_DEV void finish_adapter_loads(const LayerArgs& a, int64_t jbase, int64_t lr
 
 // One rank pass of the second product on the row-scaled fp16 T (D[row][m] = sum_j P[row][j] T[m][j]);
 // the caller unscales the sum of all passes.
-template <int FM, int kSteps>
+template <int FM, int kSteps, bool QA>
 SLIM_DEV void finish_adapter_mfma(const LayerArgs& a, int64_t jbase, int lane, const u32x4_t* aq,
-                                  const u32x4_t (*bq)[FM], uint32_t ps, f4_t* adacc) {
+                                  const u32x4_t (*bq)[FM], const uint32_t* ps, f4_t* adacc) {
   const int g = lane >> 4;
 #pragma unroll
   for (int t = 0; t < kSteps; ++t) {
-    const bool jok = finish_rank<kSteps>(jbase, g, t) < a.r;
-    const h8_t pv = a.p4 ? dequant_word(aq[t / 4][t % 4], splat_h2(ps)) : __builtin_bit_cast(h8_t, aq[t]);
+    const bool jok = jbase + 32 * t + 8 * g < a.r;
+    const h8_t pv = QA ? dequant_word(aq[t][0], splat_h2(ps[t / 4])) : __builtin_bit_cast(h8_t, aq[t]);
     const h8_t av = jok ? pv : zero_h8();
 #pragma unroll
     for (int f = 0; f < FM; ++f) {
@@ -515,7 +490,7 @@ SLIM_DEV void finish_adapter_mfma(const LayerArgs& a, int64_t jbase, int lane, c
   }
 }
 
-template <int FM, int NW>
+template <int FM, int NW, bool QA>
 __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
   constexpr int kSteps = (FM == 1 ? 16 : 8) / NW;   // 32-rank steps per pass of one wave
   __shared__ f4_t hand[NW > 1 ? FM : 1][64];
@@ -530,10 +505,10 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
   const rsrc_t pr = make_rsrc(a.part + (rt * S * 4 + w16) * (int64_t)(FM * 256), ((int64_t)(S - 1) * 4 + 1) * FM * 256 * 4);
   const int64_t jfirst = (int64_t)h * 32 * kSteps;
   u32x4_t aq[kSteps], bq[kSteps][FM];
-  uint32_t ps = 0;
+  uint32_t ps[kSteps / 4];
   float trinv[FM];
   if (a.r > 0) {
-    finish_adapter_loads<FM, kSteps>(a, jfirst, lrow, lane, aq, bq, ps);
+    finish_adapter_loads<FM, kSteps, QA>(a, jfirst, lrow, lane, aq, bq, ps);
 #pragma unroll
     for (int f = 0; f < FM; ++f) trinv[f] = a.trinv[clamp_hi(16 * f + (lane & 15), a.M - 1)];
   }
@@ -564,10 +539,10 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
     f4_t adacc[FM];
 #pragma unroll
     for (int f = 0; f < FM; ++f) adacc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-    finish_adapter_mfma<FM, kSteps>(a, jfirst, lane, aq, bq, ps, adacc);
+    finish_adapter_mfma<FM, kSteps, QA>(a, jfirst, lane, aq, bq, ps, adacc);
     for (int64_t jbase = jfirst + NW * 32 * kSteps; jbase < a.r; jbase += NW * 32 * kSteps) {
-      finish_adapter_loads<FM, kSteps>(a, jbase, lrow, lane, aq, bq, ps);
-      finish_adapter_mfma<FM, kSteps>(a, jbase, lane, aq, bq, ps, adacc);
+      finish_adapter_loads<FM, kSteps, QA>(a, jbase, lrow, lane, aq, bq, ps);
+      finish_adapter_mfma<FM, kSteps, QA>(a, jbase, lane, aq, bq, ps, adacc);
     }
 #pragma unroll
     for (int f = 0; f < FM; ++f) acc[f] = acc[f] + adacc[f] * trinv[f];
@@ -1103,20 +1078,20 @@ __global__ void __launch_bounds__(256) k_adapter_finish(const u32x4_t* __restric
 }
 
 // ------------------------------------------------------------------------------ launch
-template <bool BWD, int FM, int G, int NU>
+template <bool BWD, int FM, int G, int NU, bool QA>
 void launch_decode(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
   SlimKernelTimer timer(BWD ? "decode_bwd" : "decode_fwd", s);
   dim3 grid((unsigned)(p.sp_blocks + (a.r > 0 ? p.ad_jblocks * p.ad_split : 0)));
-  SLIM_LAUNCH(timer, (k_decode<BWD, FM, G, NU>), grid, dim3(256), s, a);
+  SLIM_LAUNCH(timer, (k_decode<BWD, FM, G, NU, QA>), grid, dim3(256), s, a);
 }
 
-template <bool BWD, int FM, int G>
+template <bool BWD, int FM, int G, bool QA>
 void launch_decode_units(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
-  if (p.dec_units > 1) launch_decode<BWD, FM, G, BWD ? 2 : kDecodeMaxUnits>(a, p, s);
-  else launch_decode<BWD, FM, G, 1>(a, p, s);
+  if (p.dec_units > 1) launch_decode<BWD, FM, G, BWD ? 2 : kDecodeMaxUnits, QA>(a, p, s);
+  else launch_decode<BWD, FM, G, 1, QA>(a, p, s);
 }
 
-template <int FM>
+template <int FM, bool QA>
 void launch_finish(const LayerArgs& a, bool bwd, hipStream_t s) {
   SlimKernelTimer timer(bwd ? "finish_bwd" : "finish_fwd", s);
   // two waves per 16 rows, splitting the rank, when the rank fills more than one wave's pass of
@@ -1124,23 +1099,36 @@ void launch_finish(const LayerArgs& a, bool bwd, hipStream_t s) {
   // loads (4096^2 layer at M 16: step 11.7 -> 11.3 us); with many rows one wave per 16 rows
   // already fills the CUs
   const dim3 grid((unsigned)((a.rows + 15) / 16));
-  if (a.r > 16 * (FM == 1 ? 16 : 8) && a.rows <= 16384) SLIM_LAUNCH(timer, (k_finish<FM, 2>), grid, dim3(128), s, a);
-  else SLIM_LAUNCH(timer, (k_finish<FM, 1>), grid, dim3(64), s, a);
+  if (a.r > 16 * (FM == 1 ? 16 : 8) && a.rows <= 16384) SLIM_LAUNCH(timer, (k_finish<FM, 2, QA>), grid, dim3(128), s, a);
+  else SLIM_LAUNCH(timer, (k_finish<FM, 1, QA>), grid, dim3(64), s, a);
+}
+
+template <bool BWD, bool QA>
+void launch_small_m(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
+  if (p.dec_fm == 1) {
+    if (p.dec_g == 1) launch_decode_units<BWD, 1, 1, QA>(a, p, s);
+    else launch_decode_units<BWD, 1, 2, QA>(a, p, s);
+  } else {
+    launch_decode_units<BWD, 2, 1, QA>(a, p, s);
+  }
 }
 
 template <bool BWD>
 int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int act_bf16, char* ws, hipStream_t s) {
   if (p.decode) {
-    if (p.dec_fm == 1) {
-      if (p.dec_g == 1) launch_decode_units<BWD, 1, 1>(a, p, s);
-      else launch_decode_units<BWD, 1, 2>(a, p, s);
-    } else {
-      launch_decode_units<BWD, 2, 1>(a, p, s);
-    }
+    // 4-bit adapters (forward only) are a template variant, so neither kernel branches around loads
+    const bool qa = !BWD && a.q4 != nullptr;
+    if (qa) launch_small_m<BWD, true>(a, p, s);
+    else launch_small_m<BWD, false>(a, p, s);
     if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
     if (a.finish) {
-      if (p.dec_fm == 1) launch_finish<1>(a, BWD, s);
-      else launch_finish<2>(a, BWD, s);
+      if (qa) {
+        if (p.dec_fm == 1) launch_finish<1, true>(a, BWD, s);
+        else launch_finish<2, true>(a, BWD, s);
+      } else {
+        if (p.dec_fm == 1) launch_finish<1, false>(a, BWD, s);
+        else launch_finish<2, false>(a, BWD, s);
+      }
       if (hipGetLastError() != hipSuccess) return SLIM_EDEVICE;
     }
     return SLIM_OK;
