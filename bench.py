@@ -33,6 +33,7 @@ METRIC = "dense-equiv TFLOP/s (M≥2048) and weight-stream HBM GB/s (M≤16), 2:
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
 MFMA_F16_PEAK_TFS = 2516.6       # MI355X dense fp16/bf16 MFMA
 PACK_BYTES_PER_WEIGHT = 0.390625  # 4-bit code x 1/2 + 2-bit index x 1/2 + fp16 scale / 128
+WARM_MS = 200.0                   # sustained work before the measured replay (clock ramp-up)
 
 
 def parse():
@@ -163,7 +164,7 @@ def adapter_bytes(K, N, r, qadapter):
     return r * K // 2 + 2 * r * ((K + 127) // 128) + N * r // 2 + 2 * N * ((r + 127) // 128)
 
 
-def measure(wk, m, steps, warmup, dispatches, cyc_per_ms, qadapter=False):
+def measure(wk, m, steps, warmup, dispatches, qadapter=False):
     """Set up one workload (synthetic inputs resident in HBM, packed once, > 3x the MALL of distinct
     weight copies) and time it: K timed steps back to back, then `dispatches` steps with per-kernel
     events. Every pass takes the next copy from one running counter, so a copy is read again only
@@ -249,39 +250,58 @@ def measure(wk, m, steps, warmup, dispatches, cyc_per_ms, qadapter=False):
             else:
                 slim.linear(pl["x"], c["pack"], c["ad"], out=pl["out"], ws=ws)
 
-    # The stream is first given a bounded busy kernel (torch.cuda._sleep) long enough for the host
-    # to enqueue every timed step behind it; the GPU then runs the K steps back to back and the two
-    # events bracket GPU time only, not Python launch overhead.
+    # Timed region: the K steps are captured once into a HIP graph (the library records only kernel
+    # launches, so a replay runs exactly the eager steps back to back, with no host launch gaps), and a
+    # second graph holds the steps over the other weight copies, so that in the cycle (filler, timed)
+    # every copy is read once. Both are replayed for at least WARM_MS before the measured replay so the
+    # GPU runs at the clock of sustained work; two events bracket exactly the K timed steps.
     stream = torch.cuda.current_stream()
-
-    def backlog(ms):
-        torch.cuda._sleep(int(cyc_per_ms * ms))
-
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     t = time.perf_counter()
     for _ in range(5):
         step()
-    host_ms = (time.perf_counter() - t) / 5 * 1e3       # host enqueue cost of one step
+    host_ms = (time.perf_counter() - t) / 5 * 1e3       # host enqueue cost of one eager step
     torch.cuda.synchronize()
+    n_fill = max(0, n_copies - steps)
+    g_fill, g_timed = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    if n_fill:
+        with torch.cuda.graph(g_fill):
+            for _ in range(n_fill):
+                step()
+    with torch.cuda.graph(g_timed):
+        for _ in range(steps):
+            step()
+    torch.cuda.synchronize()
+    tw = time.perf_counter()
+    warm_cycles = 0
+    while (time.perf_counter() - tw) * 1e3 < WARM_MS and warm_cycles < 200:
+        if n_fill:
+            g_fill.replay()
+        g_timed.replay()
+        warm_cycles += 1
+        torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    backlog(min(2000.0, 20.0 + 2.0 * host_ms * steps))
+    if n_fill:
+        g_fill.replay()
     ev0.record(stream)
-    for _ in range(steps):
-        step()
+    g_timed.replay()
     ev1.record(stream)
     torch.cuda.synchronize()
     ms_per_step = ev0.elapsed_time(ev1) / steps
+    del g_fill, g_timed
     print(f"[bench] {wk} M={M}: {ms_per_step * 1e3:.2f} us/step over {steps} steps "
-          f"({n_copies} weight copies, host enqueue {host_ms * 1e3:.0f} us/step, setup {setup_s:.1f}s)",
-          file=sys.stderr, flush=True)
+          f"({n_copies} weight copies, host enqueue {host_ms * 1e3:.0f} us/step, {warm_cycles} warm-up cycles, "
+          f"setup {setup_s:.1f}s)", file=sys.stderr, flush=True)
 
     # Per-kernel durations: each library launch records a start and a stop event as part of its own
     # dispatch (slim_timing_*, hipExtLaunchKernel), so they carry the kernel's begin and end times.
+    # Event-recorded launches leave the GPU idle for several microseconds between kernels, longer than
+    # the host needs to enqueue the next one, so the pass runs right after the warm replays without a
+    # backlog; a kernel's own duration is what the events measure.
     slim.slim_timing_reset()
     slim.slim_timing_enable(True)
-    backlog(min(2000.0, 20.0 + 3.0 * host_ms * dispatches))
     for _ in range(dispatches):
         step()
     torch.cuda.synchronize()
@@ -356,17 +376,15 @@ def main():
     import torch
 
     torch.cuda.set_device(0)
-    cyc_per_ms = sleep_calibration(torch)
     dispatches = max(args.dispatches, args.steps)
     if args.qadapter and args.workload == "mlp70b_bwd":
         print("--qadapter applies to the forward only", file=sys.stderr)
         sys.exit(2)
-    res, layers, M, bwd = measure(args.workload, args.m, args.steps, args.warmup, dispatches, cyc_per_ms,
-                                  args.qadapter)
+    res, layers, M, bwd = measure(args.workload, args.m, args.steps, args.warmup, dispatches, args.qadapter)
     second = None
     if args.workload == "decode" and not args.no_prefill:
         # the M >= 2048 half of the metric: the prefill layer (11008 x 4096, rank 384) at M = 2048
-        s_res, _, _, _ = measure("prefill", None, args.steps, args.warmup, dispatches, cyc_per_ms, args.qadapter)
+        s_res, _, _, _ = measure("prefill", None, args.steps, args.warmup, dispatches, args.qadapter)
         second = {"metric": "dense-equiv TFLOP/s (M≥2048)", **s_res}
 
     cpu = None
@@ -397,17 +415,6 @@ def main():
     if second is not None:
         out["prefill"] = second
     print(json.dumps(out))
-
-
-def sleep_calibration(torch):
-    """GPU clock cycles per millisecond of torch.cuda._sleep, measured with events."""
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda._sleep(1000)
-    e0.record()
-    torch.cuda._sleep(10_000_000)
-    e1.record()
-    torch.cuda.synchronize()
-    return 10_000_000 / max(e0.elapsed_time(e1), 1e-3)
 
 
 def host_cpu():
