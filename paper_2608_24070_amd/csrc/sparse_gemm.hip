@@ -183,7 +183,6 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
   const int64_t cl = c0 + (int64_t)qa * G;      // first chunk (group) of this lane group
 
   DecodeWords<G> wb[NU > 1 ? 2 : 1];
-  decode_load_words<BWD, G>(a, rt0, cl, lane, wave, wb[0]);
   const int64_t sgroup = rt0 * 64 / 128;
   // Activations of the slice: wave w stages rows m = w + 4 i (i < MC / 4), each row as G runs of 64
   // lanes x 8 positions (position 8 (lane + 64 j)), so a wave holds whole rows: each row's scaling
@@ -201,10 +200,16 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
 #pragma unroll
     for (int j = 0; j < G; ++j)
       sv[j] = *reinterpret_cast<const u32x4_t*>(a.scales + sgroup * a.red + clamp_hi(red0 + 8 * (lane + 64 * j), a.red - 8));
+  // the first unit's packed words after the activations: loads complete in order, so the staging
+  // below waits for the activations only and runs while the words are still in flight
+  decode_load_words<BWD, G>(a, rt0, cl, lane, wave, wb[0]);
   // The staged B operand in fp32: the activations, in the backward times the fp16 scales of the
   // block's 128-row group (the product is formed exactly in fp32 and rounded once, below), scaled
   // per row (see act_exponent).
+  // (the input type is one uniform choice around the whole staging, not a branch per vector)
   __shared__ float runscale[MC];
+  auto stage = [&](auto bfc) {
+  constexpr bool kBf16 = decltype(bfc)::value;
 #pragma unroll
   for (int i = 0; i < RW; ++i) {
     const int m = wave + 4 * i;
@@ -213,7 +218,7 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
 #pragma unroll
     for (int j = 0; j < G; ++j) {
       const bool ok = m < a.M && red0 + 8 * (lane + 64 * j) < a.red;
-      act8_to_f(xv[i][j], bf16, xf[j]);
+      act8_to_f(xv[i][j], kBf16, xf[j]);
       if (BWD) {
         float sf[8];
         act8_to_f(sv[j], false, sf);
@@ -230,6 +235,9 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
 #pragma unroll
     for (int j = 0; j < G; ++j) *reinterpret_cast<h8_t*>(&xs[m * LDX + 8 * (lane + 64 * j)]) = scale8_to_h(xf[j], sc);
   }
+  };
+  if (bf16) stage(std::true_type{});
+  else stage(std::false_type{});
   __syncthreads();
   float unscale[FM];
 #pragma unroll
@@ -237,19 +245,10 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
 
   const int qb = lane >> 4;
   const int pbase = 128 * G * (qb >> 1) + 8 * (qb & 1);
-  f4_t out[NU][FM];
-#pragma unroll
-  for (int k = 0; k < NU; ++k) {
-    if (rt0 + k >= rt1) break;
-    // the next unit's words (the last unit reloads itself: loads stay unconditional)
-    if (NU > 1) {
-      decode_load_words<BWD, G>(a, rt0 + k + 1 < rt1 ? rt0 + k + 1 : rt1 - 1, cl, lane, wave, wb[(k + 1) & 1]);
-      __builtin_amdgcn_sched_barrier(0);   // keep them ahead of this unit's work
-    }
-    const DecodeWords<G>& w = wb[k & 1];
-    f4_t acc[FM];
-#pragma unroll
-    for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+  // the sparse product of one unit; groups past the reduction (a ragged last slice) are masked,
+  // which only a block whose slice runs past the end needs (a uniform choice between two copies)
+  auto unit_mfma = [&](const DecodeWords<G>& w, f4_t* acc, auto maskc) {
+    constexpr bool kMask = decltype(maskc)::value;
 #pragma unroll
     for (int gi = 0; gi < G; ++gi) {
       const bool gok = cl + gi < nchunks;
@@ -258,7 +257,7 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
       for (int t4 = 0; t4 < 8; ++t4) {
         const uint32_t word = w.cw[2 * gi + (t4 >> 2)][t4 & 3];
         h8_t av = BWD ? dequant_word_int(word) : dequant_word(word, s2);
-        av = gok ? av : zero_h8();
+        if (kMask) av = gok ? av : zero_h8();
         const int idx = (int)w.mw[gi][t4 >> 1];
         const int p0 = pbase + 16 * (8 * gi + t4);
 #pragma unroll
@@ -269,6 +268,22 @@ SLIM_DEV void decode_sparse_range(const LayerArgs& a, int s, int64_t rt0, int64_
         }
       }
     }
+  };
+  const bool ragged = c0 + 4 * G > nchunks;
+  f4_t out[NU][FM];
+#pragma unroll
+  for (int k = 0; k < NU; ++k) {
+    if (rt0 + k >= rt1) break;
+    // the next unit's words (the last unit reloads itself: loads stay unconditional)
+    if (NU > 1) {
+      decode_load_words<BWD, G>(a, rt0 + k + 1 < rt1 ? rt0 + k + 1 : rt1 - 1, cl, lane, wave, wb[(k + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);   // keep them ahead of this unit's work
+    }
+    f4_t acc[FM];
+#pragma unroll
+    for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
+    if (ragged) unit_mfma(wb[k & 1], acc, std::true_type{});
+    else unit_mfma(wb[k & 1], acc, std::false_type{});
 #pragma unroll
     for (int f = 0; f < FM; ++f) out[k][f] = acc[f] * unscale[f];   // lane (m + 16 (row / 4)): column m = lane % 16
   }
@@ -334,6 +349,9 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
   // round lies in one 128-group (one scale).
   const int64_t red8 = a.red / 8, ngk = (a.red + 127) / 128;
   const rsrc_t rq4 = make_rsrc(a.q4, a.r * a.red / 2);
+  // (the input type is one uniform choice around the rounds, not a branch per vector)
+  auto rounds = [&](auto bfc) {
+  constexpr bool kBf16 = decltype(bfc)::value;
   for (int sub = 0; sub < a.ad_sub; ++sub) {
     const int64_t rs = r0 + (int64_t)sub * kAdSlice;
     u32x4_t aq[kSteps][FM], bq[kSteps];
@@ -358,7 +376,7 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
 #pragma unroll
       for (int t = 0; t < kSteps; ++t) {
         const bool ok = mok && rs + 32 * t + 8 * g < a.red;
-        act8_to_f(aq[t][f], bf16, xf[t]);
+        act8_to_f(aq[t][f], kBf16, xf[t]);
 #pragma unroll
         for (int e = 0; e < 8; ++e) xf[t][e] = ok ? xf[t][e] : 0.f;
         mx = max(mx, max_abs_bits8(xf[t]));
@@ -379,6 +397,9 @@ SLIM_DEV void decode_adapter_unit(const LayerArgs& a, int64_t v, f4_t* red_lds) 
       acc[f] = acc[f] + racc * inv;
     }
   }
+  };
+  if (bf16) rounds(std::true_type{});
+  else rounds(std::false_type{});
   // the unit's sum: waves 1..3 hand theirs (and their maxima) to wave 0 through LDS
   __shared__ uint32_t mx_lds[3][FM][64];
   if (wave > 0)
