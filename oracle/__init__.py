@@ -16,7 +16,13 @@ the thesis' definitions:
   eq. sparse_plus_low_rank).
 * SLoPe's double-pruned input gradient dX = dY W^{R,C} (eq. sparse_backward_input)
   and Lemma sparsity_ratio.
+* The steps of SLoPe's training step after the input gradient (``slope_train``): the
+  half-precision value packs of W^R and W^{R,C}, the masked and compressed weight
+  gradient (eq. sparse_backward_weight), the same-pattern sparse add and the pack update
+  (Alg. "Accelerated Sparse Pretraining Algorithm for a Linear Layer"; appendix
+  "Implementation details").
 
 Parity status per function is stated in ``slim_oracle``'s module docstring.
 """
 from . import slim_oracle  # noqa: F401
+from . import slope_train  # noqa: F401
