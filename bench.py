@@ -61,7 +61,8 @@ def parse():
 ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("include/slim.h", "paper_2608_24070_amd/csrc/api.cpp", "paper_2608_24070_amd/csrc/slim_host.h",
                   "paper_2608_24070_amd/csrc/slim_device.h", "paper_2608_24070_amd/csrc/sparse_gemm.hip",
-                  "paper_2608_24070_amd/csrc/adapter_gemm.hip", "paper_2608_24070_amd/csrc/pack.hip")
+                  "paper_2608_24070_amd/csrc/adapter_gemm.hip", "paper_2608_24070_amd/csrc/pack.hip",
+                  "paper_2608_24070_amd/csrc/train.hip")
 
 
 def kernel_source_hash():

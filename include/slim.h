@@ -307,6 +307,69 @@ int slim_linear_noalloc(const void* X, int xdtype, int64_t M, int64_t N, int64_t
                         int64_t r, float* Y, void* stream);
 
 /*
+ * ---- The rest of SLoPe's sparse training step (SLoPe, Alg. "Accelerated Sparse Pretraining
+ * Algorithm for a Linear Layer": setup of the sparse weight and its transpose, the weight gradient
+ * with the weight's mask, the sparse add of the optimizer with weight decay, and the update of both
+ * sparse matrices; appendix "Implementation details"). Training weights are kept in half precision,
+ * so these calls work on value packs instead of the int4 inference pack:
+ *
+ *   vals   fp16 bits [rows, len/2], row-major: for aligned group g of four positions of a row,
+ *          the values at its two kept positions, the lower position first (2g, 2g + 1);
+ *   meta   uint8 [rows, len/8], row-major, the inference pack's index format (little-endian
+ *          half-word b covers positions 16b .. 16b+15; its group c holds the kept offsets
+ *          i0 < i1 in bits 4c..4c+1 and 4c+2..4c+3).
+ *
+ * The forward pack of W^R has rows = N, len = K (2:4 along K); its transposed pack W^{R,C} has
+ * rows = K, len = N (2:4 along N). Every pointer is device memory, 16-byte aligned, owned by the
+ * caller; every call enqueues on `stream` and returns after the launch unless stated otherwise.
+ * ----
+ *
+ * slim_pack16 - setup of W^R from fp32 W [N, K] (row-major): per aligned group of four along K,
+ * keep the two largest |w| (ties: lower position), store them rounded to fp16 (nearest, ties to
+ * even) in vals [N, K/2] with meta [N, K/8]; mask (optional, uint8 [N, K], 0/1) receives M^R.
+ * K % 16 == 0. Synchronous (reads back a status word): SLIM_ENONFINITE if W holds a NaN or Inf.
+ */
+int slim_pack16(const float* W, int64_t N, int64_t K, uint16_t* vals, uint8_t* meta, uint8_t* mask,
+                void* stream);
+
+/*
+ * slim_pack16_t - W^{R,C} from a W^R value pack (SLoPe eq. sparse_backward_input's double
+ * pruning): for each column k and aligned group of four rows, keep the two entries ranked first by
+ * (|v| descending, M^R bit descending, row ascending) and store them (0 for a kept slot M^R had
+ * dropped) in valsT [K, N/2] with metaT [K, N/8]. Run at setup and after every update of vals.
+ * N % 64 == 0 and K % 64 == 0; the values must be finite.
+ */
+int slim_pack16_t(const uint16_t* vals, const uint8_t* meta, int64_t N, int64_t K, uint16_t* valsT,
+                  uint8_t* metaT, void* stream);
+
+/*
+ * slim_grad_w - BWD-1 with the weight's mask (SLoPe eq. sparse_backward_weight and "pruneAndCompress"):
+ * gW [N, K/2] fp32 = (dY^T X) at the positions meta (M^R, [N, K/8]) keeps, in the value-pack order.
+ * dY [M, N] and X [M, K] row-major, both of `dtype` (SLIM_F16 or SLIM_BF16); products exact in
+ * fp32, accumulated in fp32 along M (the order differs from a sequential sum). N % 128 == 0,
+ * K % 128 == 0, M >= 1; SLIM_EUNSUPPORTED if M N or M K reaches 2^31 elements.
+ */
+int slim_grad_w(const void* dY, const void* X, int dtype, int64_t M, int64_t N, int64_t K, const uint8_t* meta,
+                float* gW, void* stream);
+
+/*
+ * slim_sparse_add - out = beta A + gamma B on `count` compressed values sharing one pattern ("sparseAdd":
+ * in the training step, A the masked gradient with beta = 1 / loss scale and B the weight values
+ * with gamma = the weight decay). A and out fp32, B fp16 bits; computed in fp32 as
+ * fma(gamma, B, beta A). count % 8 == 0; out may alias A.
+ */
+int slim_sparse_add(const float* A, const uint16_t* B, float beta, float gamma, float* out, int64_t count,
+                    void* stream);
+
+/*
+ * slim_update_pack16 - write the optimizer's new compressed values Wnew (fp32, `count` of them, the
+ * pack's order) into vals, rounded to fp16 (nearest, ties to even); the pattern (meta) is unchanged.
+ * Follow with slim_pack16_t to rebuild the transposed pack ("updateSparseMatrix" on both).
+ * count % 8 == 0.
+ */
+int slim_update_pack16(const float* Wnew, int64_t count, uint16_t* vals, void* stream);
+
+/*
  * Per-kernel timing for benchmarks (host-side bookkeeping; not part of the layer's math).
  * slim_timing_enable(1) makes every later kernel launch of this library record a hipEvent
  * before and after itself on the caller's stream. slim_timing_read waits for the recorded

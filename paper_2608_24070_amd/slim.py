@@ -44,6 +44,11 @@ _SIGS = {
                                       _c_p, _c_i64, _c_p, _c_p, ctypes.c_size_t, _c_p]),
     "slim_linear_noalloc": (ctypes.c_int, [_c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p,
                                            _c_i64, _c_p, _c_p]),
+    "slim_pack16": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p]),
+    "slim_pack16_t": (ctypes.c_int, [_c_p, _c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
+    "slim_grad_w": (ctypes.c_int, [_c_p, _c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
+    "slim_sparse_add": (ctypes.c_int, [_c_p, _c_p, ctypes.c_float, ctypes.c_float, _c_p, _c_i64, _c_p]),
+    "slim_update_pack16": (ctypes.c_int, [_c_p, _c_i64, _c_p, _c_p]),
     "slim_timing_enable": (ctypes.c_int, [ctypes.c_int]),
     "slim_timing_reset": (ctypes.c_int, []),
     "slim_timing_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_size_t]),
@@ -153,6 +158,26 @@ SLIM_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 def slim_linear_bwd_dx(dY, dydtype, M, N, K, codesT, metaT, scalesT, L, R, r, dX, ws, ws_bytes, stream) -> int:
     return lib().slim_linear_bwd_dx(dY, dydtype, M, N, K, codesT, metaT, scalesT, L, R, r, dX, ws, ws_bytes, stream)
+
+
+def slim_pack16(W, N, K, vals, meta, mask, stream) -> int:
+    return lib().slim_pack16(W, N, K, vals, meta, mask, stream)
+
+
+def slim_pack16_t(vals, meta, N, K, valsT, metaT, stream) -> int:
+    return lib().slim_pack16_t(vals, meta, N, K, valsT, metaT, stream)
+
+
+def slim_grad_w(dY, X, dtype, M, N, K, meta, gW, stream) -> int:
+    return lib().slim_grad_w(dY, X, dtype, M, N, K, meta, gW, stream)
+
+
+def slim_sparse_add(A, B, beta, gamma, out, count, stream) -> int:
+    return lib().slim_sparse_add(A, B, beta, gamma, out, count, stream)
+
+
+def slim_update_pack16(Wnew, count, vals, stream) -> int:
+    return lib().slim_update_pack16(Wnew, count, vals, stream)
 
 
 def slim_timing_enable(on: bool) -> int:
@@ -378,3 +403,68 @@ def linear_qa(X, packed: dict, qadapter: dict, out=None, ws=None, stream=None):
                         _ptr(qadapter["Rs"]), r, _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "slim_linear_qa")
     return out
+
+
+# ------------------------------------------------- training step (value packs, SLoPe)
+
+def pack16(W, with_mask: bool = False, stream=None) -> dict:
+    """slim_pack16 of fp32 W [N, K]: {"vals" int16 [N, K/2] (fp16 bits), "meta" uint8 [N, K/8], "N", "K"}
+    (+ "mask" uint8 [N, K])."""
+    torch = _torch()
+    _on_gpu(W)
+    N, K = W.shape
+    dev = W.device
+    out = {"vals": torch.empty((N, K // 2), dtype=torch.int16, device=dev),
+           "meta": torch.empty((N, K // 8), dtype=torch.uint8, device=dev), "N": N, "K": K}
+    mask = torch.empty((N, K), dtype=torch.uint8, device=dev) if with_mask else None
+    _check(slim_pack16(_ptr(W), N, K, _ptr(out["vals"]), _ptr(out["meta"]), _ptr(mask), _stream(stream)),
+           "slim_pack16")
+    if with_mask:
+        out["mask"] = mask
+    return out
+
+
+def pack16_t(p: dict, out: dict | None = None, stream=None) -> dict:
+    """slim_pack16_t of a value pack: {"valsT" int16 [K, N/2], "metaT" uint8 [K, N/8]} (into `out` if given)."""
+    torch = _torch()
+    N, K = p["N"], p["K"]
+    dev = p["vals"].device
+    if out is None:
+        out = {"valsT": torch.empty((K, N // 2), dtype=torch.int16, device=dev),
+               "metaT": torch.empty((K, N // 8), dtype=torch.uint8, device=dev)}
+    _check(slim_pack16_t(_ptr(p["vals"]), _ptr(p["meta"]), N, K, _ptr(out["valsT"]), _ptr(out["metaT"]),
+                         _stream(stream)), "slim_pack16_t")
+    return out
+
+
+def grad_w(dY, X, p: dict, out=None, stream=None):
+    """slim_grad_w: fp32 [N, K/2] = (dY^T X) at the kept positions of the value pack `p` (dY [M, N], X [M, K])."""
+    torch = _torch()
+    _on_gpu(dY, X, out)
+    M, N = dY.shape
+    K = X.shape[1]
+    if dY.dtype != X.dtype:
+        raise ValueError("dY and X must have one dtype")
+    if out is None:
+        out = torch.empty((N, K // 2), dtype=torch.float32, device=dY.device)
+    _check(slim_grad_w(_ptr(dY), _ptr(X), _dtype_code(dY), M, N, K, _ptr(p["meta"]), _ptr(out), _stream(stream)),
+           "slim_grad_w")
+    return out
+
+
+def sparse_add(A, B, beta: float, gamma: float, out=None, stream=None):
+    """slim_sparse_add: beta A + gamma B (A fp32, B fp16 bits as int16 or float16), same shape."""
+    torch = _torch()
+    _on_gpu(A, B, out)
+    if out is None:
+        out = torch.empty_like(A)
+    _check(slim_sparse_add(_ptr(A), _ptr(B), float(beta), float(gamma), _ptr(out), A.numel(), _stream(stream)),
+           "slim_sparse_add")
+    return out
+
+
+def update_pack16(Wnew, p: dict, stream=None) -> dict:
+    """slim_update_pack16: new fp32 values [N, K/2] into p["vals"] (in place); returns p."""
+    _on_gpu(Wnew)
+    _check(slim_update_pack16(_ptr(Wnew), Wnew.numel(), _ptr(p["vals"]), _stream(stream)), "slim_update_pack16")
+    return p

@@ -1,0 +1,173 @@
+"""The training-step calls (slim_pack16, slim_pack16_t, slim_grad_w, slim_sparse_add,
+slim_update_pack16) against the oracle in oracle/slope_train.py: bit-exact packs, and the
+gradient within the fp32 summation bound."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import slope_train as T
+from paper_2608_24070_amd import slim, synth
+from tests.gpu_common import dev, dev_bits, host
+
+pytestmark = pytest.mark.gpu
+
+
+def _weights(n, k, seed, tied=False):
+    rng = synth.stream(seed, "gtrain/W")
+    if tied:
+        lv = rng.integers(0, 5, size=(n, k)).astype(np.float32) * np.float32(0.25)
+        w = lv * np.where(rng.random((n, k)) < 0.5, -1.0, 1.0).astype(np.float32)
+        w[rng.random((n, k)) < 0.05] = -0.0
+        return w
+    return (rng.standard_normal((n, k)) * 0.02).astype(np.float32)
+
+
+def _u16(t):
+    a = host(t)
+    return a.view(np.uint16) if a.dtype == np.int16 else a
+
+
+def _act(m, n, seed, name, dtype):
+    bits, vals = synth.activations(m, n, seed=seed, name=name, dtype=dtype)
+    return bits, vals
+
+
+@pytest.mark.parametrize("n,k,tied", [(128, 256, False), (512, 512, False), (256, 128, True), (16, 48, True)])
+def test_pack16_bit_exact(n, k, tied):
+    print(f"pack16 n={n} k={k} tied={tied}", flush=True)
+    W = _weights(n, k, 11, tied)
+    p = slim.pack16(dev(W), with_mask=True)
+    ref = T.pack16(W)
+    assert np.array_equal(_u16(p["vals"]), ref["vals"])
+    assert np.array_equal(host(p["meta"]), ref["meta"])
+    assert np.array_equal(host(p["mask"]), ref["mask"])
+
+
+def test_pack16_rejects_non_finite():
+    W = _weights(64, 128, 12)
+    W[5, 7] = np.nan
+    with pytest.raises(slim.SlimError) as e:
+        slim.pack16(dev(W))
+    assert e.value.status == slim.SLIM_ENONFINITE
+
+
+@pytest.mark.parametrize("n,k,tied", [(64, 64, True), (256, 512, False), (1024, 192, True), (128, 1024, False)])
+def test_pack16_t_bit_exact(n, k, tied):
+    print(f"pack16_t n={n} k={k} tied={tied}", flush=True)
+    W = _weights(n, k, 13, tied)
+    p = slim.pack16(dev(W))
+    pt = slim.pack16_t(p)
+    ref = T.pack16_t(_u16(p["vals"]), host(p["meta"]), n, k)
+    assert np.array_equal(_u16(pt["valsT"]), ref["valsT"])
+    assert np.array_equal(host(pt["metaT"]), ref["metaT"])
+
+
+def _grad_bound(dY, X, meta, n, k):
+    """|fp32 sum - exact| <= 2 M u sum |products| (u = 2^-24), for any order of an M-term fp32 sum."""
+    m = dY.shape[0]
+    absg = T.grad_w(np.abs(dY), np.abs(X), meta, n, k)
+    return 2.0 * m * 2.0 ** -24 * absg + 1e-30
+
+
+@pytest.mark.parametrize("m,n,k", [(1, 128, 128), (37, 256, 384), (200, 512, 256), (1000, 384, 512), (64, 128, 640)])
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_grad_w_parity(m, n, k, dtype):
+    print(f"grad_w m={m} n={n} k={k} {dtype}", flush=True)
+    p = slim.pack16(dev(_weights(n, k, 14)))
+    yb, dYv = _act(m, n, 14, "gtrain/dY", dtype)
+    xb, Xv = _act(m, k, 15, "gtrain/X", dtype)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float16
+    g = host(slim.grad_w(dev_bits(yb, tdt), dev_bits(xb, tdt), p))
+    meta = host(p["meta"])
+    ref = T.grad_w(dYv, Xv, meta, n, k)
+    assert g.shape == ref.shape
+    assert np.all(np.abs(g - ref) <= _grad_bound(dYv, Xv, meta, n, k))
+
+
+def test_grad_w_full_size_sampled_rows():
+    # 70B MLP projection: dY [8192 x 28672], X [8192 x 8192], compressed gradient [28672 x 4096]
+    m, n, k = 8192, 28672, 8192
+    print(f"grad_w full size m={m} n={n} k={k}", flush=True)
+    rng = synth.stream(16, "gtrain/full")
+    dYv = (rng.standard_normal((m, n), dtype=np.float32) * 0.01).astype(np.float32)
+    Xv = rng.standard_normal((m, k), dtype=np.float32)
+    dYt = torch.from_numpy(dYv).cuda().to(torch.bfloat16)
+    Xt = torch.from_numpy(Xv).cuda().to(torch.bfloat16)
+    W = torch.from_numpy(_weights(n, k, 16)).cuda()
+    p = slim.pack16(W)
+    g = slim.grad_w(dYt, Xt, p)
+    torch.cuda.synchronize()
+    rows = [0, 1, 4095, 17000, n - 1]
+    dYr = dYt.float().cpu().numpy()
+    Xr = Xt.float().cpu().numpy()
+    meta = host(p["meta"])
+    for r in rows:
+        got = host(g[r])
+        ref = T.grad_w(dYr[:, r:r + 1], Xr, meta[r:r + 1], 1, k)[0]
+        bnd = _grad_bound(dYr[:, r:r + 1], Xr, meta[r:r + 1], 1, k)[0]
+        assert np.all(np.abs(got - ref) <= bnd), r
+
+
+def test_grad_w_rejects_bad_shapes():
+    p = slim.pack16(dev(_weights(128, 128, 17)))
+    x = torch.zeros((4, 128), dtype=torch.bfloat16, device="cuda")
+    y = torch.zeros((4, 96), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(slim.SlimError) as e:
+        slim.grad_w(y, x, p)
+    assert e.value.status == slim.SLIM_ESHAPE
+
+
+@pytest.mark.parametrize("beta,gamma", [(1.0, 0.0), (0.5, 1e-2), (1.0 / 1024, 0.1), (-3.0, 2.5)])
+def test_sparse_add(beta, gamma):
+    rng = synth.stream(18, "gtrain/add")
+    A = (rng.standard_normal(4096) * 3).astype(np.float32)
+    Bv = rng.standard_normal(4096).astype(np.float16)
+    out = host(slim.sparse_add(dev(A), dev(Bv.view(np.int16)), beta, gamma))
+    # the call takes the coefficients as fp32
+    beta, gamma = float(np.float32(beta)), float(np.float32(gamma))
+    ref = T.sparse_add(A, Bv, beta, gamma)
+    # fp32: one rounding of beta A (at most u |beta A|) and one of the fused result (u |ref|)
+    bnd = 2.0 ** -24 * (np.abs(beta * A.astype(np.float64)) + np.abs(ref)) * 1.0001
+    assert np.all(np.abs(out - ref) <= bnd)
+
+
+def test_update_pack16_and_repack():
+    n, k = 256, 512
+    p = slim.pack16(dev(_weights(n, k, 19)))
+    rng = synth.stream(19, "gtrain/upd")
+    Wn = (rng.standard_normal((n, k // 2)) * 0.02).astype(np.float32)
+    slim.update_pack16(dev(Wn), p)
+    assert np.array_equal(_u16(p["vals"]), T.update_pack16(Wn))
+    pt = slim.pack16_t(p)
+    ref = T.pack16_t(T.update_pack16(Wn), host(p["meta"]), n, k)
+    assert np.array_equal(_u16(pt["valsT"]), ref["valsT"])
+    assert np.array_equal(host(pt["metaT"]), ref["metaT"])
+
+
+def test_training_step_chain():
+    # one step of the SLoPe loop after the input gradient: masked gradient, sparse add with weight
+    # decay and loss scale, an SGD update, and both packs rebuilt; every stage against the oracle
+    m, n, k = 96, 256, 384
+    loss_scale, decay, lr = 1024.0, 0.01, 0.1
+    W = _weights(n, k, 20)
+    p = slim.pack16(dev(W))
+    ref = T.pack16(W)
+    yb, dYv = _act(m, n, 20, "gtrain/chain/dY", "bf16")
+    xb, Xv = _act(m, k, 21, "gtrain/chain/X", "bf16")
+    g = slim.grad_w(dev_bits(yb, torch.bfloat16), dev_bits(xb, torch.bfloat16), p)
+    gref = T.grad_w(dYv, Xv, ref["meta"], n, k)
+    assert np.all(np.abs(host(g) - gref) <= _grad_bound(dYv, Xv, ref["meta"], n, k))
+    upd = slim.sparse_add(g, p["vals"], 1.0 / loss_scale, decay)
+    beta, gamma = float(np.float32(1.0 / loss_scale)), float(np.float32(decay))   # passed as fp32
+    uref = T.sparse_add(host(g), ref["vals"].view(np.float16), beta, gamma)
+    bnd = 2.0 ** -24 * (np.abs(beta * host(g).astype(np.float64)) + np.abs(uref)) * 1.0001
+    assert np.all(np.abs(host(upd) - uref) <= bnd)
+    # optimizer (SGD) in fp32 on the compressed values, then the packs
+    wnew = (p["vals"].view(torch.float16).float() - lr * upd).contiguous()
+    slim.update_pack16(wnew, p)
+    assert np.array_equal(_u16(p["vals"]), T.update_pack16(host(wnew)))
+    pt = slim.pack16_t(p)
+    rt = T.pack16_t(_u16(p["vals"]), ref["meta"], n, k)
+    assert np.array_equal(_u16(pt["valsT"]), rt["valsT"])
+    assert np.array_equal(host(pt["metaT"]), rt["metaT"])
+    assert np.array_equal(host(p["meta"]), ref["meta"])          # M^R stays fixed
