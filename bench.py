@@ -36,6 +36,7 @@ MFMA_F16_PEAK_TFS = 2516.6       # MI355X dense fp16/bf16 MFMA
 PACK_BYTES_PER_WEIGHT = 0.390625  # 4-bit code x 1/2 + 2-bit index x 1/2 + fp16 scale / 128
 WARM_MS = 200.0                   # sustained work before the measured replay (clock ramp-up)
 KBURST = 4                        # event-recorded steps per burst of the per-kernel pass
+TRAIN_STEPS, TRAIN_DISPATCHES = 10, 40   # the training step runs milliseconds
 
 
 def parse():
@@ -50,6 +51,7 @@ def parse():
                     help="decode workload only: skip the second (prefill, M = 2048) measurement")
     ap.add_argument("--qadapter", action="store_true",
                     help="forward with 4-bit group-128 adapters (slim_pack_adapter_q / slim_linear_qa)")
+    ap.add_argument("--no-train", action="store_true", help="skip the training-step object of the default line")
     ap.add_argument("--dispatches", type=int, default=200,
                     help="steps of the per-kernel pass (median per kernel; at least --steps)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU budget of the oracle baseline (about 10-30 s)")
@@ -144,7 +146,7 @@ def layer_flops(M, N, K, r):
     return 2 * M * N * K + 2 * M * r * (K + N)
 
 
-WORKLOADS = ["decode", "prefill", "block13b", "mlp70b", "mlp70b_bwd", "tiny"]
+WORKLOADS = ["decode", "prefill", "block13b", "mlp70b", "mlp70b_bwd", "tiny", "train70b"]
 
 
 def workload_layers(wk, m):
@@ -373,6 +375,103 @@ def measure(wk, m, steps, warmup, dispatches, qadapter=False):
     return res, layers, M, bwd
 
 
+def measure_train(steps, warmup, dispatches, m=8192, n=28672, k=8192):
+    """The training-step calls after the input gradient (SLoPe) on the 70B MLP projection: one step =
+    slim_grad_w (dY [m, n], X [m, k] bf16 -> masked, compressed fp32 gradient) + slim_sparse_add
+    (loss scale and weight decay) + slim_update_pack16 + slim_pack16_t (transposed repack). Timed as
+    one replay of a captured K-step graph after WARM_MS of replays; per-kernel medians as measure()."""
+    import torch
+    from paper_2608_24070_amd import slim
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    W = torch.randn((n, k), device=dev, generator=gen) * 0.02
+    p = slim.pack16(W)
+    del W
+    pt = slim.pack16_t(p)
+    dY = (torch.randn((m, n), device=dev, generator=gen) * 0.01).to(torch.bfloat16)
+    X = torch.randn((m, k), device=dev, generator=gen).to(torch.bfloat16)
+    g = torch.empty((n, k // 2), dtype=torch.float32, device=dev)
+    upd = torch.empty_like(g)
+    wnew = p["vals"].view(torch.float16).float()        # the optimizer's output stands in fixed
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+
+    def step():
+        slim.grad_w(dY, X, p, out=g)
+        slim.sparse_add(g, p["vals"], 1.0 / 1024.0, 0.01, out=upd)
+        slim.update_pack16(wnew, p)
+        slim.pack16_t(p, out=pt)
+
+    # a step takes milliseconds: at most TRAIN_STEPS timed steps and TRAIN_DISPATCHES per-kernel steps
+    steps = min(steps, TRAIN_STEPS)
+    dispatches = min(dispatches, TRAIN_DISPATCHES)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    gt, g1 = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gt):
+        for _ in range(steps):
+            step()
+    with torch.cuda.graph(g1):
+        step()
+    torch.cuda.synchronize()
+    tw = time.perf_counter()
+    warm = 0
+    while (time.perf_counter() - tw) * 1e3 < WARM_MS and warm < 200:
+        gt.replay()
+        warm += 1
+        torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    gt.replay()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    print(f"[bench] train step M={m}: {ms * 1e3:.2f} us/step over {steps} steps ({warm} warm-up cycles, "
+          f"setup {setup_s:.1f}s)", file=sys.stderr, flush=True)
+    slim.slim_timing_reset()
+    done = 0
+    while done < dispatches:
+        g1.replay()
+        slim.slim_timing_enable(True)
+        for _ in range(min(KBURST, dispatches - done)):
+            step()
+        slim.slim_timing_enable(False)
+        done += KBURST
+    torch.cuda.synchronize()
+    kt = slim.slim_timing_read()
+    del gt, g1
+    kernels = {kn: {"launches": c, "avg_us": round(1e3 * tot / max(c, 1), 3), "median_us": round(1e3 * med, 3)}
+               for kn, (c, tot, med) in kt.items()}
+    flops = 2.0 * m * n * k                                  # issued by the gradient kernel (dense tile)
+    med_s = kt["grad_w"][2] * 1e-3
+    achieved = flops / med_s / 1e12
+    traffic = counter_traffic("grad_w", f"train70b_m{m}")
+    res = {
+        "metric": "dense-equiv TFLOP/s of the weight-gradient step",
+        "value": round(flops / (ms * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "ms_per_step": round(ms, 6),
+        "config": {"workload": f"train step after dX: 70B MLP projection {n}x{k}, M={m}, bf16 dY and X, "
+                               "fp16 value packs, fp32 gradient", "M": m, "N": n, "K": k,
+                   "dense_equiv_flops_per_step": flops},
+        "kernels": kernels,
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_F16_PEAK_TFS, "unit": "TFLOP/s",
+                     "frac": round(achieved / MFMA_F16_PEAK_TFS, 4), "dense_equiv_flops_per_launch": flops,
+                     "traffic": None if traffic is None else round(traffic / 1e6, 3),
+                     "traffic_unit": "MB per launch (HBM fetch + write, copy-calibrated counters)",
+                     "kernel": "grad_w",
+                     "timing": f"median of {kt['grad_w'][0]} dispatches; hip events recorded by each kernel "
+                               f"dispatch, in bursts of {KBURST} steps each right after a replayed step",
+                     "note": "the kernel computes the dense tile and keeps the half M^R selects"},
+    }
+    del p, pt, dY, X, g, upd, wnew
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     args = parse()
     if args.copy_probe is not None:
@@ -391,12 +490,25 @@ def main():
     if args.qadapter and args.workload == "mlp70b_bwd":
         print("--qadapter applies to the forward only", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "train70b":
+        # the training-step calls alone (the object the default line carries as "train")
+        tr = measure_train(args.steps, args.warmup, dispatches, m=args.m or 8192)
+        print(json.dumps({"metric": tr["metric"], "value": tr["value"], "unit": tr["unit"], "n_gpus": 1,
+                          "steps": min(args.steps, TRAIN_STEPS), "warmup": args.warmup,
+                          "ms_per_step": tr["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+                          "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+                          "config": {**tr["config"], "kernel_source_hash": kernel_source_hash()},
+                          "kernels": tr["kernels"], "roofline": tr["roofline"], "cpu_baseline": None}))
+        return
     res, layers, M, bwd = measure(args.workload, args.m, args.steps, args.warmup, dispatches, args.qadapter)
     second = None
     if args.workload == "decode" and not args.no_prefill:
         # the M >= 2048 half of the metric: the prefill layer (11008 x 4096, rank 384) at M = 2048
         s_res, _, _, _ = measure("prefill", None, args.steps, args.warmup, dispatches, args.qadapter)
         second = {"metric": "dense-equiv TFLOP/s (M≥2048)", **s_res}
+    train = None
+    if args.workload == "decode" and not args.no_train:
+        train = measure_train(args.steps, args.warmup, dispatches)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -425,6 +537,8 @@ def main():
     }
     if second is not None:
         out["prefill"] = second
+    if train is not None:
+        out["train"] = train
     print(json.dumps(out))
 
 

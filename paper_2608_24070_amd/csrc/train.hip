@@ -136,18 +136,21 @@ k_pack16_t(const uint16_t* __restrict__ vals, const uint8_t* __restrict__ meta, 
 }
 
 // ------------------------------------------------------------------------------- grad_w
-// D[k][n] = sum_m X[m][k] dY[m][n] (= grad W^T) on 32x32x16 MFMA, fp32 accumulate; tile 128 (k) x
-// 128 (n), wave (wk, wn) of four owns k rows 64 wk .. + 63 and n columns 64 wn .. + 63 (2 x 2
-// fragments). Both operands are [M, *] row-major, so the reduction runs along their rows: per
-// 32-row chunk, each thread loads four rows of four columns of each (8 B per load, rows past M
-// read as zero through the buffer resource) and writes them to LDS transposed, four reduction
-// positions per 8-byte write, into [column][32 + 8] fp16 rows (80 B: 16-byte fragment reads of
-// 8 consecutive rows hit distinct banks). Two LDS stages: chunk c + 1's loads are in flight
-// while chunk c's MFMAs run.
+// D[k][n] = sum_m X[m][k] dY[m][n] (= grad W^T) on 32x32x16 MFMA, fp32 accumulate; tile 256 (k) x
+// 256 (n), wave (wk, wn) of four owns k rows 128 wk .. + 127 and n columns 128 wn .. + 127 (4 x 4
+// fragments in the accumulation registers). The tile's operand traffic per flop is a quarter of a
+// 128 x 128 tile's (every dY column slab is read by K/256 tiles, every X slab by N/256). Both
+// operands are [M, *] row-major, so the reduction runs along their rows: per 32-row chunk, each
+// thread loads two groups of four rows of four columns of each (8 B per load; rows past M read as
+// zero through the buffer resource) and writes them to LDS transposed, four reduction positions
+// per 8-byte write, into [column][32 + 8] fp16 rows with XOR-swizzled 16-byte slots. Loads run two
+// chunks ahead in two register sets; LDS has two stages.
+// Columns past N or K (a last partial tile) read neighbouring data; D entries of such a column are
+// never stored, and no other entry depends on it.
 // Epilogue: a fragment row block 8q + 4 (L / 32) .. + 3 of lane L is one aligned 4-group of k for
 // column n = L % 32, so the two positions M^R keeps (one metadata nibble) are selected in
 // registers and stored as the compressed pair gW[n][2g], gW[n][2g + 1].
-constexpr int kGT = 128, kGM = 32, kGLd = kGM + 8;
+constexpr int kGT = 256, kGM = 32, kGLd = kGM + 8;
 
 template <bool BF16>
 SLIM_DEV f16_t mfma_acc(u32x4_t a, u32x4_t b, f16_t c) {
@@ -162,6 +165,10 @@ SLIM_DEV float sel4(const f16_t& acc, int base, int i) {
   return i == 0 ? a0 : (i == 1 ? a1 : (i == 2 ? a2 : a3));
 }
 
+struct GradRegs {
+  u32x2_t y[2][4], x[2][4];   // [column half][row]
+};
+
 template <bool BF16>
 __global__ void __launch_bounds__(256)
 k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_t M, int64_t N, int64_t K,
@@ -174,7 +181,7 @@ k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_
   // XCD-aware tile order (block b runs on XCD b % 8, which takes positions [x Q, (x + 1) Q) of an
   // order walking bands of four n tiles k tile by k tile), so blocks running together on one XCD
   // share dY and X chunks in its L2
-  const int64_t tn = N / kGT, tk = K / kGT, T = tn * tk;
+  const int64_t tn = (N + kGT - 1) / kGT, tk = (K + kGT - 1) / kGT, T = tn * tk;
   const int64_t Q = (T + 7) / 8;
   const int64_t pos = (int64_t)(blockIdx.x % 8) * Q + blockIdx.x / 8;
   if (pos >= T) return;
@@ -182,79 +189,113 @@ k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_
   const int64_t nbw = tn - band * 4 < 4 ? tn - band * 4 : 4;
   const int64_t n0 = (band * 4 + q0 % nbw) * kGT, k0 = (q0 / nbw) * kGT;
 
-  // loads: thread -> rows 4 mg .. 4 mg + 3 of the chunk (mg = tid % 8) and columns 4 cg .. + 3
-  // (cg = tid / 8); all of the offset is per lane, so the resource's extent check sees the row
-  const int mg = tid & 7, cg = tid >> 3;
+  // loads: thread -> columns 4 cg .. 4 cg + 3 of the tile (cg = tid % 64) and rows 4 mg .. + 3 and
+  // 16 + 4 mg .. + 3 of the chunk (mg = tid / 64, the wave), so that one load instruction of a wave
+  // reads one row's 512 contiguous bytes; all of the offset is per lane, so the resource's extent
+  // check sees the row
+  const int cg = tid & 63, mg = tid >> 6;
   const rsrc_t ry = make_rsrc(dY, M * N * 2), rx = make_rsrc(X, M * K * 2);
   const uint32_t yo = ((uint32_t)(4 * mg) * (uint32_t)N + (uint32_t)(n0 + 4 * cg)) * 2u;
   const uint32_t xo = ((uint32_t)(4 * mg) * (uint32_t)K + (uint32_t)(k0 + 4 * cg)) * 2u;
   const uint32_t ystep = (uint32_t)kGM * (uint32_t)N * 2u, xstep = (uint32_t)kGM * (uint32_t)K * 2u;
-  u32x2_t ry4[4], rx4[4];
-  auto load = [&](int64_t c) {
+  auto load = [&](int64_t c, GradRegs& R) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      ry4[j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
-                                                ry, yo + (uint32_t)c * ystep + (uint32_t)j * (uint32_t)N * 2u, 0, 0));
-      rx4[j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
-                                                rx, xo + (uint32_t)c * xstep + (uint32_t)j * (uint32_t)K * 2u, 0, 0));
-    }
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t row = (uint32_t)(16 * hh + j);
+        R.y[hh][j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
+                         ry, yo + (uint32_t)c * ystep + row * (uint32_t)N * 2u, 0, 0));
+        R.x[hh][j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
+                         rx, xo + (uint32_t)c * xstep + row * (uint32_t)K * 2u, 0, 0));
+      }
   };
-  // 4 x 4 transpose of 16-bit elements: column c gets rows 0..3 as one 8-byte LDS write
-  auto store = [&](int stg) {
+  // LDS rows hold the chunk's 32 reduction positions as four 16-byte slots; slot s of tile column
+  // row r sits at physical slot s ^ ((r / 4) % 4), so that the 8-byte transposed writes of a wave
+  // (64 columns 4 rows apart) and the 16-byte fragment reads (32 consecutive rows) spread over the
+  // banks
+  auto slot_of = [](int r, int s) { return s ^ ((r >> 2) & 3); };
+  // 4 x 4 transposes of 16-bit elements: column c of the thread's four gets rows 0..3 (of a half
+  // hh: positions 16 hh + 4 mg ..) as one 8-byte LDS write
+  auto store = [&](const GradRegs& R, int stg) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int w = c >> 1, sh = 16 * (c & 1);
-      auto pick = [&](const u32x2_t* r, int j) { return (r[j][w] >> sh) & 0xFFFFu; };
-      const u32x2_t yv = {pick(ry4, 0) | (pick(ry4, 1) << 16), pick(ry4, 2) | (pick(ry4, 3) << 16)};
-      const u32x2_t xv = {pick(rx4, 0) | (pick(rx4, 1) << 16), pick(rx4, 2) | (pick(rx4, 3) << 16)};
-      *reinterpret_cast<u32x2_t*>(&ys[stg][4 * cg + c][4 * mg]) = yv;
-      *reinterpret_cast<u32x2_t*>(&xs[stg][4 * cg + c][4 * mg]) = xv;
-    }
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int w = c >> 1, sh = 16 * (c & 1);
+        auto pick = [&](const u32x2_t* r, int j) { return (r[j][w] >> sh) & 0xFFFFu; };
+        const u32x2_t yv = {pick(R.y[hh], 0) | (pick(R.y[hh], 1) << 16), pick(R.y[hh], 2) | (pick(R.y[hh], 3) << 16)};
+        const u32x2_t xv = {pick(R.x[hh], 0) | (pick(R.x[hh], 1) << 16), pick(R.x[hh], 2) | (pick(R.x[hh], 3) << 16)};
+        const int r = 4 * cg + c, m = 16 * hh + 4 * mg;          // m % 8 is 0 or 4
+        const int col = 8 * slot_of(r, m >> 3) + (m & 7);
+        *reinterpret_cast<u32x2_t*>(&ys[stg][r][col]) = yv;
+        *reinterpret_cast<u32x2_t*>(&xs[stg][r][col]) = xv;
+      }
   };
 
-  f16_t acc[2][2];
+  f16_t acc[4][4];
 #pragma unroll
-  for (int x = 0; x < 2; ++x)
+  for (int x = 0; x < 4; ++x)
 #pragma unroll
-    for (int y = 0; y < 2; ++y)
+    for (int y = 0; y < 4; ++y)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[x][y][v] = 0.f;
 
-  const int64_t nch = (M + kGM - 1) / kGM;
-  load(0);
-  store(0);
-  __syncthreads();
-  for (int64_t c = 0; c < nch; ++c) {
-    const int stg = (int)(c & 1);
-    load(c + 1);   // past the last chunk every row is past M and reads as zero
-    __builtin_amdgcn_sched_barrier(0);   // issued before this chunk's work, not sunk into it
+  // all sixteen fragments of the chunk are read before its 32 MFMAs, so the LDS latency is paid
+  // once per chunk rather than once per fragment
+  auto compute = [&](int stg) {
+    u32x4_t af[kGM / 16][4], bf[kGM / 16][4];
 #pragma unroll
-    for (int st = 0; st < kGM / 16; ++st) {
-      u32x4_t af[2], bf[2];
+    for (int st = 0; st < kGM / 16; ++st)
 #pragma unroll
-      for (int f = 0; f < 2; ++f) {
-        af[f] = *reinterpret_cast<const u32x4_t*>(&xs[stg][64 * wk + 32 * f + (lane & 31)][16 * st + 8 * h]);
-        bf[f] = *reinterpret_cast<const u32x4_t*>(&ys[stg][64 * wn + 32 * f + (lane & 31)][16 * st + 8 * h]);
+      for (int f = 0; f < 4; ++f) {
+        const int ra = 128 * wk + 32 * f + (lane & 31), rb = 128 * wn + 32 * f + (lane & 31);
+        af[st][f] = *reinterpret_cast<const u32x4_t*>(&xs[stg][ra][8 * slot_of(ra, 2 * st + h)]);
+        bf[st][f] = *reinterpret_cast<const u32x4_t*>(&ys[stg][rb][8 * slot_of(rb, 2 * st + h)]);
       }
-#pragma unroll
-      for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = mfma_acc<BF16>(af[x], bf[y], acc[x][y]);
-    }
-    // the other stage was last read in chunk c - 1, before the barrier that ended it; the
-    // transpose waits for the loads, so it stays behind every MFMA of this chunk
     __builtin_amdgcn_sched_barrier(0);
-    store(stg ^ 1);
+#pragma unroll
+    for (int st = 0; st < kGM / 16; ++st)
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] = mfma_acc<BF16>(af[st][x], bf[st][y], acc[x][y]);
+  };
+
+  // chunk c: loads of chunk c + 2 into the register set chunk c occupied (stored to LDS before),
+  // this chunk's MFMAs from stage c % 2, then chunk c + 1's registers (loaded during chunk c - 1)
+  // into the other stage (last read during chunk c - 1, before the barrier that ended it). Loads
+  // past the last chunk address rows past M and read as zero.
+  const int64_t nch = (M + kGM - 1) / kGM;
+  GradRegs r0, r1;
+  load(0, r0);
+  load(1, r1);
+  store(r0, 0);
+  __syncthreads();
+  auto chunk = [&](int64_t c, GradRegs& cur, GradRegs& nxt, int stg) {
+    load(c + 2, cur);
+    __builtin_amdgcn_sched_barrier(0);   // issued before this chunk's work, not sunk into it
+    compute(stg);
+    store(nxt, stg ^ 1);
     __syncthreads();
+  };
+  int64_t c = 0;
+  for (; c + 2 <= nch; c += 2) {
+    chunk(c, r0, r1, 0);
+    chunk(c + 1, r1, r0, 1);
   }
+  if (c < nch) chunk(c, r0, r1, 0);
 
   // D[i][j] of a 32x32 fragment: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
 #pragma unroll
-  for (int y = 0; y < 2; ++y) {
-    const int64_t n = n0 + 64 * wn + 32 * y + (lane & 31);
+  for (int y = 0; y < 4; ++y) {
+    const int64_t n = n0 + 128 * wn + 32 * y + (lane & 31);
+    if (n >= N) continue;
 #pragma unroll
-    for (int x = 0; x < 2; ++x) {
-      const int64_t gb = (k0 + 64 * wk + 32 * x) / 4;          // first group of the fragment rows
+    for (int x = 0; x < 4; ++x) {
+      const int64_t kb = k0 + 128 * wk + 32 * x;                 // first row of the fragment
+      if (kb >= K) continue;
+      const int64_t gb = kb / 4;
       const uint32_t md = *reinterpret_cast<const uint32_t*>(meta + n * (K / 8) + gb / 2);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -343,14 +384,14 @@ extern "C" int slim_grad_w(const void* dY, const void* X, int dtype, int64_t M, 
                            const uint8_t* meta, float* gW, void* stream) {
   if (!dY || !X || !meta || !gW) return SLIM_EINVAL;
   if (dtype != SLIM_F16 && dtype != SLIM_BF16) return SLIM_EDTYPE;
-  if (M < 1 || N < kGT || K < kGT || N % kGT || K % kGT) return SLIM_ESHAPE;
+  if (M < 1 || N < 128 || K < 128 || N % 128 || K % 128) return SLIM_ESHAPE;
   // per-lane byte offsets are 32-bit: the operands must stay below 4 GiB
   if (M * N * 2 >= (int64_t(1) << 32) || M * K * 2 >= (int64_t(1) << 32) || N >= (int64_t(1) << 24) ||
       K >= (int64_t(1) << 24))
     return SLIM_EUNSUPPORTED;
   if (!slim_aligned16(dY) || !slim_aligned16(X) || !slim_aligned16(meta) || !slim_aligned16(gW)) return SLIM_EALIGN;
   hipStream_t s = (hipStream_t)stream;
-  const int64_t T = (N / kGT) * (K / kGT);
+  const int64_t T = ((N + kGT - 1) / kGT) * ((K + kGT - 1) / kGT);
   const dim3 grid((unsigned)(8 * ((T + 7) / 8)));
   SlimKernelTimer timer("grad_w", s);
   if (dtype == SLIM_BF16)
