@@ -141,10 +141,10 @@ k_pack16_t(const uint16_t* __restrict__ vals, const uint8_t* __restrict__ meta, 
 // fragments in the accumulation registers). The tile's operand traffic per flop is a quarter of a
 // 128 x 128 tile's (every dY column slab is read by K/256 tiles, every X slab by N/256). Both
 // operands are [M, *] row-major, so the reduction runs along their rows: per 32-row chunk, each
-// thread loads two groups of four rows of four columns of each (8 B per load; rows past M read as
-// zero through the buffer resource) and writes them to LDS transposed, four reduction positions
-// per 8-byte write, into [column][32 + 8] fp16 rows with XOR-swizzled 16-byte slots. Loads run two
-// chunks ahead in two register sets; LDS has two stages.
+// thread loads eight rows of four columns of each (8 B per load; rows past M read as zero through
+// the buffer resource) and writes them to LDS transposed, eight reduction positions per 16-byte
+// write, into [column][32 + 8] fp16 rows with XOR-swizzled 16-byte slots. Loads run two chunks
+// ahead in two register sets; LDS has two stages.
 // Columns past N or K (a last partial tile) read neighbouring data; D entries of such a column are
 // never stored, and no other entry depends on it.
 // Epilogue: a fragment row block 8q + 4 (L / 32) .. + 3 of lane L is one aligned 4-group of k for
@@ -166,7 +166,7 @@ SLIM_DEV float sel4(const f16_t& acc, int base, int i) {
 }
 
 struct GradRegs {
-  u32x2_t y[2][4], x[2][4];   // [column half][row]
+  u32x2_t y[8], x[8];   // [row]: four columns of one row
 };
 
 template <bool BF16>
@@ -189,48 +189,45 @@ k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_
   const int64_t nbw = tn - band * 4 < 4 ? tn - band * 4 : 4;
   const int64_t n0 = (band * 4 + q0 % nbw) * kGT, k0 = (q0 / nbw) * kGT;
 
-  // loads: thread -> columns 4 cg .. 4 cg + 3 of the tile (cg = tid % 64) and rows 4 mg .. + 3 and
-  // 16 + 4 mg .. + 3 of the chunk (mg = tid / 64, the wave), so that one load instruction of a wave
-  // reads one row's 512 contiguous bytes; all of the offset is per lane, so the resource's extent
-  // check sees the row
+  // loads: thread -> columns 4 cg .. 4 cg + 3 of the tile (cg = tid % 64) and rows 8 mg .. 8 mg + 7
+  // of the chunk (mg = tid / 64, the wave), so that one load instruction of a wave reads one row's
+  // 512 contiguous bytes; all of the offset is per lane, so the resource's extent check sees the row
   const int cg = tid & 63, mg = tid >> 6;
   const rsrc_t ry = make_rsrc(dY, M * N * 2), rx = make_rsrc(X, M * K * 2);
-  const uint32_t yo = ((uint32_t)(4 * mg) * (uint32_t)N + (uint32_t)(n0 + 4 * cg)) * 2u;
-  const uint32_t xo = ((uint32_t)(4 * mg) * (uint32_t)K + (uint32_t)(k0 + 4 * cg)) * 2u;
+  const uint32_t yo = ((uint32_t)(8 * mg) * (uint32_t)N + (uint32_t)(n0 + 4 * cg)) * 2u;
+  const uint32_t xo = ((uint32_t)(8 * mg) * (uint32_t)K + (uint32_t)(k0 + 4 * cg)) * 2u;
   const uint32_t ystep = (uint32_t)kGM * (uint32_t)N * 2u, xstep = (uint32_t)kGM * (uint32_t)K * 2u;
   auto load = [&](int64_t c, GradRegs& R) {
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t row = (uint32_t)(16 * hh + j);
-        R.y[hh][j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
-                         ry, yo + (uint32_t)c * ystep + row * (uint32_t)N * 2u, 0, 0));
-        R.x[hh][j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
-                         rx, xo + (uint32_t)c * xstep + row * (uint32_t)K * 2u, 0, 0));
-      }
+    for (int j = 0; j < 8; ++j) {
+      R.y[j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
+                   ry, yo + (uint32_t)c * ystep + (uint32_t)j * (uint32_t)N * 2u, 0, 0));
+      R.x[j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
+                   rx, xo + (uint32_t)c * xstep + (uint32_t)j * (uint32_t)K * 2u, 0, 0));
+    }
   };
   // LDS rows hold the chunk's 32 reduction positions as four 16-byte slots; slot s of tile column
-  // row r sits at physical slot s ^ ((r / 4) % 4), so that the 8-byte transposed writes of a wave
-  // (64 columns 4 rows apart) and the 16-byte fragment reads (32 consecutive rows) spread over the
-  // banks
-  auto slot_of = [](int r, int s) { return s ^ ((r >> 2) & 3); };
-  // 4 x 4 transposes of 16-bit elements: column c of the thread's four gets rows 0..3 (of a half
-  // hh: positions 16 hh + 4 mg ..) as one 8-byte LDS write
+  // row r sits at physical slot s ^ ((r / 8) % 4). A wave's 16-byte transposed writes (64 rows 4
+  // apart, one slot) and its 16-byte fragment reads (32 consecutive rows, one slot) then touch 8
+  // distinct groups of 4 banks per 8 lanes.
+  auto slot_of = [](int r, int s) { return s ^ ((r >> 3) & 3); };
+  // 8 x 4 transposes of 16-bit elements: column c of the thread's four gets the 8 rows (positions
+  // 8 mg .. 8 mg + 7, slot mg) as one 16-byte LDS write
   auto store = [&](const GradRegs& R, int stg) {
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
+    for (int c = 0; c < 4; ++c) {
+      const int w = c >> 1, sh = 16 * (c & 1);
+      auto pick = [&](const u32x2_t* r, int j) { return (r[j][w] >> sh) & 0xFFFFu; };
+      u32x4_t yv, xv;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int w = c >> 1, sh = 16 * (c & 1);
-        auto pick = [&](const u32x2_t* r, int j) { return (r[j][w] >> sh) & 0xFFFFu; };
-        const u32x2_t yv = {pick(R.y[hh], 0) | (pick(R.y[hh], 1) << 16), pick(R.y[hh], 2) | (pick(R.y[hh], 3) << 16)};
-        const u32x2_t xv = {pick(R.x[hh], 0) | (pick(R.x[hh], 1) << 16), pick(R.x[hh], 2) | (pick(R.x[hh], 3) << 16)};
-        const int r = 4 * cg + c, m = 16 * hh + 4 * mg;          // m % 8 is 0 or 4
-        const int col = 8 * slot_of(r, m >> 3) + (m & 7);
-        *reinterpret_cast<u32x2_t*>(&ys[stg][r][col]) = yv;
-        *reinterpret_cast<u32x2_t*>(&xs[stg][r][col]) = xv;
+      for (int i = 0; i < 4; ++i) {
+        yv[i] = pick(R.y, 2 * i) | (pick(R.y, 2 * i + 1) << 16);
+        xv[i] = pick(R.x, 2 * i) | (pick(R.x, 2 * i + 1) << 16);
       }
+      const int r = 4 * cg + c;
+      *reinterpret_cast<u32x4_t*>(&ys[stg][r][8 * slot_of(r, mg)]) = yv;
+      *reinterpret_cast<u32x4_t*>(&xs[stg][r][8 * slot_of(r, mg)]) = xv;
+    }
   };
 
   f16_t acc[4][4];
