@@ -4,14 +4,17 @@
 Default: the decode-shaped layer (X bf16 [16 x 4096], W 4096 x 4096 packed 2:4 + int4 group-128,
 rank-384 fp16 adapter), the weight-stream GB/s half of the metric, followed in the same JSON line by
 the prefill layer (X bf16 [2048 x 4096], W 11008 x 4096, rank 384), the dense-equivalent TFLOP/s
-half ("prefill" object). One step = one slim_linear call per layer on inputs resident in HBM; the
-weight copies rotate over more than 3x the 256 MB MALL, one running copy counter across the
-warm-up, timed and per-kernel passes, so the weight stream comes from HBM. Per-kernel figures are
-medians over at least 200 dispatches, timed by their own dispatches in short bursts right after
-replays of the timed steps. Prints one JSON line.
+half ("prefill" object), and by the SLoPe training step after the input gradient on the 70B MLP
+projection ("train" object: masked weight gradient, sparse add, pack update, transposed repack).
+One step = one slim_linear call per layer on inputs resident in HBM; the weight copies rotate over
+more than 3x the 256 MB MALL, one running copy counter across the warm-up, timed and per-kernel
+passes, so the weight stream comes from HBM. Per-kernel figures (average and median) come from at
+least 200 dispatches (40 for the training step), timed by their own dispatches in short bursts
+right after replays of the timed steps; the roofline uses the average. Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--workload decode|prefill|block13b|mlp70b|mlp70b_bwd|tiny]
-                  [--m M] [--no-cpu-baseline] [--no-prefill] [--dispatches D]
+  python bench.py [--steps K] [--warmup W]
+                  [--workload decode|prefill|block13b|mlp70b|mlp70b_bwd|tiny|train70b]
+                  [--m M] [--no-cpu-baseline] [--no-prefill] [--no-train] [--qadapter] [--dispatches D]
   python bench.py --copy-probe MB     # plain device copy of MB megabytes (counter calibration)
 
 The roofline's "traffic" field comes from the hardware-counter summary committed under profiles/
@@ -53,7 +56,7 @@ def parse():
                     help="forward with 4-bit group-128 adapters (slim_pack_adapter_q / slim_linear_qa)")
     ap.add_argument("--no-train", action="store_true", help="skip the training-step object of the default line")
     ap.add_argument("--dispatches", type=int, default=200,
-                    help="steps of the per-kernel pass (median per kernel; at least --steps)")
+                    help="steps of the per-kernel pass (average and median per kernel; at least --steps)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU budget of the oracle baseline (about 10-30 s)")
     ap.add_argument("--copy-probe", type=float, default=None, metavar="MB",
                     help="only run a plain device-to-device copy of MB megabytes (HBM counter calibration)")
@@ -304,7 +307,7 @@ def measure(wk, m, steps, warmup, dispatches, qadapter=False):
     # Event-recorded launches leave the GPU idle for microseconds between kernels, and a long run of
     # them lets the GPU fall out of the state of sustained work (kernel times up to 1.5x the ones in
     # the timed replay); so the pass runs in bursts of KBURST event-recorded steps, each right after a
-    # replay of the timed graphs. The medians then add up to no more than the measured step.
+    # replay of the timed graphs. The per-kernel times then add up to no more than the measured step.
     slim.slim_timing_reset()
     done = 0
     while done < dispatches:
@@ -323,7 +326,9 @@ def measure(wk, m, steps, warmup, dispatches, qadapter=False):
                for k, (n, ms, med) in kt.items()}
     dominant = max(kt.items(), key=lambda kv: kv[1][1])[0]
     launches_per_step = kt[dominant][0] / dispatches
-    med_s = kt[dominant][2] * 1e-3
+    # average launch duration: the per-launch figure below is a mean over the step's layers, which differ
+    # in shape in the 13B block, so it pairs with the mean duration (total time over launches)
+    avg_s = kt[dominant][1] / kt[dominant][0] * 1e-3
 
     tot_bytes = sum(layer_bytes(M, pl["layer"].n, pl["layer"].k, pl["layer"].r, qadapter) for pl in per_layer)
     tot_flops = sum(layer_flops(M, pl["layer"].n, pl["layer"].k, pl["layer"].r) for pl in per_layer)
@@ -334,7 +339,7 @@ def measure(wk, m, steps, warmup, dispatches, qadapter=False):
         value = tot_bytes / (ms_per_step * 1e-3) / 1e9
         dk_bytes = sum(kernel_bytes(dominant, M, pl["layer"].n, pl["layer"].k, pl["layer"].r, bwd, has_finish, qadapter)
                        for pl in per_layer) / launches_per_step
-        achieved = dk_bytes / med_s / 1e9
+        achieved = dk_bytes / avg_s / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 4), "algorithmic_bytes_per_launch": int(dk_bytes)}
     else:
@@ -343,14 +348,14 @@ def measure(wk, m, steps, warmup, dispatches, qadapter=False):
         # dominant kernel (the sparse contraction): dense-equivalent 2MNK plus the adapter's second product
         dk_flops = sum(2 * M * pl["layer"].n * pl["layer"].k + 2 * M * pl["layer"].r *
                        (pl["layer"].k if bwd else pl["layer"].n) for pl in per_layer) / launches_per_step
-        achieved = dk_flops / med_s / 1e12
+        achieved = dk_flops / avg_s / 1e12
         roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_F16_PEAK_TFS, "unit": "TFLOP/s",
                     "frac": round(achieved / MFMA_F16_PEAK_TFS, 4), "dense_equiv_flops_per_launch": int(dk_flops)}
     traffic = counter_traffic(dominant, wkey)
     roofline["traffic"] = None if traffic is None else round(traffic / 1e6, 3)
     roofline["traffic_unit"] = "MB per launch (HBM fetch + write, copy-calibrated counters)"
     roofline["kernel"] = dominant
-    roofline["timing"] = (f"median of {kt[dominant][0]} dispatches; hip events recorded by each kernel dispatch "
+    roofline["timing"] = (f"average of {kt[dominant][0]} dispatches; hip events recorded by each kernel dispatch "
                           f"(hipExtLaunchKernel), in bursts of {KBURST} steps each right after a replay of the "
                           "timed graphs")
 
@@ -379,7 +384,7 @@ def measure_train(steps, warmup, dispatches, m=8192, n=28672, k=8192):
     """The training-step calls after the input gradient (SLoPe) on the 70B MLP projection: one step =
     slim_grad_w (dY [m, n], X [m, k] bf16 -> masked, compressed fp32 gradient) + slim_sparse_add
     (loss scale and weight decay) + slim_update_pack16 + slim_pack16_t (transposed repack). Timed as
-    one replay of a captured K-step graph after WARM_MS of replays; per-kernel medians as measure()."""
+    one replay of a captured K-step graph after WARM_MS of replays; per-kernel times as measure()."""
     import torch
     from paper_2608_24070_amd import slim
     dev = torch.device("cuda:0")
@@ -447,8 +452,8 @@ def measure_train(steps, warmup, dispatches, m=8192, n=28672, k=8192):
     kernels = {kn: {"launches": c, "avg_us": round(1e3 * tot / max(c, 1), 3), "median_us": round(1e3 * med, 3)}
                for kn, (c, tot, med) in kt.items()}
     flops = 2.0 * m * n * k                                  # issued by the gradient kernel (dense tile)
-    med_s = kt["grad_w"][2] * 1e-3
-    achieved = flops / med_s / 1e12
+    avg_s = kt["grad_w"][1] / kt["grad_w"][0] * 1e-3
+    achieved = flops / avg_s / 1e12
     traffic = counter_traffic("grad_w", f"train70b_m{m}")
     res = {
         "metric": "dense-equiv TFLOP/s of the weight-gradient step",
@@ -462,7 +467,7 @@ def measure_train(steps, warmup, dispatches, m=8192, n=28672, k=8192):
                      "traffic": None if traffic is None else round(traffic / 1e6, 3),
                      "traffic_unit": "MB per launch (HBM fetch + write, copy-calibrated counters)",
                      "kernel": "grad_w",
-                     "timing": f"median of {kt['grad_w'][0]} dispatches; hip events recorded by each kernel "
+                     "timing": f"average of {kt['grad_w'][0]} dispatches; hip events recorded by each kernel "
                                f"dispatch, in bursts of {KBURST} steps each right after a replayed step",
                      "note": "the kernel computes the dense tile and keeps the half M^R selects"},
     }
