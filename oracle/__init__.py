@@ -21,8 +21,11 @@ the thesis' definitions:
   gradient (eq. sparse_backward_weight), the same-pattern sparse add and the pack update
   (Alg. "Accelerated Sparse Pretraining Algorithm for a Linear Layer"; appendix
   "Implementation details").
+* SLiM-Quant's histogram-based mean-squared-error scale search (``slim_quant``; SLiM,
+  eq. error_summation and Alg. quantization) and the forward pack with its per-tensor scale.
 
 Parity status per function is stated in ``slim_oracle``'s module docstring.
 """
 from . import slim_oracle  # noqa: F401
 from . import slope_train  # noqa: F401
+from . import slim_quant  # noqa: F401
