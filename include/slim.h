@@ -370,6 +370,43 @@ int slim_sparse_add(const float* A, const uint16_t* B, float beta, float gamma, 
 int slim_update_pack16(const float* Wnew, int64_t count, uint16_t* vals, void* stream);
 
 /*
+ * SLiM-Quant: one symmetric quantisation parameter alpha for a whole weight by minimising the
+ * expected squared quantisation error over the distribution of |w| (SLiM chapter, "SLiM-Quant
+ * quantization method": eq. error_summation = eq. quantization_error + eq. clipping_error,
+ * integrated on a histogram of |w|; Alg. quantization for the candidate grids).
+ *
+ * slim_quant_bins - the histogram size of the SLiM setup, max(512, min(floor(N K / 1000), 20000)).
+ *
+ * slim_quant_search - histogram and search.
+ *   W       fp32, `count` values (any shape, e.g. a weight [N, K]), device; count % 4 == 0,
+ *           16-byte aligned.
+ *   bits    quantiser width q, 2..8: codes in [-(2^(q-1) - 1), 2^(q-1) - 1], step alpha / (2^(q-1) - 1).
+ *   bins    1..20480 equal bins over [0, max|w|]; |w| falls in bin floor(|w| bins / max|w|) (exact
+ *           rational floor; the maximum in the last bin).
+ *   hist    out, device uint32 [bins]: the counts.
+ *   out     out, device float64 [4 + 2 * 30]: [0] alpha*, [1] E(alpha*), [2] max|w|, [3] the number C
+ *           of candidates evaluated, then C pairs (alpha_i, E(alpha_i)) in evaluation order.
+ * E(alpha) weighs each bin's count at its centre (b + 1/2) max|w| / bins: a centre c <= alpha
+ * contributes (delta rint(c / delta) - c)^2 (delta = alpha / (2^(q-1) - 1), ties to even), one
+ * above alpha (alpha - c)^2; E is their count-weighted mean, in float64. Candidates: i max|w| / 10
+ * for i = 1..10, then (a - max|w| / 10) + j max|w| / 100 for j = 0..19 around the best of those, a,
+ * the positive ones only; alpha* is the first candidate of least error. All-zero W gives alpha* = 0
+ * and C = 0. Returns SLIM_ENONFINITE for NaN/Inf in W. This call synchronises `stream` (it reads
+ * back a status word) and allocates 8 bytes of device memory for the duration of the call.
+ *
+ * slim_pack_alpha - slim_pack with the per-tensor parameter in place of each group's absmax: every
+ * group's scale is s16 = fp16_RNE(fp32(alpha) / 7.0f), so weights beyond alpha clip to +-7 (same
+ * layout, mask rule, codes, status codes and synchronisation as slim_pack).
+ *   alpha   device pointer to one float64 (e.g. `out` of slim_quant_search), 8-byte aligned;
+ *           negative or NaN gives SLIM_ERANGE.
+ */
+int slim_quant_bins(int64_t N, int64_t K);
+int slim_quant_search(const float* W, int64_t count, int bits, int64_t bins, uint32_t* hist, double* out,
+                      void* stream);
+int slim_pack_alpha(const float* W, int64_t N, int64_t K, const double* alpha, uint8_t* codes, uint8_t* meta,
+                    uint16_t* scales, uint8_t* mask, void* stream);
+
+/*
  * Per-kernel timing for benchmarks (host-side bookkeeping; not part of the layer's math).
  * slim_timing_enable(1) makes every later kernel launch of this library record a hipEvent
  * before and after itself on the caller's stream. slim_timing_read waits for the recorded

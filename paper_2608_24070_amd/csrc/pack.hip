@@ -10,11 +10,12 @@ constexpr int kPackThreads = 256;
 
 // One thread per aligned 4-group of one row; the 32 threads of a half-wave cover one
 // 128-wide quantisation group (rows hold K/4 groups and K % 128 == 0, so groups never
-// straddle half-waves).
+// straddle half-waves). With `alpha` (one float64 in device memory, SLiM-Quant's per-tensor
+// parameter) every group takes it in place of its own absmax.
 __global__ void __launch_bounds__(kPackThreads)
 k_pack(const float4* __restrict__ W, int64_t total4, int64_t K, uint32_t* __restrict__ codes,
        uint16_t* __restrict__ meta, uint16_t* __restrict__ scales, uint32_t* __restrict__ mask,
-       int* __restrict__ status) {
+       int* __restrict__ status, const double* __restrict__ alpha) {
   const int64_t t = (int64_t)blockIdx.x * kPackThreads + threadIdx.x;
   const bool valid = t < total4;
   float4 v = valid ? W[t] : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -30,7 +31,12 @@ k_pack(const float4* __restrict__ W, int64_t total4, int64_t K, uint32_t* __rest
   float gmax = fmaxf(fmaxf(a[0], a[1]), fmaxf(a[2], a[3]));
 #pragma unroll
   for (int off = 16; off >= 1; off >>= 1) gmax = fmaxf(gmax, __shfl_xor(gmax, off, 32));
-  // s16 = fp16_RNE(fp32 absmax / 7), IEEE division
+  // s16 = fp16_RNE(fp32 absmax / 7), IEEE division (alpha rounded to fp32 in its place)
+  if (alpha) {
+    const double ad = *alpha;
+    if (!(ad >= 0.0)) bad |= 2;
+    gmax = (float)ad;
+  }
   const float s32 = __fdiv_rn(gmax, 7.0f);
   const _Float16 s16 = (_Float16)s32;
   const uint16_t s16bits = __builtin_bit_cast(uint16_t, s16);
@@ -344,8 +350,10 @@ extern "C" int slim_pack_adapter(const uint16_t* L, const uint16_t* R, int64_t K
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }
 
-extern "C" int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, uint8_t* meta,
-                         uint16_t* scales, uint8_t* mask, void* stream) {
+namespace {
+
+int pack_forward(const float* W, int64_t N, int64_t K, uint8_t* codes, uint8_t* meta, uint16_t* scales,
+                 uint8_t* mask, const double* alpha, void* stream) {
   int st = slim_check_pack(W, N, K, codes, meta, scales, mask);
   if (st != SLIM_OK) return st;
   hipStream_t s = (hipStream_t)stream;
@@ -361,7 +369,7 @@ extern "C" int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, u
       SlimKernelTimer timer("pack", s);
       SLIM_LAUNCH(timer, k_pack, dim3((unsigned)blocks), dim3(kPackThreads), s, reinterpret_cast<const float4*>(W),
                   total4, K, reinterpret_cast<uint32_t*>(codes), reinterpret_cast<uint16_t*>(meta), scales,
-                  reinterpret_cast<uint32_t*>(mask), d_status);
+                  reinterpret_cast<uint32_t*>(mask), d_status, alpha);
     }
     if (hipGetLastError() != hipSuccess) { rc = SLIM_EDEVICE; break; }
     if (hipMemcpyAsync(&h_status, d_status, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess ||
@@ -371,6 +379,20 @@ extern "C" int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, u
   } while (0);
   (void)hipFree(d_status);
   return rc;
+}
+
+}  // namespace
+
+extern "C" int slim_pack(const float* W, int64_t N, int64_t K, uint8_t* codes, uint8_t* meta,
+                         uint16_t* scales, uint8_t* mask, void* stream) {
+  return pack_forward(W, N, K, codes, meta, scales, mask, nullptr, stream);
+}
+
+extern "C" int slim_pack_alpha(const float* W, int64_t N, int64_t K, const double* alpha, uint8_t* codes,
+                               uint8_t* meta, uint16_t* scales, uint8_t* mask, void* stream) {
+  if (!alpha) return SLIM_EINVAL;
+  if ((uintptr_t)alpha & 7u) return SLIM_EALIGN;
+  return pack_forward(W, N, K, codes, meta, scales, mask, alpha, stream);
 }
 
 extern "C" int slim_pack_bwd(const uint8_t* codes, const uint8_t* meta, const uint16_t* scales, int64_t N,

@@ -49,6 +49,9 @@ _SIGS = {
     "slim_grad_w": (ctypes.c_int, [_c_p, _c_p, ctypes.c_int, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p]),
     "slim_sparse_add": (ctypes.c_int, [_c_p, _c_p, ctypes.c_float, ctypes.c_float, _c_p, _c_i64, _c_p]),
     "slim_update_pack16": (ctypes.c_int, [_c_p, _c_i64, _c_p, _c_p]),
+    "slim_quant_bins": (ctypes.c_int, [_c_i64, _c_i64]),
+    "slim_quant_search": (ctypes.c_int, [_c_p, _c_i64, ctypes.c_int, _c_i64, _c_p, _c_p, _c_p]),
+    "slim_pack_alpha": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "slim_timing_enable": (ctypes.c_int, [ctypes.c_int]),
     "slim_timing_reset": (ctypes.c_int, []),
     "slim_timing_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_size_t]),
@@ -105,6 +108,18 @@ def slim_status_string(status: int) -> str:
 
 def slim_pack(W, N, K, codes, meta, scales, mask, stream) -> int:
     return lib().slim_pack(W, N, K, codes, meta, scales, mask, stream)
+
+
+def slim_quant_bins(N, K) -> int:
+    return lib().slim_quant_bins(N, K)
+
+
+def slim_quant_search(W, count, bits, bins, hist, out, stream) -> int:
+    return lib().slim_quant_search(W, count, bits, bins, hist, out, stream)
+
+
+def slim_pack_alpha(W, N, K, alpha, codes, meta, scales, mask, stream) -> int:
+    return lib().slim_pack_alpha(W, N, K, alpha, codes, meta, scales, mask, stream)
 
 
 def slim_pack_bwd(codes, meta, scales, N, K, codesT, metaT, scalesT, mask_rc, stream) -> int:
@@ -268,6 +283,55 @@ def pack(W, with_mask: bool = False, stream=None) -> dict:
     st = slim_pack(_ptr(W), N, K, _ptr(out["codes"]), _ptr(out["meta"]), _ptr(out["scales"]), _ptr(mask),
                    _stream(stream))
     _check(st, "slim_pack")
+    if with_mask:
+        out["mask"] = mask
+    return out
+
+
+QUANT_OUT_LEN = 4 + 2 * 30     # alpha*, E(alpha*), max|w|, candidate count, then (alpha_i, E_i) pairs
+
+
+def quant_search(W, bits: int = 4, bins: int | None = None, stream=None) -> dict:
+    """slim_quant_search of an fp32 tensor (SLiM-Quant). Returns {"alpha", "error", "amax", "table"
+    [(alpha_i, E_i)], "hist" int32 [bins] (uint32 counts), "out" float64 device [64]}; alpha* stays
+    on the device in out[0] for slim_pack_alpha."""
+    torch = _torch()
+    _on_gpu(W)
+    if W.dtype != torch.float32 or not W.is_contiguous():
+        raise TypeError("W must be a contiguous fp32 tensor")
+    if bins is None:
+        n, k = W.shape
+        bins = slim_quant_bins(n, k)
+    hist = torch.empty(bins, dtype=torch.int32, device=W.device)
+    out = torch.zeros(QUANT_OUT_LEN, dtype=torch.float64, device=W.device)
+    _check(slim_quant_search(_ptr(W), W.numel(), bits, bins, _ptr(hist), _ptr(out), _stream(stream)),
+           "slim_quant_search")
+    o = out.cpu().tolist()
+    c = int(o[3])
+    return {"alpha": o[0], "error": o[1], "amax": o[2], "bins": bins, "hist": hist, "out": out,
+            "table": [(o[4 + 2 * i], o[5 + 2 * i]) for i in range(c)]}
+
+
+def pack_alpha(W, alpha, with_mask: bool = False, stream=None) -> dict:
+    """slim_pack_alpha: slim_pack with SLiM-Quant's per-tensor alpha (a device float64 tensor whose
+    first element is alpha, e.g. quant_search(...)["out"]) in place of each group's absmax."""
+    torch = _torch()
+    _on_gpu(W)
+    if W.dtype != torch.float32:
+        raise TypeError("W must be fp32")
+    if alpha.dtype != torch.float64 or alpha.device != W.device:
+        raise TypeError("alpha must be a float64 tensor on W's device")
+    N, K = W.shape
+    dev = W.device
+    out = {
+        "codes": torch.empty((N // 16, K // 128, 16, 32), dtype=torch.uint8, device=dev),
+        "meta": torch.empty((N // 16, K // 128, 16, 16), dtype=torch.uint8, device=dev),
+        "scales": torch.empty((N // 16, K // 128, 16), dtype=torch.int16, device=dev),
+        "N": N, "K": K,
+    }
+    mask = torch.empty((N, K), dtype=torch.uint8, device=dev) if with_mask else None
+    _check(slim_pack_alpha(_ptr(W), N, K, _ptr(alpha), _ptr(out["codes"]), _ptr(out["meta"]), _ptr(out["scales"]),
+                           _ptr(mask), _stream(stream)), "slim_pack_alpha")
     if with_mask:
         out["mask"] = mask
     return out
