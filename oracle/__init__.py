@@ -23,9 +23,11 @@ the thesis' definitions:
   "Implementation details").
 * SLiM-Quant's histogram-based mean-squared-error scale search (``slim_quant``; SLiM,
   eq. error_summation and Alg. quantization) and the forward pack with its per-tensor scale.
+* SLiM-LoRA's saliency-based adapters (``slim_lora``; SLiM, eq. lora_svd and Alg. lora).
 
 Parity status per function is stated in ``slim_oracle``'s module docstring.
 """
 from . import slim_oracle  # noqa: F401
 from . import slope_train  # noqa: F401
 from . import slim_quant  # noqa: F401
+from . import slim_lora  # noqa: F401
