@@ -407,6 +407,39 @@ int slim_pack_alpha(const float* W, int64_t N, int64_t K, const double* alpha, u
                     uint16_t* scales, uint8_t* mask, void* stream);
 
 /*
+ * SLiM-LoRA: saliency-based low-rank adapters fitted to the compression error (SLiM chapter,
+ * "SLiM-LoRA low-rank adapters": eq. lora_wanda_objective_function, eq. lora_svd, Alg. lora).
+ *
+ * slim_lora_workspace - bytes of workspace slim_lora needs for an [N, K] weight, B calibration rows
+ * and rank r (float64 buffers: the saliency-weighted error, its d x d Gram matrix and eigenvectors,
+ * d = min(N, K) rounded up to 64; about 8 (d max(N, K) + 2 d^2) bytes).
+ *
+ * slim_lora - the adapters.
+ *   W                fp32 [N, K], device: the uncompressed weight.
+ *   codes/meta/scales its forward pack (slim_pack or slim_pack_alpha), device: W^C.
+ *   X, xdtype, B     calibration activations [B, K] (bf16 or fp16), device.
+ *   r                rank, 0 <= r <= min(N, K).
+ *   L, R             out, fp32 [K, r] and [r, N], device: W ~ W^C + (L R)^T, i.e. the layer's adapter.
+ *   sigma            out, optional (NULL to skip): float64 [r], the r largest singular values of S.
+ *   sweeps           out, optional host int: Jacobi sweeps run.
+ *   ws, ws_bytes     workspace (slim_lora_workspace), 16-byte aligned; contents undefined after.
+ * With x_k = mean_i |X[i, k]| + min_j mean_i |X[i, j]| (the per-channel mean input magnitude shifted
+ * by its smallest value) and S = diag(x) (W^C - W)^T [K, N], L = -diag(1/x) U_r Sigma_r^(1/2) and
+ * R = Sigma_r^(1/2) V_r^T from the r largest singular triplets of S (ties to the lower index of
+ * the Gram side); each row of R has its largest-magnitude entry positive (the first on equal
+ * magnitudes), L's column following. The singular vectors come from a float64 two-sided block-
+ * Jacobi eigendecomposition of S S^T (K <= N) or S^T S (N < K), run until the off-diagonal norm is
+ * below 1e-13 of the Frobenius norm (or stalls at rounding level). Returns SLIM_ERANGE if some x_k is
+ * zero (a channel that is zero in every sample and is the smallest), SLIM_ENONFINITE for NaN/Inf
+ * inputs and SLIM_EUNSUPPORTED if 40 sweeps do not converge. Synchronises `stream` (the sweep loop
+ * reads back the off-diagonal norm); allocates nothing.
+ */
+int slim_lora_workspace(int64_t N, int64_t K, int64_t B, int64_t r, size_t* bytes);
+int slim_lora(const float* W, int64_t N, int64_t K, const uint8_t* codes, const uint8_t* meta,
+              const uint16_t* scales, const void* X, int xdtype, int64_t B, int64_t r, float* L, float* R,
+              double* sigma, int* sweeps, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Per-kernel timing for benchmarks (host-side bookkeeping; not part of the layer's math).
  * slim_timing_enable(1) makes every later kernel launch of this library record a hipEvent
  * before and after itself on the caller's stream. slim_timing_read waits for the recorded

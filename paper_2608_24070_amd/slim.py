@@ -52,6 +52,9 @@ _SIGS = {
     "slim_quant_bins": (ctypes.c_int, [_c_i64, _c_i64]),
     "slim_quant_search": (ctypes.c_int, [_c_p, _c_i64, ctypes.c_int, _c_i64, _c_p, _c_p, _c_p]),
     "slim_pack_alpha": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "slim_lora_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "slim_lora": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, ctypes.c_int, _c_i64, _c_i64, _c_p,
+                                 _c_p, _c_p, ctypes.POINTER(ctypes.c_int), _c_p, ctypes.c_size_t, _c_p]),
     "slim_timing_enable": (ctypes.c_int, [ctypes.c_int]),
     "slim_timing_reset": (ctypes.c_int, []),
     "slim_timing_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.c_size_t]),
@@ -120,6 +123,16 @@ def slim_quant_search(W, count, bits, bins, hist, out, stream) -> int:
 
 def slim_pack_alpha(W, N, K, alpha, codes, meta, scales, mask, stream) -> int:
     return lib().slim_pack_alpha(W, N, K, alpha, codes, meta, scales, mask, stream)
+
+
+def slim_lora_workspace(N, K, B, r) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().slim_lora_workspace(N, K, B, r, ctypes.byref(out)), "slim_lora_workspace")
+    return out.value
+
+
+def slim_lora(W, N, K, codes, meta, scales, X, xdtype, B, r, L, R, sigma, sweeps, ws, ws_bytes, stream) -> int:
+    return lib().slim_lora(W, N, K, codes, meta, scales, X, xdtype, B, r, L, R, sigma, sweeps, ws, ws_bytes, stream)
 
 
 def slim_pack_bwd(codes, meta, scales, N, K, codesT, metaT, scalesT, mask_rc, stream) -> int:
@@ -335,6 +348,32 @@ def pack_alpha(W, alpha, with_mask: bool = False, stream=None) -> dict:
     if with_mask:
         out["mask"] = mask
     return out
+
+
+def lora(W, packed: dict, X, r: int, stream=None) -> dict:
+    """slim_lora (SLiM-LoRA): adapters L fp32 [K, r], R fp32 [r, N] with W ~ W^C + (L R)^T from the
+    uncompressed weight W fp32 [N, K], its forward pack and calibration activations X [B, K]
+    (bf16/fp16). Returns {"L", "R", "sigma" float64 [r], "sweeps"}."""
+    torch = _torch()
+    _on_gpu(W)
+    _on_gpu(X)
+    if W.dtype != torch.float32:
+        raise TypeError("W must be fp32")
+    N, K = W.shape
+    B = X.shape[0]
+    if X.shape[1] != K:
+        raise ValueError("X must be [B, K]")
+    nbytes = slim_lora_workspace(N, K, B, r)
+    dev = W.device
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    L = torch.empty((K, r), dtype=torch.float32, device=dev)
+    R = torch.empty((r, N), dtype=torch.float32, device=dev)
+    sigma = torch.empty(max(r, 1), dtype=torch.float64, device=dev)
+    sweeps = ctypes.c_int(0)
+    _check(slim_lora(_ptr(W), N, K, _ptr(packed["codes"]), _ptr(packed["meta"]), _ptr(packed["scales"]), _ptr(X),
+                     _dtype_code(X), B, r, _ptr(L), _ptr(R), _ptr(sigma), ctypes.byref(sweeps), _ptr(ws), nbytes,
+                     _stream(stream)), "slim_lora")
+    return {"L": L, "R": R, "sigma": sigma[:r], "sweeps": sweeps.value}
 
 
 def pack_bwd(packed: dict, with_mask: bool = False, stream=None) -> dict:
