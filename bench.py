@@ -13,7 +13,7 @@ least 200 dispatches (40 for the training step), timed by their own dispatches i
 right after replays of the timed steps; the roofline uses the average. Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W]
-                  [--workload decode|prefill|block13b|mlp70b|mlp70b_bwd|tiny|train70b]
+                  [--workload decode|prefill|block13b|mlp70b|mlp70b_bwd|tiny|train70b|slimquant|slimlora]
                   [--m M] [--no-cpu-baseline] [--no-prefill] [--no-train] [--qadapter] [--dispatches D]
   python bench.py --copy-probe MB     # plain device copy of MB megabytes (counter calibration)
 
@@ -67,7 +67,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("include/slim.h", "paper_2608_24070_amd/csrc/api.cpp", "paper_2608_24070_amd/csrc/slim_host.h",
                   "paper_2608_24070_amd/csrc/slim_device.h", "paper_2608_24070_amd/csrc/sparse_gemm.hip",
                   "paper_2608_24070_amd/csrc/adapter_gemm.hip", "paper_2608_24070_amd/csrc/pack.hip",
-                  "paper_2608_24070_amd/csrc/train.hip")
+                  "paper_2608_24070_amd/csrc/train.hip", "paper_2608_24070_amd/csrc/quant.hip",
+                  "paper_2608_24070_amd/csrc/lora.hip")
 
 
 def kernel_source_hash():
@@ -149,7 +150,8 @@ def layer_flops(M, N, K, r):
     return 2 * M * N * K + 2 * M * r * (K + N)
 
 
-WORKLOADS = ["decode", "prefill", "block13b", "mlp70b", "mlp70b_bwd", "tiny", "train70b"]
+WORKLOADS = ["decode", "prefill", "block13b", "mlp70b", "mlp70b_bwd", "tiny", "train70b", "slimquant", "slimlora"]
+FP64_PEAK_TFS = 78.6        # MI355X fp64 vector peak
 
 
 def workload_layers(wk, m):
@@ -477,6 +479,149 @@ def measure_train(steps, warmup, dispatches, m=8192, n=28672, k=8192):
     return res
 
 
+def _host_fields():
+    model, usable, nproc = host_cpu()
+    return {"cpu_model": model, "nproc": nproc, "usable_cpus": usable}
+
+
+def _sync_call_times(call, steps, dispatches):
+    """Wall time per call of a synchronous library call (it reads back a status word, so it cannot be
+    captured in a graph), and per-kernel times from `dispatches` further calls with the timing hooks on."""
+    import torch
+    from paper_2608_24070_amd import slim
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        call()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    slim.slim_timing_reset()
+    slim.slim_timing_enable(True)
+    for _ in range(dispatches):
+        call()
+    slim.slim_timing_enable(False)
+    torch.cuda.synchronize()
+    kt = slim.slim_timing_read()
+    kernels = {kn: {"launches": c, "avg_us": round(1e3 * tot / max(c, 1), 3), "median_us": round(1e3 * med, 3)}
+               for kn, (c, tot, med) in kt.items()}
+    return ms, kt, kernels
+
+
+def measure_slimquant(steps, warmup, dispatches, cpu, n=28672, k=8192):
+    """SLiM-Quant's scale search (slim_quant_search) on the 70B MLP projection's fp32 weight: one step
+    = one search (maximum pass, histogram pass into 20000 bins, float64 grid search)."""
+    import numpy as np
+    import torch
+    from paper_2608_24070_amd import slim
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(0)
+    W = torch.randn((n, k), device=dev, generator=gen) * 0.02
+    for _ in range(max(warmup, 1)):
+        slim.quant_search(W)
+    steps = min(steps, 50)
+    ms, kt, kernels = _sync_call_times(lambda: slim.quant_search(W), steps, min(dispatches, 50))
+    nbytes = 4.0 * n * k
+    avg_s = kt["quant_hist"][1] / kt["quant_hist"][0] * 1e-3
+    achieved = nbytes / avg_s / 1e9
+    print(f"[bench] slim-quant search {n}x{k}: {ms * 1e3:.1f} us/search", file=sys.stderr, flush=True)
+    base = None
+    if cpu:
+        from oracle import slim_quant as Q
+        rows = 2048
+        Wh = W[:rows].cpu().numpy()
+        reps, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < 10.0 or reps < 1:
+            Q.search(Wh, bins=Q.bin_count(n, k))
+            reps += 1
+        sec = (time.perf_counter() - t0) / reps
+        base = {"value": round(rows * k * 4 / sec / 1e9, 4), "unit": "GB/s", "cores": torch.get_num_threads(),
+                "kind": "oracle", "sample": f"search over the first {rows} of {n} rows ({reps} calls, "
+                                            f"{sec * 1e3:.0f} ms each)", **_host_fields()}
+    return {
+        "metric": "SLiM-Quant scale search, weight GB/s (fp32 bytes of W per search time)",
+        "value": round(nbytes / (ms * 1e-3) / 1e9, 2), "unit": "GB/s", "ms_per_step": round(ms, 6),
+        "config": {"workload": f"slim-quant search: 70B MLP projection {n}x{k} fp32 W, 4-bit, 20000 bins",
+                   "N": n, "K": k, "bins": slim.slim_quant_bins(n, k)},
+        "kernels": kernels,
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "algorithmic_bytes_per_launch": int(nbytes),
+                     "traffic": None, "kernel": "quant_hist",
+                     "timing": f"average of {kt['quant_hist'][0]} dispatches; hip events recorded by each kernel "
+                               "dispatch"},
+        "cpu_baseline": base,
+    }
+
+
+def measure_slimlora(steps, warmup, cpu, n=4096, k=4096, r=384, b=2048):
+    """SLiM-LoRA (slim_lora) on the decode layer 4096 x 4096 at rank 384 with 2048 bf16 calibration
+    rows (1% outlier channels x20): one step = one adapter fit."""
+    import numpy as np
+    import torch
+    from paper_2608_24070_amd import slim, synth
+    dev = torch.device("cuda:0")
+    W = torch.from_numpy(synth.weights(n, k, seed=0, name="bench/lora/W")).to(dev)
+    xbits, _ = synth.activations(b, k, seed=0, name="bench/lora/X", dtype="bf16", outliers=True)
+    X = torch.from_numpy(xbits.view(np.int16)).to(dev).view(torch.bfloat16)
+    p = slim.pack(W)
+    for _ in range(max(min(warmup, 1), 1)):
+        out = slim.lora(W, p, X, r)
+    steps = min(steps, 3)
+    ms, kt, kernels = _sync_call_times(lambda: slim.lora(W, p, X, r), steps, 1)
+    sweeps = out["sweeps"]
+    dp = (min(n, k) + 63) // 64 * 64                       # the Gram side, padded to the 64-wide pairs
+    npair = dp // 64
+    flops = 4.0 * 64 ** 3 * npair * (npair + 1) / 2       # J_a^T (G J_c) on the tiles a <= c
+    # the dominant kernel by total time is the tile update of G (asserted, so the line cannot
+    # silently price a kernel that is not the dominant one)
+    dom = max(kt.items(), key=lambda kv: kv[1][1])[0]
+    if dom != "lora_apply_g":
+        raise RuntimeError(f"slim-lora: dominant kernel is {dom}, the roofline below prices lora_apply_g")
+    avg_s = kt["lora_apply_g"][1] / kt["lora_apply_g"][0] * 1e-3
+    achieved = flops / avg_s / 1e12
+    print(f"[bench] slim-lora {n}x{k} r={r}: {ms:.1f} ms/fit, {sweeps} sweeps", file=sys.stderr, flush=True)
+    base = None
+    if cpu:
+        from oracle import slim_lora as LR
+        from oracle import slim_oracle as O
+        rows = 1024                                          # the oracle's SVD on a 1024-row slice of W
+        Wh = W[:rows].cpu().numpy()
+        ref = O.pack(Wh)
+        Wc = O.unpack(ref["codes"], ref["meta"], ref["scales"], rows, k)
+        Xh = X.float().cpu().numpy()
+        reps, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < 10.0 or reps < 1:
+            LR.lora(Wh, Wc, Xh, r)
+            reps += 1
+        sec = (time.perf_counter() - t0) / reps
+        base = {"value": round(1.0 / sec, 4), "unit": "fits/s", "cores": torch.get_num_threads(), "kind": "oracle",
+                "sample": f"adapter fit of a {rows} x {k} slice of W (rank {r}, {b} calibration rows; the SVD cost "
+                          f"grows with the slice), {reps} calls of {sec * 1e3:.0f} ms", **_host_fields()}
+    return {
+        "metric": "SLiM-LoRA adapter fit, fits/s",
+        "value": round(1e3 / ms, 4), "unit": "fits/s", "ms_per_step": round(ms, 3),
+        "config": {"workload": f"slim-lora: decode layer {n}x{k}, rank {r}, {b} bf16 calibration rows "
+                               "(1% outlier channels x20), float64 block-Jacobi", "N": n, "K": k, "r": r, "B": b,
+                   "jacobi_sweeps": sweeps},
+        "kernels": kernels,
+        "roofline": {"bound": "alu", "achieved": round(achieved, 2), "peak": FP64_PEAK_TFS, "unit": "TFLOP/s",
+                     "frac": round(achieved / FP64_PEAK_TFS, 4), "flops_per_launch": int(flops), "traffic": None,
+                     "kernel": "lora_apply_g",
+                     "timing": f"average of {kt['lora_apply_g'][0]} dispatches of one fit; hip events recorded by "
+                               "each kernel dispatch"},
+        "cpu_baseline": base,
+    }
+
+
+def _single_line(obj, args, dtype):
+    print(json.dumps({"metric": obj["metric"], "value": obj["value"], "unit": obj["unit"], "n_gpus": 1,
+                      "steps": args.steps, "warmup": args.warmup, "ms_per_step": obj["ms_per_step"],
+                      "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+                      "data": "synthetic", "config": {**obj["config"], "kernel_source_hash": kernel_source_hash()},
+                      "kernels": obj["kernels"], "roofline": obj["roofline"],
+                      "cpu_baseline": obj.get("cpu_baseline")}))
+
+
 def main():
     args = parse()
     if args.copy_probe is not None:
@@ -495,6 +640,12 @@ def main():
     if args.qadapter and args.workload == "mlp70b_bwd":
         print("--qadapter applies to the forward only", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "slimquant":
+        _single_line(measure_slimquant(args.steps, args.warmup, dispatches, not args.no_cpu_baseline), args, "f64")
+        return
+    if args.workload == "slimlora":
+        _single_line(measure_slimlora(args.steps, args.warmup, not args.no_cpu_baseline), args, "f64")
+        return
     if args.workload == "train70b":
         # the training-step calls alone (the object the default line carries as "train")
         tr = measure_train(args.steps, args.warmup, dispatches, m=args.m or 8192)

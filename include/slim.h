@@ -428,7 +428,8 @@ int slim_pack_alpha(const float* W, int64_t N, int64_t K, const double* alpha, u
  * R = Sigma_r^(1/2) V_r^T from the r largest singular triplets of S (ties to the lower index of
  * the Gram side); each row of R has its largest-magnitude entry positive (the first on equal
  * magnitudes), L's column following. The singular vectors come from a float64 two-sided block-
- * Jacobi eigendecomposition of S S^T (K <= N) or S^T S (N < K), run until the off-diagonal norm is
+ * Jacobi eigendecomposition (blocks of 32, one inner sweep per pair) of S S^T (K <= N) or S^T S
+ * (N < K), run until the off-diagonal norm is
  * below 1e-13 of the Frobenius norm (or stalls at rounding level). Returns SLIM_ERANGE if some x_k is
  * zero (a channel that is zero in every sample and is the smallest), SLIM_ENONFINITE for NaN/Inf
  * inputs and SLIM_EUNSUPPORTED if 40 sweeps do not converge. Synchronises `stream` (the sweep loop

@@ -10,8 +10,10 @@
 // from one more product with A.
 //
 // The eigensolver is two-sided block Jacobi. Indices are cut into blocks of 32; each round pairs
-// the blocks by the round-robin (circle) schedule, and every pair's 64 x 64 diagonal block of G is
-// diagonalised in LDS by cyclic Jacobi (k_lora_pair_solve, its own round-robin over 64 indices);
+// the blocks by the round-robin (circle) schedule, and every pair's 64 x 64 diagonal block of G gets
+// one cyclic Jacobi sweep in LDS (k_lora_pair_solve, its own round-robin over 64 indices: running
+// the inner problem to convergence instead costs about six times as much per round and saves at most
+// one outer sweep);
 // the round then applies the pairs' rotations to G (G <- J^T G J, tile by tile, k_lora_apply_g)
 // and accumulates them in V (V <- V J, k_lora_apply_v). Sweeps of nb - 1 rounds repeat until the
 // off-diagonal norm of G falls below 1e-13 of its Frobenius norm (or stalls at rounding level).
@@ -28,7 +30,7 @@ constexpr int kLB = 32;              // Jacobi block
 constexpr int kLP = 2 * kLB;         // pair size
 constexpr int kLT = 256;             // threads of the tiled kernels
 constexpr int kLPad = kLP + 1;       // LDS row pitch (doubles) of 64 x 64 tiles
-constexpr int kLInnerSweeps = 12;
+constexpr int kLInnerSweeps = 1;
 constexpr int kLMaxSweeps = 40;
 constexpr int kLCalibRows = 256;     // calibration rows per partial sum
 constexpr int kLOffBlocks = 512;
@@ -242,8 +244,9 @@ __device__ __forceinline__ bool rotation(double app, double aqq, double apq, dou
   return true;
 }
 
-// One block per pair of round t: diagonalise G's 64 x 64 block of the pair by cyclic Jacobi and
-// write its rotation J (64 x 64, row-major) to Jout[pair].
+// One block per pair of round t: kLInnerSweeps cyclic Jacobi sweeps over G's 64 x 64 block of the
+// pair (fewer if a sweep rotates nothing); its accumulated rotation J (64 x 64, row-major) goes to
+// Jout[pair].
 __global__ void __launch_bounds__(kLT)
 k_lora_pair_solve(const double* __restrict__ G, int64_t dp, int nb, int t, double* __restrict__ Jout) {
   __shared__ double a[kLP][kLPad], j[kLP][kLPad];
