@@ -24,6 +24,8 @@ the thesis' definitions:
 * SLiM-Quant's histogram-based mean-squared-error scale search (``slim_quant``; SLiM,
   eq. error_summation and Alg. quantization) and the forward pack with its per-tensor scale.
 * SLiM-LoRA's saliency-based adapters (``slim_lora``; SLiM, eq. lora_svd and Alg. lora).
+* PATCH's hybrid dense / 2:4 tile weight and its product (``patch_hybrid``; PATCH, "Efficient
+  deployment of PATCH").
 
 Parity status per function is stated in ``slim_oracle``'s module docstring.
 """
@@ -31,3 +33,4 @@ from . import slim_oracle  # noqa: F401
 from . import slope_train  # noqa: F401
 from . import slim_quant  # noqa: F401
 from . import slim_lora  # noqa: F401
+from . import patch_hybrid  # noqa: F401
