@@ -68,7 +68,7 @@ KERNEL_SOURCES = ("include/slim.h", "paper_2608_24070_amd/csrc/api.cpp", "paper_
                   "paper_2608_24070_amd/csrc/slim_device.h", "paper_2608_24070_amd/csrc/sparse_gemm.hip",
                   "paper_2608_24070_amd/csrc/adapter_gemm.hip", "paper_2608_24070_amd/csrc/pack.hip",
                   "paper_2608_24070_amd/csrc/train.hip", "paper_2608_24070_amd/csrc/quant.hip",
-                  "paper_2608_24070_amd/csrc/lora.hip")
+                  "paper_2608_24070_amd/csrc/lora.hip", "paper_2608_24070_amd/csrc/hybrid.hip")
 
 
 def kernel_source_hash():

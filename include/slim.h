@@ -441,6 +441,42 @@ int slim_lora(const float* W, int64_t N, int64_t K, const uint8_t* codes, const 
               double* sigma, int* sweeps, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * PATCH hybrid tiles: a weight whose 128 x 128 tiles are each dense or 2:4 sparse, in fp16, and its
+ * product (PATCH chapter, "Efficient deployment of PATCH": hybrid sparse-dense tiles in one GEMM,
+ * 128 x 128 as the tile size; appendix "STOICC Integration").
+ *
+ * slim_hybrid_layout - host-only: from the tile map `kinds` (host uint8 [N/128, K/128], row-major;
+ *   1 = 2:4 sparse, 0 = dense) the payload size in bytes and, if tile_info (host) is not NULL, each
+ *   tile's info word: its payload's byte offset, bit 63 set for a sparse tile. Payloads follow each
+ *   other in row-major tile order: a dense tile is 128 rows x 128 fp16 (32768 bytes); a sparse tile
+ *   is 128 rows x 64 fp16 kept values (group g of a row's 32 groups at 2g, 2g+1, the lower position
+ *   first) followed by 128 rows x 8 uint16 index half-words (half-word b covers positions
+ *   16b .. 16b+15; group c holds i0 in bits 4c..4c+1 and i1 in bits 4c+2..4c+3), 18432 bytes.
+ *   N, K multiples of 128.
+ *
+ * slim_pack_hybrid - one-time pack of fp32 W [N, K] (device) with the tile map `kinds` (host):
+ *   writes tile_info (device uint64 [N/128, K/128]) and the payload (device, payload_bytes from
+ *   slim_hybrid_layout). A sparse tile keeps the two largest |w| of every aligned group of four along
+ *   K (the lower position on equal magnitude); all kept values are rounded to fp16 (nearest, ties to
+ *   even). Returns SLIM_ENONFINITE for NaN/Inf in W; synchronises `stream` (status read-back) and
+ *   allocates 4 bytes of device memory for the call.
+ *
+ * slim_linear_hybrid_workspace / slim_linear_hybrid - Y = X Wp^T.
+ *   X          fp16 [M, K], device.            tile_info, payload   the hybrid pack, device.
+ *   Y          out, fp32 [M, N], device.       ws, ws_bytes         workspace (split partials of
+ *              small-M calls; 0 bytes when the call needs none), 16-byte aligned.
+ * Dense tiles run on v_mfma_f32_32x32x16_f16, sparse tiles on v_smfmac_f32_32x32x32_f16 (half
+ * the issue for the same K); fp32 accumulation; the split partials are summed in split order, so
+ * results are deterministic. Asynchronous; allocates nothing.
+ */
+int slim_hybrid_layout(const uint8_t* kinds, int64_t N, int64_t K, uint64_t* tile_info, size_t* payload_bytes);
+int slim_pack_hybrid(const float* W, int64_t N, int64_t K, const uint8_t* kinds, uint64_t* tile_info,
+                     uint8_t* payload, size_t payload_bytes, void* stream);
+int slim_linear_hybrid_workspace(int64_t M, int64_t N, int64_t K, size_t* bytes);
+int slim_linear_hybrid(const void* X, int64_t M, int64_t N, int64_t K, const uint64_t* tile_info,
+                       const uint8_t* payload, float* Y, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Per-kernel timing for benchmarks (host-side bookkeeping; not part of the layer's math).
  * slim_timing_enable(1) makes every later kernel launch of this library record a hipEvent
  * before and after itself on the caller's stream. slim_timing_read waits for the recorded

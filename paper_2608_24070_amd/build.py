@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libslim.so")
-SOURCES = ["api.cpp", "pack.hip", "adapter_gemm.hip", "sparse_gemm.hip", "train.hip", "quant.hip", "lora.hip", "timing.hip"]
+SOURCES = ["api.cpp", "pack.hip", "adapter_gemm.hip", "sparse_gemm.hip", "train.hip", "quant.hip", "lora.hip", "hybrid.hip", "timing.hip"]
 ARCH = "gfx950"
 
 

@@ -52,6 +52,10 @@ _SIGS = {
     "slim_quant_bins": (ctypes.c_int, [_c_i64, _c_i64]),
     "slim_quant_search": (ctypes.c_int, [_c_p, _c_i64, ctypes.c_int, _c_i64, _c_p, _c_p, _c_p]),
     "slim_pack_alpha": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "slim_hybrid_layout": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, ctypes.POINTER(ctypes.c_size_t)]),
+    "slim_pack_hybrid": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
+    "slim_linear_hybrid_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "slim_linear_hybrid": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
     "slim_lora_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
     "slim_lora": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, ctypes.c_int, _c_i64, _c_i64, _c_p,
                                  _c_p, _c_p, ctypes.POINTER(ctypes.c_int), _c_p, ctypes.c_size_t, _c_p]),
@@ -123,6 +127,24 @@ def slim_quant_search(W, count, bits, bins, hist, out, stream) -> int:
 
 def slim_pack_alpha(W, N, K, alpha, codes, meta, scales, mask, stream) -> int:
     return lib().slim_pack_alpha(W, N, K, alpha, codes, meta, scales, mask, stream)
+
+
+def slim_hybrid_layout(kinds, N, K, tile_info, payload_bytes) -> int:
+    return lib().slim_hybrid_layout(kinds, N, K, tile_info, payload_bytes)
+
+
+def slim_pack_hybrid(W, N, K, kinds, tile_info, payload, payload_bytes, stream) -> int:
+    return lib().slim_pack_hybrid(W, N, K, kinds, tile_info, payload, payload_bytes, stream)
+
+
+def slim_linear_hybrid_workspace(M, N, K) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().slim_linear_hybrid_workspace(M, N, K, ctypes.byref(out)), "slim_linear_hybrid_workspace")
+    return out.value
+
+
+def slim_linear_hybrid(X, M, N, K, tile_info, payload, Y, ws, ws_bytes, stream) -> int:
+    return lib().slim_linear_hybrid(X, M, N, K, tile_info, payload, Y, ws, ws_bytes, stream)
 
 
 def slim_lora_workspace(N, K, B, r) -> int:
@@ -348,6 +370,57 @@ def pack_alpha(W, alpha, with_mask: bool = False, stream=None) -> dict:
     if with_mask:
         out["mask"] = mask
     return out
+
+
+def pack_hybrid(W, kinds, stream=None) -> dict:
+    """slim_pack_hybrid: fp32 W [N, K] (device) with a tile map (numpy uint8 [N/128, K/128], 1 = 2:4
+    sparse) -> {"tile_info" int64 [N/128, K/128] (uint64 words), "payload" uint8, "N", "K"}."""
+    import numpy as np
+    torch = _torch()
+    _on_gpu(W)
+    if W.dtype != torch.float32:
+        raise TypeError("W must be fp32")
+    N, K = W.shape
+    kinds = np.ascontiguousarray(np.asarray(kinds, dtype=np.uint8))
+    if kinds.shape != (N // 128, K // 128):
+        raise ValueError("the tile map must be [N/128, K/128]")
+    nbytes = ctypes.c_size_t(0)
+    kp = kinds.ctypes.data_as(ctypes.c_void_p)
+    _check(slim_hybrid_layout(kp, N, K, None, ctypes.byref(nbytes)), "slim_hybrid_layout")
+    info = torch.empty((N // 128, K // 128), dtype=torch.int64, device=W.device)
+    payload = torch.empty(max(nbytes.value, 16), dtype=torch.uint8, device=W.device)
+    _check(slim_pack_hybrid(_ptr(W), N, K, kp, _ptr(info), _ptr(payload), nbytes.value, _stream(stream)),
+           "slim_pack_hybrid")
+    return {"tile_info": info, "payload": payload, "N": N, "K": K}
+
+
+_hybrid_ws: dict = {}
+
+
+def linear_hybrid(X, p: dict, out=None, stream=None):
+    """slim_linear_hybrid: Y fp32 [M, N] = X Wp^T for fp16 X [M, K] and a hybrid pack."""
+    torch = _torch()
+    _on_gpu(X)
+    if X.dtype != torch.float16:
+        raise TypeError("X must be fp16")
+    M, K = X.shape
+    N = p["N"]
+    if K != p["K"]:
+        raise ValueError("X width does not match the pack")
+    Y = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=X.device)
+    nb = slim_linear_hybrid_workspace(M, N, K)
+    ws = None
+    if nb:
+        # its own cache: the split partials must not land in slim_linear's workspace, whose counter
+        # region has to stay zero between calls
+        key = (X.device, _stream(stream))
+        ws = _hybrid_ws.get(key)
+        if ws is None or ws.numel() < nb:
+            ws = torch.empty(nb, dtype=torch.uint8, device=X.device)
+            _hybrid_ws[key] = ws
+    _check(slim_linear_hybrid(_ptr(X), M, N, K, _ptr(p["tile_info"]), _ptr(p["payload"]), _ptr(Y), _ptr(ws), nb,
+                              _stream(stream)), "slim_linear_hybrid")
+    return Y
 
 
 def lora(W, packed: dict, X, r: int, stream=None) -> dict:
