@@ -150,7 +150,8 @@ def layer_flops(M, N, K, r):
     return 2 * M * N * K + 2 * M * r * (K + N)
 
 
-WORKLOADS = ["decode", "prefill", "block13b", "mlp70b", "mlp70b_bwd", "tiny", "train70b", "slimquant", "slimlora"]
+WORKLOADS = ["decode", "prefill", "block13b", "mlp70b", "mlp70b_bwd", "tiny", "train70b", "slimquant", "slimlora",
+             "patch7b"]
 FP64_PEAK_TFS = 78.6        # MI355X fp64 vector peak
 
 
@@ -613,13 +614,122 @@ def measure_slimlora(steps, warmup, cpu, n=4096, k=4096, r=384, b=2048):
     }
 
 
-def _single_line(obj, args, dtype):
+def measure_hybrid(steps, warmup, dispatches, m, frac, n=11008, k=4096, seed=0):
+    """PATCH's hybrid dense / 2:4 tile layer (slim_linear_hybrid) on the LLaMA-2-7B gate projection
+    11008 x 4096 with a synthetic tile map (fraction `frac` of the 128 x 128 tiles 2:4, the rest
+    dense; sparsity frac / 2), fp16 X [m, 4096]. Timed like measure(): a captured graph of `steps`
+    calls over weight copies rotating past the MALL, after WARM_MS of replays."""
+    import numpy as np
+    import torch
+    from paper_2608_24070_amd import slim
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    W = torch.randn((n, k), device=dev, generator=gen) * 0.02
+    kinds = (np.random.default_rng(seed).random((n // 128, k // 128)) < frac).astype(np.uint8)
+    p0 = slim.pack_hybrid(W, kinds)
+    wbytes = int(p0["payload"].numel())
+    n_copies = max(1, min(64, -(-3 * 256 * 2 ** 20 // wbytes))) if m <= 32 else 1
+    copies = [p0] + [{"tile_info": p0["tile_info"], "payload": p0["payload"].clone(), "N": n, "K": k}
+                     for _ in range(n_copies - 1)]
+    del W
+    X = (torch.randn((m, k), device=dev, generator=gen)).to(torch.float16)
+    Y = torch.empty((m, n), dtype=torch.float32, device=dev)
+    ctr = [0]
+
+    def step():
+        slim.linear_hybrid(X, copies[ctr[0] % n_copies], out=Y)
+        ctr[0] += 1
+
+    for _ in range(max(warmup, 2)):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    graphs = []
+    for _ in range(n_copies if m <= 32 else 1):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(steps):
+                step()
+        graphs.append(g)
+    torch.cuda.synchronize()
+    tw = time.perf_counter()
+    while (time.perf_counter() - tw) * 1e3 < WARM_MS:
+        for g in graphs:
+            g.replay()
+        torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    graphs[0].replay()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / steps
+    slim.slim_timing_reset()
+    done = 0
+    while done < dispatches:
+        graphs[0].replay()
+        slim.slim_timing_enable(True)
+        for _ in range(min(KBURST, dispatches - done)):
+            step()
+        slim.slim_timing_enable(False)
+        done += KBURST
+    torch.cuda.synchronize()
+    kt = slim.slim_timing_read()
+    del graphs, copies
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    kernels = {kn: {"launches": c, "avg_us": round(1e3 * tot / max(c, 1), 3), "median_us": round(1e3 * med, 3)}
+               for kn, (c, tot, med) in kt.items()}
+    avg_s = kt["hybrid_gemm"][1] / kt["hybrid_gemm"][0] * 1e-3
+    flops = 2.0 * m * n * k
+    algo_bytes = wbytes + 2 * m * k + 4 * m * n
+    if m <= 32:
+        achieved = algo_bytes / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "algorithmic_bytes_per_launch": int(algo_bytes)}
+        value, unit = algo_bytes / (ms * 1e-3) / 1e9, "GB/s"
+    else:
+        achieved = flops / avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_F16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": round(achieved / MFMA_F16_PEAK_TFS, 4), "dense_equiv_flops_per_launch": int(flops)}
+        value, unit = flops / (ms * 1e-3) / 1e12, "TFLOP/s"
+    roof.update({"traffic": None, "kernel": "hybrid_gemm",
+                 "timing": f"average of {kt['hybrid_gemm'][0]} dispatches; hip events recorded by each kernel "
+                           f"dispatch, in bursts of {KBURST} steps each right after a replay of the timed graph"})
+    print(f"[bench] patch hybrid {n}x{k} M={m} sparse tiles {kinds.mean():.3f}: {ms * 1e3:.2f} us/step "
+          f"({n_copies} weight copies)", file=sys.stderr, flush=True)
+    return {"value": round(value, 2), "unit": unit, "ms_per_step": round(ms, 6),
+            "config": {"workload": f"patch hybrid tiles: LLaMA-2-7B gate projection {n}x{k}, M={m}, fp16 X and "
+                                   f"weights, {100 * kinds.mean():.1f}% of 128x128 tiles 2:4 (sparsity "
+                                   f"{50 * kinds.mean():.1f}%)", "M": m, "N": n, "K": k,
+                       "sparse_tile_fraction": round(float(kinds.mean()), 4), "payload_bytes": wbytes,
+                       "weight_copies_rotated": n_copies},
+            "kernels": kernels, "roofline": roof}
+
+
+def measure_patch(steps, warmup, dispatches, frac=0.7):
+    """Decode (M = 16) and prefill (M = 2048, batch 16 x 128 tokens) of the hybrid layer, each with the
+    same kernel on an all-dense tile map for the speedup PATCH is after."""
+    out = {}
+    for m in (16, 2048):
+        hyb = measure_hybrid(steps, warmup, dispatches, m, frac)
+        dense = measure_hybrid(steps, warmup, dispatches, m, 0.0)
+        hyb["speedup_vs_dense_tiles"] = round(dense["ms_per_step"] / hyb["ms_per_step"], 4)
+        hyb["dense_tiles_ms_per_step"] = dense["ms_per_step"]
+        out[m] = hyb
+    main = out[16]
+    main["metric"] = "PATCH hybrid-tile layer, weight-stream HBM GB/s (M=16)"
+    main["prefill"] = {"metric": "PATCH hybrid-tile layer, dense-equiv TFLOP/s (M=2048)", **out[2048]}
+    return main
+
+
+def _single_line(obj, args, dtype, extra=None):
     print(json.dumps({"metric": obj["metric"], "value": obj["value"], "unit": obj["unit"], "n_gpus": 1,
                       "steps": args.steps, "warmup": args.warmup, "ms_per_step": obj["ms_per_step"],
                       "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dtype,
                       "data": "synthetic", "config": {**obj["config"], "kernel_source_hash": kernel_source_hash()},
                       "kernels": obj["kernels"], "roofline": obj["roofline"],
-                      "cpu_baseline": obj.get("cpu_baseline")}))
+                      "cpu_baseline": obj.get("cpu_baseline"), **(extra or {})}))
 
 
 def main():
@@ -640,6 +750,12 @@ def main():
     if args.qadapter and args.workload == "mlp70b_bwd":
         print("--qadapter applies to the forward only", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "patch7b":
+        obj = measure_patch(args.steps, args.warmup, dispatches)
+        _single_line(obj, args, "f16", {"speedup_vs_dense_tiles": obj["speedup_vs_dense_tiles"],
+                                        "dense_tiles_ms_per_step": obj["dense_tiles_ms_per_step"],
+                                        "prefill": obj["prefill"]})
+        return
     if args.workload == "slimquant":
         _single_line(measure_slimquant(args.steps, args.warmup, dispatches, not args.no_cpu_baseline), args, "f64")
         return
