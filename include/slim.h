@@ -449,9 +449,10 @@ int slim_lora(const float* W, int64_t N, int64_t K, const uint8_t* codes, const 
  *   1 = 2:4 sparse, 0 = dense) the payload size in bytes and, if tile_info (host) is not NULL, each
  *   tile's info word: its payload's byte offset, bit 63 set for a sparse tile. Payloads follow each
  *   other in row-major tile order: a dense tile is 128 rows x 128 fp16 (32768 bytes); a sparse tile
- *   is 128 rows x 64 fp16 kept values (group g of a row's 32 groups at 2g, 2g+1, the lower position
- *   first) followed by 128 rows x 8 uint16 index half-words (half-word b covers positions
- *   16b .. 16b+15; group c holds i0 in bits 4c..4c+1 and i1 in bits 4c+2..4c+3), 18432 bytes.
+ *   is two halves (positions 0..63, then 64..127) of 9216 bytes: 128 rows x 32 fp16 kept values
+ *   (group g of the half's 16 groups at 2g, 2g+1, the lower position first), then 128 rows x 4
+ *   uint16 index half-words (half-word b covers the half's positions 16b .. 16b+15; group c holds
+ *   i0 in bits 4c..4c+1 and i1 in bits 4c+2..4c+3); 18432 bytes.
  *   N, K multiples of 128.
  *
  * slim_pack_hybrid - one-time pack of fp32 W [N, K] (device) with the tile map `kinds` (host):
@@ -462,7 +463,8 @@ int slim_lora(const float* W, int64_t N, int64_t K, const uint8_t* codes, const 
  *   allocates 4 bytes of device memory for the call.
  *
  * slim_linear_hybrid_workspace / slim_linear_hybrid - Y = X Wp^T.
- *   X          fp16 [M, K], device.            tile_info, payload   the hybrid pack, device.
+ *   X          fp16 [M, K], device.            tile_info, payload   the hybrid pack, device;
+ *                                              payload_bytes        its size, below 4 GiB.
  *   Y          out, fp32 [M, N], device.       ws, ws_bytes         workspace (split partials of
  *              small-M calls; 0 bytes when the call needs none), 16-byte aligned.
  * Dense tiles run on v_mfma_f32_32x32x16_f16, sparse tiles on v_smfmac_f32_32x32x32_f16 (half
@@ -474,7 +476,8 @@ int slim_pack_hybrid(const float* W, int64_t N, int64_t K, const uint8_t* kinds,
                      uint8_t* payload, size_t payload_bytes, void* stream);
 int slim_linear_hybrid_workspace(int64_t M, int64_t N, int64_t K, size_t* bytes);
 int slim_linear_hybrid(const void* X, int64_t M, int64_t N, int64_t K, const uint64_t* tile_info,
-                       const uint8_t* payload, float* Y, void* ws, size_t ws_bytes, void* stream);
+                       const uint8_t* payload, size_t payload_bytes, float* Y, void* ws, size_t ws_bytes,
+                       void* stream);
 
 /*
  * Per-kernel timing for benchmarks (host-side bookkeeping; not part of the layer's math).

@@ -30,9 +30,10 @@ Format
 ``tile_info`` uint64 [N/128, K/128]: byte offset of the tile's payload (16-byte aligned), with bit
 63 set for a sparse tile. Payloads follow each other in row-major tile order.
 * dense tile: 128 rows x 128 fp16 (256 bytes per row), 32768 bytes;
-* sparse tile: 128 rows x 64 fp16 kept values (group g of the row's 32 groups at 2g, 2g+1, the lower
-  kept position first), then 128 rows x 8 uint16 index half-words (half-word b covers positions
-  16b .. 16b+15; group c of it holds i0 in bits 4c..4c+1 and i1 in bits 4c+2..4c+3), 18432 bytes.
+* sparse tile: two halves (positions 0..63, then 64..127) of 9216 bytes each: 128 rows x 32 fp16 kept
+  values (group g of the half's 16 groups at 2g, 2g+1, the lower kept position first), then 128 rows
+  x 4 uint16 index half-words (half-word b covers the half's positions 16b .. 16b+15; group c of it
+  holds i0 in bits 4c..4c+1 and i1 in bits 4c+2..4c+3); 18432 bytes.
 """
 from __future__ import annotations
 
@@ -42,7 +43,8 @@ from .slim_oracle import OracleError, fp16_rne, mask_2of4
 
 TILE = 128
 DENSE_BYTES = TILE * TILE * 2
-SPARSE_BYTES = TILE * TILE + TILE * TILE // 8
+SPARSE_HALF = TILE * TILE // 2 + TILE * TILE // 16
+SPARSE_BYTES = 2 * SPARSE_HALF
 SPARSE_BIT = np.uint64(1) << np.uint64(63)
 
 
@@ -102,11 +104,15 @@ def pack(W, kinds) -> dict:
                 mg = m[rows, cols].reshape(TILE, TILE // 4, 4)
                 idx = np.sort(np.argsort(-mg.astype(np.int8), axis=2, kind="stable")[..., :2], axis=2)
                 vals = np.take_along_axis(h[rows, cols].reshape(TILE, TILE // 4, 4), idx, axis=2)
-                out[off:off + TILE * TILE] = vals.reshape(TILE, TILE // 2).view(np.uint8).reshape(-1)
                 c = np.arange(4, dtype=np.uint32)
                 ix = idx.reshape(TILE, TILE // 16, 4, 2).astype(np.uint32)
                 half = ((ix[..., 0] << (4 * c)) | (ix[..., 1] << (4 * c + 2))).sum(axis=2, dtype=np.uint32)
-                out[off + TILE * TILE:off + SPARSE_BYTES] = half.astype("<u2").view(np.uint8).reshape(-1)
+                for hf in range(2):
+                    o = off + hf * SPARSE_HALF
+                    v = vals[:, 16 * hf:16 * hf + 16].reshape(TILE, TILE // 4)
+                    out[o:o + TILE * TILE // 2] = np.ascontiguousarray(v).view(np.uint8).reshape(-1)
+                    hw = np.ascontiguousarray(half[:, 4 * hf:4 * hf + 4]).astype("<u2")
+                    out[o + TILE * TILE // 2:o + SPARSE_HALF] = hw.view(np.uint8).reshape(-1)
                 off += SPARSE_BYTES
             else:
                 info[a, b] = np.uint64(off)
@@ -125,8 +131,13 @@ def unpack(tile_info, payload, n: int, k: int) -> np.ndarray:
             off = int(info[a, b] & ~SPARSE_BIT)
             blk = Wp[a * TILE:(a + 1) * TILE, b * TILE:(b + 1) * TILE]
             if int(info[a, b] >> np.uint64(63)):
-                vals = payload[off:off + TILE * TILE].view(np.float16).reshape(TILE, TILE // 4, 2).astype(np.float64)
-                half = payload[off + TILE * TILE:off + SPARSE_BYTES].view("<u2").reshape(TILE, TILE // 16)
+                vparts, hparts = [], []
+                for hf in range(2):
+                    o = off + hf * SPARSE_HALF
+                    vparts.append(payload[o:o + TILE * TILE // 2].view(np.float16).reshape(TILE, TILE // 4))
+                    hparts.append(payload[o + TILE * TILE // 2:o + SPARSE_HALF].view("<u2").reshape(TILE, TILE // 32))
+                vals = np.concatenate(vparts, axis=1).reshape(TILE, TILE // 4, 2).astype(np.float64)
+                half = np.concatenate(hparts, axis=1)
                 c = np.arange(4)
                 i0 = (half[..., None].astype(np.int64) >> (4 * c)) & 3
                 i1 = (half[..., None].astype(np.int64) >> (4 * c + 2)) & 3

@@ -24,6 +24,8 @@ constexpr int kHDense = kHT * kHT * 2;          // bytes of a dense tile
 constexpr int kHSparse = kHT * kHT + kHT * kHT / 8;
 constexpr uint64_t kHSparseBit = 1ull << 63;
 constexpr int kHThreads = 256;
+constexpr int kHRing = 4;
+constexpr int kHMaxChunks = 256;               // K <= 32768
 
 // ------------------------------------------------------------------------------------- pack
 __global__ void __launch_bounds__(kHThreads)
@@ -87,14 +89,32 @@ k_hybrid_pack(const float* __restrict__ W, int64_t N, int64_t K, const uint64_t*
     vals[2 * c + 1] = (_Float16)w[4 * c + i1];
     half |= (uint32_t)(i0 | (i1 << 2)) << (4 * c);
   }
-  *reinterpret_cast<u32x4_t*>(payload + off + (uint64_t)r * 128 + kk) = __builtin_bit_cast(u32x4_t, vals);
-  *reinterpret_cast<uint16_t*>(payload + off + kHT * kHT + (uint64_t)r * 16 + 2 * (kk / 16)) = (uint16_t)half;
+  // the tile's half (positions 0..63 or 64..127): 128 rows x 64 bytes of values, then 128 rows x
+  // 8 bytes of index words
+  const uint64_t hb = off + (uint64_t)(kHSparse / 2) * (uint64_t)(kk >> 6);
+  const int kh = kk & 63;
+  *reinterpret_cast<u32x4_t*>(payload + hb + (uint64_t)r * 64 + kh) = __builtin_bit_cast(u32x4_t, vals);
+  *reinterpret_cast<uint16_t*>(payload + hb + 8192 + (uint64_t)r * 8 + 2 * (kh / 16)) = (uint16_t)half;
 }
 
 // ------------------------------------------------------------------------------------- GEMM
-// LDS row of the X chunk: 128 fp16 = 16 slots of 16 bytes, slot s of row m at s ^ (m % 8), so that
-// the B-operand reads of 8 consecutive rows at one slot fall in distinct banks.
-__device__ __forceinline__ int xs_off(int row, int slot) { return row * 256 + ((slot ^ (row & 7)) << 4); }
+// Ring stages hold 64 positions of K (half a weight tile) for the block's 128 weight rows and 128
+// activation rows, 32 KiB per stage, four stages, three ahead: everything reaches LDS by direct
+// loads (buffer_load ... lds, 16 bytes per lane for the values and activations, 4 for the index
+// words), so no register holds data in flight. Every stage issues 8 loads per wave whatever the
+// tile kind, the same instructions with kind-dependent offsets (no branch), so that the wait before
+// a stage is a fixed count. LDS layouts (16-byte slots XOR-swizzled so that a wave's reads of one
+// slot over consecutive rows hit distinct banks):
+//   dense weights  row r (0..127): 128 bytes, slot s at s ^ (r % 8)
+//   2:4 weights    values: row r 64 bytes, slot s at s ^ ((r / 4) % 2); index words at 8192 + 8 r
+//                  (1 KiB, loaded by wave 0; the other waves' third load and every wave's fourth
+//                  go to spare space of the stage)
+//   activations    row m (0..127): 128 bytes, slot s at s ^ (m % 8)
+constexpr int kHStageK = 64;
+struct HybridStage {
+  uint8_t a[16384];
+  uint8_t x[16384];
+};
 
 struct HybridArgs {
   const uint16_t* X;
@@ -102,23 +122,26 @@ struct HybridArgs {
   const uint8_t* payload;
   float* out;          // Y [M, N] (one split) or partials [split][M][N]
   int64_t M, N, K;
+  int64_t payload_bytes;
   int chunks_per_split;
 };
 
-// Operands of one chunk for one wave: 16 x 16 bytes of values (dense: 8 steps x 2 row fragments;
-// sparse: 4 steps x 2 fragments) and, for a sparse chunk, each fragment's four index half-words of
-// this lane's group (8 bytes).
-struct ChunkRegs {
-  u32x4_t a[16];
-  u32x2_t m[2];
-  bool sparse;
-};
-
-// One block per CU: the next chunk's operands (weights in registers, X on its way to LDS) are held
-// while the current chunk's MFMAs run, next to the 64 accumulators.
+// One block per CU: 128 KiB of ring and 64 accumulator registers per lane.
 __global__ void __launch_bounds__(kHThreads, 1)
 k_hybrid_gemm(HybridArgs g) {
-  __shared__ __attribute__((aligned(16))) uint8_t xs[2][kHT * 256];
+  // one variable per stage, selected by compile-time indices, so that the compiler can tell the
+  // stage being read from the ones direct loads are still filling
+  __shared__ __attribute__((aligned(16))) HybridStage st0, st1, st2, st3;
+  // the block's tile-info words, read once before any direct load: afterwards an info word comes
+  // from LDS (a wait on LDS reads only) into scalar registers, where the loads' offsets must be
+  __shared__ uint64_t infos[kHMaxChunks];
+  auto ring = [&](auto zc) -> HybridStage& {
+    constexpr int z = decltype(zc)::value;
+    if constexpr (z == 0) return st0;
+    else if constexpr (z == 1) return st1;
+    else if constexpr (z == 2) return st2;
+    else return st3;
+  };
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn = wave >> 1, wm = wave & 1;
   const int l32 = lane & 31, h = lane >> 5;
@@ -126,47 +149,56 @@ k_hybrid_gemm(HybridArgs g) {
   const int64_t chunks = g.K / kHT;
   const int64_t c_begin = (int64_t)blockIdx.z * g.chunks_per_split;
   const int64_t c_end = c_begin + g.chunks_per_split < chunks ? c_begin + g.chunks_per_split : chunks;
+  const int64_t s_begin = 2 * c_begin, s_end = 2 * c_end;
+  for (int64_t c = c_begin + tid; c < c_end; c += kHThreads) infos[c - c_begin] = g.info[tn * chunks + c];
+  __syncthreads();
 
-  // X chunk staging: 8 pieces of 16 bytes per thread
-  auto load_x = [&](int64_t c, u32x4_t (&v)[8]) {
+  const rsrc_t rw = make_rsrc(g.payload, g.payload_bytes);
+  const int64_t xrows = g.M - m0 < kHT ? g.M - m0 : kHT;
+  const rsrc_t rx = make_rsrc(g.X + m0 * g.K, xrows * g.K * 2);     // rows past M read as zero
+  // per-lane source offsets of the wave's loads
+  uint32_t ad[4], xo[4], as[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int p = tid + kHThreads * i, row = p >> 4, slot = p & 15;
-      const int64_t m = m0 + row;
-      v[i] = m < g.M ? *reinterpret_cast<const u32x4_t*>(g.X + m * g.K + c * kHT + 8 * slot) : u32x4_t{0, 0, 0, 0};
-    }
+  for (int i = 0; i < 4; ++i) {
+    const int p = 4 * wave + i, row = 8 * p + (lane >> 3), phys = lane & 7;
+    ad[i] = (uint32_t)row * 256u + 16u * (uint32_t)(phys ^ (row & 7));
+    xo[i] = (uint32_t)row * (uint32_t)g.K * 2u + 16u * (uint32_t)(phys ^ (row & 7));
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int p = 2 * wave + i, row = 16 * p + (lane >> 2), phys = lane & 3;
+    as[i] = (uint32_t)row * 64u + 16u * (uint32_t)(phys ^ ((row >> 2) & 1));
+  }
+  // 2:4 stage, loads 2 and 3: the half's index words (1 KiB after its 8 KiB of values), 16 bytes
+  // per lane
+  as[2] = as[3] = 8192u + 16u * (uint32_t)lane;
+  // LDS destinations of the 2:4 stage's four loads
+  const uint32_t sdst[4] = {(uint32_t)(2 * wave) * 1024u, (uint32_t)(2 * wave + 1) * 1024u,
+                            wave == 0 ? 8192u : 8192u + 1024u * (uint32_t)wave, 12288u + 1024u * (uint32_t)wave};
+
+  auto kind_of = [&](int64_t s) -> uint64_t {
+    const uint64_t v = infos[(s >> 1) - c_begin];
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
   };
-  auto store_x = [&](int stg, const u32x4_t (&v)[8]) {
+  auto issue = [&](int64_t s, auto zc) {
+    const int64_t sc = s < s_end ? s : s_end - 1;       // past the end: reload into a dead slot
+    const uint64_t ti = kind_of(sc);
+    const bool sp = (ti & kHSparseBit) != 0;
+    const uint32_t toff = (uint32_t)(ti & ~kHSparseBit), half = (uint32_t)(sc & 1);
+    const uint32_t soff = sp ? toff + (uint32_t)(kHSparse / 2) * half : toff;
+    HybridStage& S = ring(zc);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int p = tid + kHThreads * i, row = p >> 4, slot = p & 15;
-      *reinterpret_cast<u32x4_t*>(&xs[stg][xs_off(row, slot)]) = v[i];
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t dst = sp ? sdst[i] : (uint32_t)(4 * wave + i) * 1024u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)&S.a[dst], 16, sp ? as[i] : ad[i] + 128u * half, soff,
+                                               0, 0);
     }
-  };
-  // this wave's weight operands of chunk c
-  auto load_w = [&](int64_t c, ChunkRegs& w) {
-    const uint64_t ti = g.info[tn * chunks + c];
-    const uint8_t* base = g.payload + (ti & ~kHSparseBit);
-    w.sparse = (ti & kHSparseBit) != 0;
-    if (!w.sparse) {
 #pragma unroll
-      for (int fn = 0; fn < 2; ++fn) {
-        const int r = 64 * wn + 32 * fn + l32;
-#pragma unroll
-        for (int s = 0; s < 8; ++s)
-          w.a[8 * fn + s] = *reinterpret_cast<const u32x4_t*>(base + r * 256 + 32 * s + 16 * h);
-      }
-    } else {
-#pragma unroll
-      for (int fn = 0; fn < 2; ++fn) {
-        const int r = 64 * wn + 32 * fn + l32;
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-          w.a[4 * fn + s] = *reinterpret_cast<const u32x4_t*>(base + r * 128 + 64 * h + 16 * s);
-        // half-words 4 h .. 4 h + 3 of the row: lane group h covers positions 64 h .. 64 h + 63
-        w.m[fn] = *reinterpret_cast<const u32x2_t*>(base + kHT * kHT + r * 16 + 8 * h);
-      }
-    }
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)&S.x[(4 * wave + i) * 1024], 16, xo[i],
+                                               (uint32_t)(sc * kHStageK * 2), 0, 0);
   };
 
   f16_t acc[2][2];
@@ -177,65 +209,129 @@ k_hybrid_gemm(HybridArgs g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[fn][fm][e] = 0.f;
 
-  auto compute = [&](int stg, const ChunkRegs& w) {
-    const uint8_t* x = xs[stg];
-    if (!w.sparse) {
+  // The compute phase reads LDS with ds_read instructions written out, and waits for them itself:
+  // the compiler cannot tell which ring slot a direct load writes, so for reads it can see it would
+  // wait for every direct load in flight, the next stages' included. Each wait names the registers
+  // it completes, so no instruction using them is scheduled before it.
+  auto rd16 = [](uint32_t addr) -> u32x4_t {
+    u32x4_t v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+  };
+  auto rd_u16 = [](uint32_t addr) -> uint32_t {
+    uint32_t v;
+    asm volatile("ds_read_u16 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+  };
+  struct DenseOps {
+    u32x4_t a[2], b[2];
+  };
+  struct SparseOps {
+    u32x4_t a[2], b[4];
+    uint32_t i[2];
+  };
+  auto wait_dense = [](DenseOps& o) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(o.a[0]), "+v"(o.a[1]), "+v"(o.b[0]), "+v"(o.b[1]));
+  };
+  auto wait_sparse = [](SparseOps& o) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(o.a[0]), "+v"(o.a[1]), "+v"(o.b[0]), "+v"(o.b[1]), "+v"(o.b[2]), "+v"(o.b[3]), "+v"(o.i[0]),
+                   "+v"(o.i[1]));
+  };
+  // per-lane LDS byte offsets inside a stage (rows of this lane's fragments)
+  uint32_t ra_d[2], ra_s[2], ri_s[2], rx_[2];
+  int rsw[2], xsw[2], rsw_s[2];
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        h8_t b[2];
+  for (int f = 0; f < 2; ++f) {
+    const int r = 64 * wn + 32 * f + l32, m = 64 * wm + 32 * f + l32;
+    ra_d[f] = (uint32_t)r * 128u;
+    ra_s[f] = (uint32_t)r * 64u;
+    ri_s[f] = 8192u + (uint32_t)r * 8u;
+    rx_[f] = 16384u + (uint32_t)m * 128u;
+    rsw[f] = r & 7;
+    rsw_s[f] = (r >> 2) & 1;
+    xsw[f] = m & 7;
+  }
+
+  auto compute = [&](auto zc, bool sparse) {
+    const uint32_t base = (uint32_t)(uintptr_t)(lds_ptr_t)&ring(zc).a[0];   // the stage (a, then x)
+    if (!sparse) {
+      auto read = [&](int t, DenseOps& o) {
 #pragma unroll
-        for (int fm = 0; fm < 2; ++fm)
-          b[fm] = __builtin_bit_cast(h8_t, *reinterpret_cast<const u32x4_t*>(&x[xs_off(64 * wm + 32 * fm + l32, 2 * s + h)]));
-#pragma unroll
-        for (int fn = 0; fn < 2; ++fn) {
-          const h8_t a = __builtin_bit_cast(h8_t, w.a[8 * fn + s]);
-#pragma unroll
-          for (int fm = 0; fm < 2; ++fm) acc[fn][fm] = mfma32(a, b[fm], acc[fn][fm]);
+        for (int f = 0; f < 2; ++f) {
+          o.a[f] = rd16(base + ra_d[f] + ((uint32_t)((2 * t + h) ^ rsw[f]) << 4));
+          o.b[f] = rd16(base + rx_[f] + ((uint32_t)((2 * t + h) ^ xsw[f]) << 4));
         }
+      };
+      DenseOps o[2];
+      read(0, o[0]);
+      wait_dense(o[0]);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        if (t < 3) read(t + 1, o[(t + 1) & 1]);
+        const DenseOps& c = o[t & 1];
+#pragma unroll
+        for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+          for (int fm = 0; fm < 2; ++fm)
+            acc[fn][fm] = mfma32(__builtin_bit_cast(h8_t, c.a[fn]), __builtin_bit_cast(h8_t, c.b[fm]), acc[fn][fm]);
+        if (t < 3) wait_dense(o[(t + 1) & 1]);
       }
     } else {
+      auto read = [&](int t, SparseOps& o) {
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        h16_t b[2];
-#pragma unroll
-        for (int fm = 0; fm < 2; ++fm) {
-          const int row = 64 * wm + 32 * fm + l32;
-          const h8_t lo = __builtin_bit_cast(h8_t, *reinterpret_cast<const u32x4_t*>(&x[xs_off(row, 2 * s + h)]));
-          const h8_t hi = __builtin_bit_cast(h8_t, *reinterpret_cast<const u32x4_t*>(&x[xs_off(row, 8 + 2 * s + h)]));
-          b[fm] = cat16(lo, hi);
+        for (int f = 0; f < 2; ++f) {
+          // lane group h holds the 16 positions 32 t + 16 h .. + 15 of its row
+          o.a[f] = rd16(base + ra_s[f] + ((uint32_t)((2 * t + h) ^ rsw_s[f]) << 4));
+          o.i[f] = rd_u16(base + ri_s[f] + 2u * (uint32_t)(2 * t + h));
+          o.b[2 * f] = rd16(base + rx_[f] + ((uint32_t)((4 * t + h) ^ xsw[f]) << 4));
+          o.b[2 * f + 1] = rd16(base + rx_[f] + ((uint32_t)((4 * t + 2 + h) ^ xsw[f]) << 4));
         }
+      };
+      SparseOps o[2];
+      read(0, o[0]);
+      wait_sparse(o[0]);
 #pragma unroll
-        for (int fn = 0; fn < 2; ++fn) {
-          const h8_t a = __builtin_bit_cast(h8_t, w.a[4 * fn + s]);
-          const uint32_t word = w.m[fn][s >> 1];
-          const int idx = (int)((s & 1) ? (word >> 16) : (word & 0xFFFFu));
+      for (int t = 0; t < 2; ++t) {
+        if (t < 1) read(t + 1, o[1]);
+        const SparseOps& c = o[t & 1];
 #pragma unroll
-          for (int fm = 0; fm < 2; ++fm) acc[fn][fm] = smfmac32(a, b[fm], acc[fn][fm], idx, 0);
-        }
+        for (int fn = 0; fn < 2; ++fn)
+#pragma unroll
+          for (int fm = 0; fm < 2; ++fm)
+            acc[fn][fm] = smfmac32(__builtin_bit_cast(h8_t, c.a[fn]),
+                                   cat16(__builtin_bit_cast(h8_t, c.b[2 * fm]), __builtin_bit_cast(h8_t, c.b[2 * fm + 1])),
+                                   acc[fn][fm], (int)c.i[fn], 0);
+        if (t < 1) wait_sparse(o[1]);
       }
     }
   };
 
-  if (c_begin < c_end) {
-    u32x4_t xv[8];
-    ChunkRegs wc, wnx;
-    load_x(c_begin, xv);
-    load_w(c_begin, wc);
-    store_x(0, xv);
-    __syncthreads();
-    int stg = 0;
-    for (int64_t c = c_begin; c < c_end; ++c) {
-      const bool more = c + 1 < c_end;
-      if (more) {
-        load_x(c + 1, xv);
-        load_w(c + 1, wnx);
-      }
-      compute(stg, wc);
-      if (more) store_x(stg ^ 1, xv);
-      __syncthreads();
-      stg ^= 1;
-      if (more) wc = wnx;
+  // stage s in slot z: the wave's loads of stage s have landed once only those of s + 1 and s + 2
+  // are outstanding (16); the barrier then makes every wave's loads visible and ends every read of
+  // the slot that stage s + 3 refills
+  auto step = [&](int64_t s, auto zc) {
+    constexpr int z = decltype(zc)::value;
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(16));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue(s + 3, std::integral_constant<int, (z + 3) % kHRing>{});
+    compute(zc, (kind_of(s) & kHSparseBit) != 0);
+  };
+
+  if (s_begin < s_end) {
+    issue(s_begin, std::integral_constant<int, 0>{});
+    issue(s_begin + 1, std::integral_constant<int, 1>{});
+    issue(s_begin + 2, std::integral_constant<int, 2>{});
+    for (int64_t s = s_begin; s < s_end; s += kHRing) {
+      step(s, std::integral_constant<int, 0>{});
+      if (s + 1 < s_end) step(s + 1, std::integral_constant<int, 1>{});
+      if (s + 2 < s_end) step(s + 2, std::integral_constant<int, 2>{});
+      if (s + 3 < s_end) step(s + 3, std::integral_constant<int, 3>{});
     }
+    // no direct load may still be writing LDS when the workgroup ends
+    __builtin_amdgcn_s_waitcnt(0);
   }
 
   // D[i][j] of a 32x32 fragment: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
@@ -352,9 +448,13 @@ extern "C" int slim_linear_hybrid_workspace(int64_t M, int64_t N, int64_t K, siz
 }
 
 extern "C" int slim_linear_hybrid(const void* X, int64_t M, int64_t N, int64_t K, const uint64_t* tile_info,
-                                  const uint8_t* payload, float* Y, void* ws, size_t ws_bytes, void* stream) {
+                                  const uint8_t* payload, size_t payload_bytes, float* Y, void* ws, size_t ws_bytes,
+                                  void* stream) {
   if (!X || !tile_info || !payload || !Y) return SLIM_EINVAL;
   if (M < 1 || N < kHT || K < kHT || N % kHT || K % kHT) return SLIM_ESHAPE;
+  // 32-bit buffer offsets: the payload and 128 activation rows stay below 4 GiB
+  if (payload_bytes >= ((size_t)1 << 32) || (size_t)kHT * K * 2 >= ((size_t)1 << 32) || K / kHT > kHMaxChunks)
+    return SLIM_EUNSUPPORTED;
   if (M * K >= ((int64_t)1 << 40) || M * N >= ((int64_t)1 << 40) || (M + kHT) / kHT >= 65536) return SLIM_EUNSUPPORTED;
   if (!slim_aligned16(X) || !slim_aligned16(payload) || !slim_aligned16(Y) || ((uintptr_t)tile_info & 7u))
     return SLIM_EALIGN;
@@ -363,7 +463,7 @@ extern "C" int slim_linear_hybrid(const void* X, int64_t M, int64_t N, int64_t K
   if (p.splits > 1 && !slim_aligned16(ws)) return SLIM_EALIGN;
   hipStream_t s = (hipStream_t)stream;
   HybridArgs a{static_cast<const uint16_t*>(X), tile_info, payload, p.splits > 1 ? static_cast<float*>(ws) : Y,
-               M, N, K, (int)p.chunks_per_split};
+               M, N, K, (int64_t)payload_bytes, (int)p.chunks_per_split};
   {
     SlimKernelTimer timer("hybrid_gemm", s);
     SLIM_LAUNCH(timer, k_hybrid_gemm, dim3((unsigned)(N / kHT), (unsigned)((M + kHT - 1) / kHT), (unsigned)p.splits),

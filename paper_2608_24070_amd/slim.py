@@ -55,7 +55,8 @@ _SIGS = {
     "slim_hybrid_layout": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, ctypes.POINTER(ctypes.c_size_t)]),
     "slim_pack_hybrid": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
     "slim_linear_hybrid_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
-    "slim_linear_hybrid": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, ctypes.c_size_t, _c_p]),
+    "slim_linear_hybrid": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_i64, _c_p, _c_p, ctypes.c_size_t, _c_p, _c_p,
+                                          ctypes.c_size_t, _c_p]),
     "slim_lora_workspace": (ctypes.c_int, [_c_i64, _c_i64, _c_i64, _c_i64, ctypes.POINTER(ctypes.c_size_t)]),
     "slim_lora": (ctypes.c_int, [_c_p, _c_i64, _c_i64, _c_p, _c_p, _c_p, _c_p, ctypes.c_int, _c_i64, _c_i64, _c_p,
                                  _c_p, _c_p, ctypes.POINTER(ctypes.c_int), _c_p, ctypes.c_size_t, _c_p]),
@@ -143,8 +144,8 @@ def slim_linear_hybrid_workspace(M, N, K) -> int:
     return out.value
 
 
-def slim_linear_hybrid(X, M, N, K, tile_info, payload, Y, ws, ws_bytes, stream) -> int:
-    return lib().slim_linear_hybrid(X, M, N, K, tile_info, payload, Y, ws, ws_bytes, stream)
+def slim_linear_hybrid(X, M, N, K, tile_info, payload, payload_bytes, Y, ws, ws_bytes, stream) -> int:
+    return lib().slim_linear_hybrid(X, M, N, K, tile_info, payload, payload_bytes, Y, ws, ws_bytes, stream)
 
 
 def slim_lora_workspace(N, K, B, r) -> int:
@@ -418,8 +419,8 @@ def linear_hybrid(X, p: dict, out=None, stream=None):
         if ws is None or ws.numel() < nb:
             ws = torch.empty(nb, dtype=torch.uint8, device=X.device)
             _hybrid_ws[key] = ws
-    _check(slim_linear_hybrid(_ptr(X), M, N, K, _ptr(p["tile_info"]), _ptr(p["payload"]), _ptr(Y), _ptr(ws), nb,
-                              _stream(stream)), "slim_linear_hybrid")
+    _check(slim_linear_hybrid(_ptr(X), M, N, K, _ptr(p["tile_info"]), _ptr(p["payload"]), p["payload"].numel(),
+                              _ptr(Y), _ptr(ws), nb, _stream(stream)), "slim_linear_hybrid")
     return Y
 
 

@@ -80,7 +80,8 @@ def test_byte_layout_hand_built_tile():
     vals = pay[:8].view(np.float16)
     # group 0 keeps positions 0, 2 (4, 3); group 1 keeps 5, 6 (-2, 2), lower position first
     assert list(vals) == [4.0, 3.0, -2.0, 2.0]
-    half0 = int(pay[P.TILE * P.TILE:P.TILE * P.TILE + 2].view("<u2")[0])
+    # the first half's index words follow its 128 rows x 32 values
+    half0 = int(pay[P.TILE * P.TILE // 2:P.TILE * P.TILE // 2 + 2].view("<u2")[0])
     assert half0 & 0xF == (0 | 2 << 2) and (half0 >> 4) & 0xF == (1 | 2 << 2)
     # the dense tile: row 0 of W's columns 128.. as fp16, 256 bytes per row
     d0 = pay[P.SPARSE_BYTES:P.SPARSE_BYTES + 256].view(np.float16)
