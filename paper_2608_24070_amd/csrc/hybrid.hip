@@ -24,7 +24,7 @@ constexpr int kHDense = kHT * kHT * 2;          // bytes of a dense tile
 constexpr int kHSparse = kHT * kHT + kHT * kHT / 8;
 constexpr uint64_t kHSparseBit = 1ull << 63;
 constexpr int kHThreads = 256;
-constexpr int kHRing = 4;
+constexpr int kHRing = 3;
 constexpr int kHMaxChunks = 256;               // K <= 32768
 
 // ------------------------------------------------------------------------------------- pack
@@ -98,21 +98,24 @@ k_hybrid_pack(const float* __restrict__ W, int64_t N, int64_t K, const uint64_t*
 }
 
 // ------------------------------------------------------------------------------------- GEMM
-// Ring stages hold 64 positions of K (half a weight tile) for the block's 128 weight rows and 128
-// activation rows, 32 KiB per stage, four stages, three ahead: everything reaches LDS by direct
-// loads (buffer_load ... lds, 16 bytes per lane for the values and activations, 4 for the index
-// words), so no register holds data in flight. Every stage issues 8 loads per wave whatever the
-// tile kind, the same instructions with kind-dependent offsets (no branch), so that the wait before
-// a stage is a fixed count. LDS layouts (16-byte slots XOR-swizzled so that a wave's reads of one
-// slot over consecutive rows hit distinct banks):
+// A block computes 256 rows (two weight-tile rows) x 128 columns with 8 waves of 64 x 64; each
+// 128-row half has its own tile kind per chunk. Ring stages hold 64 positions of K (half a weight
+// tile) of both tile rows and of the 128 activation rows, 48 KiB per stage, three stages, two
+// ahead: everything reaches LDS by direct loads (buffer_load ... lds, 16 bytes per lane), so no
+// register holds data in flight. Waves 0-3 load tile row 0's weights and waves 4-7 tile row 1's:
+// 4 loads per wave for a dense half-tile, 2 for a 2:4 one (+1 in the group's first wave, the
+// index words); every wave loads 2 of the activations. The wait before stage s lets the loads of
+// stage s + 1 be in flight, a count known from its kinds (a switch over the three possible
+// immediates). LDS layouts (16-byte slots XOR-swizzled so that a wave's reads of one slot over
+// consecutive rows hit distinct banks), per tile row at 16384 tr:
 //   dense weights  row r (0..127): 128 bytes, slot s at s ^ (r % 8)
 //   2:4 weights    values: row r 64 bytes, slot s at s ^ ((r / 4) % 2); index words at 8192 + 8 r
-//                  (1 KiB, loaded by wave 0; the other waves' third load and every wave's fourth
-//                  go to spare space of the stage)
-//   activations    row m (0..127): 128 bytes, slot s at s ^ (m % 8)
+//   activations    (at 32768) row m (0..127): 128 bytes, slot s at s ^ (m % 8)
 constexpr int kHStageK = 64;
+constexpr int kHRows = 256;                   // output rows per block
+constexpr int kHGemmThreads = 512;
 struct HybridStage {
-  uint8_t a[16384];
+  uint8_t a[32768];
   uint8_t x[16384];
 };
 
@@ -126,78 +129,92 @@ struct HybridArgs {
   int chunks_per_split;
 };
 
-// One block per CU: 128 KiB of ring and 64 accumulator registers per lane.
-__global__ void __launch_bounds__(kHThreads, 1)
+// One block per CU: 144 KiB of ring.
+__global__ void __launch_bounds__(kHGemmThreads, 1)
 k_hybrid_gemm(HybridArgs g) {
-  // one variable per stage, selected by compile-time indices, so that the compiler can tell the
-  // stage being read from the ones direct loads are still filling
-  __shared__ __attribute__((aligned(16))) HybridStage st0, st1, st2, st3;
-  // the block's tile-info words, read once before any direct load: afterwards an info word comes
-  // from LDS (a wait on LDS reads only) into scalar registers, where the loads' offsets must be
-  __shared__ uint64_t infos[kHMaxChunks];
+  // one variable per stage, selected by compile-time indices
+  __shared__ __attribute__((aligned(16))) HybridStage st0, st1, st2;
+  // the block's tile-info words (two tile rows), read once before any direct load: afterwards an
+  // info word comes from LDS into scalar registers, where the loads' offsets must be
+  __shared__ uint64_t infos[2][kHMaxChunks];
   auto ring = [&](auto zc) -> HybridStage& {
     constexpr int z = decltype(zc)::value;
     if constexpr (z == 0) return st0;
     else if constexpr (z == 1) return st1;
-    else if constexpr (z == 2) return st2;
-    else return st3;
+    else return st2;
   };
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn = wave >> 1, wm = wave & 1;
+  // the wave index in a scalar register: load counts and waits are wave-uniform branches
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave >> 1, wm = wave & 1;       // rows 64 wn .. + 63 of the block, columns 64 wm ..
+  const int tr = wn >> 1;                        // the wave's tile row (for compute)
+  const int lt = wave >> 2, lw = wave & 3;       // the tile row this wave loads, and its rank there
   const int l32 = lane & 31, h = lane >> 5;
-  const int64_t tn = blockIdx.x, n0 = tn * kHT, m0 = (int64_t)blockIdx.y * kHT;
+  const int64_t n0 = (int64_t)blockIdx.x * kHRows, m0 = (int64_t)blockIdx.y * kHT;
   const int64_t chunks = g.K / kHT;
   const int64_t c_begin = (int64_t)blockIdx.z * g.chunks_per_split;
   const int64_t c_end = c_begin + g.chunks_per_split < chunks ? c_begin + g.chunks_per_split : chunks;
   const int64_t s_begin = 2 * c_begin, s_end = 2 * c_end;
-  for (int64_t c = c_begin + tid; c < c_end; c += kHThreads) infos[c - c_begin] = g.info[tn * chunks + c];
+  const int64_t tn0 = n0 / kHT;
+  // a last block of a 128-row remainder (N % 256 == 128) loads and computes tile row 0 twice; the
+  // second copy's rows lie past N and are never stored
+  const int64_t tn1 = tn0 + 1 < g.N / kHT ? tn0 + 1 : tn0;
+  for (int64_t c = c_begin + tid; c < c_end; c += kHGemmThreads) {
+    infos[0][c - c_begin] = g.info[tn0 * chunks + c];
+    infos[1][c - c_begin] = g.info[tn1 * chunks + c];
+  }
   __syncthreads();
 
   const rsrc_t rw = make_rsrc(g.payload, g.payload_bytes);
   const int64_t xrows = g.M - m0 < kHT ? g.M - m0 : kHT;
   const rsrc_t rx = make_rsrc(g.X + m0 * g.K, xrows * g.K * 2);     // rows past M read as zero
   // per-lane source offsets of the wave's loads
-  uint32_t ad[4], xo[4], as[4];
+  uint32_t ad[4], as[2], xo[2];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int p = 4 * wave + i, row = 8 * p + (lane >> 3), phys = lane & 7;
+    const int p = 4 * lw + i, row = 8 * p + (lane >> 3), phys = lane & 7;
     ad[i] = (uint32_t)row * 256u + 16u * (uint32_t)(phys ^ (row & 7));
-    xo[i] = (uint32_t)row * (uint32_t)g.K * 2u + 16u * (uint32_t)(phys ^ (row & 7));
   }
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int p = 2 * wave + i, row = 16 * p + (lane >> 2), phys = lane & 3;
+    const int p = 2 * lw + i, row = 16 * p + (lane >> 2), phys = lane & 3;
     as[i] = (uint32_t)row * 64u + 16u * (uint32_t)(phys ^ ((row >> 2) & 1));
+    const int px = 2 * wave + i, rx_row = 8 * px + (lane >> 3), pxs = lane & 7;
+    xo[i] = (uint32_t)rx_row * (uint32_t)g.K * 2u + 16u * (uint32_t)(pxs ^ (rx_row & 7));
   }
-  // 2:4 stage, loads 2 and 3: the half's index words (1 KiB after its 8 KiB of values), 16 bytes
-  // per lane
-  as[2] = as[3] = 8192u + 16u * (uint32_t)lane;
-  // LDS destinations of the 2:4 stage's four loads
-  const uint32_t sdst[4] = {(uint32_t)(2 * wave) * 1024u, (uint32_t)(2 * wave + 1) * 1024u,
-                            wave == 0 ? 8192u : 8192u + 1024u * (uint32_t)wave, 12288u + 1024u * (uint32_t)wave};
+  const uint32_t ami = 8192u + 16u * (uint32_t)lane;     // the half's index words, 16 bytes per lane
 
-  auto kind_of = [&](int64_t s) -> uint64_t {
-    const uint64_t v = infos[(s >> 1) - c_begin];
+  auto kind_of = [&](int t, int64_t s) -> uint64_t {
+    const uint64_t v = infos[t][(s >> 1) - c_begin];
     const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
     const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
     return ((uint64_t)hi << 32) | lo;
   };
+  auto clamp_s = [&](int64_t s) -> int64_t { return s < s_end ? s : s_end - 1; };   // past the end: a dead slot
+  // loads this wave issues for stage s
+  auto loads_of = [&](int64_t s) -> int {
+    return 2 + ((kind_of(lt, clamp_s(s)) & kHSparseBit) ? (lw == 0 ? 3 : 2) : 4);
+  };
   auto issue = [&](int64_t s, auto zc) {
-    const int64_t sc = s < s_end ? s : s_end - 1;       // past the end: reload into a dead slot
-    const uint64_t ti = kind_of(sc);
-    const bool sp = (ti & kHSparseBit) != 0;
+    const int64_t sc = clamp_s(s);
+    const uint64_t ti = kind_of(lt, sc);
     const uint32_t toff = (uint32_t)(ti & ~kHSparseBit), half = (uint32_t)(sc & 1);
-    const uint32_t soff = sp ? toff + (uint32_t)(kHSparse / 2) * half : toff;
     HybridStage& S = ring(zc);
+    uint8_t* A = &S.a[16384 * lt];
+    if (!(ti & kHSparseBit)) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t dst = sp ? sdst[i] : (uint32_t)(4 * wave + i) * 1024u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)&S.a[dst], 16, sp ? as[i] : ad[i] + 128u * half, soff,
-                                               0, 0);
+      for (int i = 0; i < 4; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)&A[(4 * lw + i) * 1024], 16, ad[i] + 128u * half, toff,
+                                                 0, 0);
+    } else {
+      const uint32_t soff = toff + (uint32_t)(kHSparse / 2) * half;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)&A[(2 * lw + i) * 1024], 16, as[i], soff, 0, 0);
+      if (lw == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)&A[8192], 16, ami, soff, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)&S.x[(4 * wave + i) * 1024], 16, xo[i],
+    for (int i = 0; i < 2; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)&S.x[(2 * wave + i) * 1024], 16, xo[i],
                                                (uint32_t)(sc * kHStageK * 2), 0, 0);
   };
 
@@ -211,7 +228,7 @@ k_hybrid_gemm(HybridArgs g) {
 
   // The compute phase reads LDS with ds_read instructions written out, and waits for them itself:
   // the compiler cannot tell which ring slot a direct load writes, so for reads it can see it would
-  // wait for every direct load in flight, the next stages' included. Each wait names the registers
+  // wait for every direct load in flight, the next stage's included. Each wait names the registers
   // it completes, so no instruction using them is scheduled before it.
   auto rd16 = [](uint32_t addr) -> u32x4_t {
     u32x4_t v;
@@ -243,11 +260,11 @@ k_hybrid_gemm(HybridArgs g) {
   int rsw[2], xsw[2], rsw_s[2];
 #pragma unroll
   for (int f = 0; f < 2; ++f) {
-    const int r = 64 * wn + 32 * f + l32, m = 64 * wm + 32 * f + l32;
-    ra_d[f] = (uint32_t)r * 128u;
-    ra_s[f] = (uint32_t)r * 64u;
-    ri_s[f] = 8192u + (uint32_t)r * 8u;
-    rx_[f] = 16384u + (uint32_t)m * 128u;
+    const int r = 64 * (wn & 1) + 32 * f + l32, m = 64 * wm + 32 * f + l32;   // r: row within the tile row
+    ra_d[f] = 16384u * (uint32_t)tr + (uint32_t)r * 128u;
+    ra_s[f] = 16384u * (uint32_t)tr + (uint32_t)r * 64u;
+    ri_s[f] = 16384u * (uint32_t)tr + 8192u + (uint32_t)r * 8u;
+    rx_[f] = 32768u + (uint32_t)m * 128u;
     rsw[f] = r & 7;
     rsw_s[f] = (r >> 2) & 1;
     xsw[f] = m & 7;
@@ -307,28 +324,34 @@ k_hybrid_gemm(HybridArgs g) {
     }
   };
 
-  // stage s in slot z: the wave's loads of stage s have landed once only those of s + 1 and s + 2
-  // are outstanding (16); the barrier then makes every wave's loads visible and ends every read of
-  // the slot that stage s + 3 refills
+  // stage s in slot z: the wave's loads of stage s have landed once only those of s + 1 are
+  // outstanding; the barrier then makes every wave's loads visible and ends every read of the slot
+  // that stage s + 2 refills
+  auto wait_ahead = [&](int n) {
+    switch (n) {
+      case 4: __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(4)); break;
+      case 5: __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(5)); break;
+      default: __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(6)); break;
+    }
+  };
   auto step = [&](int64_t s, auto zc) {
     constexpr int z = decltype(zc)::value;
+    const int ahead = loads_of(s + 1);
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(16));
+    wait_ahead(ahead);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    issue(s + 3, std::integral_constant<int, (z + 3) % kHRing>{});
-    compute(zc, (kind_of(s) & kHSparseBit) != 0);
+    issue(s + 2, std::integral_constant<int, (z + 2) % kHRing>{});
+    compute(zc, (kind_of(tr, s) & kHSparseBit) != 0);
   };
 
   if (s_begin < s_end) {
     issue(s_begin, std::integral_constant<int, 0>{});
     issue(s_begin + 1, std::integral_constant<int, 1>{});
-    issue(s_begin + 2, std::integral_constant<int, 2>{});
     for (int64_t s = s_begin; s < s_end; s += kHRing) {
       step(s, std::integral_constant<int, 0>{});
       if (s + 1 < s_end) step(s + 1, std::integral_constant<int, 1>{});
       if (s + 2 < s_end) step(s + 2, std::integral_constant<int, 2>{});
-      if (s + 3 < s_end) step(s + 3, std::integral_constant<int, 3>{});
     }
     // no direct load may still be writing LDS when the workgroup ends
     __builtin_amdgcn_s_waitcnt(0);
@@ -345,6 +368,7 @@ k_hybrid_gemm(HybridArgs g) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int64_t nn = n0 + 64 * wn + 32 * fn + 8 * q + 4 * h;
+        if (nn >= g.N) continue;
         const f4_t o = {acc[fn][fm][4 * q], acc[fn][fm][4 * q + 1], acc[fn][fm][4 * q + 2], acc[fn][fm][4 * q + 3]};
         *reinterpret_cast<f4_t*>(out + m * g.N + nn) = o;
       }
@@ -369,7 +393,7 @@ struct HybridPlan {
 HybridPlan hybrid_plan(int64_t M, int64_t N, int64_t K) {
   HybridPlan p{};
   const int64_t chunks = K / kHT;
-  p.tiles = (N / kHT) * ((M + kHT - 1) / kHT);
+  p.tiles = ((N + kHRows - 1) / kHRows) * ((M + kHT - 1) / kHT);
   int64_t s = 1;
   if (p.tiles < 256) s = (512 + p.tiles - 1) / p.tiles;          // at least ~512 blocks
   if (s > chunks) s = chunks;
@@ -466,8 +490,9 @@ extern "C" int slim_linear_hybrid(const void* X, int64_t M, int64_t N, int64_t K
                M, N, K, (int64_t)payload_bytes, (int)p.chunks_per_split};
   {
     SlimKernelTimer timer("hybrid_gemm", s);
-    SLIM_LAUNCH(timer, k_hybrid_gemm, dim3((unsigned)(N / kHT), (unsigned)((M + kHT - 1) / kHT), (unsigned)p.splits),
-                dim3(kHThreads), s, a);
+    SLIM_LAUNCH(timer, k_hybrid_gemm, dim3((unsigned)((N + kHRows - 1) / kHRows), (unsigned)((M + kHT - 1) / kHT),
+                                           (unsigned)p.splits),
+                dim3(kHGemmThreads), s, a);
   }
   if (p.splits > 1) {
     const int64_t count4 = M * N / 4;

@@ -66,6 +66,18 @@ def test_linear_parity(m, frac):
     _check_product(Y, X, P.hybrid_weight(W, kinds))
 
 
+@pytest.mark.parametrize("n,k,m", [(384, 640, 40), (128, 256, 3), (640, 384, 200)])
+def test_linear_odd_tile_rows(n, k, m):
+    # N % 256 == 128: the last 256-row block holds one tile row (its second half lies past N)
+    print(f"hybrid linear odd tile rows n={n} k={k} m={m}", flush=True)
+    W = _w(n, k, 5)
+    kinds = _kinds(n, k, 5, 0.5)
+    X = _x(m, k, 5)
+    p = slim.pack_hybrid(dev(W), kinds)
+    Y = host(slim.linear_hybrid(dev(X), p))
+    _check_product(Y, X, P.hybrid_weight(W, kinds))
+
+
 @pytest.mark.parametrize("m", [16, 2048])
 def test_llama7b_gate_proj_full_size(m):
     # 11008 x 4096 at 35% sparsity (70% of the tiles 2:4), sampled rows of Y
