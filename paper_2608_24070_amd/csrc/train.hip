@@ -137,20 +137,20 @@ k_pack16_t(const uint16_t* __restrict__ vals, const uint8_t* __restrict__ meta, 
 
 // ------------------------------------------------------------------------------- grad_w
 // D[k][n] = sum_m X[m][k] dY[m][n] (= grad W^T) on 32x32x16 MFMA, fp32 accumulate; tile 256 (k) x
-// 256 (n), wave (wk, wn) of four owns k rows 128 wk .. + 127 and n columns 128 wn .. + 127 (4 x 4
-// fragments in the accumulation registers). The tile's operand traffic per flop is a quarter of a
-// 128 x 128 tile's (every dY column slab is read by K/256 tiles, every X slab by N/256). Both
-// operands are [M, *] row-major, so the reduction runs along their rows: per 32-row chunk, each
-// thread loads eight rows of four columns of each (8 B per load; rows past M read as zero through
-// the buffer resource) and writes them to LDS transposed, eight reduction positions per 16-byte
-// write, into [column][32 + 8] fp16 rows with XOR-swizzled 16-byte slots. Loads run two chunks
-// ahead in two register sets; LDS has two stages.
+// 256 (n) for 8 waves, two per SIMD: wave (wk, wn) owns k rows 128 wk .. + 127 and n columns
+// 64 wn .. + 63 (4 x 2 fragments in the accumulation registers). The tile's operand traffic per
+// flop is a quarter of a 128 x 128 tile's (every dY column slab is read by K/256 tiles, every X
+// slab by N/256). Both operands are [M, *] row-major, so the reduction runs along their rows: per
+// 64-row chunk, each thread loads eight rows of four columns of each (8 B per load; rows past M read
+// as zero through the buffer resource) and writes them to LDS transposed, eight reduction positions
+// per 16-byte write, into [column][64 + 8] fp16 rows with XOR-swizzled 16-byte slots. Loads run one
+// chunk ahead in registers (the SIMD's other wave covers the rest of the latency); LDS has two stages.
 // Columns past N or K (a last partial tile) read neighbouring data; D entries of such a column are
 // never stored, and no other entry depends on it.
 // Epilogue: a fragment row block 8q + 4 (L / 32) .. + 3 of lane L is one aligned 4-group of k for
 // column n = L % 32, so the two positions M^R keeps (one metadata nibble) are selected in
 // registers and stored as the compressed pair gW[n][2g], gW[n][2g + 1].
-constexpr int kGT = 256, kGM = 32, kGLd = kGM + 8;
+constexpr int kGT = 256, kGM = 64, kGLd = kGM + 8, kGThreads = 512;
 
 template <bool BF16>
 SLIM_DEV f16_t mfma_acc(u32x4_t a, u32x4_t b, f16_t c) {
@@ -170,7 +170,7 @@ struct GradRegs {
 };
 
 template <bool BF16>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(kGThreads)
 k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_t M, int64_t N, int64_t K,
          const uint8_t* __restrict__ meta, float* __restrict__ gW) {
   __shared__ __attribute__((aligned(16))) uint16_t xs[2][kGT][kGLd];   // [stage][k][m]
@@ -206,11 +206,11 @@ k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_
                    rx, xo + (uint32_t)c * xstep + (uint32_t)j * (uint32_t)K * 2u, 0, 0));
     }
   };
-  // LDS rows hold the chunk's 32 reduction positions as four 16-byte slots; slot s of tile column
-  // row r sits at physical slot s ^ ((r / 8) % 4). A wave's 16-byte transposed writes (64 rows 4
-  // apart, one slot) and its 16-byte fragment reads (32 consecutive rows, one slot) then touch 8
-  // distinct groups of 4 banks per 8 lanes.
-  auto slot_of = [](int r, int s) { return s ^ ((r >> 3) & 3); };
+  // LDS rows (144 bytes) hold the chunk's 64 reduction positions as eight 16-byte slots and 16
+  // bytes of padding; slot s of tile column row r sits at physical slot s ^ ((r / 8) % 8). Eight
+  // lanes of a wave's 16-byte transposed writes (rows 4 apart, one slot) and eight of its 16-byte
+  // fragment reads (consecutive rows, one slot) then fall in distinct 16-byte bank groups.
+  auto slot_of = [](int r, int s) { return s ^ ((r >> 3) & 7); };
   // 8 x 4 transposes of 16-bit elements: column c of the thread's four gets the 8 rows (positions
   // 8 mg .. 8 mg + 7, slot mg) as one 16-byte LDS write
   auto store = [&](const GradRegs& R, int stg) {
@@ -230,63 +230,63 @@ k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_
     }
   };
 
-  f16_t acc[4][4];
+  f16_t acc[4][2];
 #pragma unroll
   for (int x = 0; x < 4; ++x)
 #pragma unroll
-    for (int y = 0; y < 4; ++y)
+    for (int y = 0; y < 2; ++y)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[x][y][v] = 0.f;
 
-  // all sixteen fragments of the chunk are read before its 32 MFMAs, so the LDS latency is paid
-  // once per chunk rather than once per fragment
+  // per step (16 positions) the wave reads 4 A and 2 B fragments, then issues their 8 MFMAs (the
+  // SIMD's other wave covers the LDS latency)
   auto compute = [&](int stg) {
-    u32x4_t af[kGM / 16][4], bf[kGM / 16][4];
 #pragma unroll
-    for (int st = 0; st < kGM / 16; ++st)
+    for (int st = 0; st < kGM / 16; ++st) {
+      u32x4_t af[4], bf[2];
 #pragma unroll
       for (int f = 0; f < 4; ++f) {
-        const int ra = 128 * wk + 32 * f + (lane & 31), rb = 128 * wn + 32 * f + (lane & 31);
-        af[st][f] = *reinterpret_cast<const u32x4_t*>(&xs[stg][ra][8 * slot_of(ra, 2 * st + h)]);
-        bf[st][f] = *reinterpret_cast<const u32x4_t*>(&ys[stg][rb][8 * slot_of(rb, 2 * st + h)]);
+        const int ra = 128 * wk + 32 * f + (lane & 31);
+        af[f] = *reinterpret_cast<const u32x4_t*>(&xs[stg][ra][8 * slot_of(ra, 2 * st + h)]);
       }
-    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int st = 0; st < kGM / 16; ++st)
+      for (int f = 0; f < 2; ++f) {
+        const int rb = 64 * wn + 32 * f + (lane & 31);
+        bf[f] = *reinterpret_cast<const u32x4_t*>(&ys[stg][rb][8 * slot_of(rb, 2 * st + h)]);
+      }
 #pragma unroll
       for (int x = 0; x < 4; ++x)
 #pragma unroll
-        for (int y = 0; y < 4; ++y) acc[x][y] = mfma_acc<BF16>(af[st][x], bf[st][y], acc[x][y]);
+        for (int y = 0; y < 2; ++y) acc[x][y] = mfma_acc<BF16>(af[x], bf[y], acc[x][y]);
+    }
   };
 
-  // chunk c: loads of chunk c + 2 into the register set chunk c occupied (stored to LDS before),
-  // this chunk's MFMAs from stage c % 2, then chunk c + 1's registers (loaded during chunk c - 1)
-  // into the other stage (last read during chunk c - 1, before the barrier that ended it). Loads
-  // past the last chunk address rows past M and read as zero.
+  // chunk c: loads of chunk c + 1 into registers, this chunk's MFMAs from stage c % 2, then the
+  // registers into the other stage (last read during chunk c - 1, before the barrier that ended
+  // it). Loads past the last chunk address rows past M and read as zero.
   const int64_t nch = (M + kGM - 1) / kGM;
-  GradRegs r0, r1;
+  GradRegs r0;
   load(0, r0);
-  load(1, r1);
   store(r0, 0);
   __syncthreads();
-  auto chunk = [&](int64_t c, GradRegs& cur, GradRegs& nxt, int stg) {
-    load(c + 2, cur);
+  auto chunk = [&](int64_t c, int stg) {
+    load(c + 1, r0);
     __builtin_amdgcn_sched_barrier(0);   // issued before this chunk's work, not sunk into it
     compute(stg);
-    store(nxt, stg ^ 1);
+    store(r0, stg ^ 1);
     __syncthreads();
   };
   int64_t c = 0;
   for (; c + 2 <= nch; c += 2) {
-    chunk(c, r0, r1, 0);
-    chunk(c + 1, r1, r0, 1);
+    chunk(c, 0);
+    chunk(c + 1, 1);
   }
-  if (c < nch) chunk(c, r0, r1, 0);
+  if (c < nch) chunk(c, 0);
 
   // D[i][j] of a 32x32 fragment: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
 #pragma unroll
-  for (int y = 0; y < 4; ++y) {
-    const int64_t n = n0 + 128 * wn + 32 * y + (lane & 31);
+  for (int y = 0; y < 2; ++y) {
+    const int64_t n = n0 + 64 * wn + 32 * y + (lane & 31);
     if (n >= N) continue;
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
@@ -392,10 +392,10 @@ extern "C" int slim_grad_w(const void* dY, const void* X, int dtype, int64_t M, 
   const dim3 grid((unsigned)(8 * ((T + 7) / 8)));
   SlimKernelTimer timer("grad_w", s);
   if (dtype == SLIM_BF16)
-    SLIM_LAUNCH(timer, k_grad_w<true>, grid, dim3(256), s, reinterpret_cast<const uint16_t*>(dY),
+    SLIM_LAUNCH(timer, k_grad_w<true>, grid, dim3(kGThreads), s, reinterpret_cast<const uint16_t*>(dY),
                 reinterpret_cast<const uint16_t*>(X), M, N, K, meta, gW);
   else
-    SLIM_LAUNCH(timer, k_grad_w<false>, grid, dim3(256), s, reinterpret_cast<const uint16_t*>(dY),
+    SLIM_LAUNCH(timer, k_grad_w<false>, grid, dim3(kGThreads), s, reinterpret_cast<const uint16_t*>(dY),
                 reinterpret_cast<const uint16_t*>(X), M, N, K, meta, gW);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }
