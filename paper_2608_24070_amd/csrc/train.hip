@@ -138,19 +138,25 @@ k_pack16_t(const uint16_t* __restrict__ vals, const uint8_t* __restrict__ meta, 
 // ------------------------------------------------------------------------------- grad_w
 // D[k][n] = sum_m X[m][k] dY[m][n] (= grad W^T) on 32x32x16 MFMA, fp32 accumulate; tile 256 (k) x
 // 256 (n) for 8 waves, two per SIMD: wave (wk, wn) owns k rows 128 wk .. + 127 and n columns
-// 64 wn .. + 63 (4 x 2 fragments in the accumulation registers). The tile's operand traffic per
-// flop is a quarter of a 128 x 128 tile's (every dY column slab is read by K/256 tiles, every X
-// slab by N/256). Both operands are [M, *] row-major, so the reduction runs along their rows: per
-// 64-row chunk, each thread loads eight rows of four columns of each (8 B per load; rows past M read
-// as zero through the buffer resource) and writes them to LDS transposed, eight reduction positions
-// per 16-byte write, into [column][64 + 8] fp16 rows with XOR-swizzled 16-byte slots. Loads run one
-// chunk ahead in registers (the SIMD's other wave covers the rest of the latency); LDS has two stages.
+// 64 wn .. + 63 (4 x 2 fragments). The tile's operand traffic per flop is a quarter of a 128 x 128
+// tile's (every dY column slab is read by K/256 tiles, every X slab by N/256).
+// Both operands are [M, *] row-major and the reduction runs along their rows, so the MFMA operands
+// (eight consecutive reduction positions of one column per lane) are columns of the stored tiles.
+// The tiles go to LDS as they are, by direct loads (buffer_load ... lds, 16 bytes per lane): per
+// 32-row chunk 16 KiB of X and 16 KiB of dY, a ring of four stages three ahead, no register holding
+// data in flight. The operands are read back transposed with ds_read_b64_tr_b16: in each group of 16
+// lanes, lane 16 G + 4 a + b receives element b of the 8-byte rows addressed by lanes
+// 16 G + a + 4 i (i = 0..3). Lane q of group G addresses row m0 + 8 (G / 2) + q / 4 (+ 4 for the
+// second read) at column c0 + 16 (G % 2) + 4 (q % 4), so lane l gets the eight reduction positions
+// 8 (l / 32) .. + 7 of column c0 + l % 32: the MFMA's operand layout.
+// LDS rows are 512 bytes; 32-byte pieces are XOR-swizzled by 2 (row % 4) so that the four rows one
+// group reads at once fall in distinct banks.
 // Columns past N or K (a last partial tile) read neighbouring data; D entries of such a column are
 // never stored, and no other entry depends on it.
 // Epilogue: a fragment row block 8q + 4 (L / 32) .. + 3 of lane L is one aligned 4-group of k for
 // column n = L % 32, so the two positions M^R keeps (one metadata nibble) are selected in
 // registers and stored as the compressed pair gW[n][2g], gW[n][2g + 1].
-constexpr int kGT = 256, kGM = 64, kGLd = kGM + 8, kGThreads = 512;
+constexpr int kGT = 256, kGM = 32, kGThreads = 512, kGRing = 4;
 
 template <bool BF16>
 SLIM_DEV f16_t mfma_acc(u32x4_t a, u32x4_t b, f16_t c) {
@@ -165,16 +171,19 @@ SLIM_DEV float sel4(const f16_t& acc, int base, int i) {
   return i == 0 ? a0 : (i == 1 ? a1 : (i == 2 ? a2 : a3));
 }
 
-struct GradRegs {
-  u32x2_t y[8], x[8];   // [row]: four columns of one row
-};
+// byte offset of 16-bit column c of row r in a swizzled 512-byte LDS row
+SLIM_DEV uint32_t gw_off(int r, int c) {
+  return (uint32_t)r * 512u + ((uint32_t)(((c >> 4) ^ (2 * (r & 3))) << 5)) + (uint32_t)((c & 15) * 2);
+}
 
 template <bool BF16>
 __global__ void __launch_bounds__(kGThreads)
 k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_t M, int64_t N, int64_t K,
          const uint8_t* __restrict__ meta, float* __restrict__ gW) {
-  __shared__ __attribute__((aligned(16))) uint16_t xs[2][kGT][kGLd];   // [stage][k][m]
-  __shared__ __attribute__((aligned(16))) uint16_t ys[2][kGT][kGLd];   // [stage][n][m]
+  // the ring: X chunks [m][k] in slots of 16 KiB at 0, dY chunks [m][n] at 64 KiB (512-byte rows);
+  // every offset a read adds to its lane's address then fits the 16-bit immediate of a DS read
+  constexpr uint32_t kSlot = kGM * kGT * 2, kYBase = kGRing * kSlot;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kGRing * kSlot];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wk = wave & 1, wn = wave >> 1, h = lane >> 5;
@@ -189,44 +198,27 @@ k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_
   const int64_t nbw = tn - band * 4 < 4 ? tn - band * 4 : 4;
   const int64_t n0 = (band * 4 + q0 % nbw) * kGT, k0 = (q0 / nbw) * kGT;
 
-  // loads: thread -> columns 4 cg .. 4 cg + 3 of the tile (cg = tid % 64) and rows 8 mg .. 8 mg + 7
-  // of the chunk (mg = tid / 64, the wave), so that one load instruction of a wave reads one row's
-  // 512 contiguous bytes; all of the offset is per lane, so the resource's extent check sees the row
-  const int cg = tid & 63, mg = tid >> 6;
+  // direct loads: each wave loads two 1 KiB pieces (rows 2 p, 2 p + 1, p = 2 wave + i) of X and of
+  // dY per chunk; lane L writes LDS bytes 16 L of the piece, i.e. row 2 p + L / 32 at physical
+  // 16-byte slot L % 32, which holds logical slot (L % 32) ^ (4 (row % 4)) (the 32-byte XOR above)
   const rsrc_t ry = make_rsrc(dY, M * N * 2), rx = make_rsrc(X, M * K * 2);
-  const uint32_t yo = ((uint32_t)(8 * mg) * (uint32_t)N + (uint32_t)(n0 + 4 * cg)) * 2u;
-  const uint32_t xo = ((uint32_t)(8 * mg) * (uint32_t)K + (uint32_t)(k0 + 4 * cg)) * 2u;
-  const uint32_t ystep = (uint32_t)kGM * (uint32_t)N * 2u, xstep = (uint32_t)kGM * (uint32_t)K * 2u;
-  auto load = [&](int64_t c, GradRegs& R) {
+  uint32_t xo[2], yo[2];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      R.y[j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
-                   ry, yo + (uint32_t)c * ystep + (uint32_t)j * (uint32_t)N * 2u, 0, 0));
-      R.x[j] = __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(
-                   rx, xo + (uint32_t)c * xstep + (uint32_t)j * (uint32_t)K * 2u, 0, 0));
-    }
-  };
-  // LDS rows (144 bytes) hold the chunk's 64 reduction positions as eight 16-byte slots and 16
-  // bytes of padding; slot s of tile column row r sits at physical slot s ^ ((r / 8) % 8). Eight
-  // lanes of a wave's 16-byte transposed writes (rows 4 apart, one slot) and eight of its 16-byte
-  // fragment reads (consecutive rows, one slot) then fall in distinct 16-byte bank groups.
-  auto slot_of = [](int r, int s) { return s ^ ((r >> 3) & 7); };
-  // 8 x 4 transposes of 16-bit elements: column c of the thread's four gets the 8 rows (positions
-  // 8 mg .. 8 mg + 7, slot mg) as one 16-byte LDS write
-  auto store = [&](const GradRegs& R, int stg) {
+  for (int i = 0; i < 2; ++i) {
+    const int p = 2 * wave + i, row = 2 * p + (lane >> 5), ls = (lane & 31) ^ (4 * (row & 3));
+    xo[i] = ((uint32_t)row * (uint32_t)K + (uint32_t)(k0 + 8 * ls)) * 2u;
+    yo[i] = ((uint32_t)row * (uint32_t)N + (uint32_t)(n0 + 8 * ls)) * 2u;
+  }
+  const uint32_t xstep = (uint32_t)kGM * (uint32_t)K * 2u, ystep = (uint32_t)kGM * (uint32_t)N * 2u;
+  const int64_t nch = (M + kGM - 1) / kGM;
+  auto issue = [&](int64_t c, auto zc) {
+    const uint32_t cc = (uint32_t)(c < nch ? c : nch - 1);      // past the end: reload into a dead slot
+    constexpr uint32_t z = decltype(zc)::value;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int w = c >> 1, sh = 16 * (c & 1);
-      auto pick = [&](const u32x2_t* r, int j) { return (r[j][w] >> sh) & 0xFFFFu; };
-      u32x4_t yv, xv;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        yv[i] = pick(R.y, 2 * i) | (pick(R.y, 2 * i + 1) << 16);
-        xv[i] = pick(R.x, 2 * i) | (pick(R.x, 2 * i + 1) << 16);
-      }
-      const int r = 4 * cg + c;
-      *reinterpret_cast<u32x4_t*>(&ys[stg][r][8 * slot_of(r, mg)]) = yv;
-      *reinterpret_cast<u32x4_t*>(&xs[stg][r][8 * slot_of(r, mg)]) = xv;
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t o = z * kSlot + (uint32_t)(2 * wave + i) * 1024u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (lds_ptr_t)&lds[o], 16, xo[i], cc * xstep, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ry, (lds_ptr_t)&lds[kYBase + o], 16, yo[i], cc * ystep, 0, 0);
     }
   };
 
@@ -238,50 +230,95 @@ k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[x][y][v] = 0.f;
 
-  // per step (16 positions) the wave reads 4 A and 2 B fragments, then issues their 8 MFMAs (the
-  // SIMD's other wave covers the LDS latency)
-  auto compute = [&](int stg) {
+  // transposed operand reads, written out (the compiler cannot tell ring slots apart for direct
+  // loads and would wait for every one in flight); each wait names the registers it completes
+  auto rd_tr = [](uint32_t addr, auto oc) -> u32x2_t {
+    u32x2_t v;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(decltype(oc)::value));
+    return v;
+  };
+  // per-lane part of the read addresses: row 8 (G / 2) + q / 4 and column 16 (G % 2) + 4 (q % 4)
+  const int G = lane >> 4, q = lane & 15;
+  const int rr = 8 * (G >> 1) + (q >> 2), cr = 16 * (G & 1) + 4 * (q & 3);
+  const uint32_t lb = (uint32_t)(uintptr_t)(lds_ptr_t)&lds[0];
+  uint32_t ax[4][2], by[2][2];           // [fragment][read]: addresses in slot 0, for step 0
 #pragma unroll
-    for (int st = 0; st < kGM / 16; ++st) {
-      u32x4_t af[4], bf[2];
+  for (int j = 0; j < 2; ++j) {
 #pragma unroll
-      for (int f = 0; f < 4; ++f) {
-        const int ra = 128 * wk + 32 * f + (lane & 31);
-        af[f] = *reinterpret_cast<const u32x4_t*>(&xs[stg][ra][8 * slot_of(ra, 2 * st + h)]);
+    for (int f = 0; f < 4; ++f) ax[f][j] = lb + gw_off(rr + 4 * j, 128 * wk + 32 * f + cr);
+#pragma unroll
+    for (int f = 0; f < 2; ++f) by[f][j] = lb + kYBase + gw_off(rr + 4 * j, 64 * wn + 32 * f + cr);
+  }
+  // operands of one 16-row step: X fragments [4][2 reads], dY fragments [2][2 reads]
+  struct Frags {
+    u32x2_t a[4][2], b[2][2];
+  };
+  auto read = [&](Frags& F, auto zc, auto stc) {    // step st (0, 1) of the chunk in slot z
+    using off = std::integral_constant<uint32_t, decltype(zc)::value * kSlot + decltype(stc)::value * 16u * 512u>;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+#pragma unroll
+      for (int f = 0; f < 4; ++f) F.a[f][j] = rd_tr(ax[f][j], off{});
+#pragma unroll
+      for (int f = 0; f < 2; ++f) F.b[f][j] = rd_tr(by[f][j], off{});
+    }
+  };
+  auto landed = [](Frags& F) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(F.a[0][0]), "+v"(F.a[0][1]), "+v"(F.a[1][0]), "+v"(F.a[1][1]), "+v"(F.a[2][0]),
+                   "+v"(F.a[2][1]), "+v"(F.a[3][0]), "+v"(F.a[3][1]), "+v"(F.b[0][0]), "+v"(F.b[0][1]),
+                   "+v"(F.b[1][0]), "+v"(F.b[1][1]));
+  };
+  auto mma = [&](const Frags& F) {
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const u32x4_t av = {F.a[x][0][0], F.a[x][0][1], F.a[x][1][0], F.a[x][1][1]};
+#pragma unroll
+      for (int y = 0; y < 2; ++y) {
+        const u32x4_t bv = {F.b[y][0][0], F.b[y][0][1], F.b[y][1][0], F.b[y][1][1]};
+        acc[x][y] = mfma_acc<BF16>(av, bv, acc[x][y]);
       }
-#pragma unroll
-      for (int f = 0; f < 2; ++f) {
-        const int rb = 64 * wn + 32 * f + (lane & 31);
-        bf[f] = *reinterpret_cast<const u32x4_t*>(&ys[stg][rb][8 * slot_of(rb, 2 * st + h)]);
-      }
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = mfma_acc<BF16>(af[x], bf[y], acc[x][y]);
     }
   };
 
-  // chunk c: loads of chunk c + 1 into registers, this chunk's MFMAs from stage c % 2, then the
-  // registers into the other stage (last read during chunk c - 1, before the barrier that ended
-  // it). Loads past the last chunk address rows past M and read as zero.
-  const int64_t nch = (M + kGM - 1) / kGM;
-  GradRegs r0;
-  load(0, r0);
-  store(r0, 0);
-  __syncthreads();
-  auto chunk = [&](int64_t c, int stg) {
-    load(c + 1, r0);
-    __builtin_amdgcn_sched_barrier(0);   // issued before this chunk's work, not sunk into it
-    compute(stg);
-    store(r0, stg ^ 1);
-    __syncthreads();
+  // Software pipeline over chunks: the operands of the next step are read while the MFMAs of the
+  // current one run, and the barrier sits between a chunk's two steps, so no wave starts a chunk
+  // waiting for LDS. Chunk c + 1 has landed for this wave once only the loads of c + 2 and c + 3
+  // are outstanding (8); the barrier then makes every wave's loads of c + 1 visible and ends every
+  // read of chunk c, whose slot chunk c + 4 refills. After the last chunk the same steps read a
+  // slot refilled with a copy of the last chunk (loads past the end repeat it) and use none of it.
+  Frags A, B;
+  auto step = [&](int64_t c, auto zc) {
+    constexpr int z = decltype(zc)::value;
+    read(B, zc, std::integral_constant<int, 1>{});
+    mma(A);
+    landed(B);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(8));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue(c + 4, zc);
+    read(A, std::integral_constant<int, (z + 1) % kGRing>{}, std::integral_constant<int, 0>{});
+    mma(B);
+    landed(A);
   };
-  int64_t c = 0;
-  for (; c + 2 <= nch; c += 2) {
-    chunk(c, 0);
-    chunk(c + 1, 1);
+  issue(0, std::integral_constant<int, 0>{});
+  issue(1, std::integral_constant<int, 1>{});
+  issue(2, std::integral_constant<int, 2>{});
+  __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(8));
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  issue(3, std::integral_constant<int, 3>{});
+  read(A, std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{});
+  landed(A);
+  for (int64_t c = 0; c < nch; c += kGRing) {
+    step(c, std::integral_constant<int, 0>{});
+    if (c + 1 < nch) step(c + 1, std::integral_constant<int, 1>{});
+    if (c + 2 < nch) step(c + 2, std::integral_constant<int, 2>{});
+    if (c + 3 < nch) step(c + 3, std::integral_constant<int, 3>{});
   }
-  if (c < nch) chunk(c, 0);
+  // no direct load may still be writing LDS when the workgroup ends
+  __builtin_amdgcn_s_waitcnt(0);
 
   // D[i][j] of a 32x32 fragment: lane j + 32 ((i / 4) % 2), element 4 (i / 8) + i % 4
 #pragma unroll
@@ -295,10 +332,10 @@ k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_
       const int64_t gb = kb / 4;
       const uint32_t md = *reinterpret_cast<const uint32_t*>(meta + n * (K / 8) + gb / 2);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int t = 2 * q + h;                                // group gb + t holds rows 8q + 4h ..
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int t = 2 * q4 + h;                               // group gb + t holds rows 8 q4 + 4h ..
         const uint32_t nib = (md >> (4 * t)) & 0xFu;
-        const float v0 = sel4(acc[x][y], 4 * q, (int)(nib & 3u)), v1 = sel4(acc[x][y], 4 * q, (int)(nib >> 2));
+        const float v0 = sel4(acc[x][y], 4 * q4, (int)(nib & 3u)), v1 = sel4(acc[x][y], 4 * q4, (int)(nib >> 2));
         *reinterpret_cast<u32x2_t*>(gW + n * (K / 2) + 2 * (gb + t)) =
             u32x2_t{__builtin_bit_cast(uint32_t, v0), __builtin_bit_cast(uint32_t, v1)};
       }
