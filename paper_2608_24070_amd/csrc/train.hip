@@ -269,37 +269,53 @@ k_grad_w(const uint16_t* __restrict__ dY, const uint16_t* __restrict__ X, int64_
                    "+v"(F.a[2][1]), "+v"(F.a[3][0]), "+v"(F.a[3][1]), "+v"(F.b[0][0]), "+v"(F.b[0][1]),
                    "+v"(F.b[1][0]), "+v"(F.b[1][1]));
   };
-  auto mma = [&](const Frags& F) {
+  // MFMAs I0 .. I1 - 1 of the step in F (i = 2 x + y); with RD the twelve reads of the step N
+  // (slot z, step st) are spread over them, two before each of the first six, so that no wave
+  // sends a burst of reads and the last ones have an MFMA or two to land
+  auto mma_rng = [&](const Frags& F, Frags& N, auto zc, auto stc, auto i0c, auto i1c, auto rdc) {
+    using off = std::integral_constant<uint32_t, decltype(zc)::value * kSlot + decltype(stc)::value * 16u * 512u>;
+    constexpr int I0 = decltype(i0c)::value, I1 = decltype(i1c)::value, n = I1 - I0;
+    constexpr int m = n > 7 ? 6 : (n > 1 ? n - 1 : 1);
 #pragma unroll
-    for (int x = 0; x < 4; ++x) {
-      const u32x4_t av = {F.a[x][0][0], F.a[x][0][1], F.a[x][1][0], F.a[x][1][1]};
+    for (int i = I0; i < I1; ++i) {
+      const int x = i >> 1, y = i & 1, k = i - I0;
+      if (decltype(rdc)::value && k < m) {
 #pragma unroll
-      for (int y = 0; y < 2; ++y) {
-        const u32x4_t bv = {F.b[y][0][0], F.b[y][0][1], F.b[y][1][0], F.b[y][1][1]};
-        acc[x][y] = mfma_acc<BF16>(av, bv, acc[x][y]);
+        for (int r = 12 * k / m; r < 12 * (k + 1) / m; ++r) {
+          if (r < 8) N.a[r >> 1][r & 1] = rd_tr(ax[r >> 1][r & 1], off{});
+          else N.b[(r - 8) >> 1][(r - 8) & 1] = rd_tr(by[(r - 8) >> 1][(r - 8) & 1], off{});
+        }
       }
+      __builtin_amdgcn_sched_barrier(0);
+      const u32x4_t av = {F.a[x][0][0], F.a[x][0][1], F.a[x][1][0], F.a[x][1][1]};
+      const u32x4_t bv = {F.b[y][0][0], F.b[y][0][1], F.b[y][1][0], F.b[y][1][1]};
+      acc[x][y] = mfma_acc<BF16>(av, bv, acc[x][y]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
+  using I_0 = std::integral_constant<int, 0>;
+  using I_1 = std::integral_constant<int, 1>;
+  using I_8 = std::integral_constant<int, 8>;
 
   // Software pipeline over chunks: the operands of the next step are read while the MFMAs of the
   // current one run, and the barrier sits between a chunk's two steps, so no wave starts a chunk
   // waiting for LDS. Chunk c + 1 has landed for this wave once only the loads of c + 2 and c + 3
   // are outstanding (8); the barrier then makes every wave's loads of c + 1 visible and ends every
-  // read of chunk c, whose slot chunk c + 4 refills. After the last chunk the same steps read a
-  // slot refilled with a copy of the last chunk (loads past the end repeat it) and use none of it.
+  // read of chunk c, whose slot chunk c + 4 refills (after one MFMA, so that the SIMD has work
+  // while the loads issue). After the last chunk the same steps read a slot refilled with a copy
+  // of the last chunk (loads past the end repeat it) and use none of it.
   Frags A, B;
   auto step = [&](int64_t c, auto zc) {
     constexpr int z = decltype(zc)::value;
-    read(B, zc, std::integral_constant<int, 1>{});
-    mma(A);
+    using zn = std::integral_constant<int, (z + 1) % kGRing>;
+    mma_rng(A, B, zc, I_1{}, I_0{}, I_8{}, std::true_type{});
     landed(B);
-    __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(8));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
+    mma_rng(B, A, zn{}, I_0{}, I_0{}, I_1{}, std::false_type{});
     issue(c + 4, zc);
-    read(A, std::integral_constant<int, (z + 1) % kGRing>{}, std::integral_constant<int, 0>{});
-    mma(B);
+    mma_rng(B, A, zn{}, I_0{}, I_1{}, I_8{}, std::true_type{});
     landed(A);
   };
   issue(0, std::integral_constant<int, 0>{});
