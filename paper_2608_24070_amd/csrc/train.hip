@@ -67,72 +67,101 @@ k_pack16(const float4* __restrict__ W, int64_t n16, u32x4_t* __restrict__ vals, 
 }
 
 // ----------------------------------------------------------------------------- pack16_t
-// Block = 64 rows (n) x 64 columns (k). Phase 1 expands the value pack of the tile into LDS (fp16
-// bits, 0 where M^R drops, and the M^R bit); phase 2 gives each thread one column k and one
-// 16-row block, keeps the top two of each aligned 4-row group by (|v| desc, M^R bit desc, n asc)
-// and writes 8 values (16 B) of valsT and one metaT half-word.
-constexpr int kTT = 64;
+// Block = 128 rows (n) x 128 columns (k). Phase 1 expands the value pack of the tile into LDS (fp16
+// bits, 0 where M^R drops, and the M^R bit), each thread 16 columns of four rows with 16-byte LDS
+// writes; phase 2 gives each thread a 16-row block nb and a column k, keeps the top two of each
+// aligned 4-row group by (|v| desc, M^R bit desc, n asc) and writes 8 values (16 B) of valsT and
+// one metaT half-word. A tile row is one whole 128-byte line of the value pack, and the eight
+// 16-row blocks of one column go to eight consecutive threads, so every load and store moves whole
+// lines. LDS columns are XOR-swizzled by the 16-row block (values by 8 nb, flags by 16 nb), so the
+// phase-2 reads of one wave fall in distinct banks. A last partial tile (64 rows or 64 columns) is
+// loaded from clamped addresses and stores only its own part.
+constexpr int kTTn = 128, kTTk = 128;
 
 __global__ void __launch_bounds__(256)
 k_pack16_t(const uint16_t* __restrict__ vals, const uint8_t* __restrict__ meta, int64_t N, int64_t K,
            u32x4_t* __restrict__ valsT, uint16_t* __restrict__ metaT) {
-  __shared__ uint16_t v_s[kTT][kTT + 2];
-  __shared__ uint8_t f_s[kTT][kTT + 4];
+  __shared__ __attribute__((aligned(16))) uint16_t v_s[kTTn][kTTk];
+  __shared__ __attribute__((aligned(16))) uint8_t f_s[kTTn][kTTk];
   const int tid = threadIdx.x;
-  const int64_t k0 = (int64_t)blockIdx.x * kTT, n0 = (int64_t)blockIdx.y * kTT;
-  {
-    // thread -> (row tid / 4, 16 columns 16 (tid % 4)): four groups
-    const int row = tid >> 2, w = tid & 3;
-    const int64_t n = n0 + row;
-    const int64_t kc = k0 + 16 * w;                        // first column of the 16
-    const uint16_t mw = *reinterpret_cast<const uint16_t*>(meta + n * (K / 8) + kc / 8);
-    const u32x4_t v8 = *reinterpret_cast<const u32x4_t*>(vals + n * (K / 2) + kc / 2);
+  const int64_t k0 = (int64_t)blockIdx.x * kTTk, n0 = (int64_t)blockIdx.y * kTTn;
+  const int rows = N - n0 < kTTn ? (int)(N - n0) : kTTn;   // 64 or 128
+  const int cols = K - k0 < kTTk ? (int)(K - k0) : kTTk;   // 64 or 128
+  // every load first, then the LDS writes; thread -> (row tid / 8 + 32 j, 16 columns 16 (tid % 8))
+  const int w = tid & 7;
+  const int64_t kc = k0 + (16 * w < cols ? 16 * w : 0);    // first column of the thread's 16
+  uint16_t mws[4];
+  u32x4_t v8s[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = (tid >> 3) + 32 * j;
+    const int64_t n = n0 + (row < rows ? row : rows - 1);
+    mws[j] = *reinterpret_cast<const uint16_t*>(meta + n * (K / 8) + kc / 8);
+    v8s[j] = *reinterpret_cast<const u32x4_t*>(vals + n * (K / 2) + kc / 2);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = (tid >> 3) + 32 * j;
+    const int nb = (row >> 4) & 7;
+    uint32_t vd[8], fd[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const int i0 = (mw >> (4 * c)) & 3, i1 = (mw >> (4 * c + 2)) & 3;
+      const uint32_t i0 = (mws[j] >> (4 * c)) & 3u, i1 = (mws[j] >> (4 * c + 2)) & 3u;
+      const uint32_t pr = v8s[j][c], lo = pr & 0xFFFFu, hi = pr >> 16;
+      uint32_t e[4];
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int col = 16 * w + 4 * c + p;
-        const uint32_t pr = v8[c];
-        v_s[row][col] = p == i0 ? (uint16_t)(pr & 0xFFFFu) : (p == i1 ? (uint16_t)(pr >> 16) : (uint16_t)0);
-        f_s[row][col] = (p == i0 || p == i1) ? 1 : 0;
-      }
+      for (int p = 0; p < 4; ++p) e[p] = (uint32_t)p == i0 ? lo : ((uint32_t)p == i1 ? hi : 0u);
+      vd[2 * c] = e[0] | (e[1] << 16);
+      vd[2 * c + 1] = e[2] | (e[3] << 16);
+      fd[c] = (1u << (8 * i0)) | (1u << (8 * i1));
+    }
+    if (row < rows && 16 * w < cols) {
+      *reinterpret_cast<u32x4_t*>(&v_s[row][(16 * w) ^ (8 * nb)]) = u32x4_t{vd[0], vd[1], vd[2], vd[3]};
+      *reinterpret_cast<u32x4_t*>(&v_s[row][(16 * w + 8) ^ (8 * nb)]) = u32x4_t{vd[4], vd[5], vd[6], vd[7]};
+      *reinterpret_cast<u32x4_t*>(&f_s[row][(16 * w) ^ (16 * nb)]) = u32x4_t{fd[0], fd[1], fd[2], fd[3]};
     }
   }
   __syncthreads();
-  // thread -> (column tid % 64, 16-row block tid / 64)
-  const int col = tid & 63, blk = tid >> 6;
-  uint32_t hv[4], mw = 0;
+  // thread -> (16-row block tid % 8, column tid / 8 + 32 j)
+  const int blk = tid & 7;
+  if (16 * blk >= rows) return;
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int r0 = 16 * blk + 4 * c;
-    uint32_t mag[4], f[4], bits[4];
+  for (int j = 0; j < 4; ++j) {
+    const int col = (tid >> 3) + 32 * j;
+    if (col >= cols) break;
+    uint32_t hv[4], mw = 0;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      bits[p] = v_s[r0 + p][col];
-      mag[p] = bits[p] & 0x7FFFu;          // fp16 magnitude order (finite values)
-      f[p] = f_s[r0 + p][col];
-    }
-    int i0 = -1, i1 = -1;
+    for (int c = 0; c < 4; ++c) {
+      const int r0 = 16 * blk + 4 * c;
+      // key: fp16 magnitude (finite values order as their bit patterns), then the M^R bit, then
+      // the lower row; distinct within a group, so q comes before p exactly when key[q] > key[p]
+      uint32_t key[4], bits[4];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      int rank = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const bool before = mag[q] > mag[p] || (mag[q] == mag[p] && (f[q] > f[p] || (f[q] == f[p] && q < p)));
-        if (q != p && before) ++rank;
+      for (int p = 0; p < 4; ++p) {
+        bits[p] = v_s[r0 + p][col ^ (8 * blk)];
+        key[p] = ((bits[p] & 0x7FFFu) << 3) | ((uint32_t)f_s[r0 + p][col ^ (16 * blk)] << 2) | (uint32_t)(3 - p);
       }
-      if (rank < 2) {
-        if (i0 < 0) i0 = p;
-        else i1 = p;
+      // keep[p]: fewer than two entries come before p; exactly two are kept, so the first kept is
+      // among 0..2 and the last among 1..3 (selects, no branches)
+      bool keep[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        uint32_t rank = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (q != p) rank += key[q] > key[p] ? 1u : 0u;
+        keep[p] = rank < 2;
       }
+      const uint32_t i0 = keep[0] ? 0u : (keep[1] ? 1u : 2u), i1 = keep[3] ? 3u : (keep[2] ? 2u : 1u);
+      const uint32_t b0 = keep[0] ? bits[0] : (keep[1] ? bits[1] : bits[2]);
+      const uint32_t b1 = keep[3] ? bits[3] : (keep[2] ? bits[2] : bits[1]);
+      hv[c] = b0 | (b1 << 16);
+      mw |= (i0 | (i1 << 2)) << (4 * c);
     }
-    hv[c] = bits[i0] | (bits[i1] << 16);
-    mw |= (uint32_t)(i0 | (i1 << 2)) << (4 * c);
+    const int64_t k = k0 + col, nb = n0 / 16 + blk;       // 16-row block along n
+    valsT[k * (N / 16) + nb] = u32x4_t{hv[0], hv[1], hv[2], hv[3]};
+    metaT[k * (N / 16) + nb] = (uint16_t)mw;
   }
-  const int64_t k = k0 + col, nb = n0 / 16 + blk;       // 16-row block along n
-  valsT[k * (N / 16) + nb] = u32x4_t{hv[0], hv[1], hv[2], hv[3]};
-  metaT[k * (N / 16) + nb] = (uint16_t)mw;
 }
 
 // ------------------------------------------------------------------------------- grad_w
@@ -425,7 +454,8 @@ extern "C" int slim_pack16_t(const uint16_t* vals, const uint8_t* meta, int64_t 
     return SLIM_EALIGN;
   hipStream_t s = (hipStream_t)stream;
   SlimKernelTimer timer("pack16_t", s);
-  SLIM_LAUNCH(timer, k_pack16_t, dim3((unsigned)(K / kTT), (unsigned)(N / kTT)), dim3(256), s, vals, meta, N, K,
+  SLIM_LAUNCH(timer, k_pack16_t, dim3((unsigned)((K + kTTk - 1) / kTTk), (unsigned)((N + kTTn - 1) / kTTn)), dim3(256),
+              s, vals, meta, N, K,
               reinterpret_cast<u32x4_t*>(valsT), reinterpret_cast<uint16_t*>(metaT));
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }

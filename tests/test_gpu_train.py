@@ -51,8 +51,10 @@ def test_pack16_rejects_non_finite():
     assert e.value.status == slim.SLIM_ENONFINITE
 
 
-@pytest.mark.parametrize("n,k,tied", [(64, 64, True), (256, 512, False), (1024, 192, True), (128, 1024, False)])
+@pytest.mark.parametrize("n,k,tied", [(64, 64, True), (256, 512, False), (1024, 192, True), (128, 1024, False),
+                                      (320, 128, True), (704, 64, False)])
 def test_pack16_t_bit_exact(n, k, tied):
+    # 256-row tiles: 64 and 128 rows are one partial tile, 320 and 704 end in one
     print(f"pack16_t n={n} k={k} tied={tied}", flush=True)
     W = _weights(n, k, 13, tied)
     p = slim.pack16(dev(W))
