@@ -167,8 +167,8 @@ k_pack16_t(const uint16_t* __restrict__ vals, const uint8_t* __restrict__ meta, 
 // ------------------------------------------------------------------------------- grad_w
 // D[k][n] = sum_m X[m][k] dY[m][n] (= grad W^T) on 32x32x16 MFMA, fp32 accumulate; tile 256 (k) x
 // 256 (n) for 8 waves, two per SIMD: wave (wk, wn) owns k rows 128 wk .. + 127 and n columns
-// 64 wn .. + 63 (4 x 2 fragments). The tile's operand traffic per flop is a quarter of a 128 x 128
-// tile's (every dY column slab is read by K/256 tiles, every X slab by N/256).
+// 64 wn .. + 63 (4 x 2 fragments). The tile's operand traffic per flop is half a 128 x 128 tile's
+// (every dY column slab is read by K/256 tiles, every X slab by N/256).
 // Both operands are [M, *] row-major and the reduction runs along their rows, so the MFMA operands
 // (eight consecutive reduction positions of one column per lane) are columns of the stored tiles.
 // The tiles go to LDS as they are, by direct loads (buffer_load ... lds, 16 bytes per lane): per
