@@ -16,6 +16,7 @@ right after replays of the timed steps; the roofline uses the average. Prints on
                   [--workload decode|prefill|block13b|mlp70b|mlp70b_bwd|tiny|train70b|slimquant|slimlora]
                   [--m M] [--no-cpu-baseline] [--no-prefill] [--no-train] [--qadapter] [--dispatches D]
   python bench.py --copy-probe MB     # plain device copy of MB megabytes (counter calibration)
+  python bench.py --vendor-probe      # torch.mm (the vendor dense GEMM) on the same shapes, as context
 
 The roofline's "traffic" field comes from the hardware-counter summary committed under profiles/
 for the same kernel and workload; it is null when no summary matches, or when the kernel sources
@@ -58,6 +59,8 @@ def parse():
     ap.add_argument("--dispatches", type=int, default=200,
                     help="steps of the per-kernel pass (average and median per kernel; at least --steps)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU budget of the oracle baseline (about 10-30 s)")
+    ap.add_argument("--vendor-probe", action="store_true",
+                    help="time torch.mm, the vendor's dense GEMM, on the large-M shapes of the workloads (context only)")
     ap.add_argument("--copy-probe", type=float, default=None, metavar="MB",
                     help="only run a plain device-to-device copy of MB megabytes (HBM counter calibration)")
     return ap.parse_args()
@@ -117,6 +120,39 @@ def copy_probe(mb):
     ms = e0.elapsed_time(e1) / 10
     print(json.dumps({"copy_probe_bytes_each_way": n * 4, "launches": 11, "avg_ms": round(ms, 4),
                       "read_plus_write_GBps": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}))
+
+
+def vendor_probe():
+    """torch.mm (rocBLAS / hipBLASLt) on dense operands of the large-M shapes measured here: the
+    weight gradient's [N x M] . [M x K] in bf16, and the prefill and 70B forward products in fp16
+    with the dense weight; a point of comparison for the library's kernels, not part of the path."""
+    import torch
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(0)
+
+    def timeit(fn, reps):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    out = {}
+    for name, (m, k, n, dt, reps) in {
+            "grad_w 70B: [28672 x 8192] . [8192 x 8192] bf16": (28672, 8192, 8192, torch.bfloat16, 10),
+            "prefill: [2048 x 4096] . [4096 x 11008] fp16": (2048, 4096, 11008, torch.float16, 50),
+            "70B MLP M 8192: [8192 x 8192] . [8192 x 28672] fp16": (8192, 8192, 28672, torch.float16, 10)}.items():
+        a = torch.randn(m, k, device="cuda:0", dtype=dt, generator=g)
+        b = torch.randn(k, n, device="cuda:0", dtype=dt, generator=g)
+        us = timeit(lambda: torch.mm(a, b), reps)
+        out[name] = {"us": round(us, 1), "TFLOP/s": round(2 * m * k * n / us / 1e6, 1)}
+        del a, b
+    print(json.dumps({"vendor_probe": out}))
 
 
 def layer_bytes(M, N, K, r, qadapter=False):
@@ -736,6 +772,9 @@ def main():
     args = parse()
     if args.copy_probe is not None:
         copy_probe(args.copy_probe)
+        return
+    if args.vendor_probe:
+        vendor_probe()
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
