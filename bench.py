@@ -60,7 +60,7 @@ def parse():
                     help="steps of the per-kernel pass (average and median per kernel; at least --steps)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU budget of the oracle baseline (about 10-30 s)")
     ap.add_argument("--vendor-probe", action="store_true",
-                    help="time torch.mm, the vendor's dense GEMM, on the large-M shapes of the workloads (context only)")
+                    help="time torch.mm, the vendor's dense GEMM, on the shapes of the workloads (context only)")
     ap.add_argument("--copy-probe", type=float, default=None, metavar="MB",
                     help="only run a plain device-to-device copy of MB megabytes (HBM counter calibration)")
     return ap.parse_args()
@@ -123,9 +123,10 @@ def copy_probe(mb):
 
 
 def vendor_probe():
-    """torch.mm (rocBLAS / hipBLASLt) on dense operands of the large-M shapes measured here: the
-    weight gradient's [N x M] . [M x K] in bf16, and the prefill and 70B forward products in fp16
-    with the dense weight; a point of comparison for the library's kernels, not part of the path."""
+    """torch.mm (rocBLAS / hipBLASLt) on dense operands of the shapes measured here: the weight
+    gradient's [N x M] . [M x K] in bf16, and the forward products in fp16 with the dense weight
+    (prefill, 70B at M 8192, decode at M 16); a point of comparison for the library's kernels, not
+    part of the path. Back-to-back calls on one weight, so small ones may be served from cache."""
     import torch
     g = torch.Generator(device="cuda:0")
     g.manual_seed(0)
@@ -146,11 +147,14 @@ def vendor_probe():
     for name, (m, k, n, dt, reps) in {
             "grad_w 70B: [28672 x 8192] . [8192 x 8192] bf16": (28672, 8192, 8192, torch.bfloat16, 10),
             "prefill: [2048 x 4096] . [4096 x 11008] fp16": (2048, 4096, 11008, torch.float16, 50),
-            "70B MLP M 8192: [8192 x 8192] . [8192 x 28672] fp16": (8192, 8192, 28672, torch.float16, 10)}.items():
+            "70B MLP M 8192: [8192 x 8192] . [8192 x 28672] fp16": (8192, 8192, 28672, torch.float16, 10),
+            "decode: [16 x 4096] . [4096 x 4096] fp16": (16, 4096, 4096, torch.float16, 200),
+            "70B MLP M 16: [16 x 8192] . [8192 x 28672] fp16": (16, 8192, 28672, torch.float16, 100)}.items():
         a = torch.randn(m, k, device="cuda:0", dtype=dt, generator=g)
         b = torch.randn(k, n, device="cuda:0", dtype=dt, generator=g)
         us = timeit(lambda: torch.mm(a, b), reps)
-        out[name] = {"us": round(us, 1), "TFLOP/s": round(2 * m * k * n / us / 1e6, 1)}
+        out[name] = {"us": round(us, 2), "TFLOP/s": round(2 * m * k * n / us / 1e6, 1),
+                     "GB/s (weight)": round(2 * k * n / us / 1e3, 1)}
         del a, b
     print(json.dumps({"vendor_probe": out}))
 
