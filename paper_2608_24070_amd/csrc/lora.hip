@@ -43,6 +43,58 @@ __device__ __forceinline__ int64_t pair_index(int p, int t, int nb, int i) {
   return (int64_t)blk * kLB + (i & (kLB - 1));
 }
 
+// 64 x 64 tiles between a dp-pitch matrix and LDS. Tile row r is matrix row row_of(r); the tile's
+// columns are two runs of 32 contiguous doubles (a pair's two blocks), at c0 (tile columns 0..31)
+// and c1 (32..63). Thread e of a 16-byte piece: run e / 16 (row run / 2, half run % 2), doubles
+// 2 (e % 16) and 2 (e % 16) + 1 of it; eight pieces per thread. All loads are issued before the
+// first LDS write: a loop that stored each element as its load arrived waited for every load in
+// turn.
+template <typename RowOf>
+__device__ __forceinline__ void tile_load(const double* __restrict__ M, int64_t dp, RowOf row_of, int64_t c0,
+                                          int64_t c1, double (*s)[kLPad]) {
+  double2 v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int e = threadIdx.x + kLT * i, run = e >> 4, q = e & 15;
+    v[i] = *reinterpret_cast<const double2*>(M + row_of(run >> 1) * dp + ((run & 1) ? c1 : c0) + 2 * q);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int e = threadIdx.x + kLT * i, run = e >> 4, q = e & 15, r = run >> 1, c = 32 * (run & 1) + 2 * q;
+    s[r][c] = v[i].x;
+    s[r][c + 1] = v[i].y;
+  }
+}
+// the same tile stored back; TRANS stores s transposed (matrix row row_of(r), column c <- s[c][r])
+template <bool TRANS, typename RowOf>
+__device__ __forceinline__ void tile_store(double* __restrict__ M, int64_t dp, RowOf row_of, int64_t c0, int64_t c1,
+                                           const double (*s)[kLPad]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int e = threadIdx.x + kLT * i, run = e >> 4, q = e & 15, r = run >> 1, c = 32 * (run & 1) + 2 * q;
+    double2 w;
+    w.x = TRANS ? s[c][r] : s[r][c];
+    w.y = TRANS ? s[c + 1][r] : s[r][c + 1];
+    *reinterpret_cast<double2*>(M + row_of(r) * dp + ((run & 1) ? c1 : c0) + 2 * q) = w;
+  }
+}
+// a contiguous row-major 64 x 64 matrix into LDS, loads first
+__device__ __forceinline__ void j_load(const double* __restrict__ J, double (*s)[kLPad]) {
+  double2 v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = reinterpret_cast<const double2*>(J)[threadIdx.x + kLT * i];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int e = threadIdx.x + kLT * i, r = e >> 5, c = 2 * (e & 31);
+    s[r][c] = v[i].x;
+    s[r][c + 1] = v[i].y;
+  }
+}
+// the two column runs of pair p in round t
+__device__ __forceinline__ int64_t pair_run(int p, int t, int nb, int h) {
+  return (int64_t)rr_slot(h ? nb - 1 - p : p, t, nb) * kLB;
+}
+
 // ---------------------------------------------------------------- calibration statistic
 // part[c][k] = sum over rows c*kLCalibRows .. +kLCalibRows-1 of |X[row][k]| (float64)
 __global__ void __launch_bounds__(kLT)
@@ -253,9 +305,9 @@ k_lora_pair_solve(const double* __restrict__ G, int64_t dp, int nb, int t, doubl
   __shared__ double cc[kLB], ss[kLB];
   __shared__ int rotated;
   const int pr = blockIdx.x;
+  tile_load(G, dp, [&](int r) { return pair_index(pr, t, nb, r); }, pair_run(pr, t, nb, 0), pair_run(pr, t, nb, 1), a);
   for (int e = threadIdx.x; e < kLP * kLP; e += kLT) {
     const int r = e >> 6, c = e & 63;
-    a[r][c] = G[pair_index(pr, t, nb, r) * dp + pair_index(pr, t, nb, c)];
     j[r][c] = r == c ? 1.0 : 0.0;
   }
   __syncthreads();
@@ -334,12 +386,11 @@ k_lora_apply_g(double* __restrict__ G, int64_t dp, int nb, int t, const double* 
   __shared__ double g[kLP][kLPad], ja[kLP][kLPad], jc[kLP][kLPad];
   const double* Ja = J + (int64_t)pa * kLP * kLP;
   const double* Jc = J + (int64_t)pc * kLP * kLP;
-  for (int e = threadIdx.x; e < kLP * kLP; e += kLT) {
-    const int r = e >> 6, c = e & 63;
-    g[r][c] = G[pair_index(pa, t, nb, r) * dp + pair_index(pc, t, nb, c)];
-    ja[r][c] = Ja[e];
-    jc[r][c] = Jc[e];
-  }
+  auto rows_a = [&](int r) { return pair_index(pa, t, nb, r); };
+  auto rows_c = [&](int r) { return pair_index(pc, t, nb, r); };
+  tile_load(G, dp, rows_a, pair_run(pc, t, nb, 0), pair_run(pc, t, nb, 1), g);
+  j_load(Ja, ja);
+  j_load(Jc, jc);
   __syncthreads();
   double acc[4][4];
   tile_mm<false>(g, jc, acc);           // T = G J_c
@@ -357,11 +408,8 @@ k_lora_apply_g(double* __restrict__ G, int64_t dp, int nb, int t, const double* 
 #pragma unroll
     for (int v = 0; v < 4; ++v) g[4 * tr + u][4 * tc + v] = acc[u][v];
   __syncthreads();
-  for (int e = threadIdx.x; e < kLP * kLP; e += kLT) {
-    const int r = e >> 6, c = e & 63;
-    G[pair_index(pa, t, nb, r) * dp + pair_index(pc, t, nb, c)] = g[r][c];
-    if (pa != pc) G[pair_index(pc, t, nb, r) * dp + pair_index(pa, t, nb, c)] = g[c][r];
-  }
+  tile_store<false>(G, dp, rows_a, pair_run(pc, t, nb, 0), pair_run(pc, t, nb, 1), g);
+  if (pa != pc) tile_store<true>(G, dp, rows_c, pair_run(pa, t, nb, 0), pair_run(pa, t, nb, 1), g);
 }
 
 // V[row block, pair a cols] <- V[..] J_a
@@ -371,11 +419,9 @@ k_lora_apply_v(double* __restrict__ V, int64_t dp, int nb, int t, const double* 
   const int64_t r0 = (int64_t)blockIdx.y * kLP;
   __shared__ double v[kLP][kLPad], ja[kLP][kLPad];
   const double* Ja = J + (int64_t)pa * kLP * kLP;
-  for (int e = threadIdx.x; e < kLP * kLP; e += kLT) {
-    const int r = e >> 6, c = e & 63;
-    v[r][c] = V[(r0 + r) * dp + pair_index(pa, t, nb, c)];
-    ja[r][c] = Ja[e];
-  }
+  auto rows = [&](int r) { return r0 + r; };
+  tile_load(V, dp, rows, pair_run(pa, t, nb, 0), pair_run(pa, t, nb, 1), v);
+  j_load(Ja, ja);
   __syncthreads();
   double acc[4][4];
   tile_mm<false>(v, ja, acc);
@@ -386,10 +432,7 @@ k_lora_apply_v(double* __restrict__ V, int64_t dp, int nb, int t, const double* 
 #pragma unroll
     for (int w = 0; w < 4; ++w) v[4 * tr + u][4 * tc + w] = acc[u][w];
   __syncthreads();
-  for (int e = threadIdx.x; e < kLP * kLP; e += kLT) {
-    const int r = e >> 6, c = e & 63;
-    V[(r0 + r) * dp + pair_index(pa, t, nb, c)] = v[r][c];
-  }
+  tile_store<false>(V, dp, rows, pair_run(pa, t, nb, 0), pair_run(pa, t, nb, 1), v);
 }
 
 // ---------------------------------------------------------------- selection and adapters
