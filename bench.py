@@ -612,13 +612,17 @@ def measure_slimlora(steps, warmup, cpu, n=4096, k=4096, r=384, b=2048):
     sweeps = out["sweeps"]
     dp = (min(n, k) + 63) // 64 * 64                       # the Gram side, padded to the 64-wide pairs
     npair = dp // 64
-    flops = 4.0 * 64 ** 3 * npair * (npair + 1) / 2       # J_a^T (G J_c) on the tiles a <= c
-    # the dominant kernel by total time is the tile update of G (asserted, so the line cannot
-    # silently price a kernel that is not the dominant one)
+    # FLOPs per launch of the two kernels that can dominate a fit: the tile update of G, J_a^T (G J_c)
+    # on the tiles a <= c, and the pair solves, 63 steps of 32 rotations per pair, each rotating two
+    # rows (6 FLOPs per element) and two columns of the pair's G block and of its J (12)
+    flops_of = {"lora_apply_g": 4.0 * 64 ** 3 * npair * (npair + 1) / 2,
+                "lora_pair_solve": float(npair * 63 * 32 * 64 * 18)}
+    # the roofline prices the dominant kernel by total time (raises if it is neither of those)
     dom = max(kt.items(), key=lambda kv: kv[1][1])[0]
-    if dom != "lora_apply_g":
-        raise RuntimeError(f"slim-lora: dominant kernel is {dom}, the roofline below prices lora_apply_g")
-    avg_s = kt["lora_apply_g"][1] / kt["lora_apply_g"][0] * 1e-3
+    if dom not in flops_of:
+        raise RuntimeError(f"slim-lora: dominant kernel is {dom}, which has no FLOP model here")
+    flops = flops_of[dom]
+    avg_s = kt[dom][1] / kt[dom][0] * 1e-3
     achieved = flops / avg_s / 1e12
     print(f"[bench] slim-lora {n}x{k} r={r}: {ms:.1f} ms/fit, {sweeps} sweeps", file=sys.stderr, flush=True)
     base = None
@@ -647,8 +651,8 @@ def measure_slimlora(steps, warmup, cpu, n=4096, k=4096, r=384, b=2048):
         "kernels": kernels,
         "roofline": {"bound": "alu", "achieved": round(achieved, 2), "peak": FP64_PEAK_TFS, "unit": "TFLOP/s",
                      "frac": round(achieved / FP64_PEAK_TFS, 4), "flops_per_launch": int(flops), "traffic": None,
-                     "kernel": "lora_apply_g",
-                     "timing": f"average of {kt['lora_apply_g'][0]} dispatches of one fit; hip events recorded by "
+                     "kernel": dom,
+                     "timing": f"average of {kt[dom][0]} dispatches of one fit; hip events recorded by "
                                "each kernel dispatch"},
         "cpu_baseline": base,
     }

@@ -303,6 +303,7 @@ __global__ void __launch_bounds__(kLT)
 k_lora_pair_solve(const double* __restrict__ G, int64_t dp, int nb, int t, double* __restrict__ Jout) {
   __shared__ double a[kLP][kLPad], j[kLP][kLPad];
   __shared__ double cc[kLB], ss[kLB];
+  __shared__ int pp[kLB], qq[kLB];
   __shared__ int rotated;
   const int pr = blockIdx.x;
   tile_load(G, dp, [&](int r) { return pair_index(pr, t, nb, r); }, pair_run(pr, t, nb, 0), pair_run(pr, t, nb, 1), a);
@@ -315,35 +316,63 @@ k_lora_pair_solve(const double* __restrict__ G, int64_t dp, int nb, int t, doubl
     if (threadIdx.x == 0) rotated = 0;
     __syncthreads();
     for (int u = 0; u < kLP - 1; ++u) {
+      // the step's 32 rotations, and their index pairs for the updates below (computed once here:
+      // the round-robin slot is a remainder, costly per element)
       if (threadIdx.x < kLB) {
         const int p = rr_slot(threadIdx.x, u, kLP), q = rr_slot(kLP - 1 - threadIdx.x, u, kLP);
         double c, s;
         if (rotation(a[p][p], a[q][q], a[p][q], c, s)) rotated = 1;
         cc[threadIdx.x] = c;
         ss[threadIdx.x] = s;
+        pp[threadIdx.x] = p;
+        qq[threadIdx.x] = q;
       }
       __syncthreads();
-      // rows p, q <- J^T rows
-      for (int e = threadIdx.x; e < kLB * kLP; e += kLT) {
-        const int w = e >> 6, col = e & 63;
-        const int p = rr_slot(w, u, kLP), q = rr_slot(kLP - 1 - w, u, kLP);
-        const double c = cc[w], s = ss[w];
-        const double ap = a[p][col], aq = a[q][col];
-        a[p][col] = c * ap - s * aq;
-        a[q][col] = s * ap + c * aq;
+      // Each thread updates one column (row phase) or one row (column phase) of the rotations
+      // w = wave + 4 i (i < 8): their parameters are read once, and every LDS read of a phase is
+      // issued before its arithmetic (an element loop waited for each dependent read in turn).
+      const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+      int pw[8], qw[8];
+      double cw[8], sw[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        pw[i] = pp[wv + 4 * i];
+        qw[i] = qq[wv + 4 * i];
+        cw[i] = cc[wv + 4 * i];
+        sw[i] = ss[wv + 4 * i];
+      }
+      // rows p, q <- J^T rows (this thread: column lane)
+      {
+        double ap[8], aq[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          ap[i] = a[pw[i]][lane];
+          aq[i] = a[qw[i]][lane];
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          a[pw[i]][lane] = cw[i] * ap[i] - sw[i] * aq[i];
+          a[qw[i]][lane] = sw[i] * ap[i] + cw[i] * aq[i];
+        }
       }
       __syncthreads();
-      // columns p, q of a and of j <- times J
-      for (int e = threadIdx.x; e < kLB * kLP; e += kLT) {
-        const int w = e >> 6, row = e & 63;
-        const int p = rr_slot(w, u, kLP), q = rr_slot(kLP - 1 - w, u, kLP);
-        const double c = cc[w], s = ss[w];
-        const double ap = a[row][p], aq = a[row][q];
-        a[row][p] = c * ap - s * aq;
-        a[row][q] = s * ap + c * aq;
-        const double jp = j[row][p], jq = j[row][q];
-        j[row][p] = c * jp - s * jq;
-        j[row][q] = s * jp + c * jq;
+      // columns p, q of a and of j <- times J (this thread: row lane)
+      {
+        double ap[8], aq[8], jp[8], jq[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          ap[i] = a[lane][pw[i]];
+          aq[i] = a[lane][qw[i]];
+          jp[i] = j[lane][pw[i]];
+          jq[i] = j[lane][qw[i]];
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          a[lane][pw[i]] = cw[i] * ap[i] - sw[i] * aq[i];
+          a[lane][qw[i]] = sw[i] * ap[i] + cw[i] * aq[i];
+          j[lane][pw[i]] = cw[i] * jp[i] - sw[i] * jq[i];
+          j[lane][qw[i]] = sw[i] * jp[i] + cw[i] * jq[i];
+        }
       }
       __syncthreads();
     }
@@ -355,27 +384,45 @@ k_lora_pair_solve(const double* __restrict__ G, int64_t dp, int nb, int t, doubl
   for (int e = threadIdx.x; e < kLP * kLP; e += kLT) out[e] = j[e >> 6][e & 63];
 }
 
-// 64 x 64 product in LDS: out[r][c] = sum_k L(r, k) R(k, c) for the thread's 4 x 4 outputs.
+// 64 x 64 product in LDS, out[r][c] = sum_k L(r, k) R(k, c) (L(r, k) = l[r][k], or l[k][r] with
+// TRANS_L), on v_mfma_f64_16x16x4_f64: wave w computes rows 32 (w / 2) .. + 31 and columns 32 (w % 2)
+// .. + 31 as 2 x 2 tiles of 16 x 16, 16 steps of 4 along k. Operand layouts (from an in-bounds probe
+// of the instruction): A[i][k] in lane i + 16 k, B[k][j] in lane j + 16 k, one double each; D[i][j]
+// in lane j + 16 (i % 4), element i / 4. Each lane reads 4 doubles from LDS per step for 4
+// instructions of 1024 multiply-adds (the thread-tiled VALU product read 8 per 16).
+typedef double d4_t __attribute__((ext_vector_type(4)));
 template <bool TRANS_L>
-__device__ __forceinline__ void tile_mm(const double (*l)[kLPad], const double (*r)[kLPad], double acc[4][4]) {
-  const int tr = threadIdx.x >> 4, tc = threadIdx.x & 15;
+__device__ __forceinline__ void tile_mma(const double (*l)[kLPad], const double (*r)[kLPad], d4_t acc[2][2]) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, i = lane & 15, kk = lane >> 4;
+  const int r0 = 32 * (w >> 1), c0 = 32 * (w & 1);
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
+    for (int b = 0; b < 2; ++b) acc[a][b] = d4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll 4
-  for (int k = 0; k < kLP; ++k) {
-    double x[4], y[4];
+  for (int s = 0; s < kLP / 4; ++s) {
+    const int k = 4 * s + kk;
+    double x[2], y[2];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      x[u] = TRANS_L ? l[k][4 * tr + u] : l[4 * tr + u][k];
-      y[u] = r[k][4 * tc + u];
-    }
+    for (int a = 0; a < 2; ++a) x[a] = TRANS_L ? l[k][r0 + 16 * a + i] : l[r0 + 16 * a + i][k];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int b = 0; b < 2; ++b) y[b] = r[k][c0 + 16 * b + i];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) acc[u][v] = fma(x[u], y[v], acc[u][v]);
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(x[a], y[b], acc[a][b], 0, 0, 0);
   }
+}
+// the product's 64 x 64 result (tile_mma's layout) into s
+__device__ __forceinline__ void tile_put(const d4_t acc[2][2], double (*s)[kLPad]) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r0 = 32 * (w >> 1), c0 = 32 * (w & 1);
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s[r0 + 16 * a + 4 * e + (lane >> 4)][c0 + 16 * b + (lane & 15)] = acc[a][b][e];
 }
 
 // G[pair a rows, pair c cols] <- J_a^T G[..] J_c for a <= c; the mirror block from the same result.
@@ -392,21 +439,14 @@ k_lora_apply_g(double* __restrict__ G, int64_t dp, int nb, int t, const double* 
   j_load(Ja, ja);
   j_load(Jc, jc);
   __syncthreads();
-  double acc[4][4];
-  tile_mm<false>(g, jc, acc);           // T = G J_c
+  d4_t acc[2][2];
+  tile_mma<false>(g, jc, acc);          // T = G J_c
   __syncthreads();
-  const int tr = threadIdx.x >> 4, tc = threadIdx.x & 15;
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) g[4 * tr + u][4 * tc + v] = acc[u][v];
+  tile_put(acc, g);
   __syncthreads();
-  tile_mm<true>(ja, g, acc);            // J_a^T T
+  tile_mma<true>(ja, g, acc);           // J_a^T T
   __syncthreads();
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) g[4 * tr + u][4 * tc + v] = acc[u][v];
+  tile_put(acc, g);
   __syncthreads();
   tile_store<false>(G, dp, rows_a, pair_run(pc, t, nb, 0), pair_run(pc, t, nb, 1), g);
   if (pa != pc) tile_store<true>(G, dp, rows_c, pair_run(pa, t, nb, 0), pair_run(pa, t, nb, 1), g);
@@ -423,14 +463,10 @@ k_lora_apply_v(double* __restrict__ V, int64_t dp, int nb, int t, const double* 
   tile_load(V, dp, rows, pair_run(pa, t, nb, 0), pair_run(pa, t, nb, 1), v);
   j_load(Ja, ja);
   __syncthreads();
-  double acc[4][4];
-  tile_mm<false>(v, ja, acc);
+  d4_t acc[2][2];
+  tile_mma<false>(v, ja, acc);          // V J_a
   __syncthreads();
-  const int tr = threadIdx.x >> 4, tc = threadIdx.x & 15;
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int w = 0; w < 4; ++w) v[4 * tr + u][4 * tc + w] = acc[u][w];
+  tile_put(acc, v);
   __syncthreads();
   tile_store<false>(V, dp, rows, pair_run(pa, t, nb, 0), pair_run(pa, t, nb, 1), v);
 }
