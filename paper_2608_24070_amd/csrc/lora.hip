@@ -78,18 +78,6 @@ __device__ __forceinline__ void tile_store(double* __restrict__ M, int64_t dp, R
     *reinterpret_cast<double2*>(M + row_of(r) * dp + ((run & 1) ? c1 : c0) + 2 * q) = w;
   }
 }
-// a contiguous row-major 64 x 64 matrix into LDS, loads first
-__device__ __forceinline__ void j_load(const double* __restrict__ J, double (*s)[kLPad]) {
-  double2 v[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = reinterpret_cast<const double2*>(J)[threadIdx.x + kLT * i];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int e = threadIdx.x + kLT * i, r = e >> 5, c = 2 * (e & 31);
-    s[r][c] = v[i].x;
-    s[r][c + 1] = v[i].y;
-  }
-}
 // the two column runs of pair p in round t
 __device__ __forceinline__ int64_t pair_run(int p, int t, int nb, int h) {
   return (int64_t)rr_slot(h ? nb - 1 - p : p, t, nb) * kLB;
@@ -384,36 +372,50 @@ k_lora_pair_solve(const double* __restrict__ G, int64_t dp, int nb, int t, doubl
   for (int e = threadIdx.x; e < kLP * kLP; e += kLT) out[e] = j[e >> 6][e & 63];
 }
 
-// 64 x 64 product in LDS, out[r][c] = sum_k L(r, k) R(k, c) (L(r, k) = l[r][k], or l[k][r] with
-// TRANS_L), on v_mfma_f64_16x16x4_f64: wave w computes rows 32 (w / 2) .. + 31 and columns 32 (w % 2)
-// .. + 31 as 2 x 2 tiles of 16 x 16, 16 steps of 4 along k. Operand layouts (from an in-bounds probe
-// of the instruction): A[i][k] in lane i + 16 k, B[k][j] in lane j + 16 k, one double each; D[i][j]
-// in lane j + 16 (i % 4), element i / 4. Each lane reads 4 doubles from LDS per step for 4
-// instructions of 1024 multiply-adds (the thread-tiled VALU product read 8 per 16).
+// 64 x 64 products, out[r][c] = sum_k L(r, k) R(k, c), on v_mfma_f64_16x16x4_f64: wave w computes
+// rows 32 (w / 2) .. + 31 and columns 32 (w % 2) .. + 31 as 2 x 2 tiles of 16 x 16, 16 steps of 4
+// along k. Operand layouts (from an in-bounds probe of the instruction): A[i][k] in lane i + 16 k,
+// B[k][j] in lane j + 16 k, one double each; D[i][j] in lane j + 16 (i % 4), element i / 4. A
+// lane reads 2 doubles from LDS per step for 4 instructions of 1024 multiply-adds (the
+// thread-tiled VALU product read 8 per 16 multiply-adds).
 typedef double d4_t __attribute__((ext_vector_type(4)));
-template <bool TRANS_L>
-__device__ __forceinline__ void tile_mma(const double (*l)[kLPad], const double (*r)[kLPad], d4_t acc[2][2]) {
+// A rotation J (64 x 64, row-major, in global memory; a round's J are 2 MB and stay in L2) as the
+// operand fragments of tile_mma_j, loaded into registers at once: f[s][t] = J[4 s + k][base + 16 t + i]
+// for lane i + 16 k. With base = the wave's column start this is the B operand J; with the row
+// start, the A operand J^T.
+__device__ __forceinline__ void j_frags(const double* __restrict__ J, int base, double f[kLP / 4][2]) {
+  const int lane = threadIdx.x & 63, i = lane & 15, kk = lane >> 4;
+#pragma unroll
+  for (int s = 0; s < kLP / 4; ++s)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) f[s][t] = J[(4 * s + kk) * kLP + base + 16 * t + i];
+}
+// the product with one operand in registers (j_frags, f): L = m (LDS) times R = J, or (JL)
+// L = J^T times R = m (LDS)
+template <bool JL>
+__device__ __forceinline__ void tile_mma_j(const double (*m)[kLPad], const double f[kLP / 4][2], d4_t acc[2][2]) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, i = lane & 15, kk = lane >> 4;
   const int r0 = 32 * (w >> 1), c0 = 32 * (w & 1);
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = d4_t{0.0, 0.0, 0.0, 0.0};
-#pragma unroll 4
+#pragma unroll
   for (int s = 0; s < kLP / 4; ++s) {
     const int k = 4 * s + kk;
     double x[2], y[2];
 #pragma unroll
-    for (int a = 0; a < 2; ++a) x[a] = TRANS_L ? l[k][r0 + 16 * a + i] : l[r0 + 16 * a + i][k];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) y[b] = r[k][c0 + 16 * b + i];
+    for (int t = 0; t < 2; ++t) {
+      x[t] = JL ? f[s][t] : m[r0 + 16 * t + i][k];
+      y[t] = JL ? m[k][c0 + 16 * t + i] : f[s][t];
+    }
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
       for (int b = 0; b < 2; ++b) acc[a][b] = __builtin_amdgcn_mfma_f64_16x16x4f64(x[a], y[b], acc[a][b], 0, 0, 0);
   }
 }
-// the product's 64 x 64 result (tile_mma's layout) into s
+// the product's 64 x 64 result (tile_mma_j's layout) into s
 __device__ __forceinline__ void tile_put(const d4_t acc[2][2], double (*s)[kLPad]) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r0 = 32 * (w >> 1), c0 = 32 * (w & 1);
@@ -430,21 +432,25 @@ __global__ void __launch_bounds__(kLT)
 k_lora_apply_g(double* __restrict__ G, int64_t dp, int nb, int t, const double* __restrict__ J) {
   const int pa = blockIdx.y, pc = blockIdx.x;
   if (pa > pc) return;
-  __shared__ double g[kLP][kLPad], ja[kLP][kLPad], jc[kLP][kLPad];
+  // only the G tile lives in LDS (two blocks share a CU, so one's loads overlap the other's MFMAs);
+  // the rotations come straight from L2 into registers, with the tile's loads
+  __shared__ double g[kLP][kLPad];
+  const int w = threadIdx.x >> 6;
   const double* Ja = J + (int64_t)pa * kLP * kLP;
   const double* Jc = J + (int64_t)pc * kLP * kLP;
   auto rows_a = [&](int r) { return pair_index(pa, t, nb, r); };
   auto rows_c = [&](int r) { return pair_index(pc, t, nb, r); };
+  double fc[kLP / 4][2], fa[kLP / 4][2];
+  j_frags(Jc, 32 * (w & 1), fc);
+  j_frags(Ja, 32 * (w >> 1), fa);
   tile_load(G, dp, rows_a, pair_run(pc, t, nb, 0), pair_run(pc, t, nb, 1), g);
-  j_load(Ja, ja);
-  j_load(Jc, jc);
   __syncthreads();
   d4_t acc[2][2];
-  tile_mma<false>(g, jc, acc);          // T = G J_c
+  tile_mma_j<false>(g, fc, acc);        // T = G J_c
   __syncthreads();
   tile_put(acc, g);
   __syncthreads();
-  tile_mma<true>(ja, g, acc);           // J_a^T T
+  tile_mma_j<true>(g, fa, acc);         // J_a^T T
   __syncthreads();
   tile_put(acc, g);
   __syncthreads();
@@ -457,14 +463,16 @@ __global__ void __launch_bounds__(kLT)
 k_lora_apply_v(double* __restrict__ V, int64_t dp, int nb, int t, const double* __restrict__ J) {
   const int pa = blockIdx.x;
   const int64_t r0 = (int64_t)blockIdx.y * kLP;
-  __shared__ double v[kLP][kLPad], ja[kLP][kLPad];
+  __shared__ double v[kLP][kLPad];
+  const int w = threadIdx.x >> 6;
   const double* Ja = J + (int64_t)pa * kLP * kLP;
   auto rows = [&](int r) { return r0 + r; };
+  double fa[kLP / 4][2];
+  j_frags(Ja, 32 * (w & 1), fa);
   tile_load(V, dp, rows, pair_run(pa, t, nb, 0), pair_run(pa, t, nb, 1), v);
-  j_load(Ja, ja);
   __syncthreads();
   d4_t acc[2][2];
-  tile_mma<false>(v, ja, acc);          // V J_a
+  tile_mma_j<false>(v, fa, acc);        // V J_a
   __syncthreads();
   tile_put(acc, v);
   __syncthreads();
