@@ -316,48 +316,60 @@ k_lora_pair_solve(const double* __restrict__ G, int64_t dp, int nb, int t, doubl
         qq[threadIdx.x] = q;
       }
       __syncthreads();
-      // Each thread updates one column (row phase) or one row (column phase) of the rotations
-      // w = wave + 4 i (i < 8): their parameters are read once, and every LDS read of a phase is
-      // issued before its arithmetic (an element loop waited for each dependent read in turn).
-      const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-      int pw[8], qw[8];
-      double cw[8], sw[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        pw[i] = pp[wv + 4 * i];
-        qw[i] = qq[wv + 4 * i];
-        cw[i] = cc[wv + 4 * i];
-        sw[i] = ss[wv + 4 * i];
-      }
-      // rows p, q <- J^T rows (this thread: column lane)
+      // A <- J^T A J in one pass: the rotations are disjoint index pairs, so every element of A lies
+      // in exactly one 2 x 2 block (rows p1, q1 of rotation w1, columns p2, q2 of rotation w2), which
+      // becomes R1^T block R2 from its own four values; thread: rotation w1 = tid / 8 and w2 =
+      // tid % 8 + 8 i (i < 4). J <- J R by columns: thread row tid % 64, rotations w = tid / 64 + 4 i
+      // (i < 8). Every LDS read of a phase is issued before its arithmetic.
       {
-        double ap[8], aq[8];
+        const int w1 = threadIdx.x >> 3;
+        const int p1 = pp[w1], q1 = qq[w1];
+        const double c1 = cc[w1], s1 = ss[w1];
+        int p2[4], q2[4];
+        double c2[4], s2[4], b00[4], b01[4], b10[4], b11[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int w2 = (threadIdx.x & 7) + 8 * i;
+          p2[i] = pp[w2];
+          q2[i] = qq[w2];
+          c2[i] = cc[w2];
+          s2[i] = ss[w2];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          b00[i] = a[p1][p2[i]];
+          b01[i] = a[p1][q2[i]];
+          b10[i] = a[q1][p2[i]];
+          b11[i] = a[q1][q2[i]];
+        }
+        const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+        int pw[8], qw[8];
+        double cw[8], sw[8], jp[8], jq[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          ap[i] = a[pw[i]][lane];
-          aq[i] = a[qw[i]][lane];
+          pw[i] = pp[wv + 4 * i];
+          qw[i] = qq[wv + 4 * i];
+          cw[i] = cc[wv + 4 * i];
+          sw[i] = ss[wv + 4 * i];
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          a[pw[i]][lane] = cw[i] * ap[i] - sw[i] * aq[i];
-          a[qw[i]][lane] = sw[i] * ap[i] + cw[i] * aq[i];
-        }
-      }
-      __syncthreads();
-      // columns p, q of a and of j <- times J (this thread: row lane)
-      {
-        double ap[8], aq[8], jp[8], jq[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          ap[i] = a[lane][pw[i]];
-          aq[i] = a[lane][qw[i]];
           jp[i] = j[lane][pw[i]];
           jq[i] = j[lane][qw[i]];
         }
 #pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          // rows: (R1^T B) with R1 = [[c1, s1], [-s1, c1]] acting as p' = c p - s q, q' = s p + c q
+          const double r00 = c1 * b00[i] - s1 * b10[i], r01 = c1 * b01[i] - s1 * b11[i];
+          const double r10 = s1 * b00[i] + c1 * b10[i], r11 = s1 * b01[i] + c1 * b11[i];
+          // then columns, the same rotation form with rotation w2
+          a[p1][p2[i]] = c2[i] * r00 - s2[i] * r01;
+          a[p1][q2[i]] = s2[i] * r00 + c2[i] * r01;
+          a[q1][p2[i]] = c2[i] * r10 - s2[i] * r11;
+          a[q1][q2[i]] = s2[i] * r10 + c2[i] * r11;
+        }
+#pragma unroll
         for (int i = 0; i < 8; ++i) {
-          a[lane][pw[i]] = cw[i] * ap[i] - sw[i] * aq[i];
-          a[lane][qw[i]] = sw[i] * ap[i] + cw[i] * aq[i];
           j[lane][pw[i]] = cw[i] * jp[i] - sw[i] * jq[i];
           j[lane][qw[i]] = sw[i] * jp[i] + cw[i] * jq[i];
         }
