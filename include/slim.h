@@ -392,7 +392,7 @@ int slim_update_pack16(const float* Wnew, int64_t count, uint16_t* vals, void* s
  * for i = 1..10, then (a - max|w| / 10) + j max|w| / 100 for j = 0..19 around the best of those, a,
  * the positive ones only; alpha* is the first candidate of least error. All-zero W gives alpha* = 0
  * and C = 0. Returns SLIM_ENONFINITE for NaN/Inf in W. This call synchronises `stream` (it reads
- * back a status word) and allocates 8 bytes of device memory for the duration of the call.
+ * back a status word) and allocates under 4 KiB of device memory for the duration of the call.
  *
  * slim_pack_alpha - slim_pack with the per-tensor parameter in place of each group's absmax: every
  * group's scale is s16 = fp16_RNE(fp32(alpha) / 7.0f), so weights beyond alpha clip to +-7 (same

@@ -8,9 +8,10 @@
 //                   and a status bit for non-finite weights
 //   k_quant_hist    per-block histogram of |w| in LDS, added into the global one; bin
 //                   b = floor(|w| bins / amax) exactly (see bin_of)
-//   k_quant_search  one block: E(alpha) = E_quant + E_clip in float64 by the midpoint rule on the
-//                   bin centres, ten coarse candidates, twenty fine ones around the coarse
-//                   minimum, argmin
+//   k_quant_cand    E(alpha) = E_quant + E_clip in float64 by the midpoint rule on the bin centres,
+//                   one block per candidate: the ten coarse ones and the twenty fine ones around
+//                   each of them
+//   k_quant_pick    the search's order: the coarse minimum, its fine candidates, the argmin
 #include <math.h>
 
 #include "slim_device.h"
@@ -23,7 +24,7 @@ constexpr int kQThreads = 256;
 constexpr int kQMaxBins = 20480;           // 80 KiB of LDS counters: two blocks per CU
 constexpr int kQHistThreads = 1024;
 constexpr int kQCoarse = 10, kQFine = 20;  // candidates of the two grids
-constexpr int kQSearchThreads = 1024;
+constexpr int kQSearchThreads = 512;
 
 __global__ void __launch_bounds__(kQThreads)
 k_quant_clear(uint32_t* __restrict__ hist, int bins, uint32_t* __restrict__ amax_bits, int* __restrict__ status) {
@@ -141,84 +142,116 @@ __device__ double block_sum(double v, double* red) {
 // E(alpha) of Alg. quantization on the histogram: bin b stands for its count at the centre
 // (b + 1/2) amax / bins; magnitudes up to alpha reconstruct on the grid of step alpha / qmax
 // (eq. quantization_error), larger ones as alpha (eq. clipping_error).
-__device__ double estimate_error(const uint32_t* __restrict__ hist, int bins, double amax, double alpha, double qmax,
+// The thread's counts, bins b = threadIdx.x + kQSearchThreads i, sit in registers (loaded once for
+// all candidates: a loop that loaded each count as it went waited for every load in turn).
+constexpr int kQPerThread = kQMaxBins / kQSearchThreads;
+__device__ double estimate_error(const uint32_t (&cnts)[kQPerThread], int bins, double amax, double alpha, double qmax,
                                  double total, double* red) {
   const double width = amax / (double)bins;
   const double delta = alpha / qmax;
   double sq = 0.0, sc = 0.0;
-  for (int b = threadIdx.x; b < bins; b += kQSearchThreads) {
-    const uint32_t cnt = hist[b];
-    if (!cnt) continue;
+  // branch-free: a zero count, or the side a centre is not on, adds +0.0, which leaves a
+  // non-negative sum unchanged; one bin at a time (the scheduler would otherwise interleave all the
+  // divisions and spill)
+#pragma unroll
+  for (int i = 0; i < kQPerThread; ++i) {
+    const int b = threadIdx.x + kQSearchThreads * i;
+    const double cnt = (double)cnts[i];
     const double c = ((double)b + 0.5) * width;
-    if (c <= alpha) {
-      const double d = delta * rint(c / delta) - c;
-      sq += (double)cnt * (d * d);
-    } else {
-      const double d = alpha - c;
-      sc += (double)cnt * (d * d);
-    }
+    const double dq = delta * rint(c / delta) - c;
+    const double dc = alpha - c;
+    const bool in = c <= alpha;
+    sq += in ? cnt * (dq * dq) : 0.0;
+    sc += in ? 0.0 : cnt * (dc * dc);
+    __builtin_amdgcn_sched_barrier(0);
   }
   const double q = block_sum(sq, red);
   const double s = block_sum(sc, red);
   return q / total + s / total;
 }
 
-// out: [0] alpha*, [1] E(alpha*), [2] amax, [3] candidates evaluated C, [4 + 2i] alpha_i,
-// [5 + 2i] E(alpha_i) in evaluation order.
+// Every candidate the search can evaluate, one block each: the ten coarse ones i amax / 10, and
+// for each of them the twenty fine ones (i amax / 10 - amax / 10) + j amax / 100 that the search
+// evaluates if i is the coarse minimum (kQCand blocks; a non-positive one is marked NaN). Each
+// block sums its candidate exactly as a single block evaluating the candidates in turn would, so
+// the errors do not depend on this split; k_quant_pick then walks the search's order.
+constexpr int kQCand = kQCoarse + kQCoarse * kQFine;
 __global__ void __launch_bounds__(kQSearchThreads)
-k_quant_search(const uint32_t* __restrict__ hist, int bins, const uint32_t* __restrict__ amax_bits, int bits,
-               double total, double* __restrict__ out) {
+k_quant_cand(const uint32_t* __restrict__ hist, int bins, const uint32_t* __restrict__ amax_bits, int bits,
+             double total, double* __restrict__ cand) {
   __shared__ double red[kQSearchThreads / 64];
   const double amax = (double)__uint_as_float(*amax_bits);
+  if (amax == 0.0) return;
   const double qmax = (double)((1 << (bits - 1)) - 1);
-  const bool lead = threadIdx.x == 0;
-  if (amax == 0.0) {
-    if (lead) {
-      out[0] = 0.0;
-      out[1] = 0.0;
-      out[2] = 0.0;
-      out[3] = 0.0;
+  const double eta_low = amax / (double)kQCoarse;
+  const int c = blockIdx.x;
+  double a;
+  if (c < kQCoarse) {
+    a = (double)(c + 1) * eta_low;
+  } else {
+    const int i = (c - kQCoarse) / kQFine + 1, j = (c - kQCoarse) % kQFine;
+    const double alpha_low = (double)i * eta_low, eta_high = eta_low / 10.0;
+    a = (alpha_low - eta_low) + (double)j * eta_high;
+  }
+  double e = __builtin_nan("");
+  if (a > 0.0) {     // uniform per block
+    uint32_t cnts[kQPerThread];
+#pragma unroll
+    for (int i = 0; i < kQPerThread; ++i) {
+      const int b = threadIdx.x + kQSearchThreads * i;
+      cnts[i] = b < bins ? hist[b] : 0u;
     }
+    e = estimate_error(cnts, bins, amax, a, qmax, total, red);
+  }
+  if (threadIdx.x == 0) {
+    cand[2 * c] = a;
+    cand[2 * c + 1] = e;
+  }
+}
+
+// out: [0] alpha*, [1] E(alpha*), [2] amax, [3] candidates evaluated C, [4 + 2i] alpha_i,
+// [5 + 2i] E(alpha_i) in evaluation order: the ten coarse candidates, then the positive fine ones
+// around the first coarse minimum; alpha* is the first candidate of least error. One thread.
+__global__ void __launch_bounds__(64)
+k_quant_pick(const uint32_t* __restrict__ amax_bits, const double* __restrict__ cand, double* __restrict__ out) {
+  if (threadIdx.x != 0) return;
+  const double amax = (double)__uint_as_float(*amax_bits);
+  if (amax == 0.0) {
+    out[0] = 0.0;
+    out[1] = 0.0;
+    out[2] = 0.0;
+    out[3] = 0.0;
     return;
   }
-  int n = 0;
+  int n = 0, ibest = 0;
   double best_a = 0.0, best_e = 0.0;
-  const double eta_low = amax / (double)kQCoarse;
-  for (int i = 1; i <= kQCoarse; ++i) {
-    const double a = (double)i * eta_low;
-    const double e = estimate_error(hist, bins, amax, a, qmax, total, red);
-    if (lead) {
-      out[4 + 2 * n] = a;
-      out[5 + 2 * n] = e;
-    }
+  for (int i = 0; i < kQCoarse; ++i) {
+    const double a = cand[2 * i], e = cand[2 * i + 1];
+    out[4 + 2 * n] = a;
+    out[5 + 2 * n] = e;
     if (n == 0 || e < best_e) {
       best_a = a;
       best_e = e;
+      ibest = i;
     }
     ++n;
   }
-  const double alpha_low = best_a;
-  const double eta_high = eta_low / 10.0;
   for (int j = 0; j < kQFine; ++j) {
-    const double a = (alpha_low - eta_low) + (double)j * eta_high;
+    const int c = kQCoarse + ibest * kQFine + j;
+    const double a = cand[2 * c], e = cand[2 * c + 1];
     if (!(a > 0.0)) continue;
-    const double e = estimate_error(hist, bins, amax, a, qmax, total, red);
-    if (lead) {
-      out[4 + 2 * n] = a;
-      out[5 + 2 * n] = e;
-    }
+    out[4 + 2 * n] = a;
+    out[5 + 2 * n] = e;
     if (e < best_e) {
       best_a = a;
       best_e = e;
     }
     ++n;
   }
-  if (lead) {
-    out[0] = best_a;
-    out[1] = best_e;
-    out[2] = amax;
-    out[3] = (double)n;
-  }
+  out[0] = best_a;
+  out[1] = best_e;
+  out[2] = amax;
+  out[3] = (double)n;
 }
 
 }  // namespace
@@ -236,11 +269,13 @@ extern "C" int slim_quant_search(const float* W, int64_t count, int bits, int64_
   if (count >= ((int64_t)1 << 40)) return SLIM_EUNSUPPORTED;
   if (!slim_aligned16(W) || ((uintptr_t)hist & 3u) || ((uintptr_t)out & 7u)) return SLIM_EALIGN;
   hipStream_t s = (hipStream_t)stream;
-  // maximum and status live in one 8-byte device allocation for the duration of the call
+  // maximum, status and the candidates' errors live in one small device allocation for the
+  // duration of the call
   uint32_t* d_aux = nullptr;
-  if (hipMalloc(&d_aux, 2 * sizeof(uint32_t)) != hipSuccess) return SLIM_EDEVICE;
+  if (hipMalloc(&d_aux, 16 + 2 * kQCand * sizeof(double)) != hipSuccess) return SLIM_EDEVICE;
   uint32_t* d_amax = d_aux;
   int* d_status = reinterpret_cast<int*>(d_aux + 1);
+  double* d_cand = reinterpret_cast<double*>(d_aux + 4);
   int h_status = 0, rc = SLIM_OK;
   const int64_t n4 = count / 4;
   int64_t grid = (n4 + kQThreads - 1) / kQThreads;
@@ -265,8 +300,12 @@ extern "C" int slim_quant_search(const float* W, int64_t count, int bits, int64_
     }
     {
       SlimKernelTimer timer("quant_search", s);
-      SLIM_LAUNCH(timer, k_quant_search, dim3(1), dim3(kQSearchThreads), s, (const uint32_t*)hist, (int)bins,
-                  (const uint32_t*)d_amax, bits, (double)count, out);
+      SLIM_LAUNCH(timer, k_quant_cand, dim3(kQCand), dim3(kQSearchThreads), s, (const uint32_t*)hist, (int)bins,
+                  (const uint32_t*)d_amax, bits, (double)count, d_cand);
+    }
+    {
+      SlimKernelTimer timer("quant_pick", s);
+      SLIM_LAUNCH(timer, k_quant_pick, dim3(1), dim3(64), s, (const uint32_t*)d_amax, (const double*)d_cand, out);
     }
     if (hipGetLastError() != hipSuccess) { rc = SLIM_EDEVICE; break; }
     if (hipMemcpyAsync(&h_status, d_status, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess ||
