@@ -117,7 +117,22 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     q.sp_col_tiles = cdiv(M, q.sp_cols_tile);
     q.sp_split = 1;
     q.sp_chunks_per_split = nchunks;
-    if (r > 0) {
+    // 256 x 256 adapter tiles (half the operand bytes per flop) with a 128 KiB ring, one block per
+    // CU, when they fill the 256 CUs with reduction slices of at least 2048: the long reductions
+    // at large M (the 70B dX product took 320 -> 253 us with its split sum; the 13B layers, whose
+    // slices would be shorter or whose blocks too few, were slower); 256 rows of the reduction
+    // stay within 32-bit byte offsets
+    const int64_t wtiles = cdiv(M, 256) * (r / 256);
+    const int64_t wsplit = wtiles > 0 ? std::max<int64_t>(1, std::min<int64_t>(256 / wtiles, red / 1024)) : 0;
+    if (r > 0 && r % 256 == 0 && red < (int64_t(1) << 22) && wtiles * wsplit >= 256 && red / wsplit >= 2048) {
+      q.ad_wide = true;
+      q.ad_tiles_m = (int)cdiv(M, 256);
+      q.ad_tiles_j = (int)(r / 256);
+      const int64_t slice = cdiv(cdiv(red, wsplit), 32) * 32;
+      q.ad_split = (int)cdiv(red, slice);
+      q.ad_slice = slice;
+      if (q.ad_split > 1) tpart_bytes = (size_t)q.ad_split * (size_t)cdiv(M, 32) * 32 * (size_t)r * 4;
+    } else if (r > 0) {
       q.ad_tiles_m = (int)cdiv(M, 128);
       q.ad_tiles_j = (int)cdiv(r, 128);
       const int64_t tiles = (int64_t)q.ad_tiles_m * q.ad_tiles_j;

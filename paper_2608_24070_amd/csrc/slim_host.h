@@ -27,6 +27,7 @@ int slim_check_pack_bwd(const void* codes, const void* meta, const void* scales,
 struct SlimPlan {
   // dense adapter GEMM (T = X L forward, U = dY R^T backward)
   int ad_tiles_m = 0, ad_tiles_j = 0, ad_split = 1;
+  bool ad_wide = false;                // large M: 256 x 256 adapter tiles (k_adapter_gemm_wide)
   int64_t ad_slice = 0;               // reduction length per split
   int ad_sub = 1;                      // small M: SLIM_DECODE_AD_SLICE slices per adapter wave
   int64_t ad_jblocks = 0;             // small-M path: 16-wide blocks of the adapter rank

@@ -114,6 +114,15 @@ def test_tile_kernel_wide_tiles_ragged_m():
     _fwd_case(11008, 2048, 48, 1400, rows=rows, ms=ms, name="wide")
 
 
+@pytest.mark.parametrize("n,k,r,m", [(256, 33024, 512, 1900), (128, 16384, 512, 4096)])
+def test_adapter_gemm_wide_tiles(n, k, r, m):
+    # the 256 x 256 adapter GEMM takes shapes whose 256 x 256 tiles times reduction splits of at least
+    # 2048 fill 256 blocks: a ragged last m tile (M = 1900, 16 tiles) over 16 splits whose last one is
+    # short (reduction 33024 in slices of 2080), and 32 tiles over 8 splits of exactly 2048
+    ms = np.unique(np.concatenate([synth.stream(8, "ms").choice(m, size=40, replace=False), np.arange(m - 8, m)]))
+    _fwd_case(n, k, r, m, ms=ms, name="adwide")
+
+
 def test_linear_on_oracle_pack():
     _fwd_case(1024, 1024, 64, 16, use_oracle_pack=True, name="opack")
     _fwd_case(1024, 1024, 64, 256, use_oracle_pack=True, name="opack")
@@ -224,6 +233,13 @@ def test_bwd_wide_tiles_ragged_m():
     # backward rows = K = 11008 (22 row tiles), 1400 columns: 512 x 128 tiles with a ragged last one
     ms = np.unique(np.concatenate([synth.stream(7, "ms").choice(1400, size=24, replace=False), np.arange(1390, 1400)]))
     _bwd_case(2048, 11008, 48, 1400, seed=3, ks=(0, 85), ms=ms, name="bwide")
+
+
+def test_bwd_adapter_gemm_wide_tiles():
+    # U = dY R^T on the 256 x 256 adapter GEMM: r 512, M 1900 (eight m tiles, the last ragged),
+    # reduction N = 33024 in 16 splits, the last one short
+    ms = np.unique(np.concatenate([synth.stream(9, "ms").choice(1900, size=24, replace=False), np.arange(1892, 1900)]))
+    _bwd_case(33024, 256, 512, 1900, seed=4, ks=(0, 1), ms=ms, name="bwd_adwide")
 
 
 def test_bwd_is_deterministic():
