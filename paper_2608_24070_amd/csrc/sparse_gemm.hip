@@ -588,31 +588,42 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
 }
 
 // ============================================================ large-M tile kernel
-// Block = 4 waves; wave w owns rows [row0 + 128 w, +128) as 4 fragments of 32 and all columns
-// [m0, m0 + TC) as TC / 32 fragments of 32 (TC = 96 or 128): a 128 x TC accumulator (TC * 2
-// registers per lane, in the accumulation registers) on 32x32x32 sparse MFMA. Each dequantised
+// Block = 512 / WR waves over a 512 x TC tile; wave w owns rows [row0 + WR w, +WR) as WR / 32
+// fragments of 32 and all columns [m0, m0 + TC) as TC / 32 fragments of 32 (TC = 96 or 128): a
+// WR x TC accumulator (in the accumulation registers) on 32x32x32 sparse MFMA. Each dequantised
 // weight fragment feeds TC / 32 MFMAs and no weight row is dequantised by two waves; the wider
 // tile spends less dequantisation per MFMA, the narrower one gives more tiles to even out the
-// last round of blocks (the plan picks per shape).
-// Per 128-wide reduction chunk, each wave's packed words (codes, index words and scales of its
-// 128 rows) and the fp16 activation tile [TC x 128] go straight from memory to LDS (direct
-// loads), so no register holds data still in flight: the words into a ring of three stages, two
+// last round of blocks (the plan picks per shape). WR = 128 runs one wave per SIMD (4 waves,
+// 128 x TC accumulators); WR = 64 runs two (8 waves, half the accumulators each), so that one
+// wave's dequantisation, LDS reads and waits overlap the other's MFMAs, at twice the B-fragment
+// reads from LDS.
+// Per 128-wide reduction chunk, the tile's packed words (codes, index words and scales of its
+// 512 rows, in four 128-row groups) and the fp16 activation tile [TC x 128] go straight from
+// memory to LDS (direct loads), so no register holds data still in flight: the words into a ring of three stages, two
 // chunks ahead; the activations into a ring of three stages, two chunks ahead, at TC = 96, or of
 // two stages, one chunk ahead, at TC = 128 (three would not fit in LDS next to the words). A
 // chunk's words are read from LDS, and its first step dequantised, during the last step of the
 // chunk before. Activation rows in LDS are 256 B with the 16-byte column index XOR-swizzled by
 // the row, so B-fragment reads (32 rows at one column) hit distinct banks. The backward also
-// brings each wave's scale row (its 128-row group) into LDS with the activations.
-constexpr int kTR = 512, kTThreads = 256, kBand = 4;
-template <int TC> struct TileShape {
+// brings each 128-row group's scale row into LDS with the activations.
+// Each wave loads the words of its own rows; the scales (and in the backward the scale row) of a
+// 128-row group are loaded by every wave of the group, so that all waves issue the same loads
+// (two waves then write the same bytes).
+constexpr int kTR = 512, kBand = 4;
+template <int TC, int WR> struct TileShape {
+  static constexpr int kWaves = kTR / WR;              // waves per block
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kFn = WR / 32;                  // row fragments per wave
   static constexpr int kFm = TC / 32;                  // column fragments per wave
-  static constexpr int kActRows = TC / 4;              // activation rows each wave brings in
-  static constexpr int kActLoads = TC / 16;            // ... four rows per direct load
+  static constexpr int kActRows = TC / kWaves;         // activation rows each wave brings in
+  static constexpr int kActLoads = kActRows / 4;       // ... four rows per direct load
   static constexpr int kStagesX = TC == 128 ? 2 : 3;   // activation stages
   static constexpr int kAhead = kStagesX - 1;          // chunks of activations in flight ahead
+  static_assert(kActRows % 4 == 0, "whole direct loads of four rows");
 };
-// Direct loads per thread per chunk: activation loads (TC / 16, and in the backward one scale-row
-// load) and packed words (4 code loads, 2 index word loads, and in the forward 1 scale load).
+// Direct loads per thread per chunk: activation loads (kActLoads, and in the backward one
+// scale-row load) and packed words (WR / 32 code loads, WR / 64 index word loads, and in the
+// forward 1 scale load).
 // kAhead 2: chunk c issues chunk c + 2's words in its first step and chunk c + 2's activations in
 // its second.
 //  * at the top of chunk c its words and activations must have landed: only chunk c + 1's loads
@@ -627,23 +638,22 @@ template <int TC> struct TileShape {
 //    activations and chunk c + 2's words may still be outstanding.
 // The prologue issues the loads of the chunks before in the same order, so the same counts hold
 // from the start.
-constexpr int kTileWordsFwd = 4 + 2 + 1, kTileWordsBwd = 4 + 2;
-template <bool BWD, int TC> struct TileCounts {
-  static constexpr bool kActFirst = TileShape<TC>::kAhead == 1;
-  static constexpr int kWords = BWD ? kTileWordsBwd : kTileWordsFwd;
-  static constexpr int kAct = TileShape<TC>::kActLoads + (BWD ? 1 : 0);
+template <bool BWD, int TC, int WR> struct TileCounts {
+  static constexpr bool kActFirst = TileShape<TC, WR>::kAhead == 1;
+  static constexpr int kWords = WR / 32 + WR / 64 + (BWD ? 0 : 1);
+  static constexpr int kAct = TileShape<TC, WR>::kActLoads + (BWD ? 1 : 0);
   static constexpr int kTop = kActFirst ? kWords : kAct + kWords;
   static constexpr int kNext = kActFirst ? kAct + kWords : kAct + kWords + kAct;
 };
 
-static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && TileCounts<true, 128>::kNext < 64, "s_waitcnt encoding");
+static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && TileCounts<true, 128, 128>::kNext < 64, "s_waitcnt encoding");
 static_assert(vmcnt_lgkm0_wait(20) == 0x4074u, "s_waitcnt encoding");
 
 
-// One chunk's packed words of the four waves, as the direct loads lay them down (lane L of a load
-// at 16 L, or 4 L for 2-byte loads): codes [wave][fragment][lane] (16 B: the lane's four code
-// words), index words [wave][row slot] (16 B: the row's four words; row slot = 32 fragment + row
-// in fragment), scales [wave][row slot] (fp16 in the low half of a dword). Reads index these
+// One chunk's packed words of the tile's four 128-row groups, as the direct loads lay them down
+// (lane L of a load at 16 L, or 4 L for 2-byte loads): codes [group][fragment][lane] (16 B: the
+// lane's four code words), index words [group][row slot] (16 B: the row's four words; row slot =
+// 32 fragment + row in fragment), scales [group][row slot] (fp16 in the low half of a dword). Reads index these
 // arrays directly (no pointer casts, and no 8-byte reads the compiler would pair into one
 // instruction that has lost track of its address), so that the compiler can tell the stages
 // apart and does not wait for every direct load in flight.
@@ -653,18 +663,19 @@ struct TileWordsLds {
   u32x4_t mw[4][128];
   uint16_t sw[BWD ? 1 : 4][BWD ? 2 : 128];
 };
-// one chunk's packed words of one lane, read from LDS
+// one chunk's packed words of one lane (FN row fragments), read from LDS
+template <int FN>
 struct TileWords {
-  u32x4_t cw[4];
-  u32x2_t mw[4];
-  uint32_t sw[4];
+  u32x4_t cw[FN];
+  u32x2_t mw[FN];
+  uint32_t sw[FN];
 };
 
-template <bool BWD, int TC>
+template <bool BWD, int TC, int WR>
 SLIM_DEV void tile_body(const LayerArgs& a) {
-  using Sh = TileShape<TC>;
-  using Ct = TileCounts<BWD, TC>;
-  constexpr int kTC = TC, kFm = Sh::kFm, kStagesX = Sh::kStagesX;
+  using Sh = TileShape<TC, WR>;
+  using Ct = TileCounts<BWD, TC, WR>;
+  constexpr int kTC = TC, kFn = Sh::kFn, kFm = Sh::kFm, kStagesX = Sh::kStagesX;
   // one array per stage (the stages of chunk c are c % 3 for the words and c % kStagesX for the
   // activations, constants in the loop unrolled by six), so that reads of one stage are not
   // ordered behind loads still landing in another
@@ -678,6 +689,8 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ha = lane >> 5;
+  // the wave's 128-row group and its first fragment there
+  const int grp = WR == 128 ? wave : wave >> 1, fbase = WR == 128 ? 0 : 2 * (wave & 1);
   // XCD-aware tile order: block b runs on XCD b % 8 (workgroups are dealt round robin), and XCD x
   // takes positions [x Q, (x + 1) Q) of a tile order that walks bands of kBand row tiles column
   // by column. The blocks an XCD runs together then cover a few row tiles x a few column tiles,
@@ -690,30 +703,31 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   const int64_t rb = R - band * kBand < kBand ? R - band * kBand : kBand;   // rows in this band
   const int64_t rt = band * kBand + q % rb, ct = q / rb;
   const int64_t row0 = rt * kTR, m0 = ct * kTC;
-  const int64_t wrow0 = row0 + 128 * wave;
+  const int64_t wrow0 = row0 + WR * wave;
   const int64_t nch = a.red / 128;
 
   // Addresses. Per-lane offsets are derived inside each chunk from a few base registers (made
   // opaque per chunk) instead of being kept live across the loop. Rows past the matrix (or past
   // M) get offsets at or beyond their resource's extent and read as zero; their results are not
   // stored. The uniform chunk offset only ever moves a valid row within that row.
-  // packed words: resources from the wave's first 16-row block (clamped into the matrix; rows is
-  // a multiple of 16). Relative to it, row d of chunk c sits in slot
+  // packed words: resources from the first 16-row block of the wave's 128-row group (clamped
+  // into the matrix; rows is a multiple of 16). Relative to it, row d of chunk c sits in slot
   // ((d / 16) nch + c) 16 + d % 16; the chunk adds 16 slots, and 32 rows (two blocks) add
   // 32 nch slots, fstep bytes of codes (32 B per slot) and, per 64 rows, of index words (16 B).
-  const int64_t wblk = (wrow0 < a.rows ? wrow0 : a.rows - 16) / 16;
+  const int64_t grow0 = row0 + 128 * grp;
+  const int64_t wblk = (grow0 < a.rows ? grow0 : a.rows - 16) / 16;
   const int64_t nblk = a.rows / 16 - wblk;
   const rsrc_t rc = make_rsrc(a.codes + wblk * nch * 128, nblk * nch * 512);
   const rsrc_t rm = make_rsrc(a.meta + wblk * nch * 64, nblk * nch * 256);
   const rsrc_t rs = make_rsrc(a.scales + wblk * nch * 16, nblk * nch * 32);
-  const uint32_t d0 = (uint32_t)(wrow0 - 16 * wblk), snch = 16u * (uint32_t)nch;
+  const uint32_t d0 = (uint32_t)(grow0 - 16 * wblk) + 32u * (uint32_t)fbase, snch = 16u * (uint32_t)nch;
   auto rel_slot = [&](uint32_t d) { return (d >> 4) * snch + (d & 15u); };
   const uint32_t fstep = 1024u * (uint32_t)nch;
-  const uint32_t co0 = rel_slot(d0 + (uint32_t)(lane & 31)) * 32u + 16u * ha;   // codes: fragment 0
-  const uint32_t mo0 = rel_slot(d0 + (uint32_t)lane) * 16u;                     // index words: rows 0..63
-  const uint32_t so0 = rel_slot(d0 + 2u * (uint32_t)lane) * 2u;                 // scales: rows 2 L, 2 L + 1
+  const uint32_t co0 = rel_slot(d0 + (uint32_t)(lane & 31)) * 32u + 16u * ha;   // codes: the wave's fragment 0
+  const uint32_t mo0 = rel_slot(d0 + (uint32_t)lane) * 16u;                     // index words: the wave's rows 0..63
+  const uint32_t so0 = rel_slot(d0 - 32u * (uint32_t)fbase + 2u * (uint32_t)lane) * 2u;   // scales: group rows 2 L, 2 L + 1
 
-  // activation chunk c -> stage c % kStagesX: wave w writes rows R w .. R w + R - 1 (R = TC / 4),
+  // activation chunk c -> stage c % kStagesX: wave w writes rows R w .. R w + R - 1 (R = kActRows),
   // four per load (lane L: row + L / 16, LDS column slot L % 16 holding column
   // (L % 16) ^ (row % 16)). Load i covers rows R w + 4 i + L / 16; with S = 16 ((L % 16) ^ (L / 16))
   // its byte offset is (R w + L / 16) 2 red + 8 i red + (S ^ 16 ((R w + 4 i) % 16)), as 2 red is a
@@ -723,18 +737,18 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   const rsrc_t rx = make_rsrc(a.act16 + m0 * a.red, brows * a.red * 2);    // the block's activation rows
   const uint32_t xo0 = (uint32_t)(Sh::kActRows * wave + lrow) * (uint32_t)a.red * 2u + 16u * (uint32_t)(lslot ^ lrow);
   const uint32_t xstep = 8u * (uint32_t)a.red;
-  const rsrc_t rg = make_rsrc(a.scales + (16 * wblk / 128) * a.red, a.red * 2);   // backward: the wave's scale row
+  const rsrc_t rg = make_rsrc(a.scales + (16 * wblk / 128) * a.red, a.red * 2);   // backward: the group's scale row
 
   auto dma_words = [&](int64_t c, int stg, uint32_t co, uint32_t mo, uint32_t so) {
     const int cc = (int)clamp_hi(c, nch - 1);
     TileWordsLds<BWD>& W = ws_at(stg);
 #pragma unroll
-    for (int fn = 0; fn < 4; ++fn)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (lds_ptr_t)&W.cw[wave][fn][0], 16, co + fn * fstep, 512 * cc, 0, 0);
+    for (int fn = 0; fn < kFn; ++fn)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, (lds_ptr_t)&W.cw[grp][fbase + fn][0], 16, co + fn * fstep, 512 * cc, 0, 0);
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rm, (lds_ptr_t)&W.mw[wave][64 * j], 16, mo + j * fstep, 256 * cc, 0, 0);
-    if (!BWD) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)&W.sw[wave][0], 4, so, 32 * cc, 0, 0);
+    for (int j = 0; j < kFn / 2; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rm, (lds_ptr_t)&W.mw[grp][32 * fbase + 64 * j], 16, mo + j * fstep, 256 * cc, 0, 0);
+    if (!BWD) __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)&W.sw[grp][0], 4, so, 32 * cc, 0, 0);
   };
   auto dma_act = [&](int64_t c, int stg, uint32_t xo) {
     const int cc = (int)clamp_hi(c, nch - 1);
@@ -744,24 +758,24 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
                                                (xo ^ (16u * ((uint32_t)(Sh::kActRows * wave + 4 * i) & 15u))) + (uint32_t)i * xstep,
                                                256 * cc, 0, 0);
     if (BWD) {
-      // the wave's scale row s16[n, g] for this chunk (g = its 128-row group), four copies
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, (lds_ptr_t)&ss_at(stg)[wave][0], 16, 16u * lslot, 256 * cc, 0, 0);
+      // the group's scale row s16[n, g] for this chunk (g = the wave's 128-row group), four copies
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rg, (lds_ptr_t)&ss_at(stg)[grp][0], 16, 16u * lslot, 256 * cc, 0, 0);
     }
   };
-  auto read_words = [&](int stg, TileWords& t) {
+  auto read_words = [&](int stg, TileWords<kFn>& t) {
     const TileWordsLds<BWD>& W = ws_at(stg);
 #pragma unroll
-    for (int fn = 0; fn < 4; ++fn) {
-      t.cw[fn] = W.cw[wave][fn][lane];
-      const u32x4_t m4 = W.mw[wave][32 * fn + (lane & 31)];
+    for (int fn = 0; fn < kFn; ++fn) {
+      t.cw[fn] = W.cw[grp][fbase + fn][lane];
+      const u32x4_t m4 = W.mw[grp][32 * (fbase + fn) + (lane & 31)];
       t.mw[fn] = ha ? u32x2_t{m4[2], m4[3]} : u32x2_t{m4[0], m4[1]};
-      t.sw[fn] = BWD ? 0u : W.sw[wave][32 * fn + (lane & 31)];
+      t.sw[fn] = BWD ? 0u : W.sw[grp][32 * (fbase + fn) + (lane & 31)];
     }
   };
   const NibbleConsts nk = nibble_consts_reg();
-  auto dequant = [&](const TileWords& t, int st, h8_t* av) {
+  auto dequant = [&](const TileWords<kFn>& t, int st, h8_t* av) {
 #pragma unroll
-    for (int fn = 0; fn < 4; ++fn)
+    for (int fn = 0; fn < kFn; ++fn)
       av[fn] = BWD ? dequant_word_int(t.cw[fn][st], nk) : dequant_word(t.cw[fn][st], splat_h2(t.sw[fn]), nk);
   };
   // B-fragment reads: fragment fm of step st reads row 32 fm + L % 32 at 16-byte column slots
@@ -770,17 +784,17 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   // 8192 fm + (bo ^ (32 st + 128)) of the stage.
   const uint32_t bo0 = 256u * (uint32_t)(lane & 31) + 16u * (uint32_t)((lane & 15) ^ ha);
 
-  f16_t acc[4][kFm];
+  f16_t acc[kFn][kFm];
 #pragma unroll
-  for (int fn = 0; fn < 4; ++fn)
+  for (int fn = 0; fn < kFn; ++fn)
 #pragma unroll
     for (int fm = 0; fm < kFm; ++fm)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[fn][fm][v] = 0.f;
 
   // words of chunk c in set c % 3 (read during chunk c - 1); A operands double-buffered by step
-  TileWords tw[3];
-  h8_t aq[2][4];
+  TileWords<kFn> tw[3];
+  h8_t aq[2][kFn];
   dma_words(0, 0, co0, mo0, so0);
   dma_act(0, 0, xo0);
   dma_words(1, 1, co0, mo0, so0);
@@ -804,8 +818,8 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
     // this chunk's copies of the base offsets (opaque, so nothing derived from them is hoisted)
     uint32_t xo = xo0, co = co0, mo = mo0, so = so0, bo = bo0;
     asm volatile("" : "+v"(xo), "+v"(co), "+v"(mo), "+v"(so), "+v"(bo));
-    const TileWords& cur = tw[z];
-    TileWords& nxt = tw[(z + 1) % 3];
+    const TileWords<kFn>& cur = tw[z];
+    TileWords<kFn>& nxt = tw[(z + 1) % 3];
 
     auto read_b = [&](int st, int fm, h16_t& bv) {
       const char* xsb = reinterpret_cast<const char*>(&xs_at(stg)[0][0]);
@@ -813,13 +827,13 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
       h8_t hi = *reinterpret_cast<const h8_t*>(xsb + (bo ^ (32u * st + 128u)) + 8192 * fm);
       if (BWD) {
         const int c16 = 2 * st + ha;
-        lo = mul_h8(lo, *reinterpret_cast<const h8_t*>(&ss_at(stg)[wave][8 * c16]));
-        hi = mul_h8(hi, *reinterpret_cast<const h8_t*>(&ss_at(stg)[wave][8 * c16 + 64]));
+        lo = mul_h8(lo, *reinterpret_cast<const h8_t*>(&ss_at(stg)[grp][8 * c16]));
+        hi = mul_h8(hi, *reinterpret_cast<const h8_t*>(&ss_at(stg)[grp][8 * c16 + 64]));
       }
       bv = cat16(lo, hi);
     };
     // Software pipeline over the four steps. The MFMAs of a step run column fragment by column
-    // fragment; once the four MFMAs of fragment fm have issued, its registers are refilled with
+    // fragment; once the kFn MFMAs of fragment fm have issued, its registers are refilled with
     // the next step's fragment fm (one B buffer), while the next step's dequantised weights go to
     // the other A buffer. During the last step the next chunk's words are read and its first step
     // dequantised.
@@ -830,7 +844,7 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
     for (int st = 0; st < 4; ++st) {
       // direct loads into the stages read in chunk c - 1 (chunk c + kAhead's activations, chunk
       // c + 2's words) during steps 0 and 1, one load after each MFMA (issued in a burst at the
-      // barrier, the four waves' loads would fill the address unit's queue and stall issue)
+      // barrier, the waves' loads would fill the address unit's queue and stall issue)
       if (st == (Ct::kActFirst ? 0 : 1)) dma_act(c + Sh::kAhead, (stg + Sh::kAhead) % kStagesX, xo);
       if (st == (Ct::kActFirst ? 1 : 0)) dma_words(c + 2, (z + 2) % 3, co, mo, so);
       if (st < 3) {
@@ -843,7 +857,7 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
 #pragma unroll
       for (int fm = 0; fm < kFm; ++fm) {
 #pragma unroll
-        for (int fn = 0; fn < 4; ++fn)
+        for (int fn = 0; fn < kFn; ++fn)
           acc[fn][fm] = smfmac32(aq[st & 1][fn], bq[fm], acc[fn][fm], (int)cur.mw[fn][st >> 1], st & 1);
         if (st < 3) read_b(st + 1, fm, bq[fm]);
       }
@@ -852,12 +866,12 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
       // are read at the start of the last step)
       const int nvm = st == 0 ? (Ct::kActFirst ? Ct::kAct : Ct::kWords) : st == 1 ? (Ct::kActFirst ? Ct::kWords : Ct::kAct) : 0;
 #pragma unroll
-      for (int i = 0; i < 4 * kFm; ++i) {
-        if (st == 3 && i < 6) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);   // DS read
+      for (int i = 0; i < kFn * kFm; ++i) {
+        if (st == 3 && i < 3 * kFn / 2) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);   // DS read
         __builtin_amdgcn_sched_group_barrier(0x0008, 1, 0);                          // MFMA
         if (i < nvm) __builtin_amdgcn_sched_group_barrier(0x0020, 1, 0);             // VMEM read
         __builtin_amdgcn_sched_group_barrier(0x0002, 4, 0);                          // VALU
-        if (st < 3 && i % 4 == 3) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);   // DS read
+        if (st < 3 && i % kFn == kFn - 1) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);   // DS read
       }
     }
   };
@@ -900,17 +914,17 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
     const int64_t nj = a.r / 16;
     const rsrc_t rp = make_rsrc(a.ad_pb, (a.rows + 31) / 32 * 32 * a.r * 2), rt = make_rsrc(a.tm, (a.M + 31) / 32 * 32 * a.r * 2);
     const uint32_t lo16 = 32u * (uint32_t)(lane & 31) + 16u * ha;   // the lane's bytes within a 1 KB tile
-    uint32_t po[4], to[kFm];
+    uint32_t po[kFn], to[kFm];
 #pragma unroll
-    for (int fn = 0; fn < 4; ++fn) po[fn] = (uint32_t)((wrow0 + 32 * fn) / 32 * nj) * 1024u + lo16;
+    for (int fn = 0; fn < kFn; ++fn) po[fn] = (uint32_t)((wrow0 + 32 * fn) / 32 * nj) * 1024u + lo16;
 #pragma unroll
     for (int fm = 0; fm < kFm; ++fm) to[fm] = (uint32_t)((m0 + 32 * fm) / 32 * nj) * 1024u + lo16;
-    struct AdRegs { u32x4_t pa[4], pb[kFm]; };
+    struct AdRegs { u32x4_t pa[kFn], pb[kFm]; };
     AdRegs ar[4];
     auto ad_load = [&](int64_t t, AdRegs& R) {
       const int so = (int)(clamp_hi(t, nj - 1) * 1024);
 #pragma unroll
-      for (int fn = 0; fn < 4; ++fn) R.pa[fn] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, po[fn], so, 0));
+      for (int fn = 0; fn < kFn; ++fn) R.pa[fn] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, po[fn], so, 0));
 #pragma unroll
       for (int fm = 0; fm < kFm; ++fm) R.pb[fm] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rt, to[fm], so, 0));
     };
@@ -921,15 +935,15 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
       constexpr int u = decltype(uc)::value;
       ad_load(t + 3, ar[(u + 3) % 4]);
       // step t's loads have landed once only the three later steps' loads are outstanding
-      __builtin_amdgcn_s_waitcnt(vmcnt_wait(3 * (4 + kFm)));
+      __builtin_amdgcn_s_waitcnt(vmcnt_wait(3 * (kFn + kFm)));
       AdRegs& R = ar[u];
 #pragma unroll
-      for (int fn = 0; fn < 4; ++fn) asm volatile("" : "+v"(R.pa[fn]));
+      for (int fn = 0; fn < kFn; ++fn) asm volatile("" : "+v"(R.pa[fn]));
 #pragma unroll
       for (int fm = 0; fm < kFm; ++fm) asm volatile("" : "+v"(R.pb[fm]));
       if (t < nj) {
 #pragma unroll
-        for (int fn = 0; fn < 4; ++fn)
+        for (int fn = 0; fn < kFn; ++fn)
 #pragma unroll
           for (int fm = 0; fm < kFm; ++fm)
             acc[fn][fm] = mfma32(__builtin_bit_cast(h8_t, R.pa[fn]), __builtin_bit_cast(h8_t, R.pb[fm]), acc[fn][fm]);
@@ -952,7 +966,7 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
     if (m >= a.M) continue;
     const float inv = a.rowinv ? a.rowinv[m] : 1.0f;
 #pragma unroll
-    for (int fn = 0; fn < 4; ++fn)
+    for (int fn = 0; fn < kFn; ++fn)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int64_t rr = wrow0 + 32 * fn + 8 * q + 4 * ha;
@@ -964,9 +978,9 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   }
 }
 
-template <bool BWD, int TC>
-__global__ void __launch_bounds__(kTThreads) k_tile(LayerArgs a) {
-  tile_body<BWD, TC>(a);
+template <bool BWD, int TC, int WR>
+__global__ void __launch_bounds__(64 * (kTR / WR)) k_tile(LayerArgs a) {
+  tile_body<BWD, TC, WR>(a);
 }
 
 // Large-M activation preparation, one block per row m of act [M, red] (bf16 or fp16): the row's
@@ -1201,8 +1215,12 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
   dim3 grid((unsigned)(8 * ((p.sp_row_tiles * p.sp_col_tiles + 7) / 8)));
-  if (p.sp_cols_tile == 128) SLIM_LAUNCH(timer, (k_tile<BWD, 128>), grid, dim3(kTThreads), s, a);
-  else SLIM_LAUNCH(timer, (k_tile<BWD, 96>), grid, dim3(kTThreads), s, a);
+  // 64-row waves only for the forward's 512 x 128 tiles (the plan's choice)
+  if (!BWD && p.sp_wave_rows == 64 && p.sp_cols_tile == 128)
+    SLIM_LAUNCH(timer, (k_tile<false, 128, 64>), grid, dim3(TileShape<128, 64>::kThreads), s, a);
+  else if (p.sp_wave_rows != 128) return SLIM_EUNSUPPORTED;
+  else if (p.sp_cols_tile == 128) SLIM_LAUNCH(timer, (k_tile<BWD, 128, 128>), grid, dim3(TileShape<128, 128>::kThreads), s, a);
+  else SLIM_LAUNCH(timer, (k_tile<BWD, 96, 128>), grid, dim3(TileShape<96, 128>::kThreads), s, a);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }
 

@@ -114,6 +114,16 @@ def test_tile_kernel_wide_tiles_ragged_m():
     _fwd_case(11008, 2048, 48, 1400, rows=rows, ms=ms, name="wide")
 
 
+def test_tile_kernel_eight_waves_ragged_rows():
+    # 512 x 128 forward tiles run 8 waves of 64 rows: 2064 rows leave 16 in the last row tile, so
+    # one wave there holds 16 rows and seven hold none; 128 column tiles
+    rows = np.unique(np.concatenate([synth.stream(7, "rows").choice(2064, size=200, replace=False),
+                                     np.arange(2040, 2064)]))
+    ms = np.unique(np.concatenate([synth.stream(7, "ms").choice(16384, size=40, replace=False),
+                                   np.arange(16380, 16384)]))
+    _fwd_case(2064, 256, 32, 16384, rows=rows, ms=ms, name="w8")
+
+
 @pytest.mark.parametrize("n,k,r,m", [(256, 33024, 512, 1900), (128, 16384, 512, 4096)])
 def test_adapter_gemm_wide_tiles(n, k, r, m):
     # the 256 x 256 adapter GEMM takes shapes whose 256 x 256 tiles times reduction splits of at least
