@@ -625,28 +625,19 @@ template <int TC, int WR> struct TileShape {
 // scale-row load) and packed words (WR / 32 code loads, WR / 64 index word loads, and in the
 // forward 1 scale load).
 // kAhead 2: chunk c issues chunk c + 2's words in its first step and chunk c + 2's activations in
-// its second.
-//  * at the top of chunk c its words and activations must have landed: only chunk c + 1's loads
-//    may still be outstanding;
-//  * in the last step of chunk c, chunk c + 1's words must have landed: only chunk c + 1's
-//    activations and chunk c + 2's loads may still be outstanding.
-// kAhead 1: chunk c issues chunk c + 1's activations in its first step and chunk c + 2's words in
-// its second.
-//  * at the top of chunk c its activations and words must have landed: only chunk c + 1's words
-//    (issued after chunk c's activations) may still be outstanding;
-//  * in the last step of chunk c, chunk c + 1's words must have landed: only chunk c + 1's
-//    activations and chunk c + 2's words may still be outstanding.
-// The prologue issues the loads of the chunks before in the same order, so the same counts hold
-// from the start.
+// its second; kAhead 1: chunk c + 1's activations in its first step and chunk c + 2's words in its
+// second. The one barrier of chunk c opens its last step, after which the wave reads chunk c + 1's
+// words and first B fragments: there chunk c + 1 must have landed, so only the loads chunk c
+// issued for chunk c + 2 may still be outstanding (kTop). The prologue issues the loads of chunks
+// 0 and 1 in the same order and waits with the same count before a barrier of its own.
 template <bool BWD, int TC, int WR> struct TileCounts {
   static constexpr bool kActFirst = TileShape<TC, WR>::kAhead == 1;
   static constexpr int kWords = WR / 32 + WR / 64 + (BWD ? 0 : 1);
   static constexpr int kAct = TileShape<TC, WR>::kActLoads + (BWD ? 1 : 0);
   static constexpr int kTop = kActFirst ? kWords : kAct + kWords;
-  static constexpr int kNext = kActFirst ? kAct + kWords : kAct + kWords + kAct;
 };
 
-static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && TileCounts<true, 128, 128>::kNext < 64, "s_waitcnt encoding");
+static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && TileCounts<true, 96, 128>::kTop < 64, "s_waitcnt encoding");
 static_assert(vmcnt_lgkm0_wait(20) == 0x4074u, "s_waitcnt encoding");
 
 
@@ -795,51 +786,51 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   // words of chunk c in set c % 3 (read during chunk c - 1); A operands double-buffered by step
   TileWords<kFn> tw[3];
   h8_t aq[2][kFn];
+  // B fragment fm of step st from activation stage xstg
+  auto read_b = [&](int xstg, int st, int fm, uint32_t bo, h16_t& bv) {
+    const char* xsb = reinterpret_cast<const char*>(&xs_at(xstg)[0][0]);
+    h8_t lo = *reinterpret_cast<const h8_t*>(xsb + (bo ^ (32u * st)) + 8192 * fm);
+    h8_t hi = *reinterpret_cast<const h8_t*>(xsb + (bo ^ (32u * st + 128u)) + 8192 * fm);
+    if (BWD) {
+      const int c16 = 2 * st + ha;
+      lo = mul_h8(lo, *reinterpret_cast<const h8_t*>(&ss_at(xstg)[grp][8 * c16]));
+      hi = mul_h8(hi, *reinterpret_cast<const h8_t*>(&ss_at(xstg)[grp][8 * c16 + 64]));
+    }
+    bv = cat16(lo, hi);
+  };
+  // one B buffer, refilled fragment by fragment (below)
+  h16_t bq[kFm];
+
   dma_words(0, 0, co0, mo0, so0);
   dma_act(0, 0, xo0);
   dma_words(1, 1, co0, mo0, so0);
   if (!Ct::kActFirst) dma_act(1, 1, xo0);
-  __builtin_amdgcn_s_waitcnt(vmcnt_wait(Ct::kNext));   // chunk 0's words
+  // chunk 0 has landed once only chunk 1's loads are outstanding; the other waves brought in
+  // part of it. The barrier is issued as a bare instruction: the builtin would also make this
+  // wave wait for every direct-to-LDS load in flight, including the ones for the next chunk.
+  __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(Ct::kTop));
+  asm volatile("s_barrier" ::: "memory");
   read_words(0, tw[0]);
   dequant(tw[0], 0, aq[0]);
+#pragma unroll
+  for (int fm = 0; fm < kFm; ++fm) read_b(0, 0, fm, bo0, bq[fm]);
 
   auto chunk = [&](int64_t c, auto zc, auto xc) {
     constexpr int z = decltype(zc)::value;    // c % 3: word stage and register set
     constexpr int stg = decltype(xc)::value;  // c % kStagesX: activation stage
     // Nothing of the previous chunk is scheduled past this point.
     __builtin_amdgcn_sched_barrier(0);
-    // chunk c's activations have landed once only chunk c - 1's loads are outstanding; and this
-    // wave's LDS reads of the stage refilled below have returned (lgkmcnt 0), so after the
-    // barrier no wave still reads it.
-    // The barrier is issued as a bare instruction: the builtin would also make this wave wait
-    // for every direct-to-LDS load in flight, including the ones for the next chunk.
-    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(Ct::kTop));
-    asm volatile("s_barrier" ::: "memory");
     // this chunk's copies of the base offsets (opaque, so nothing derived from them is hoisted)
     uint32_t xo = xo0, co = co0, mo = mo0, so = so0, bo = bo0;
     asm volatile("" : "+v"(xo), "+v"(co), "+v"(mo), "+v"(so), "+v"(bo));
     const TileWords<kFn>& cur = tw[z];
     TileWords<kFn>& nxt = tw[(z + 1) % 3];
-
-    auto read_b = [&](int st, int fm, h16_t& bv) {
-      const char* xsb = reinterpret_cast<const char*>(&xs_at(stg)[0][0]);
-      h8_t lo = *reinterpret_cast<const h8_t*>(xsb + (bo ^ (32u * st)) + 8192 * fm);
-      h8_t hi = *reinterpret_cast<const h8_t*>(xsb + (bo ^ (32u * st + 128u)) + 8192 * fm);
-      if (BWD) {
-        const int c16 = 2 * st + ha;
-        lo = mul_h8(lo, *reinterpret_cast<const h8_t*>(&ss_at(stg)[grp][8 * c16]));
-        hi = mul_h8(hi, *reinterpret_cast<const h8_t*>(&ss_at(stg)[grp][8 * c16 + 64]));
-      }
-      bv = cat16(lo, hi);
-    };
     // Software pipeline over the four steps. The MFMAs of a step run column fragment by column
     // fragment; once the kFn MFMAs of fragment fm have issued, its registers are refilled with
-    // the next step's fragment fm (one B buffer), while the next step's dequantised weights go to
-    // the other A buffer. During the last step the next chunk's words are read and its first step
-    // dequantised.
-    h16_t bq[kFm];
-#pragma unroll
-    for (int fm = 0; fm < kFm; ++fm) read_b(0, fm, bq[fm]);
+    // the next step's fragment fm, while the next step's dequantised weights go to the other A
+    // buffer. The chunk's one barrier opens its last step: after it the next chunk's words are
+    // read and its first step dequantised, and its first B fragments are read during this step's
+    // MFMAs (step 0 of a chunk then starts without waiting on LDS).
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
       // direct loads into the stages read in chunk c - 1 (chunk c + kAhead's activations, chunk
@@ -850,7 +841,14 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
       if (st < 3) {
         dequant(cur, st + 1, aq[(st + 1) & 1]);
       } else {
-        __builtin_amdgcn_s_waitcnt(vmcnt_wait(Ct::kNext));   // chunk c + 1's words
+        // chunk c + 1 has landed once only chunk c + 2's loads are outstanding, and this wave's
+        // reads of chunk c's activation stage (the last ones, for this step, were issued in the
+        // step before) have returned (lgkmcnt 0): after the barrier no wave reads that stage, and
+        // the next chunk's direct loads may refill it.
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(Ct::kTop));
+        asm volatile("s_barrier" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
         read_words((z + 1) % 3, nxt);
         dequant(nxt, 0, aq[0]);
       }
@@ -859,11 +857,12 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
 #pragma unroll
         for (int fn = 0; fn < kFn; ++fn)
           acc[fn][fm] = smfmac32(aq[st & 1][fn], bq[fm], acc[fn][fm], (int)cur.mw[fn][st >> 1], st & 1);
-        if (st < 3) read_b(st + 1, fm, bq[fm]);
+        if (st < 3) read_b(stg, st + 1, fm, bo, bq[fm]);
+        else read_b((stg + 1) % kStagesX, 0, fm, bo, bq[fm]);
       }
       // interleave: each MFMA followed by a share of the VALU work and, in steps 0 and 1, by one
-      // direct load; the LDS reads of fragment fm follow its four MFMAs (the next chunk's words
-      // are read at the start of the last step)
+      // direct load; the LDS reads of fragment fm follow its MFMAs (in the last step the next
+      // chunk's words are read first)
       const int nvm = st == 0 ? (Ct::kActFirst ? Ct::kAct : Ct::kWords) : st == 1 ? (Ct::kActFirst ? Ct::kWords : Ct::kAct) : 0;
 #pragma unroll
       for (int i = 0; i < kFn * kFm; ++i) {
@@ -871,7 +870,7 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
         __builtin_amdgcn_sched_group_barrier(0x0008, 1, 0);                          // MFMA
         if (i < nvm) __builtin_amdgcn_sched_group_barrier(0x0020, 1, 0);             // VMEM read
         __builtin_amdgcn_sched_group_barrier(0x0002, 4, 0);                          // VALU
-        if (st < 3 && i % kFn == kFn - 1) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);   // DS read
+        if (i % kFn == kFn - 1) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);   // DS read
       }
     }
   };
