@@ -1214,12 +1214,13 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
   dim3 grid((unsigned)(8 * ((p.sp_row_tiles * p.sp_col_tiles + 7) / 8)));
-  // 64-row waves only for the forward's 512 x 128 tiles (the plan's choice)
-  if (!BWD && p.sp_wave_rows == 64 && p.sp_cols_tile == 128)
-    SLIM_LAUNCH(timer, (k_tile<false, 128, 64>), grid, dim3(TileShape<128, 64>::kThreads), s, a);
-  else if (p.sp_wave_rows != 128) return SLIM_EUNSUPPORTED;
-  else if (p.sp_cols_tile == 128) SLIM_LAUNCH(timer, (k_tile<BWD, 128, 128>), grid, dim3(TileShape<128, 128>::kThreads), s, a);
-  else SLIM_LAUNCH(timer, (k_tile<BWD, 96, 128>), grid, dim3(TileShape<96, 128>::kThreads), s, a);
+  if (p.sp_wave_rows == 64) {
+    if (p.sp_cols_tile == 128) SLIM_LAUNCH(timer, (k_tile<BWD, 128, 64>), grid, dim3(TileShape<128, 64>::kThreads), s, a);
+    else SLIM_LAUNCH(timer, (k_tile<BWD, 96, 64>), grid, dim3(TileShape<96, 64>::kThreads), s, a);
+  } else {
+    if (p.sp_cols_tile == 128) SLIM_LAUNCH(timer, (k_tile<BWD, 128, 128>), grid, dim3(TileShape<128, 128>::kThreads), s, a);
+    else SLIM_LAUNCH(timer, (k_tile<BWD, 96, 128>), grid, dim3(TileShape<96, 128>::kThreads), s, a);
+  }
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }
 

@@ -115,13 +115,13 @@ def test_tile_kernel_wide_tiles_ragged_m():
 
 
 def test_tile_kernel_eight_waves_ragged_rows():
-    # 512 x 128 forward tiles run 8 waves of 64 rows: 2064 rows leave 16 in the last row tile, so
-    # one wave there holds 16 rows and seven hold none; 128 column tiles
+    # reductions of 5120 and more run 8 waves of 64 rows: 2064 rows leave 16 in the last row tile,
+    # so one wave there holds 16 rows and seven hold none; 128 column tiles of 128
     rows = np.unique(np.concatenate([synth.stream(7, "rows").choice(2064, size=200, replace=False),
                                      np.arange(2040, 2064)]))
     ms = np.unique(np.concatenate([synth.stream(7, "ms").choice(16384, size=40, replace=False),
                                    np.arange(16380, 16384)]))
-    _fwd_case(2064, 256, 32, 16384, rows=rows, ms=ms, name="w8")
+    _fwd_case(2064, 5120, 32, 16384, rows=rows, ms=ms, name="w8")
 
 
 @pytest.mark.parametrize("n,k,r,m", [(256, 33024, 512, 1900), (128, 16384, 512, 4096)])
