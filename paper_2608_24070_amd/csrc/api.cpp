@@ -115,11 +115,6 @@ int slim_make_plan(bool bwd, int64_t M, int64_t N, int64_t K, int64_t r, SlimPla
     const int64_t r96 = cdiv(q.sp_row_tiles * cdiv(M, 96), 256), r128 = cdiv(q.sp_row_tiles * cdiv(M, 128), 256);
     q.sp_cols_tile = 112 * r128 <= 100 * r96 ? 128 : 96;
     q.sp_col_tiles = cdiv(M, q.sp_cols_tile);
-    // 8 waves of 64 rows (two per SIMD) for reductions of at least 40 chunks, 4 waves of 128 rows
-    // below: measured with the barrier opening each chunk's last step, the 70B backward at M 8192
-    // took 2217 -> 2112 us and the 13B block's tile kernels 269 -> 261 us, but prefill
-    // (reduction 4096, with r 384 a heavier share of per-tile work) 144.5 -> 148 us
-    q.sp_wave_rows = red >= 5120 ? 64 : 128;
     q.sp_split = 1;
     q.sp_chunks_per_split = nchunks;
     // 256 x 256 adapter tiles (half the operand bytes per flop) with a 128 KiB ring, one block per

@@ -36,7 +36,6 @@ struct SlimPlan {
   int dec_fm = 1;                     // 16-column fragments per wave in the small-M kernel
   int dec_g = 1;                      // quantisation groups per lane group in a small-M sparse unit
   int sp_rows_tile = 0, sp_cols_tile = 0;  // output tile (rows of W or W^T, columns = M)
-  int sp_wave_rows = 128;                  // large M: rows per wave of the tile kernel (128: 4 waves, 64: 8)
   int64_t sp_row_tiles = 0, sp_col_tiles = 0;
   int sp_split = 1;                   // reduction splits (small-M kernel only)
   int dec_units = 1;                  // small M: row tiles per sparse block

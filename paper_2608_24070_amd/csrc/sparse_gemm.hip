@@ -593,10 +593,10 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
 // WR x TC accumulator (in the accumulation registers) on 32x32x32 sparse MFMA. Each dequantised
 // weight fragment feeds TC / 32 MFMAs and no weight row is dequantised by two waves; the wider
 // tile spends less dequantisation per MFMA, the narrower one gives more tiles to even out the
-// last round of blocks (the plan picks per shape). WR = 128 runs one wave per SIMD (4 waves,
-// 128 x TC accumulators); WR = 64 runs two (8 waves, half the accumulators each), so that one
-// wave's dequantisation, LDS reads and waits overlap the other's MFMAs, at twice the B-fragment
-// reads from LDS.
+// last round of blocks (the plan picks per shape). WR = 64 (the launched form) runs two waves per
+// SIMD (8 waves, 64 x TC accumulators each), so that one wave's dequantisation, LDS reads and
+// waits overlap the other's MFMAs, at twice the B-fragment reads from LDS; WR = 128 runs one (4
+// waves, 128 x TC accumulators).
 // Per 128-wide reduction chunk, the tile's packed words (codes, index words and scales of its
 // 512 rows, in four 128-row groups) and the fp16 activation tile [TC x 128] go straight from
 // memory to LDS (direct loads), so no register holds data still in flight: the words into a ring of three stages, two
@@ -637,7 +637,7 @@ template <bool BWD, int TC, int WR> struct TileCounts {
   static constexpr int kTop = kActFirst ? kWords : kAct + kWords;
 };
 
-static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && TileCounts<true, 96, 128>::kTop < 64, "s_waitcnt encoding");
+static_assert(vmcnt_wait(40) == 0x8F78u && vmcnt_wait(5) == 0x0F75u && TileCounts<true, 96, 64>::kTop < 64, "s_waitcnt encoding");
 static_assert(vmcnt_lgkm0_wait(20) == 0x4074u, "s_waitcnt encoding");
 
 
@@ -904,56 +904,99 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
 
   // adapter second product: out^T[row, m] += sum_j P[row, j] tm[m, j], on 32x32x16 fp16 MFMA.
   // Both operands are in 32 x 16 tiles (P re-laid and tm finished by k_adapter_finish, or tm
-  // written so by the adapter GEMM): step t (ranks [16 t, 16 t + 16), r a multiple of 16) of one 32-row fragment is 1 KB of
-  // contiguous memory, lane (L % 32, L / 32) reading row L % 32, ranks 8 (L / 32) ... + 7. The
-  // operands of step t are loaded three steps ahead into a ring of four register sets (the loop is
-  // unrolled by four; loads past the last step repeat it and are not used). Fragments past the
-  // tiled extent read zero; their results are not stored.
+  // written so by the adapter GEMM): step t (ranks [16 t, 16 t + 16), r a multiple of 16) of one
+  // 32-row fragment is 1 KB of contiguous memory, lane (L % 32, L / 32) reading row L % 32, ranks
+  // 8 (L / 32) ... + 7. Each wave loads its own rows of P straight into registers, three steps
+  // ahead into a ring of four register sets. tm, which every wave needs for all TC columns, comes
+  // through LDS: groups of eight steps (kFm x 8 tiles, the size of one activation stage) go to the
+  // activation stages in turn by direct loads one group ahead, spread over the waves, and each
+  // wave reads its fragments there. Loads past the last step repeat it and are not used;
+  // fragments past the tiled extent read zero and their results are not stored.
   if (a.r > 0) {
-    const int64_t nj = a.r / 16;
+    const int64_t nj = a.r / 16, ngrp = (nj + 7) / 8;
     const rsrc_t rp = make_rsrc(a.ad_pb, (a.rows + 31) / 32 * 32 * a.r * 2), rt = make_rsrc(a.tm, (a.M + 31) / 32 * 32 * a.r * 2);
     const uint32_t lo16 = 32u * (uint32_t)(lane & 31) + 16u * ha;   // the lane's bytes within a 1 KB tile
-    uint32_t po[kFn], to[kFm];
+    uint32_t po[kFn];
 #pragma unroll
     for (int fn = 0; fn < kFn; ++fn) po[fn] = (uint32_t)((wrow0 + 32 * fn) / 32 * nj) * 1024u + lo16;
+    // tm tiles of a group per wave: tile q = 8 fm + (step % 8) goes to byte 1024 q of the stage
+    constexpr int kTT = kFm * 8 / Sh::kWaves;
+    static_assert(kTT * Sh::kWaves == kFm * 8, "tm tiles of a group spread evenly over the waves");
+    auto dma_t = [&](int64_t g, int stg) {
+      char* dst = reinterpret_cast<char*>(&xs_at(stg)[0][0]);
 #pragma unroll
-    for (int fm = 0; fm < kFm; ++fm) to[fm] = (uint32_t)((m0 + 32 * fm) / 32 * nj) * 1024u + lo16;
-    struct AdRegs { u32x4_t pa[kFn], pb[kFm]; };
+      for (int i = 0; i < kTT; ++i) {
+        // the tile row's offset per lane (rows past M lie beyond the resource's extent and read
+        // zero), the step's within that row as the uniform offset
+        const int q = wave + Sh::kWaves * i, fm = q >> 3;
+        const int64_t t = clamp_hi(8 * g + (q & 7), nj - 1);
+        const uint32_t vo = (uint32_t)((m0 + 32 * fm) / 32 * nj) * 1024u + 16u * (uint32_t)lane;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rt, (lds_ptr_t)(dst + 1024 * q), 16, vo, (int)(t * 1024), 0, 0);
+      }
+    };
+    struct AdRegs { u32x4_t pa[kFn]; };
     AdRegs ar[4];
     auto ad_load = [&](int64_t t, AdRegs& R) {
       const int so = (int)(clamp_hi(t, nj - 1) * 1024);
 #pragma unroll
       for (int fn = 0; fn < kFn; ++fn) R.pa[fn] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rp, po[fn], so, 0));
-#pragma unroll
-      for (int fm = 0; fm < kFm; ++fm) R.pb[fm] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rt, to[fm], so, 0));
     };
+    // every wave is done with the ring (its reads returned, its direct loads landed) before the
+    // first group overwrites a stage
+    asm volatile("s_barrier" ::: "memory");
+    dma_t(0, 0);
     ad_load(0, ar[0]);
     ad_load(1, ar[1]);
     ad_load(2, ar[2]);
-    auto ad_step = [&](int64_t t, auto uc) {
-      constexpr int u = decltype(uc)::value;
-      ad_load(t + 3, ar[(u + 3) % 4]);
-      // step t's loads have landed once only the three later steps' loads are outstanding
-      __builtin_amdgcn_s_waitcnt(vmcnt_wait(3 * (kFn + kFm)));
-      AdRegs& R = ar[u];
+    // group 0 has landed once only the three steps of P loads issued after it are outstanding
+    __builtin_amdgcn_s_waitcnt(vmcnt_wait(3 * kFn));
+    asm volatile("s_barrier" ::: "memory");
+    // step t = 8 g + tt of group g (stage xstg); group g + 1 was issued at the group's start, after
+    // step g 8 + 2's P loads and before step 8 g + 3's
+    auto ad_step = [&](int64_t g, auto ttc, int xstg) {
+      constexpr int tt = decltype(ttc)::value;
+      const int64_t t = 8 * g + tt;
+      ad_load(t + 3, ar[(tt + 3) % 4]);
+      __builtin_amdgcn_s_waitcnt(vmcnt_wait(3 * kFn + (tt < 3 ? kTT : 0)));
+      AdRegs& R = ar[tt % 4];
 #pragma unroll
       for (int fn = 0; fn < kFn; ++fn) asm volatile("" : "+v"(R.pa[fn]));
+      const char* src = reinterpret_cast<const char*>(&xs_at(xstg)[0][0]);
+      h8_t tb[kFm];
 #pragma unroll
-      for (int fm = 0; fm < kFm; ++fm) asm volatile("" : "+v"(R.pb[fm]));
+      for (int fm = 0; fm < kFm; ++fm) tb[fm] = *reinterpret_cast<const h8_t*>(src + 1024 * (8 * fm + tt) + lo16);
       if (t < nj) {
 #pragma unroll
         for (int fn = 0; fn < kFn; ++fn)
 #pragma unroll
           for (int fm = 0; fm < kFm; ++fm)
-            acc[fn][fm] = mfma32(__builtin_bit_cast(h8_t, R.pa[fn]), __builtin_bit_cast(h8_t, R.pb[fm]), acc[fn][fm]);
+            acc[fn][fm] = mfma32(__builtin_bit_cast(h8_t, R.pa[fn]), tb[fm], acc[fn][fm]);
       }
     };
-    for (int64_t t0 = 0; t0 < nj; t0 += 4) {
-      ad_step(t0, std::integral_constant<int, 0>{});
-      ad_step(t0 + 1, std::integral_constant<int, 1>{});
-      ad_step(t0 + 2, std::integral_constant<int, 2>{});
-      ad_step(t0 + 3, std::integral_constant<int, 3>{});
+    auto group = [&](int64_t g, int xstg) {
+      // the next group into the next stage (read two or three groups ago, before the last
+      // barrier); issued also after the last group, whose repeats land in a stage no wave reads
+      dma_t(g + 1, (xstg + 1) % kStagesX);
+      ad_step(g, std::integral_constant<int, 0>{}, xstg);
+      ad_step(g, std::integral_constant<int, 1>{}, xstg);
+      ad_step(g, std::integral_constant<int, 2>{}, xstg);
+      ad_step(g, std::integral_constant<int, 3>{}, xstg);
+      ad_step(g, std::integral_constant<int, 4>{}, xstg);
+      ad_step(g, std::integral_constant<int, 5>{}, xstg);
+      ad_step(g, std::integral_constant<int, 6>{}, xstg);
+      ad_step(g, std::integral_constant<int, 7>{}, xstg);
+      // this wave's reads of the stage have returned and the next group has landed (waited for
+      // at step 3): after the barrier the stage may be refilled and the next group read
+      __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_wait(3 * kFn));
+      asm volatile("s_barrier" ::: "memory");
+    };
+    int64_t g = 0;
+    for (; g + kStagesX <= ngrp; g += kStagesX) {
+      group(g, 0);
+      group(g + 1, 1);
+      if constexpr (kStagesX == 3) group(g + 2, 2);
     }
+    for (int xstg = 0; g < ngrp; ++g, ++xstg) group(g, xstg);
     __builtin_amdgcn_s_waitcnt(0);
   }
 
@@ -1214,13 +1257,10 @@ int launch_layer(const LayerArgs& a, const SlimPlan& p, const uint16_t* act, int
   }
   SlimKernelTimer timer(BWD ? "tile_bwd" : "tile_fwd", s);
   dim3 grid((unsigned)(8 * ((p.sp_row_tiles * p.sp_col_tiles + 7) / 8)));
-  if (p.sp_wave_rows == 64) {
-    if (p.sp_cols_tile == 128) SLIM_LAUNCH(timer, (k_tile<BWD, 128, 64>), grid, dim3(TileShape<128, 64>::kThreads), s, a);
-    else SLIM_LAUNCH(timer, (k_tile<BWD, 96, 64>), grid, dim3(TileShape<96, 64>::kThreads), s, a);
-  } else {
-    if (p.sp_cols_tile == 128) SLIM_LAUNCH(timer, (k_tile<BWD, 128, 128>), grid, dim3(TileShape<128, 128>::kThreads), s, a);
-    else SLIM_LAUNCH(timer, (k_tile<BWD, 96, 128>), grid, dim3(TileShape<96, 128>::kThreads), s, a);
-  }
+  // 8 waves of 64 rows (the kernel also builds with 4 of 128, one wave per SIMD, which measured
+  // slower on every workload once tm came through LDS)
+  if (p.sp_cols_tile == 128) SLIM_LAUNCH(timer, (k_tile<BWD, 128, 64>), grid, dim3(TileShape<128, 64>::kThreads), s, a);
+  else SLIM_LAUNCH(timer, (k_tile<BWD, 96, 64>), grid, dim3(TileShape<96, 64>::kThreads), s, a);
   return hipGetLastError() == hipSuccess ? SLIM_OK : SLIM_EDEVICE;
 }
 

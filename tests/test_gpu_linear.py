@@ -115,8 +115,8 @@ def test_tile_kernel_wide_tiles_ragged_m():
 
 
 def test_tile_kernel_eight_waves_ragged_rows():
-    # reductions of 5120 and more run 8 waves of 64 rows: 2064 rows leave 16 in the last row tile,
-    # so one wave there holds 16 rows and seven hold none; 128 column tiles of 128
+    # the tile kernel runs 8 waves of 64 rows: 2064 rows leave 16 in the last row tile, so one wave
+    # there holds 16 rows and seven hold none; 128 column tiles of 128
     rows = np.unique(np.concatenate([synth.stream(7, "rows").choice(2064, size=200, replace=False),
                                      np.arange(2040, 2064)]))
     ms = np.unique(np.concatenate([synth.stream(7, "ms").choice(16384, size=40, replace=False),
