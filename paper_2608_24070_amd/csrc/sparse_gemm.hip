@@ -927,10 +927,13 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
 #pragma unroll
       for (int i = 0; i < kTT; ++i) {
         // the tile row's offset per lane (rows past M lie beyond the resource's extent and read
-        // zero), the step's within that row as the uniform offset
+        // zero), the step's within that row as the uniform offset. Lane L fetches the 16 bytes
+        // that lane L of a fragment read needs (lo16) and lays them at 16 L, so the read of a
+        // fragment is 1 KB in lane order (a read at lo16 would put lanes L and L + 8 of one
+        // 16-lane pass in the same bank).
         const int q = wave + Sh::kWaves * i, fm = q >> 3;
         const int64_t t = clamp_hi(8 * g + (q & 7), nj - 1);
-        const uint32_t vo = (uint32_t)((m0 + 32 * fm) / 32 * nj) * 1024u + 16u * (uint32_t)lane;
+        const uint32_t vo = (uint32_t)((m0 + 32 * fm) / 32 * nj) * 1024u + lo16;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rt, (lds_ptr_t)(dst + 1024 * q), 16, vo, (int)(t * 1024), 0, 0);
       }
     };
@@ -964,7 +967,7 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
       const char* src = reinterpret_cast<const char*>(&xs_at(xstg)[0][0]);
       h8_t tb[kFm];
 #pragma unroll
-      for (int fm = 0; fm < kFm; ++fm) tb[fm] = *reinterpret_cast<const h8_t*>(src + 1024 * (8 * fm + tt) + lo16);
+      for (int fm = 0; fm < kFm; ++fm) tb[fm] = *reinterpret_cast<const h8_t*>(src + 1024 * (8 * fm + tt) + 16 * lane);
       if (t < nj) {
 #pragma unroll
         for (int fn = 0; fn < kFn; ++fn)
