@@ -43,8 +43,16 @@ k_adapter_gemm(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const uint
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wr = wave >> 1, ha = lane >> 5;
-  const int64_t m0 = (int64_t)blockIdx.x * kT, j0 = (int64_t)blockIdx.y * kT;
-  const int s = blockIdx.z;
+  // XCD-aware order: block b runs on XCD b % 8 (workgroups are dealt round robin), and XCD x takes
+  // positions [x Q, (x + 1) Q) of an order that walks splits, then m tiles, then j tiles, so that the
+  // blocks of one XCD share one split's slice of Q and read each activation tile once from its L2
+  const int64_t tm = (M + kT - 1) / kT, tj = (r + kT - 1) / kT, total = tm * tj * split;
+  const int64_t Qx = (total + 7) / 8;
+  const int64_t pos = (int64_t)(blockIdx.x % 8) * Qx + blockIdx.x / 8;
+  if (pos >= total) return;
+  const int s = (int)(pos / (tm * tj));
+  const int64_t rem = pos - (int64_t)s * tm * tj;
+  const int64_t m0 = rem / tj * kT, j0 = rem % tj * kT;
   const int64_t kbeg = (int64_t)s * slice, kend = min(Kd, kbeg + slice);
   const int nst = (int)((kend - kbeg) / kBK);   // slice and Kd are multiples of 64
 
@@ -304,7 +312,9 @@ k_adapter_gemm_wide(const uint16_t* __restrict__ A, int64_t M, int64_t Kd, const
 
 int slim_launch_adapter_gemm(const uint16_t* A, int64_t M, int64_t Kd, const uint16_t* Q, int64_t r, const SlimPlan& p,
                              char* ws, hipStream_t s) {
-  dim3 grid((unsigned)p.ad_tiles_m, (unsigned)p.ad_tiles_j, (unsigned)p.ad_split);
+  const int64_t nblk = (int64_t)p.ad_tiles_m * p.ad_tiles_j * p.ad_split;
+  dim3 grid = p.ad_wide ? dim3((unsigned)p.ad_tiles_m, (unsigned)p.ad_tiles_j, (unsigned)p.ad_split)
+                        : dim3((unsigned)(8 * ((nblk + 7) / 8)));
   uint16_t* out = reinterpret_cast<uint16_t*>(ws + p.off_t);
   float* part = reinterpret_cast<float*>(ws + p.off_tpart);
   SlimKernelTimer timer("adapter_gemm", s);
