@@ -124,6 +124,17 @@ def test_tile_kernel_eight_waves_ragged_rows():
     _fwd_case(2064, 5120, 32, 16384, rows=rows, ms=ms, name="w8")
 
 
+@pytest.mark.parametrize("n,k,r,m", [(4096, 1024, 384, 4096), (4096, 1024, 272, 4096), (768, 1024, 272, 300)])
+def test_tile_epilogue_rank_groups(n, k, r, m):
+    # the epilogue's adapter product takes tm through LDS in groups of eight 16-rank steps, one
+    # activation stage per group: 512 x 128 tiles (two stages) with three groups, the last one whole
+    # (r 384) or of one step (r 272), and 512 x 96 tiles (three stages) with r 272
+    rows = np.unique(np.concatenate([synth.stream(10, "rows").choice(n, size=min(n, 256), replace=False),
+                                     np.arange(n - 16, n)]))
+    ms = np.unique(np.concatenate([synth.stream(10, "ms").choice(m, size=40, replace=False), np.arange(m - 8, m)]))
+    _fwd_case(n, k, r, m, rows=rows, ms=ms, name="epi")
+
+
 @pytest.mark.parametrize("n,k,r,m", [(256, 33024, 512, 1900), (128, 16384, 512, 4096)])
 def test_adapter_gemm_wide_tiles(n, k, r, m):
     # the 256 x 256 adapter GEMM takes shapes whose 256 x 256 tiles times reduction splits of at least
@@ -250,6 +261,13 @@ def test_bwd_adapter_gemm_wide_tiles():
     # reduction N = 33024 in 16 splits, the last one short
     ms = np.unique(np.concatenate([synth.stream(9, "ms").choice(1900, size=24, replace=False), np.arange(1892, 1900)]))
     _bwd_case(33024, 256, 512, 1900, seed=4, ks=(0, 1), ms=ms, name="bwd_adwide")
+
+
+def test_bwd_tile_epilogue_rank_groups():
+    # dX = dY W^{R,C} + (dY R^T) L^T at r 272 on 512 x 128 tiles: three groups of rank steps, the
+    # last of one step
+    ms = np.unique(np.concatenate([synth.stream(11, "ms").choice(4096, size=24, replace=False), np.arange(4088, 4096)]))
+    _bwd_case(1024, 4096, 272, 4096, seed=5, ks=(0, 31), ms=ms, name="bwd_epi")
 
 
 def test_bwd_is_deterministic():
