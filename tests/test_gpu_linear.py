@@ -135,11 +135,12 @@ def test_tile_epilogue_rank_groups(n, k, r, m):
     _fwd_case(n, k, r, m, rows=rows, ms=ms, name="epi")
 
 
-@pytest.mark.parametrize("n,k,r,m", [(256, 33024, 512, 1900), (128, 16384, 512, 4096)])
+@pytest.mark.parametrize("n,k,r,m", [(256, 33024, 512, 1900), (128, 16384, 512, 4096), (128, 2048, 512, 32768)])
 def test_adapter_gemm_wide_tiles(n, k, r, m):
     # the 256 x 256 adapter GEMM takes shapes whose 256 x 256 tiles times reduction splits of at least
     # 2048 fill 256 blocks: a ragged last m tile (M = 1900, 16 tiles) over 16 splits whose last one is
-    # short (reduction 33024 in slices of 2080), and 32 tiles over 8 splits of exactly 2048
+    # short (reduction 33024 in slices of 2080), 32 tiles over 8 splits of exactly 2048, and 256 tiles
+    # with no split (T written in fp16 by the GEMM itself)
     ms = np.unique(np.concatenate([synth.stream(8, "ms").choice(m, size=40, replace=False), np.arange(m - 8, m)]))
     _fwd_case(n, k, r, m, ms=ms, name="adwide")
 
