@@ -514,7 +514,11 @@ SLIM_DEV void finish_adapter_mfma(const LayerArgs& a, int64_t jbase, int lane, c
 template <int FM, int NW, bool QA>
 __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
   constexpr int kSteps = (FM == 1 ? 16 : 8) / NW;   // 32-rank steps per pass of one wave
-  __shared__ f4_t hand[NW > 1 ? FM : 1][64];
+  static_assert(kSteps % 4 == 0, "whole groups of four steps (4-bit adapter scales)");
+  // the wave that sums the split partials: the first, or with four waves the last (which has the
+  // fewest rank passes when the rank is not a multiple of four passes)
+  constexpr int kPartWave = NW == 4 ? 3 : 0;
+  __shared__ f4_t hand[NW > 1 ? NW - 1 : 1][NW > 1 ? FM : 1][64];
   const int lane = threadIdx.x & 63, g = lane >> 4;
   const int h = NW > 1 ? __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6) : 0;
   const int64_t row0 = (int64_t)blockIdx.x * 16;
@@ -536,7 +540,7 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
   f4_t acc[FM];
 #pragma unroll
   for (int f = 0; f < FM; ++f) acc[f] = f4_t{0.f, 0.f, 0.f, 0.f};
-  for (int s0 = 0; s0 < (h == 0 ? S : 0); s0 += 8) {   // the partials: wave 0
+  for (int s0 = 0; s0 < (h == kPartWave ? S : 0); s0 += 8) {   // the partials
     f4_t pv[8][FM];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -569,14 +573,17 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
     for (int f = 0; f < FM; ++f) acc[f] = acc[f] + adacc[f] * trinv[f];
   }
   if (NW > 1) {
-    // wave 1 hands its sum to wave 0, which adds it last (a fixed order) and stores
-    if (h == 1)
+    // waves 1 .. NW - 1 hand their sums to wave 0, which adds them in wave order (a fixed order)
+    // and stores
+    if (h > 0)
 #pragma unroll
-      for (int f = 0; f < FM; ++f) hand[f][lane] = acc[f];
+      for (int f = 0; f < FM; ++f) hand[h - 1][f][lane] = acc[f];
     __syncthreads();
     if (h != 0) return;
 #pragma unroll
-    for (int f = 0; f < FM; ++f) acc[f] = acc[f] + hand[f][lane];
+    for (int w = 0; w < NW - 1; ++w)
+#pragma unroll
+      for (int f = 0; f < FM; ++f) acc[f] = acc[f] + hand[w][f][lane];
   }
   if (rr < a.rows) {
 #pragma unroll
@@ -1174,12 +1181,18 @@ void launch_decode_units(const LayerArgs& a, const SlimPlan& p, hipStream_t s) {
 template <int FM, bool QA>
 void launch_finish(const LayerArgs& a, bool bwd, hipStream_t s) {
   SlimKernelTimer timer(bwd ? "finish_bwd" : "finish_fwd", s);
-  // two waves per 16 rows, splitting the rank, when the rank fills more than one wave's pass of
-  // half the steps and there are few rows (at most 1024 blocks): each wave issues half the adapter
-  // loads (4096^2 layer at M 16: step 11.7 -> 11.3 us); with many rows one wave per 16 rows
-  // already fills the CUs
+  // several waves per 16 rows, splitting the rank, when the rank fills more than one wave's pass
+  // and there are few rows (at most 1024 blocks): each wave issues a share of the adapter loads
+  // (4096^2 layer at M 16: step 11.7 -> 11.3 us with two). Four waves (one of them summing the
+  // split partials) for at most 4096 rows and at most 8 columns, where the adapter pass outweighs
+  // the partials (4096^2 layer at M 1: 10.21 -> 10.02 us; at M 16 two waves were as fast). The
+  // choice never depends on the adapter's format, so 4-bit and fp16 factors of the same values
+  // are summed in the same order.
+  // With many rows one wave per 16 rows already fills the CUs.
   const dim3 grid((unsigned)((a.rows + 15) / 16));
-  if (a.r > 16 * (FM == 1 ? 16 : 8) && a.rows <= 16384) SLIM_LAUNCH(timer, (k_finish<FM, 2, QA>), grid, dim3(128), s, a);
+  if (FM == 1 && a.r > 16 * 8 && a.rows <= 4096 && a.M <= 8)
+    SLIM_LAUNCH(timer, (k_finish<1, 4, QA>), grid, dim3(256), s, a);
+  else if (a.r > 16 * (FM == 1 ? 16 : 8) && a.rows <= 16384) SLIM_LAUNCH(timer, (k_finish<FM, 2, QA>), grid, dim3(128), s, a);
   else SLIM_LAUNCH(timer, (k_finish<FM, 1, QA>), grid, dim3(64), s, a);
 }
 
