@@ -224,7 +224,13 @@ def _bwd_case(n, k, r, m, seed=0, ks=None, ms=None, name="bwd", dydtype="bf16", 
         assert_close(dX[np.ix_(ms, np.arange(128 * g, 128 * g + 128))], ref, f"bwd group {g}")
 
 
-@pytest.mark.parametrize("m,r", [(16, 32), (1, 0), (5, 32), (64, 32), (200, 32), (256, 0)])
+def test_tile_kernel_exact_tiles():
+    # rows and columns that fill whole 512 x 96 tiles: no ragged edge anywhere (two row tiles, four
+    # column tiles, a reduction of eight chunks)
+    _fwd_case(1024, 1024, 64, 384, name="exact")
+
+
+@pytest.mark.parametrize("m,r", [(16, 32), (1, 0), (5, 32), (33, 32), (64, 32), (200, 32), (256, 0)])
 def test_bwd_small(m, r):
     _bwd_case(512, 512, r, m, name="bwd_small")
 
