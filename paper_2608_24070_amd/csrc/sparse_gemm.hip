@@ -616,7 +616,7 @@ __global__ void __launch_bounds__(64 * NW) k_finish(LayerArgs a) {
 // Each wave loads the words of its own rows; the scales (and in the backward the scale row) of a
 // 128-row group are loaded by every wave of the group, so that all waves issue the same loads
 // (two waves then write the same bytes).
-constexpr int kTR = 512, kBand = 4;
+constexpr int kTR = 512;
 template <int TC, int WR> struct TileShape {
   static constexpr int kWaves = kTR / WR;              // waves per block
   static constexpr int kThreads = 64 * kWaves;
@@ -690,16 +690,20 @@ SLIM_DEV void tile_body(const LayerArgs& a) {
   // the wave's 128-row group and its first fragment there
   const int grp = WR == 128 ? wave : wave >> 1, fbase = WR == 128 ? 0 : 2 * (wave & 1);
   // XCD-aware tile order: block b runs on XCD b % 8 (workgroups are dealt round robin), and XCD x
-  // takes positions [x Q, (x + 1) Q) of a tile order that walks bands of kBand row tiles column
+  // takes positions [x Q, (x + 1) Q) of a tile order that walks bands of kb row tiles column
   // by column. The blocks an XCD runs together then cover a few row tiles x a few column tiles,
   // so they share packed weights and activations in that XCD's L2.
   const int64_t R = a.row_tiles, C = a.col_tiles, T = R * C;
   const int64_t Q = (T + 7) / 8;
   const int64_t pos = (int64_t)(blockIdx.x % 8) * Q + blockIdx.x / 8;
   if (pos >= T) return;
-  const int64_t band = pos / (kBand * C), q = pos - band * kBand * C;
-  const int64_t rb = R - band * kBand < kBand ? R - band * kBand : kBand;   // rows in this band
-  const int64_t rt = band * kBand + q % rb, ct = q / rb;
+  // bands of 8 row tiles when there are at most 32 row tiles, else 4 (prefill's 22 row tiles:
+  // tile kernel 136.6 -> 134.9 us; the 70B layers' 56 were 0.5% slower with 8, all shapes slower
+  // with 2)
+  const int64_t kb = R <= 32 ? 8 : 4;
+  const int64_t band = pos / (kb * C), q = pos - band * kb * C;
+  const int64_t rb = R - band * kb < kb ? R - band * kb : kb;   // rows in this band
+  const int64_t rt = band * kb + q % rb, ct = q / rb;
   const int64_t row0 = rt * kTR, m0 = ct * kTC;
   const int64_t wrow0 = row0 + WR * wave;
   const int64_t nch = a.red / 128;
